@@ -1,0 +1,240 @@
+"""CPU oracle of MobileQuant's integer-only quantized linear layer.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU
+baseline leg of the benchmark may import this package; the product path
+never does.  It shares no code with the HIP library: the arithmetic lives
+in ``mq_oracle.c`` (plain C loops, int64 accumulation, IEEE fp32/fp64) and
+this module only marshals numpy arrays into it.
+
+Functions and the passages they follow (arXiv 2408.13933):
+
+* ``act_params``      -- Section 4.2, Eq.(2)-(3) (alpha, beta from a range)
+* ``quantize_act``    -- Section 4.2, Eq.(4) (static per-tensor quantizer)
+* ``dequant``         -- inverse of Eq.(4)
+* ``fold_weights`` / ``fold_acts`` -- Section 3.2, Eq.(1) (S W and X S^-1)
+* ``pack_weights``    -- Section 5.1 / appendix: symmetric per-channel W8, W4
+* ``requant_params`` / ``requant_value`` -- fixed-point rescale to the next
+  layer's integer format (Section 1, Section 3.1: integer-only arithmetic)
+* ``qlinear``         -- the integer-only linear layer end to end
+* ``int_matmul``      -- the raw integer product, for pinning the accumulate
+
+Parity status: every function is pinned by ``tests/test_oracle_pins.py``
+(closed forms, invariants, library routines, exact rational brute force).
+Nothing here is pinned to a printed number of the paper: the paper prints
+no worked numeric example of its quantizer or of a linear layer.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libmq_oracle.so")
+_lib = None
+
+_f32p = np.ctypeslib.ndpointer(dtype=np.float32, flags="C_CONTIGUOUS")
+_i32p = np.ctypeslib.ndpointer(dtype=np.int32, flags="C_CONTIGUOUS")
+_i64p = np.ctypeslib.ndpointer(dtype=np.int64, flags="C_CONTIGUOUS")
+_i8p = np.ctypeslib.ndpointer(dtype=np.int8, flags="C_CONTIGUOUS")
+_vp = ctypes.c_void_p
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.oracle_act_params.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_float),
+                                      ctypes.POINTER(ctypes.c_int32)]
+    lib.oracle_act_params.restype = ctypes.c_int
+    lib.oracle_quantize_act.argtypes = [_f32p, ctypes.c_int64, ctypes.c_float,
+                                        ctypes.c_int32, ctypes.c_int, _vp]
+    lib.oracle_quantize_act.restype = None
+    lib.oracle_dequant.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_float,
+                                   ctypes.c_int32, _f32p]
+    lib.oracle_dequant.restype = None
+    lib.oracle_fold_weights.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int64, _f32p]
+    lib.oracle_fold_weights.restype = None
+    lib.oracle_fold_acts.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int64, _f32p]
+    lib.oracle_fold_acts.restype = None
+    lib.oracle_pack_weights.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                        _vp, _f32p, _i32p]
+    lib.oracle_pack_weights.restype = None
+    lib.oracle_requant_params.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                          ctypes.POINTER(ctypes.c_float),
+                                          ctypes.POINTER(ctypes.c_int64),
+                                          ctypes.POINTER(ctypes.c_int32),
+                                          ctypes.POINTER(ctypes.c_int64)]
+    lib.oracle_requant_params.restype = None
+    lib.oracle_requant_value.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_int]
+    lib.oracle_requant_value.restype = ctypes.c_int64
+    lib.oracle_requant_round.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32]
+    lib.oracle_requant_round.restype = ctypes.c_int64
+    lib.oracle_qlinear.argtypes = [_i8p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                   _vp, ctypes.c_int, _f32p, ctypes.c_float, ctypes.c_int32,
+                                   ctypes.c_float, ctypes.c_int32, ctypes.c_int, _vp, _vp,
+                                   ctypes.c_int]
+    lib.oracle_qlinear.restype = None
+    lib.oracle_int_matmul.argtypes = [_i8p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                      _vp, ctypes.c_int, _i64p]
+    lib.oracle_int_matmul.restype = None
+    _lib = lib
+    return lib
+
+
+def _act_dtype(bits: int):
+    if bits == 8:
+        return np.int8
+    if bits == 16:
+        return np.int16
+    raise ValueError(f"activation bits must be 8 or 16, got {bits}")
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def default_threads() -> int:
+    return max(1, len(os.sched_getaffinity(0)))
+
+
+# --------------------------------------------------------------------------
+def act_params(f_min: float, f_max: float, bits: int):
+    """(alpha, zp) for a static per-tensor range, Section 4.2 Eq.(2)-(3)."""
+    a = ctypes.c_float()
+    z = ctypes.c_int32()
+    rc = _load().oracle_act_params(float(f_min), float(f_max), int(bits),
+                                   ctypes.byref(a), ctypes.byref(z))
+    if rc != 0:
+        raise ValueError("invalid activation range")
+    return float(a.value), int(z.value)
+
+
+def quantize_act(x: np.ndarray, alpha: float, zp: int, bits: int) -> np.ndarray:
+    """Static per-tensor quantizer, Section 4.2 Eq.(4), signed storage."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    q = np.empty(x.shape, dtype=_act_dtype(bits))
+    _load().oracle_quantize_act(x.reshape(-1), x.size, alpha, zp, bits, _ptr(q))
+    return q
+
+
+def dequant(q: np.ndarray, alpha: float, zp: int) -> np.ndarray:
+    """alpha * (q - zp) in fp32 (inverse of Eq.(4))."""
+    q = np.ascontiguousarray(q)
+    bits = {np.dtype(np.int8): 8, np.dtype(np.int16): 16}[q.dtype]
+    y = np.empty(q.shape, dtype=np.float32)
+    _load().oracle_dequant(_ptr(q), bits, q.size, alpha, zp, y.reshape(-1))
+    return y
+
+
+def fold_weights(w: np.ndarray, s: np.ndarray) -> np.ndarray:
+    """S W of Eq.(1): W_hat[n][k] = W[n][k] * s[k]."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    N, K = w.shape
+    assert s.shape == (K,)
+    out = np.empty_like(w)
+    _load().oracle_fold_weights(w, s, N, K, out)
+    return out
+
+
+def fold_acts(x: np.ndarray, s: np.ndarray) -> np.ndarray:
+    """X S^-1 of Eq.(1): X_hat[m][k] = X[m][k] / s[k]."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    M, K = x.shape
+    assert s.shape == (K,)
+    out = np.empty_like(x)
+    _load().oracle_fold_acts(x, s, M, K, out)
+    return out
+
+
+def pack_weights(w: np.ndarray, bits: int):
+    """Symmetric per-output-channel quantizer and packer.
+
+    Returns (w_q, w_scale, colsum); w_q is int8 [N][K] for bits=8 and
+    uint8 [N][K/2] (low nibble = even k) for bits=4.
+    """
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    N, K = w.shape
+    if bits == 8:
+        wq = np.empty((N, K), dtype=np.int8)
+    elif bits == 4:
+        if K % 2:
+            raise ValueError("int4 packing needs an even K")
+        wq = np.empty((N, K // 2), dtype=np.uint8)
+    else:
+        raise ValueError("bits must be 8 or 4")
+    scale = np.empty(N, dtype=np.float32)
+    colsum = np.empty(N, dtype=np.int32)
+    _load().oracle_pack_weights(w, N, K, bits, _ptr(wq), scale, colsum)
+    return wq, scale, colsum
+
+
+def requant_params(alpha_a: float, w_scale: float, alpha_y: float, bias=None):
+    """(M0, sh, bias_q) for one output channel."""
+    M0 = ctypes.c_int64()
+    sh = ctypes.c_int32()
+    bq = ctypes.c_int64()
+    b = None if bias is None else ctypes.byref(ctypes.c_float(float(bias)))
+    _load().oracle_requant_params(alpha_a, w_scale, alpha_y, b, ctypes.byref(M0),
+                                  ctypes.byref(sh), ctypes.byref(bq))
+    return int(M0.value), int(sh.value), int(bq.value)
+
+
+def requant_round(c: int, M0: int, sh: int) -> int:
+    """r = floor((c*M0 + 2^(sh-1)) / 2^sh) for one corrected accumulator."""
+    return int(_load().oracle_requant_round(int(c), int(M0), int(sh)))
+
+
+def requant_value(c: int, M0: int, sh: int, zp_y: int, bits_y: int) -> int:
+    """Requantize one corrected int32 accumulator value."""
+    return int(_load().oracle_requant_value(int(c), int(M0), int(sh), int(zp_y), int(bits_y)))
+
+
+def qlinear(a_q: np.ndarray, w_q: np.ndarray, bits: int, w_scale: np.ndarray,
+            alpha_a: float, zp_a: int, alpha_y: float, zp_y: int, bits_y: int,
+            bias=None, nthreads: int | None = None) -> np.ndarray:
+    """Integer-only linear layer: Y_q[m][n] from A_q[M][K] and W_q."""
+    a_q = np.ascontiguousarray(a_q, dtype=np.int8)
+    M, K = a_q.shape
+    w_q = np.ascontiguousarray(w_q)
+    N = w_q.shape[0]
+    if bits == 8:
+        assert w_q.dtype == np.int8 and w_q.shape == (N, K)
+    elif bits == 4:
+        assert w_q.dtype == np.uint8 and w_q.shape == (N, K // 2) and K % 2 == 0
+    else:
+        raise ValueError("bits must be 8 or 4")
+    w_scale = np.ascontiguousarray(w_scale, dtype=np.float32)
+    assert w_scale.shape == (N,)
+    bptr = None
+    if bias is not None:
+        bias = np.ascontiguousarray(bias, dtype=np.float32)
+        assert bias.shape == (N,)
+        bptr = _ptr(bias)
+    y = np.empty((M, N), dtype=_act_dtype(bits_y))
+    if M == 0 or N == 0:
+        return y
+    _load().oracle_qlinear(a_q, M, K, N, _ptr(w_q), bits, w_scale, alpha_a, zp_a,
+                           alpha_y, zp_y, bits_y, bptr, _ptr(y),
+                           nthreads or default_threads())
+    return y
+
+
+def int_matmul(a_q: np.ndarray, w_q: np.ndarray, bits: int) -> np.ndarray:
+    """sum_k A_q[m][k] * W_q[n][k], exact, int64 [M][N]."""
+    a_q = np.ascontiguousarray(a_q, dtype=np.int8)
+    M, K = a_q.shape
+    w_q = np.ascontiguousarray(w_q)
+    N = w_q.shape[0]
+    acc = np.empty((M, N), dtype=np.int64)
+    _load().oracle_int_matmul(a_q, M, K, N, _ptr(w_q), bits, acc)
+    return acc

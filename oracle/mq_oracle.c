@@ -1,0 +1,354 @@
+/*
+ * mq_oracle.c -- plain, slow CPU oracle of MobileQuant's integer-only
+ * quantized linear layer (arXiv 2408.13933).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file exists to check the HIP library
+ * against the paper.  Only the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark may load it.  The product never calls it
+ * and it shares no code, header, table or helper with the HIP sources.
+ *
+ * Every function below is the definition written out with plain loops,
+ * int64 accumulation and IEEE fp32/fp64 (compile with -O2, no fast-math,
+ * -ffp-contract=off).  Where the paper is silent the reading used is named
+ * in the comment (the same readings are listed in the design notes).
+ *
+ * Storage conventions (the paper writes Y = XW with W of shape
+ * [in, out]; here tokens are rows):
+ *   A_q  int8   [M][K]   activations, K contiguous
+ *   W_q  int8   [N][K]   weights, K contiguous  (bits = 8)
+ *        uint8  [N][K/2] two int4 weights per byte (bits = 4):
+ *                        low nibble = even k, high nibble = odd k,
+ *                        two's-complement nibbles
+ *   Y_q  int8 / int16 [M][N]
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ */
+/* integer helpers                                                     */
+/* ------------------------------------------------------------------ */
+static int64_t clamp_i64(int64_t v, int64_t lo, int64_t hi)
+{
+    return v < lo ? lo : (v > hi ? hi : v);
+}
+
+static int64_t qmin_of(int bits) { return -((int64_t)1 << (bits - 1)); }
+static int64_t qmax_of(int bits) { return ((int64_t)1 << (bits - 1)) - 1; }
+
+static void store_q(void* dst, int bits, int64_t i, int64_t v)
+{
+    if (bits == 8)
+        ((int8_t*)dst)[i] = (int8_t)v;
+    else
+        ((int16_t*)dst)[i] = (int16_t)v;
+}
+
+static int64_t load_q(const void* src, int bits, int64_t i)
+{
+    return bits == 8 ? ((const int8_t*)src)[i] : ((const int16_t*)src)[i];
+}
+
+/* ------------------------------------------------------------------ */
+/* Activation range -> (alpha, zero-point)                             */
+/* Section 4.2, Eq.(2)-(3): q_max = 2^bw - 1, alpha = (f_max-f_min)/q_max,
+ * beta = f_min/alpha.
+ * Readings: the range is widened to contain 0; the offset -beta is
+ * rounded half-to-even to an integer zero-point and clamped to
+ * [0, q_max]; values are stored signed, shifted by 2^(bw-1), so the
+ * signed zero-point is round(-beta) - 2^(bw-1).  alpha is computed in
+ * fp64 and rounded once to fp32.  A zero-width range gives alpha = 1,
+ * beta = 0.                                                            */
+/* ------------------------------------------------------------------ */
+int oracle_act_params(float f_min, float f_max, int bits,
+                      float* alpha_out, int32_t* zp_out)
+{
+    if (bits != 8 && bits != 16) return 1;
+    if (!isfinite(f_min) || !isfinite(f_max) || f_min > f_max) return 1;
+    double lo = f_min < 0.0f ? (double)f_min : 0.0;
+    double hi = f_max > 0.0f ? (double)f_max : 0.0;
+    double q_max = (double)(((int64_t)1 << bits) - 1);     /* Eq.(2) */
+    float alpha;
+    double beta;
+    if (hi - lo == 0.0) {
+        alpha = 1.0f;
+        beta = 0.0;
+    } else {
+        alpha = (float)((hi - lo) / q_max);                /* Eq.(3) */
+        if (!(alpha > 0.0f) || !isfinite(alpha)) return 1;
+        beta = lo / (double)alpha;                         /* Eq.(3) */
+    }
+    double zu = rint(-beta);
+    if (zu < 0.0) zu = 0.0;
+    if (zu > q_max) zu = q_max;
+    *alpha_out = alpha;
+    *zp_out = (int32_t)((int64_t)zu - ((int64_t)1 << (bits - 1)));
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Activation quantizer, Section 4.2 Eq.(4):
+ *   X_int = min(max(round(X/alpha) - beta, 0), q_max)
+ * in signed storage: q = clamp(rint(x/alpha) + zp, -2^(bw-1), 2^(bw-1)-1).
+ * x/alpha is one IEEE fp32 division, rint is half-to-even.  The quotient
+ * is first limited to +-2^20 so that it converts to an integer; NaN takes
+ * the fmaxf/fminf convention (the non-NaN bound) and ends at the low end.  */
+/* ------------------------------------------------------------------ */
+void oracle_quantize_act(const float* x, int64_t n, float alpha, int32_t zp,
+                         int bits, void* q)
+{
+    const float lim = 1048576.0f; /* 2^20 */
+    for (int64_t i = 0; i < n; ++i) {
+        float t = x[i] / alpha;
+        t = fminf(fmaxf(t, -lim), lim);
+        int64_t v = (int64_t)rintf(t) + zp;
+        store_q(q, bits, i, clamp_i64(v, qmin_of(bits), qmax_of(bits)));
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Dequantization: the inverse map of Eq.(4), y = alpha * (q - zp), one
+ * exact integer subtraction and one fp32 multiply.                    */
+/* ------------------------------------------------------------------ */
+void oracle_dequant(const void* q, int bits, int64_t n, float alpha,
+                    int32_t zp, float* y)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        int64_t d = load_q(q, bits, i) - zp;
+        y[i] = alpha * (float)d;
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Equivalent transformation, Section 3.2 Eq.(1): Y = X W = (X S^-1)(S W).
+ * With S = diag(s) on the input channels: W_hat[n][k] = W[n][k] * s[k]
+ * and X_hat[m][k] = X[m][k] / s[k], one fp32 rounding each.            */
+/* ------------------------------------------------------------------ */
+void oracle_fold_weights(const float* w, const float* s, int64_t N, int64_t K,
+                         float* w_hat)
+{
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k)
+            w_hat[n * K + k] = w[n * K + k] * s[k];
+}
+
+void oracle_fold_acts(const float* x, const float* s, int64_t M, int64_t K,
+                      float* x_hat)
+{
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t k = 0; k < K; ++k)
+            x_hat[m * K + k] = x[m * K + k] / s[k];
+}
+
+/* ------------------------------------------------------------------ */
+/* Symmetric per-output-channel weight quantizer (Section 5.1 W8A8/W4A8
+ * settings and the appendix's symmetric per-channel W4).
+ * Readings: narrow range +-Q with Q = 2^(b-1)-1; scale = absmax/Q in fp32
+ * (1 when that is not positive); q = rint(w/scale) limited to [-Q, Q]
+ * (NaN -> -Q by the fmaxf/fminf convention).  colsum[n] = sum_k q[n][k].
+ * bits = 4 packs two weights per byte, low nibble = even k.           */
+/* ------------------------------------------------------------------ */
+void oracle_pack_weights(const float* w, int64_t N, int64_t K, int bits,
+                         void* w_q, float* w_scale, int32_t* colsum)
+{
+    const float Q = bits == 8 ? 127.0f : 7.0f;
+    int8_t* tmp = (int8_t*)malloc((size_t)K);
+    for (int64_t n = 0; n < N; ++n) {
+        const float* row = w + n * K;
+        float m = 0.0f;
+        for (int64_t k = 0; k < K; ++k) m = fmaxf(m, fabsf(row[k]));
+        float s = m / Q;
+        if (!(s > 0.0f)) s = 1.0f;
+        int64_t sum = 0;
+        for (int64_t k = 0; k < K; ++k) {
+            float t = row[k] / s;
+            t = fminf(fmaxf(t, -Q), Q);
+            tmp[k] = (int8_t)rintf(t);
+            sum += tmp[k];
+        }
+        w_scale[n] = s;
+        colsum[n] = (int32_t)sum;
+        if (bits == 8) {
+            memcpy((int8_t*)w_q + n * K, tmp, (size_t)K);
+        } else {
+            uint8_t* dst = (uint8_t*)w_q + n * (K / 2);
+            for (int64_t j = 0; j < K / 2; ++j)
+                dst[j] = (uint8_t)(((unsigned)tmp[2 * j] & 0xFu) |
+                                   (((unsigned)tmp[2 * j + 1] & 0xFu) << 4));
+        }
+    }
+    free(tmp);
+}
+
+/* Weight code of row n, input channel k, read from the stored layout.
+ * int4: the nibble is a two's-complement 4-bit integer.               */
+static int64_t weight_at(const void* w_q, int bits, int64_t K, int64_t n,
+                         int64_t k)
+{
+    if (bits == 8) return ((const int8_t*)w_q)[n * K + k];
+    unsigned byte = ((const uint8_t*)w_q)[n * (K / 2) + k / 2];
+    unsigned nib = (k & 1) ? (byte >> 4) : (byte & 0xFu);
+    return nib >= 8 ? (int64_t)nib - 16 : (int64_t)nib;
+}
+
+/* ------------------------------------------------------------------ */
+/* Fixed-point requantization parameters for output channel n.
+ * The paper only states that every operation runs on fixed-point integers
+ * (Section 1 and the design choices of Section 3.1).  Reading: the real
+ * rescale M = (alpha_a * w_scale[n]) / alpha_y is computed in fp64 and
+ * written M = M0 * 2^-sh with a 31-bit integer M0 in [2^30, 2^31): with
+ * M = f * 2^e, f in [0.5, 1), M0 = rint(f * 2^31) (2^31 is renormalised
+ * to 2^30 with e + 1), sh = 31 - e.
+ * The bias enters in accumulator units: bias_q = rint(b / (alpha_a *
+ * w_scale)) in fp64, limited to +-2^30 (0 without bias).               */
+/* ------------------------------------------------------------------ */
+void oracle_requant_params(float alpha_a, float w_scale, float alpha_y,
+                           const float* bias_n, int64_t* M0_out,
+                           int32_t* sh_out, int64_t* bias_q_out)
+{
+    double M = ((double)alpha_a * (double)w_scale) / (double)alpha_y;
+    if (!(M > 0.0)) {
+        /* not a usable scale (w_scale <= 0 or NaN): the rescaled value is 0 */
+        *M0_out = 0;
+        *sh_out = 31;
+    } else if (isinf(M)) {
+        /* infinite rescale: every non-zero accumulator saturates */
+        *M0_out = (int64_t)1 << 30;
+        *sh_out = 0;
+    } else {
+        int e = 0;
+        double f = frexp(M, &e);
+        int64_t M0 = (int64_t)rint(ldexp(f, 31));
+        if (M0 == ((int64_t)1 << 31)) {
+            M0 = (int64_t)1 << 30;
+            e += 1;
+        }
+        *M0_out = M0;
+        *sh_out = 31 - e;
+    }
+    int64_t bq = 0;
+    if (bias_n) {
+        double t = (double)*bias_n / ((double)alpha_a * (double)w_scale);
+        t = fmin(fmax(t, -1073741824.0), 1073741824.0);
+        bq = (int64_t)rint(t);
+    }
+    *bias_q_out = bq;
+}
+
+/* ------------------------------------------------------------------ */
+/* One requantized output value from its corrected accumulator c:
+ *   r = floor((c * M0 + 2^(sh-1)) / 2^sh)   (one rounding, ties up)
+ *   y = clamp(r + zp_y, qmin, qmax)
+ * c has already been limited to int32, so |c * M0| < 2^62 and the int64
+ * arithmetic below is exact.  sh >= 63 gives r = 0 exactly.  sh <= 0
+ * means M >= 2^30, so |r| >= 2^30 * |c| and any non-zero c saturates.  */
+/* ------------------------------------------------------------------ */
+int64_t oracle_requant_round(int64_t c, int64_t M0, int32_t sh)
+{
+    if (sh >= 63) return 0;
+    if (sh >= 1) {
+        int64_t p = c * M0 + ((int64_t)1 << (sh - 1));
+        /* floor division by 2^sh, written without shifting a negative value */
+        return p >= 0 ? p >> sh : -((-p + ((int64_t)1 << sh) - 1) >> sh);
+    }
+    /* sh <= 0: |r| >= 2^30 |c|; any value beyond the int16 range will do */
+    return c > 0 ? ((int64_t)1 << 40) : (c < 0 ? -((int64_t)1 << 40) : 0);
+}
+
+int64_t oracle_requant_value(int64_t c, int64_t M0, int32_t sh, int32_t zp_y,
+                             int bits_y)
+{
+    int64_t r = oracle_requant_round(c, M0, sh);
+    return clamp_i64(r + zp_y, qmin_of(bits_y), qmax_of(bits_y));
+}
+
+/* ------------------------------------------------------------------ */
+/* Integer-only linear layer (the hot path):
+ *   c[m][n] = sat_int32( sum_k (A_q[m][k] - zp_a) * W_q[n][k] + bias_q[n] )
+ *   Y_q[m][n] = requant(c[m][n])
+ * The sum is the plain definition, accumulated exactly in int64 (integer
+ * MACs with a wide accumulator: Section 1, Section 3.1).               */
+/* ------------------------------------------------------------------ */
+typedef struct {
+    const int8_t* a;
+    int64_t M, K, N;
+    const void* w_q;
+    int bits;
+    const float* w_scale;
+    float alpha_a;
+    int32_t zp_a;
+    float alpha_y;
+    int32_t zp_y;
+    int bits_y;
+    const float* bias;
+    void* y;
+    int64_t row_begin, row_end;
+    int64_t* M0;
+    int32_t* sh;
+    int64_t* bq;
+} qlinear_job;
+
+static void* qlinear_rows(void* arg)
+{
+    qlinear_job* j = (qlinear_job*)arg;
+    for (int64_t m = j->row_begin; m < j->row_end; ++m) {
+        const int8_t* arow = j->a + m * j->K;
+        for (int64_t n = 0; n < j->N; ++n) {
+            int64_t acc = 0;
+            for (int64_t k = 0; k < j->K; ++k)
+                acc += ((int64_t)arow[k] - j->zp_a) *
+                       weight_at(j->w_q, j->bits, j->K, n, k);
+            int64_t c = clamp_i64(acc + j->bq[n], INT32_MIN, INT32_MAX);
+            int64_t v = oracle_requant_value(c, j->M0[n], j->sh[n], j->zp_y,
+                                             j->bits_y);
+            store_q(j->y, j->bits_y, m * j->N + n, v);
+        }
+    }
+    return NULL;
+}
+
+void oracle_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                    const void* w_q, int bits, const float* w_scale,
+                    float alpha_a, int32_t zp_a, float alpha_y, int32_t zp_y,
+                    int bits_y, const float* bias, void* y_q, int nthreads)
+{
+    int64_t* M0 = (int64_t*)malloc(sizeof(int64_t) * (size_t)N);
+    int32_t* sh = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+    int64_t* bq = (int64_t*)malloc(sizeof(int64_t) * (size_t)N);
+    for (int64_t n = 0; n < N; ++n)
+        oracle_requant_params(alpha_a, w_scale[n], alpha_y,
+                              bias ? bias + n : NULL, &M0[n], &sh[n], &bq[n]);
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > M) nthreads = (int)(M > 0 ? M : 1);
+    pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
+    qlinear_job* jobs = (qlinear_job*)malloc(sizeof(qlinear_job) * (size_t)nthreads);
+    for (int t = 0; t < nthreads; ++t) {
+        qlinear_job j = {a_q, M, K, N, w_q, bits, w_scale, alpha_a, zp_a,
+                         alpha_y, zp_y, bits_y, bias, y_q,
+                         M * t / nthreads, M * (t + 1) / nthreads, M0, sh, bq};
+        jobs[t] = j;
+        pthread_create(&th[t], NULL, qlinear_rows, &jobs[t]);
+    }
+    for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+    free(jobs);
+    free(th);
+    free(M0);
+    free(sh);
+    free(bq);
+}
+
+/* The raw integer product sum_k A_q[m][k] * W_q[n][k] (no zero-point, no
+ * bias, no rescale), exposed so tests can pin the accumulation alone.  */
+void oracle_int_matmul(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                       const void* w_q, int bits, int64_t* acc)
+{
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t n = 0; n < N; ++n) {
+            int64_t s = 0;
+            for (int64_t k = 0; k < K; ++k)
+                s += (int64_t)a_q[m * K + k] * weight_at(w_q, bits, K, n, k);
+            acc[m * N + n] = s;
+        }
+}

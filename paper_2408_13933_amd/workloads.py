@@ -1,0 +1,256 @@
+"""Seeded synthetic workloads for the integer-only linear layer.
+
+This module only draws random numbers and describes shapes.  It holds none
+of the quantization arithmetic: it hands both the HIP library and the CPU
+oracle the same fp32 tensors and the same static float ranges, and each
+side derives scales, zero-points and integer codes on its own.
+
+Recipe (stand-in for the paper's calibration and evaluation data, which
+are not used): layer shapes are those of the small Llama-style and
+Gemma-2B-style models the paper deploys; activations carry a few
+large-magnitude channels, the property that makes per-tensor activation
+quantization hard (Section 3.2).
+
+* activations X_hat [M][K] fp32: N(0, 1) with 4 outlier channels scaled by
+  20 (TinyLlama-shaped layers), or N(0, 1) with max(4, round(0.01 K))
+  channels drawn from Student-t(3) instead (Gemma-shaped layers).  These
+  are the activations as they reach the layer, i.e. already in the
+  smoothed domain of Eq.(1).
+* weights W [N][K] fp32: N(0, 0.02^2), before folding.
+* smoothing vector s [K] (only where a layer folds one): exp(U(ln 0.5,
+  ln 2)); the fold W_hat = W diag(s) is done by the code under test.
+* bias [N] fp32: N(0, 0.01^2) where the layer has one.
+* static activation range: min and max of X_hat (a plain data statistic).
+* static output range: the layer output has standard deviation
+  sigma_y = 0.02 * rms_m sqrt(sum_k (X_hat[m,k] s[k])^2) under this recipe;
+  the range is [-4.5 sigma_y - 3 sigma_b, 5.5 sigma_y + 3 sigma_b], skewed
+  so the output zero-point is not zero and a few outputs saturate.
+"""
+from __future__ import annotations
+
+import dataclasses
+import zlib
+from typing import Optional
+
+import numpy as np
+
+W_STD = 0.02
+B_STD = 0.01
+
+
+@dataclasses.dataclass(frozen=True)
+class Layer:
+    name: str
+    M: int
+    K: int
+    N: int
+    w_bits: int = 8          # 8 or 4
+    out_bits: int = 8        # 8 or 16
+    bias: bool = True
+    act: str = "outlier"     # "outlier" | "student_t"
+    smooth: Optional[str] = None   # name of the smoothing vector folded in
+    smooth_len: int = 0            # length of that vector
+
+    @property
+    def ops(self) -> int:
+        return 2 * self.M * self.N * self.K
+
+    def alg_bytes(self) -> int:
+        """Minimum bytes one qlinear call moves: A, W, Y and per-column params."""
+        w = self.N * self.K * self.w_bits // 8
+        a = self.M * self.K
+        y = self.M * self.N * self.out_bits // 8
+        params = self.N * (8 + (4 if self.bias else 0))
+        return w + a + y + params
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    description: str
+    layers: tuple
+
+
+def _tinyllama_block(M: int):
+    L = dict(out_bits=16, bias=False)
+    return (
+        Layer("q_proj", M, 2048, 2048, smooth="attn_norm", smooth_len=2048, **L),
+        Layer("k_proj", M, 2048, 256, smooth="attn_norm", smooth_len=2048, **L),
+        Layer("v_proj", M, 2048, 256, smooth="attn_norm", smooth_len=2048, **L),
+        Layer("o_proj", M, 2048, 2048, smooth="v_to_o", smooth_len=256, **L),
+        Layer("gate_proj", M, 2048, 5632, smooth="mlp_norm", smooth_len=2048, **L),
+        Layer("up_proj", M, 2048, 5632, smooth="mlp_norm", smooth_len=2048, **L),
+        Layer("down_proj", M, 5632, 2048, smooth="up_to_down", smooth_len=5632, **L),
+    )
+
+
+WORKLOADS = {
+    "decode_w8a8_m16": Workload(
+        "decode_w8a8_m16",
+        "single W8A8 qlinear, M=16, K=2048, N=2048, int8 out, bias",
+        (Layer("linear", 16, 2048, 2048),)),
+    "prefill_w8a8_tinyllama_m2048": Workload(
+        "prefill_w8a8_tinyllama_m2048",
+        "TinyLlama-shaped MLP gate/up (M=2048, K=2048, N=5632) and attention "
+        "o-proj (M=2048, K=2048, N=2048), W8A8, int8 out, bias",
+        (Layer("gate_proj", 2048, 2048, 5632),
+         Layer("up_proj", 2048, 2048, 5632),
+         Layer("o_proj", 2048, 2048, 2048))),
+    "w4a8_down_tinyllama": Workload(
+        "w4a8_down_tinyllama",
+        "W4A8 down-proj K=5632, N=2048, symmetric per-channel int4, int16 out, "
+        "at M=1 (decode) and M=1024 (prefill)",
+        (Layer("down_proj_m1", 1, 5632, 2048, w_bits=4, out_bits=16),
+         Layer("down_proj_m1024", 1024, 5632, 2048, w_bits=4, out_bits=16))),
+    "block_w8a8_tinyllama_s1024": Workload(
+        "block_w8a8_tinyllama_s1024",
+        "the seven linears of one hidden-2048, 32-head, 4-KV-head, "
+        "intermediate-5632 decoder block at batch 1, seq 1024, W8A8 with "
+        "folded smoothing vectors, int8 in, int16 out",
+        _tinyllama_block(1024)),
+    "gemma2b_w8a8": Workload(
+        "gemma2b_w8a8",
+        "Gemma-2B-shaped W8A8 layers: MLP gate/up K=2048 N=16384 and down "
+        "K=16384 N=2048 at M=512, LM head K=2048 N=256000 at M=1 and M=512, "
+        "int16 out, heavy-tailed activation channels",
+        (Layer("gate_proj", 512, 2048, 16384, out_bits=16, bias=False, act="student_t"),
+         Layer("up_proj", 512, 2048, 16384, out_bits=16, bias=False, act="student_t"),
+         Layer("down_proj", 512, 16384, 2048, out_bits=16, bias=False, act="student_t"),
+         Layer("lm_head_m1", 1, 2048, 256000, out_bits=16, bias=False, act="student_t"),
+         Layer("lm_head_m512", 512, 2048, 256000, out_bits=16, bias=False,
+               act="student_t"))),
+}
+
+
+def _rng(*keys) -> np.random.Generator:
+    seed = [zlib.crc32(str(k).encode()) for k in keys]
+    return np.random.default_rng(seed)
+
+
+def gen_activations(M: int, K: int, act: str, seed_key) -> np.ndarray:
+    rng = _rng("act", *seed_key)
+    x = rng.standard_normal((M, K), dtype=np.float32)
+    if act == "outlier":
+        ch = rng.choice(K, 4, replace=False)
+        x[:, ch] *= np.float32(20.0)
+    elif act == "student_t":
+        n_ch = max(4, int(round(0.01 * K)))
+        ch = rng.choice(K, n_ch, replace=False)
+        x[:, ch] = rng.standard_t(3.0, size=(M, n_ch)).astype(np.float32)
+    else:
+        raise ValueError(act)
+    return x
+
+
+def gen_weights(N: int, K: int, seed_key) -> np.ndarray:
+    rng = _rng("w", *seed_key)
+    w = rng.standard_normal((N, K), dtype=np.float32)
+    w *= np.float32(W_STD)
+    return w
+
+
+def gen_bias(N: int, seed_key) -> np.ndarray:
+    rng = _rng("b", *seed_key)
+    return (rng.standard_normal(N, dtype=np.float32) * np.float32(B_STD)).astype(np.float32)
+
+
+def gen_smoothing(length: int, seed_key) -> np.ndarray:
+    rng = _rng("s", *seed_key)
+    return np.exp(rng.uniform(np.log(0.5), np.log(2.0), size=length)).astype(np.float32)
+
+
+def smoothing_for(layer: Layer, workload: str) -> Optional[np.ndarray]:
+    """The per-input-channel smoothing vector folded into this layer, or None.
+
+    The v->o vector has one entry per value channel (4 KV heads x 64); each
+    KV head's entries are shared by the 8 query heads of its group, so it is
+    repeated along o_proj's 2048 inputs (32 heads x 64).
+    """
+    if layer.smooth is None:
+        return None
+    if layer.smooth == "v_to_o" and layer.K == 2048:
+        s = gen_smoothing(256, (workload, layer.smooth))
+        kv_heads, head_dim, q_heads = 4, 64, 32
+        s = s.reshape(kv_heads, 1, head_dim)
+        s = np.broadcast_to(s, (kv_heads, q_heads // kv_heads, head_dim)).reshape(-1)
+        return np.ascontiguousarray(s, dtype=np.float32)
+    return gen_smoothing(layer.K, (workload, layer.smooth))
+
+
+@dataclasses.dataclass
+class LayerData:
+    layer: Layer
+    x: np.ndarray                  # fp32 [M][K], smoothed-domain activations
+    w: np.ndarray                  # fp32 [N][K], before folding
+    s: Optional[np.ndarray]        # fp32 [K] or None
+    bias: Optional[np.ndarray]     # fp32 [N] or None
+    act_range: tuple               # (f_min, f_max) of x
+    out_range: tuple               # static output range
+
+
+def _output_range(x: np.ndarray, s: Optional[np.ndarray], has_bias: bool):
+    xs = x.astype(np.float64)
+    if s is not None:
+        xs = xs * s.astype(np.float64)[None, :]
+    row_ss = np.einsum("mk,mk->m", xs, xs)
+    sigma_y = W_STD * float(np.sqrt(np.mean(row_ss)))
+    sb = 3.0 * B_STD if has_bias else 0.0
+    return (float(np.float32(-4.5 * sigma_y - sb)), float(np.float32(5.5 * sigma_y + sb)))
+
+
+def make_layer(workload: str, layer: Layer, rows: Optional[slice] = None,
+               shared_x: Optional[np.ndarray] = None) -> LayerData:
+    """Draw one layer's tensors.
+
+    Layers that read the same activation in the model (q/k/v, gate/up) share
+    one draw; the M=1 decode variants take row 0 of their prefill partner.
+    """
+    key_x = _x_key(workload, layer)
+    if shared_x is not None:
+        x = shared_x
+    else:
+        x = gen_activations(_x_rows(workload, layer), layer.K, layer.act, key_x)
+    x = np.ascontiguousarray(x[: layer.M])
+    w = gen_weights(layer.N, layer.K, (workload, _w_name(layer)))
+    s = smoothing_for(layer, workload)
+    bias = gen_bias(layer.N, (workload, _w_name(layer))) if layer.bias else None
+    act_range = (float(x.min()), float(x.max()))
+    out_range = _output_range(x, s, layer.bias)
+    if rows is not None:
+        x = np.ascontiguousarray(x[rows])
+    return LayerData(layer, x, w, s, bias, act_range, out_range)
+
+
+def _w_name(layer: Layer) -> str:
+    # decode and prefill variants of one layer share the weight matrix
+    for suf in ("_m1024", "_m512", "_m1"):
+        if layer.name.endswith(suf):
+            return layer.name[: -len(suf)]
+    return layer.name
+
+
+def _x_key(workload: str, layer: Layer):
+    name = _w_name(layer)
+    if name in ("q_proj", "k_proj", "v_proj"):
+        name = "qkv_in"
+    if name in ("gate_proj", "up_proj"):
+        name = "mlp_in"
+    return (workload, name)
+
+
+def _x_rows(workload: str, layer: Layer) -> int:
+    """Rows to draw so that an M=1 variant reuses row 0 of its prefill twin."""
+    wl = WORKLOADS.get(workload)
+    if wl is None:
+        return layer.M
+    base = _w_name(layer)
+    return max([l.M for l in wl.layers if _w_name(l) == base] + [layer.M])
+
+
+def scaled_layer(layer: Layer, M=None, K=None, N=None, name=None) -> Layer:
+    """A copy of ``layer`` at another shape (for oracle-sized parity cases)."""
+    K2 = layer.K if K is None else K
+    return dataclasses.replace(layer, M=layer.M if M is None else M, K=K2,
+                               N=layer.N if N is None else N,
+                               name=layer.name if name is None else name,
+                               smooth_len=K2 if layer.smooth else 0)

@@ -1,0 +1,501 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+None of these compares the oracle with itself: each check uses a hand-worked
+value (tests/golden), a closed form stated in the paper, an invariant of the
+definition, a library routine standing in for one step (numpy's int64
+matmul), or exact rational brute force on tiny inputs.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import bruteforce as bf
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden_lines(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                yield line
+
+
+# ---------------------------------------------------------------------------
+# Section 4.2, Eq.(2)-(4): the activation quantizer
+# ---------------------------------------------------------------------------
+def test_arl_quantizer_worked_examples():
+    n_cases = 0
+    for line in _golden_lines("arl_quantizer_worked.txt"):
+        head, params, pairs = [p.strip() for p in line.split("|")]
+        _, bw, fmin, fmax = head.split()
+        alpha_ref, zp_ref = params.split()
+        bw = int(bw)
+        alpha, zp = oracle.act_params(float(fmin), float(fmax), bw)
+        assert alpha == float(alpha_ref) and zp == int(zp_ref), line
+        xs, qs = zip(*[p.split(":") for p in pairs.split()])
+        x = np.array([float(v) for v in xs], dtype=np.float32)
+        q = oracle.quantize_act(x, alpha, zp, bw)
+        assert q.tolist() == [int(v) for v in qs], line
+        n_cases += 1
+    assert n_cases == 4
+
+
+@pytest.mark.parametrize("bw", [8, 16])
+def test_arl_closed_forms(bw):
+    # Under Eq.(4) the paper states f_min = alpha*beta and
+    # f_max = alpha*q_max + alpha*beta.  With beta rounded to the integer
+    # -zp_u the learned range is reproduced to within alpha/2 at each end.
+    rng = np.random.default_rng(1)
+    q_max = 2 ** bw - 1
+    for _ in range(200):
+        lo = -float(np.float32(abs(rng.standard_normal()) * 10 + 1e-3))
+        hi = float(np.float32(abs(rng.standard_normal()) * 10 + 1e-3))
+        alpha, zp = oracle.act_params(lo, hi, bw)
+        beta_int = -(zp + 2 ** (bw - 1))          # -zp_u
+        f_min = alpha * beta_int
+        f_max = alpha * q_max + alpha * beta_int
+        assert abs(f_min - lo) <= alpha * 0.5 + 1e-6 * abs(lo)
+        assert abs(f_max - hi) <= alpha * 0.5 + 1e-6 * abs(hi)
+        # alpha is the fp32 rounding of the exact (hi - lo)/q_max
+        exact = Fraction(hi) - Fraction(lo)
+        assert abs(Fraction(alpha) - exact / q_max) <= Fraction(alpha) * Fraction(1, 2 ** 23)
+
+
+@pytest.mark.parametrize("bw", [8, 16])
+def test_quantizer_invariants(bw):
+    rng = np.random.default_rng(2)
+    qmin, qmax = -(2 ** (bw - 1)), 2 ** (bw - 1) - 1
+    for lo, hi in [(-3.0, 5.0), (-80.0, 20.0), (-1e-3, 4e-3), (0.0, 7.0), (-7.0, 0.0)]:
+        alpha, zp = oracle.act_params(lo, hi, bw)
+        # zero maps exactly to the zero-point
+        assert oracle.quantize_act(np.zeros(3, np.float32), alpha, zp, bw).tolist() == [zp] * 3
+        # the ends of the range map to the ends of the integer grid
+        ends = oracle.quantize_act(np.array([hi, lo, 10 * hi + 1, 10 * lo - 1], np.float32),
+                                   alpha, zp, bw).tolist()
+        if hi > 0:
+            assert ends[0] >= qmax - 1 and ends[2] == qmax
+        if lo < 0:
+            assert ends[1] <= qmin + 1 and ends[3] == qmin
+        # monotone non-decreasing
+        x = np.sort(rng.uniform(2 * lo - 1, 2 * hi + 1, 5000).astype(np.float32))
+        q = oracle.quantize_act(x, alpha, zp, bw).astype(np.int64)
+        assert np.all(np.diff(q) >= 0)
+        # every grid point is a fixed point of quantize(dequantize(.))
+        grid = np.arange(qmin, qmax + 1, dtype=np.int64)
+        if bw == 16:
+            grid = grid[:: 97]
+        g = grid.astype(np.int8 if bw == 8 else np.int16)
+        xr = oracle.dequant(g, alpha, zp)
+        assert np.array_equal(oracle.quantize_act(xr, alpha, zp, bw).astype(np.int64), grid)
+        # |x - dequant(quantize(x))| <= alpha/2 inside the range
+        xin = rng.uniform(lo, hi, 2000).astype(np.float32)
+        back = oracle.dequant(oracle.quantize_act(xin, alpha, zp, bw), alpha, zp)
+        assert np.max(np.abs(back.astype(np.float64) - xin)) <= alpha * (0.5 + 1e-5) + 1e-7
+
+
+def test_quantizer_nonfinite_inputs():
+    alpha, zp = oracle.act_params(-4.0, 4.0, 8)
+    q = oracle.quantize_act(np.array([np.inf, -np.inf, np.nan, 3e38, -3e38], np.float32),
+                            alpha, zp, 8).tolist()
+    assert q == [127, -128, -128, 127, -128]
+
+
+def test_quantizer_matches_numpy_rounding():
+    # numpy's fp32 true division and rint are IEEE operations of their own;
+    # agreement over many random values pins the division and the tie rule.
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal(200000) * 30).astype(np.float32)
+    x[:1000] = (np.arange(1000, dtype=np.float32) - 500) * np.float32(0.5)  # ties
+    for bw in (8, 16):
+        alpha, zp = oracle.act_params(float(x.min()), float(x.max()), bw)
+        t = np.clip(x / np.float32(alpha), -2.0 ** 20, 2.0 ** 20)
+        ref = np.clip(np.rint(t).astype(np.int64) + zp, -(2 ** (bw - 1)), 2 ** (bw - 1) - 1)
+        assert np.array_equal(oracle.quantize_act(x, alpha, zp, bw).astype(np.int64), ref)
+
+
+def test_dequant_is_single_multiply():
+    q = np.arange(-128, 128, dtype=np.int64).astype(np.int8)
+    alpha, zp = 0.037, -5
+    y = oracle.dequant(q, alpha, zp)
+    ref = [float(np.float32(alpha) * np.float32(int(v) - zp)) for v in q]
+    assert y.tolist() == ref
+    q16 = np.array([-32768, -1, 0, 1, 32767], dtype=np.int16)
+    y16 = oracle.dequant(q16, 2.0, 7)
+    assert y16.tolist() == [2.0 * (v - 7) for v in q16.tolist()]
+
+
+# ---------------------------------------------------------------------------
+# Per-channel symmetric weight quantizer and int4 packing
+# ---------------------------------------------------------------------------
+def _unpack_nibbles(b: np.ndarray) -> np.ndarray:
+    """Two's-complement nibbles, low nibble first (independent of the oracle)."""
+    b = b.astype(np.int64)
+    lo = b & 0xF
+    hi = (b >> 4) & 0xF
+    lo = np.where(lo >= 8, lo - 16, lo)
+    hi = np.where(hi >= 8, hi - 16, hi)
+    out = np.empty(b.shape[:-1] + (2 * b.shape[-1],), dtype=np.int64)
+    out[..., 0::2] = lo
+    out[..., 1::2] = hi
+    return out
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_weight_quantizer_properties(bits):
+    rng = np.random.default_rng(4)
+    N, K = 37, 96
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    w[3] = 0.0                                 # an all-zero row
+    w[5, 7] = -1.0                             # a negative extreme
+    wq, scale, colsum = oracle.pack_weights(w, bits)
+    Q = 127 if bits == 8 else 7
+    q = wq.astype(np.int64) if bits == 8 else _unpack_nibbles(wq)
+    assert q.shape == (N, K)
+    assert np.all(np.abs(q) <= Q)
+    for n in range(N):
+        if n == 3:
+            assert scale[n] == 1.0 and np.all(q[n] == 0)
+            continue
+        k = int(np.argmax(np.abs(w[n])))
+        assert q[n, k] == (Q if w[n, k] > 0 else -Q)     # the absmax hits the grid end
+        assert scale[n] == np.float32(np.float32(np.max(np.abs(w[n]))) / np.float32(Q))
+        # reconstruction error within half a step
+        err = np.abs(w[n].astype(np.float64) - scale[n] * q[n])
+        assert np.max(err) <= 0.5 * scale[n] * (1 + 1e-6)
+    assert np.array_equal(colsum.astype(np.int64), q.sum(axis=1))
+
+
+def test_int4_pack_all_nibble_pairs():
+    # every byte value arises from exactly one (even, odd) weight pair
+    vals = np.arange(-8, 8)
+    pairs = np.array([(a, b) for a in vals for b in vals], dtype=np.int64)
+    # build weights whose per-row scale is exactly 1 (absmax 7 -> scale 1)
+    # and run one pair per row, padded with the row's scale anchor
+    K = 4
+    rows = []
+    for a, b in pairs:
+        if a == -8 or b == -8:
+            continue        # -8 is outside the narrow symmetric grid
+        rows.append([float(a), float(b), 7.0, 0.0])
+    w = np.array(rows, dtype=np.float32)
+    wq, scale, _ = oracle.pack_weights(w, 4)
+    assert np.all(scale == 1.0)
+    un = _unpack_nibbles(wq)
+    assert np.array_equal(un, w.astype(np.int64))
+    # and the packed byte is exactly lo | hi << 4
+    expect = [((int(a) & 0xF) | ((int(b) & 0xF) << 4)) for a, b, _, _ in rows]
+    assert wq[:, 0].tolist() == expect
+    assert K == w.shape[1]
+
+
+def test_int4_qlinear_reads_all_256_bytes():
+    # the oracle's reading of packed weights must agree with the independent
+    # nibble decoder for every byte value, including the unused -8 nibble
+    K = 2 * 256
+    wq = np.arange(256, dtype=np.uint8).reshape(1, 256)
+    a = np.zeros((1, K), np.int8)
+    want = _unpack_nibbles(wq)[0]
+    for k in range(0, K, 37):
+        a[:] = 0
+        a[0, k] = 1
+        acc = oracle.int_matmul(a, wq, 4)
+        assert acc[0, 0] == want[k]
+
+
+# ---------------------------------------------------------------------------
+# Integer accumulation and fixed-point requantization
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("shape", [(1, 1, 1), (3, 5, 2), (16, 64, 33), (67, 130, 96)])
+def test_int_matmul_matches_numpy(shape):
+    M, K, N = shape
+    rng = np.random.default_rng(5)
+    a = rng.integers(-128, 128, (M, K), dtype=np.int64).astype(np.int8)
+    w = rng.integers(-128, 128, (N, K), dtype=np.int64).astype(np.int8)
+    ref = a.astype(np.int64) @ w.astype(np.int64).T
+    assert np.array_equal(oracle.int_matmul(a, w, 8), ref)
+    if K % 2 == 0:
+        w4 = rng.integers(-8, 8, (N, K), dtype=np.int64)
+        packed = ((w4[:, 0::2] & 0xF) | ((w4[:, 1::2] & 0xF) << 4)).astype(np.uint8)
+        ref4 = a.astype(np.int64) @ w4.T
+        assert np.array_equal(oracle.int_matmul(a, packed, 4), ref4)
+
+
+def test_int_matmul_extremes():
+    K = 4096
+    a = np.full((2, K), -128, np.int8)
+    a[1] = 127
+    w = np.full((2, K), -128, np.int8)
+    w[1] = 127
+    acc = oracle.int_matmul(a, w, 8)
+    assert acc.tolist() == [[128 * 128 * K, -128 * 127 * K], [-127 * 128 * K, 127 * 127 * K]]
+
+
+def test_requant_worked_examples():
+    scale = None
+    n_vals = 0
+    for line in _golden_lines("requant_worked.txt"):
+        tag = line[0]
+        if tag == "S":
+            head, want = line[1:].split("|")
+            aa, ws, ay = [float(v) for v in head.split()]
+            M0_ref, sh_ref = [int(v) for v in want.split()]
+            M0, sh, _ = oracle.requant_params(aa, ws, ay)
+            assert (M0, sh) == (M0_ref, sh_ref), line
+            scale = (M0, sh)
+        elif tag == "V":
+            for p in line[1:].split():
+                c, r = [int(v) for v in p.split(":")]
+                assert oracle.requant_round(c, *scale) == r, (line, p)
+                n_vals += 1
+        elif tag == "B":
+            head, pairs = line[1:].split("|")
+            aa, ws = [float(v) for v in head.split()]
+            for p in pairs.split():
+                b, bq = p.split(":")
+                assert oracle.requant_params(aa, ws, 1.0, float(b))[2] == int(bq), p
+        elif tag == "L":
+            f = dict(kv.split("=") for kv in line[1:].split())
+            A = np.array([[int(v) for v in r.split(",")] for r in f["A"].split(";")], np.int8)
+            W = np.array([[int(v) for v in r.split(",")] for r in f["W"].split(";")], np.int8)
+            bias = np.array([float(v) for v in f["bias"].split(",")], np.float32)
+            Y = [[int(v) for v in r.split(",")] for r in f["Y"].split(";")]
+            y = oracle.qlinear(A, W, 8, np.full(W.shape[0], 0.25, np.float32), 0.5,
+                               int(f["zp_a"]), 0.125, int(f["zp_y"]), 8, bias=bias)
+            assert y.tolist() == Y
+    assert n_vals >= 20
+
+
+def test_requant_round_matches_exact_rationals():
+    rng = np.random.default_rng(6)
+    for _ in range(20000):
+        c = int(rng.integers(-2 ** 31, 2 ** 31))
+        M0 = int(rng.integers(2 ** 30, 2 ** 31))
+        sh = int(rng.integers(1, 70))
+        assert oracle.requant_round(c, M0, sh) == (bf.requant_exact(c, M0, sh) if sh < 63 else 0)
+    # small |c| near ties, every shift
+    for sh in range(1, 63):
+        for c in range(-9, 10):
+            M0 = 2 ** 30 + 12345
+            assert oracle.requant_round(c, M0, sh) == bf.requant_exact(c, M0, sh)
+
+
+def test_requant_params_represent_the_real_scale():
+    rng = np.random.default_rng(7)
+    for _ in range(5000):
+        aa = float(np.float32(10 ** rng.uniform(-4, 1)))
+        ws = float(np.float32(10 ** rng.uniform(-5, 0)))
+        ay = float(np.float32(10 ** rng.uniform(-6, 0)))
+        M0, sh, _ = oracle.requant_params(aa, ws, ay)
+        assert 2 ** 30 <= M0 < 2 ** 31
+        M_exact = Fraction(aa) * Fraction(ws) / Fraction(ay)
+        M_fixed = Fraction(M0, 2 ** sh) if sh >= 0 else Fraction(M0 * 2 ** (-sh))
+        # one fp64 division then one rounding to 31 bits
+        assert abs(M_fixed - M_exact) <= M_exact * (Fraction(1, 2 ** 31) + Fraction(1, 2 ** 52))
+
+
+def test_requant_close_to_ideal_rounding():
+    # |r - c*M| <= 1/2 + |c| * M * 2^-30: the fixed-point result is the ideal
+    # rounding of the real rescale except within a hair of a tie
+    rng = np.random.default_rng(8)
+    for _ in range(20000):
+        aa = float(np.float32(10 ** rng.uniform(-3, 0)))
+        ws = float(np.float32(10 ** rng.uniform(-4, -1)))
+        ay = float(np.float32(10 ** rng.uniform(-4, 0)))
+        M0, sh, _ = oracle.requant_params(aa, ws, ay)
+        c = int(rng.integers(-2 ** 24, 2 ** 24))
+        r = oracle.requant_round(c, M0, sh)
+        M = Fraction(aa) * Fraction(ws) / Fraction(ay)
+        assert abs(r - c * M) <= Fraction(1, 2) + abs(c) * M * Fraction(1, 2 ** 30)
+
+
+def test_requant_special_scales_reduce_to_integer_ops():
+    # M = 1: r = c (plain integer matmul plus zero-point);
+    # M = 2^-j: r = (c + 2^(j-1)) >> j, i.e. numpy's arithmetic shift
+    cs = np.random.default_rng(9).integers(-2 ** 31, 2 ** 31, 4000)
+    M0, sh, _ = oracle.requant_params(0.5, 0.25, 0.125)
+    assert [oracle.requant_round(int(c), M0, sh) for c in cs[:500]] == cs[:500].tolist()
+    for j in range(1, 30):
+        M0, sh, _ = oracle.requant_params(1.0, 2.0 ** -j, 1.0)
+        want = (cs + (1 << (j - 1))) >> j
+        got = [oracle.requant_round(int(c), M0, sh) for c in cs[:300]]
+        assert got == want[:300].tolist()
+
+
+def test_requant_degenerate_scales():
+    # a zero weight scale gives r = 0; an enormous rescale saturates by sign
+    assert oracle.requant_params(1.0, 0.0, 1.0)[:2] == (0, 31)
+    M0, sh, _ = oracle.requant_params(3e38, 3e38, 1e-45)
+    assert sh <= 0
+    assert oracle.requant_value(5, M0, sh, 3, 8) == 127
+    assert oracle.requant_value(-5, M0, sh, 3, 8) == -128
+    assert oracle.requant_value(0, M0, sh, 3, 8) == 3
+    M0, sh, _ = oracle.requant_params(1e-30, 1e-30, 1.0)
+    assert sh > 62 and oracle.requant_round(2 ** 31 - 1, M0, sh) == 0
+
+
+# ---------------------------------------------------------------------------
+# The whole layer
+# ---------------------------------------------------------------------------
+def _exact_params(alpha_a, w_scale, alpha_y, bias):
+    M0, sh, bq = [], [], []
+    for n in range(len(w_scale)):
+        m0, s, b = oracle.requant_params(alpha_a, float(w_scale[n]), alpha_y,
+                                         None if bias is None else float(bias[n]))
+        M0.append(m0)
+        sh.append(s)
+        bq.append(b)
+    return M0, sh, bq
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("out_bits", [8, 16])
+def test_qlinear_bruteforce_tiny(bits, out_bits):
+    rng = np.random.default_rng(10 + bits + out_bits)
+    sizes = [1, 2, 3, 5, 8]
+    for M in sizes:
+        for N in sizes:
+            for K in sizes:
+                if bits == 4 and K % 2:
+                    continue
+                Q = 127 if bits == 8 else 7
+                a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+                a[0, 0] = -128
+                wv = rng.integers(-Q, Q + 1, (N, K))
+                if bits == 8:
+                    wq = wv.astype(np.int8)
+                else:
+                    wq = ((wv[:, 0::2] & 0xF) | ((wv[:, 1::2] & 0xF) << 4)).astype(np.uint8)
+                w_scale = rng.uniform(1e-3, 3e-2, N).astype(np.float32)
+                bias = rng.normal(0, 0.05, N).astype(np.float32) if N % 2 else None
+                alpha_a = float(np.float32(rng.uniform(0.01, 0.5)))
+                zp_a = int(rng.choice([-128, -3, 0, 40, 127]))
+                alpha_y = float(np.float32(rng.uniform(0.001, 0.2) * (1e-2 if out_bits == 16 else 1)))
+                zp_y = int(rng.integers(-100, 100))
+                y = oracle.qlinear(a, wq, bits, w_scale, alpha_a, zp_a, alpha_y, zp_y, out_bits,
+                                   bias=bias, nthreads=2)
+                M0, sh, bq = _exact_params(alpha_a, w_scale, alpha_y, bias)
+                ref = bf.qlinear_exact(a.astype(int).tolist(), wv.tolist(), zp_a, bq, M0, sh,
+                                       zp_y, out_bits)
+                assert y.astype(int).tolist() == ref, (M, N, K)
+
+
+def test_qlinear_textbook_reduction():
+    # alpha_a * w_scale == alpha_y makes the rescale exactly 1: the layer is
+    # then the integer matmul with zero-point plus the output zero-point,
+    # computed here with numpy's int64 matmul.
+    rng = np.random.default_rng(11)
+    M, K, N = 33, 200, 45
+    a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    w = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    zp_a, zp_y = 17, -9
+    y = oracle.qlinear(a, w, 8, np.full(N, 0.25, np.float32), 0.5, zp_a, 0.125, zp_y, 16)
+    c = (a.astype(np.int64) - zp_a) @ w.astype(np.int64).T
+    ref = np.clip(c + zp_y, -32768, 32767)
+    assert np.array_equal(y.astype(np.int64), ref)
+
+
+def test_qlinear_zero_input_maps_to_zero_point():
+    rng = np.random.default_rng(12)
+    M, K, N = 9, 64, 31
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    for bits in (8, 4):
+        wq, ws, _ = oracle.pack_weights(w, bits)
+        alpha_a, zp_a = oracle.act_params(-3.0, 5.0, 8)
+        a = oracle.quantize_act(np.zeros((M, K), np.float32), alpha_a, zp_a, 8)
+        assert np.all(a == zp_a)
+        for out_bits, zp_y in ((8, -37), (16, 1234)):
+            y = oracle.qlinear(a, wq, bits, ws, alpha_a, zp_a, 0.01, zp_y, out_bits)
+            assert np.all(y == zp_y)
+
+
+def test_qlinear_saturation_bounds():
+    rng = np.random.default_rng(13)
+    M, K, N = 12, 96, 40
+    a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    w = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    ws = rng.uniform(0.001, 0.01, N).astype(np.float32)
+    zp_a = 3
+    c = (a.astype(np.int64) - zp_a) @ w.astype(np.int64).T
+    for out_bits in (8, 16):
+        lo, hi = -(2 ** (out_bits - 1)), 2 ** (out_bits - 1) - 1
+        # a normal scale: every output inside the grid
+        y = oracle.qlinear(a, w, 8, ws, 0.1, zp_a, 0.05, 5, out_bits)
+        assert y.min() >= lo and y.max() <= hi
+        # a vanishing output scale: the sign of c picks the grid end
+        y = oracle.qlinear(a, w, 8, ws, 0.1, zp_a, 1e-30, 5, out_bits).astype(np.int64)
+        assert np.array_equal(y, np.where(c > 0, hi, np.where(c < 0, lo, 5)))
+
+
+def test_qlinear_rows_are_independent_and_int4_equals_int8():
+    rng = np.random.default_rng(14)
+    M, K, N = 20, 64, 24
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    alpha_a, zp_a = oracle.act_params(float(x.min()), float(x.max()), 8)
+    a = oracle.quantize_act(x, alpha_a, zp_a, 8)
+    wq4, ws4, _ = oracle.pack_weights(w, 4)
+    y = oracle.qlinear(a, wq4, 4, ws4, alpha_a, zp_a, 0.003, -4, 16)
+    for m in (0, 7, 19):
+        assert np.array_equal(oracle.qlinear(a[m:m + 1], wq4, 4, ws4, alpha_a, zp_a, 0.003, -4, 16),
+                              y[m:m + 1])
+    w8 = _unpack_nibbles(wq4).astype(np.int8)
+    assert np.array_equal(oracle.qlinear(a, w8, 8, ws4, alpha_a, zp_a, 0.003, -4, 16), y)
+
+
+def test_qlinear_dequantized_output_tracks_the_real_layer():
+    # end to end against fp64 X W^T + b: error within the quantization
+    # steps of the three rounding points (input, weight, output)
+    rng = np.random.default_rng(15)
+    M, K, N = 16, 256, 64
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    b = (rng.standard_normal(N) * 0.01).astype(np.float32)
+    alpha_a, zp_a = oracle.act_params(float(x.min()), float(x.max()), 8)
+    a = oracle.quantize_act(x, alpha_a, zp_a, 8)
+    wq, ws, _ = oracle.pack_weights(w, 8)
+    ideal = x.astype(np.float64) @ w.astype(np.float64).T + b
+    alpha_y, zp_y = oracle.act_params(float(ideal.min()) * 1.1, float(ideal.max()) * 1.1, 16)
+    y = oracle.qlinear(a, wq, 8, ws, alpha_a, zp_a, alpha_y, zp_y, 16, bias=b)
+    deq = oracle.dequant(y, alpha_y, zp_y).astype(np.float64)
+    # the integer pipeline computes dequant(A) dequant(W)^T + b exactly up to
+    # the output rounding
+    a_deq = alpha_a * (a.astype(np.float64) - zp_a)
+    w_deq = ws[:, None].astype(np.float64) * wq.astype(np.float64)
+    pipe = a_deq @ w_deq.T + b
+    assert np.max(np.abs(deq - pipe)) <= alpha_y * 0.5 + alpha_a * ws.max() * 0.5 + 1e-6
+    # and that is within the input/weight quantization error of the real layer
+    bound = (np.abs(x) @ (ws[None, :].repeat(K, 0) * 0.5) + alpha_a * 0.5 * np.abs(w_deq).sum(1)
+             + alpha_y + alpha_a * ws.max())
+    assert np.all(np.abs(deq - ideal) <= bound)
+
+
+# ---------------------------------------------------------------------------
+# Section 3.2, Eq.(1): folding the smoothing vector
+# ---------------------------------------------------------------------------
+def test_fold_invariance():
+    rng = np.random.default_rng(16)
+    M, K, N = 64, 512, 96
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    x[:, rng.choice(K, 4, replace=False)] *= 20
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    s = np.exp(rng.uniform(np.log(0.5), np.log(2.0), K)).astype(np.float32)
+    xh = oracle.fold_acts(x, s)
+    wh = oracle.fold_weights(w, s)
+    assert np.array_equal(wh, w * s[None, :])
+    y = x @ w.T
+    yh = xh @ wh.T
+    rel = np.linalg.norm(y - yh) / np.linalg.norm(y)
+    assert rel <= 1e-3
+    # in fp64 the only difference left is the two fp32 roundings of the fold
+    y64 = x.astype(np.float64) @ w.astype(np.float64).T
+    yh64 = xh.astype(np.float64) @ wh.astype(np.float64).T
+    assert np.linalg.norm(y64 - yh64) / np.linalg.norm(y64) <= 4 * 2.0 ** -24
+    # a wrong fold (S applied on the same side twice) would break invariance
+    bad = xh.astype(np.float64) @ (w / s[None, :]).astype(np.float64).T
+    assert np.linalg.norm(y64 - bad) / np.linalg.norm(y64) > 1e-2
