@@ -1,0 +1,197 @@
+/*
+ * mq.h -- C ABI of the MI355X (gfx950) integer-only quantized linear layer
+ * of MobileQuant (arXiv 2408.13933).
+ *
+ * The layer maps static per-tensor int8 activations and per-output-channel
+ * symmetric int8 (or packed int4) weights to int8/int16 activations of the
+ * next layer with integer arithmetic only: int32 accumulation, zero-point
+ * and bias correction, a fixed-point multiplier and shift, saturation.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Layout: row-major, the reduction (input-channel) dimension K contiguous.
+ *     activations  A_q  int8          [M][K]
+ *     weights      W_q  int8          [N][K]      (w_bits = 8)
+ *                       uint8         [N][K/2]    (w_bits = 4): byte j of a
+ *                       row holds the weight of input channel 2j in its low
+ *                       nibble and of channel 2j+1 in its high nibble, as
+ *                       two's-complement 4-bit integers
+ *     outputs      Y_q  int8 / int16  [M][N]
+ *   The paper writes Y = XW with W of shape [in][out]; here tokens are rows
+ *   and each output channel owns one contiguous weight row.
+ * - Pointers named as device pointers are HIP device memory (or memory the
+ *   device can address) owned by the caller; the library never keeps,
+ *   frees or allocates memory.  A pointer may be NULL only where its
+ *   element count is 0 or where the comment says so.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Device
+ *   work is enqueued on it and the call returns without synchronising;
+ *   errors raised while the kernels run surface at the caller's next
+ *   synchronisation on that stream.
+ * - Arguments are validated on the host before anything is enqueued; an
+ *   invalid call returns MQ_ERR_INVALID_ARG and touches no memory.  A failed
+ *   kernel launch returns MQ_ERR_HIP.  No C++ exception crosses this ABI.
+ * - Activation formats are signed: bits = 8 stores [-128, 127], bits = 16
+ *   stores [-32768, 32767].  The paper's unsigned code X_int in
+ *   [0, 2^bw - 1] (Section 4.2, Eq.(4)) equals the stored value plus
+ *   2^(bw-1); the zero-point carries the same shift.
+ */
+#ifndef MQ_H
+#define MQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MQ_OK = 0,
+    MQ_ERR_INVALID_ARG = 1,
+    MQ_ERR_UNSUPPORTED = 2,
+    MQ_ERR_HIP = 3
+} mq_status;
+
+/* Kernel path selection for mq_qlinear_ex (cross-checks and timing). */
+typedef enum {
+    MQ_PATH_AUTO = 0,     /* M <= 16 -> decode, otherwise prefill          */
+    MQ_PATH_DECODE = 1,   /* wavefront GEMV kernel, any M <= 16            */
+    MQ_PATH_PREFILL = 2,  /* LDS-tiled MFMA GEMM kernel, any M             */
+    MQ_PATH_GENERIC = 3   /* one thread per output, any shape or alignment */
+} mq_path;
+
+/* Largest K accepted: keeps |sum_k A_q W_q| below 2^30 so the int32
+ * accumulator cannot overflow. */
+#define MQ_MAX_K 65536
+
+/* Human-readable name of a status code (static storage). */
+const char* mq_status_string(mq_status status);
+
+/* ABI version; bumped on any incompatible change. */
+int32_t mq_version(void);
+
+/*
+ * mq_act_params -- static per-tensor activation format from a range.
+ * Section 4.2, Eq.(2)-(3): q_max = 2^bw - 1, alpha = (f_max - f_min)/q_max,
+ * beta = f_min/alpha.  The range is first widened to contain 0; alpha is
+ * computed in fp64 and rounded once to fp32; the offset -beta is rounded
+ * half-to-even to an integer and clamped to [0, q_max]; the signed
+ * zero-point returned is round(-beta) - 2^(bw-1).  A zero-width range
+ * gives alpha = 1 and zero-point -2^(bw-1).
+ *   f_min, f_max  finite, f_min <= f_max
+ *   bits          8 or 16
+ *   alpha, zp     host pointers receiving the scale and signed zero-point
+ * Host-only arithmetic; touches no device.
+ */
+mq_status mq_act_params(float f_min, float f_max, int32_t bits,
+                        float* alpha, int32_t* zp);
+
+/*
+ * mq_fold_weights -- equivalent transformation of Section 3.2, Eq.(1):
+ * Y = XW = (X S^-1)(S W).  With S = diag(s) on the input channels,
+ *   w_hat[n][k] = w[n][k] * s[k]      (one fp32 multiply)
+ *   w, w_hat  device fp32 [N][K] (may alias)   s  device fp32 [K]
+ */
+mq_status mq_fold_weights(const float* w, const float* s, int64_t N, int64_t K,
+                          float* w_hat, void* stream);
+
+/*
+ * mq_fold_acts -- the activation side of Eq.(1):
+ *   x_hat[m][k] = x[m][k] / s[k]      (one IEEE fp32 division)
+ *   x, x_hat  device fp32 [M][K] (may alias)   s  device fp32 [K]
+ */
+mq_status mq_fold_acts(const float* x, const float* s, int64_t M, int64_t K,
+                       float* x_hat, void* stream);
+
+/*
+ * mq_quantize_act -- static per-tensor activation quantizer, Section 4.2
+ * Eq.(4) in signed storage:
+ *   q = clamp(rint(x / alpha) + zp, -2^(bits-1), 2^(bits-1) - 1)
+ * x/alpha is one IEEE fp32 division, rint rounds half to even; the
+ * quotient is limited to +-2^20 first (NaN ends at the low end).
+ *   x      device fp32 [numel]
+ *   alpha  finite, > 0        zp  within the signed range of `bits`
+ *   bits   8 (x_q is int8) or 16 (x_q is int16)
+ *   x_q    device [numel]
+ */
+mq_status mq_quantize_act(const float* x, int64_t numel, float alpha, int32_t zp,
+                          int32_t bits, void* x_q, void* stream);
+
+/*
+ * mq_pack_weights -- symmetric per-output-channel weight quantizer and
+ * packer (Section 5.1 W8A8/W4A8 settings; appendix: symmetric per-channel
+ * W4).  For each row n, with Q = 127 (bits 8) or 7 (bits 4):
+ *   w_scale[n] = max_k |w[n][k]| / Q  (fp32; 1 when that is not > 0)
+ *   q[n][k]    = rint(clamp(w[n][k] / w_scale[n], -Q, Q))
+ *   w_colsum[n] = sum_k q[n][k]      (used for the zero-point correction)
+ *   w        device fp32 [N][K], smoothing already folded (mq_fold_weights)
+ *   bits     8 -> w_q int8 [N][K];  4 -> w_q uint8 [N][K/2] (K even)
+ *   w_scale  device fp32 [N]          w_colsum  device int32 [N]
+ *   1 <= K <= MQ_MAX_K.
+ */
+mq_status mq_pack_weights(const float* w, int64_t N, int64_t K, int32_t bits,
+                          void* w_q, float* w_scale, int32_t* w_colsum,
+                          void* stream);
+
+/*
+ * mq_qlinear -- integer-only linear layer (the hot path).  For every
+ * token m and output channel n:
+ *   acc      = sum_k A_q[m][k] * W_q[n][k]                     (int32)
+ *   c        = sat_int32(acc - a_zp * w_colsum[n] + bias_q[n])
+ *   M_n      = (a_scale * w_scale[n]) / out_scale   (fp64)  = M0 * 2^-sh,
+ *              M0 = rint(f * 2^31) in [2^30, 2^31) for M_n = f * 2^e,
+ *              f in [0.5, 1), sh = 31 - e
+ *   r        = floor((c * M0 + 2^(sh-1)) / 2^sh)   (exact; 0 if sh >= 63;
+ *              sh <= 0 saturates every non-zero c)
+ *   Y_q[m][n] = clamp(r + out_zp, -2^(out_bits-1), 2^(out_bits-1) - 1)
+ *   bias_q[n] = rint(clamp(bias[n] / (a_scale * w_scale[n]), -2^30, 2^30))
+ *              in fp64, or 0 when bias is NULL.
+ * The paper fixes integer-only execution with static per-tensor
+ * activations and per-channel weights (Section 3.1, Section 5.1) but not
+ * the rescale; this Q31 single-rounding form is the reading implemented.
+ *   a_q       device int8 [M][K]
+ *   w_q       device, layout of mq_pack_weights for w_bits (8 or 4)
+ *   w_scale   device fp32 [N]     w_colsum  device int32 [N], equal to
+ *             sum_k W_q[n][k] (as written by mq_pack_weights)
+ *   a_scale, out_scale  finite, > 0
+ *   a_zp      in [-128, 127]      out_zp within the range of out_bits
+ *   out_bits  8 (y_q int8) or 16 (y_q int16)
+ *   bias      device fp32 [N], or NULL
+ *   y_q       device [M][N]; must not overlap the inputs
+ *   M >= 0, N >= 0 (0 -> nothing to do), 1 <= K <= MQ_MAX_K, K even for
+ *   w_bits = 4.  Any shape and alignment is accepted; 16-byte-aligned
+ *   buffers with K % 16 == 0 (int8) or K % 32 == 0 (int4) take the tuned
+ *   kernels.
+ */
+mq_status mq_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                     const void* w_q, int32_t w_bits, const float* w_scale,
+                     const int32_t* w_colsum, float a_scale, int32_t a_zp,
+                     float out_scale, int32_t out_zp, int32_t out_bits,
+                     const float* bias, void* y_q, void* stream);
+
+/*
+ * mq_qlinear_ex -- mq_qlinear with an explicit kernel path; every path
+ * computes the same bits.  MQ_PATH_DECODE requires M <= 16; the tuned
+ * paths fall back to MQ_PATH_GENERIC when the shape or alignment rules
+ * above are not met.
+ */
+mq_status mq_qlinear_ex(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                        const void* w_q, int32_t w_bits, const float* w_scale,
+                        const int32_t* w_colsum, float a_scale, int32_t a_zp,
+                        float out_scale, int32_t out_zp, int32_t out_bits,
+                        const float* bias, void* y_q, int32_t path, void* stream);
+
+/*
+ * mq_dequant -- inverse of Eq.(4): y = alpha * (float)(q - zp), one exact
+ * integer subtraction and one fp32 multiply.
+ *   q      device int8 (bits 8) or int16 (bits 16) [numel]
+ *   alpha  finite, > 0     zp  within the signed range of `bits`
+ *   y      device fp32 [numel]
+ */
+mq_status mq_dequant(const void* q, int32_t bits, int64_t numel, float alpha,
+                     int32_t zp, float* y, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MQ_H */

@@ -1,0 +1,230 @@
+"""MI355X (gfx950) integer-only quantized linear layer of MobileQuant
+(arXiv 2408.13933), behind a C ABI (include/mq.h, libmq.so).
+
+This module is the thin Python binding: each ``mq_*`` function has the
+name of the C entry point it calls and only marshals arguments (torch
+device tensors -> pointers, the current HIP stream -> ``void*``).  All
+arithmetic runs in the HIP kernels of libmq.so; there is no fallback.  If
+the library is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "MQError", "lib", "lib_path", "mq_version", "mq_act_params", "mq_fold_weights",
+    "mq_fold_acts", "mq_quantize_act", "mq_pack_weights", "mq_qlinear", "mq_dequant",
+    "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+lib_path = os.path.join(_HERE, "libmq.so")
+
+MQ_OK, MQ_ERR_INVALID_ARG, MQ_ERR_UNSUPPORTED, MQ_ERR_HIP = 0, 1, 2, 3
+PATH_AUTO, PATH_DECODE, PATH_PREFILL, PATH_GENERIC = 0, 1, 2, 3
+MAX_K = 65536
+
+_lib = None
+
+
+class MQError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {_status_string(status)}")
+
+
+def _status_string(status: int) -> str:
+    try:
+        return lib().mq_status_string(status).decode()
+    except Exception:
+        return f"status {status}"
+
+
+def lib():
+    """The loaded libmq.so (ctypes), with argument types declared."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(lib_path):
+        raise ImportError(f"{lib_path} is missing: build it with "
+                          "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(lib_path)
+    c_i64, c_i32, c_f, c_p = ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_void_p
+    L.mq_status_string.argtypes = [ctypes.c_int]
+    L.mq_status_string.restype = ctypes.c_char_p
+    L.mq_version.argtypes = []
+    L.mq_version.restype = c_i32
+    L.mq_act_params.argtypes = [c_f, c_f, c_i32, ctypes.POINTER(c_f), ctypes.POINTER(c_i32)]
+    L.mq_fold_weights.argtypes = [c_p, c_p, c_i64, c_i64, c_p, c_p]
+    L.mq_fold_acts.argtypes = [c_p, c_p, c_i64, c_i64, c_p, c_p]
+    L.mq_quantize_act.argtypes = [c_p, c_i64, c_f, c_i32, c_i32, c_p, c_p]
+    L.mq_pack_weights.argtypes = [c_p, c_i64, c_i64, c_i32, c_p, c_p, c_p, c_p]
+    L.mq_qlinear.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32, c_f,
+                             c_i32, c_i32, c_p, c_p, c_p]
+    L.mq_qlinear_ex.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32,
+                                c_f, c_i32, c_i32, c_p, c_p, c_i32, c_p]
+    L.mq_dequant.argtypes = [c_p, c_i32, c_i64, c_f, c_i32, c_p, c_p]
+    for name in ("mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
+                 "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_dequant"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str):
+    if status != MQ_OK:
+        raise MQError(status, where)
+
+
+# --------------------------------------------------------------------------
+# marshalling helpers (torch is only device memory and streams here)
+def _torch():
+    import torch
+    return torch
+
+
+def _dev_ptr(t, dtype, name, shape=None):
+    torch = _torch()
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_ptr(stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _act_dtype(bits):
+    torch = _torch()
+    if bits == 8:
+        return torch.int8
+    if bits == 16:
+        return torch.int16
+    raise ValueError("activation bits must be 8 or 16")
+
+
+def _bits_of(t):
+    torch = _torch()
+    return {torch.int8: 8, torch.int16: 16}.get(t.dtype)
+
+
+# --------------------------------------------------------------------------
+def mq_version() -> int:
+    return int(lib().mq_version())
+
+
+def mq_act_params(f_min: float, f_max: float, bits: int):
+    """(alpha, zp) of a static per-tensor range (Section 4.2, Eq.(2)-(3))."""
+    a = ctypes.c_float()
+    z = ctypes.c_int32()
+    _check(lib().mq_act_params(float(f_min), float(f_max), int(bits), ctypes.byref(a),
+                               ctypes.byref(z)), "mq_act_params")
+    return float(a.value), int(z.value)
+
+
+def mq_fold_weights(w, s, out=None, stream=None):
+    """S W of Eq.(1): out[n][k] = w[n][k] * s[k] (fp32, on the GPU)."""
+    torch = _torch()
+    N, K = w.shape
+    out = torch.empty_like(w) if out is None else out
+    _check(lib().mq_fold_weights(_dev_ptr(w, torch.float32, "w"),
+                                 _dev_ptr(s, torch.float32, "s", (K,)), N, K,
+                                 _dev_ptr(out, torch.float32, "out", (N, K)),
+                                 _stream_ptr(stream)), "mq_fold_weights")
+    return out
+
+
+def mq_fold_acts(x, s, out=None, stream=None):
+    """X S^-1 of Eq.(1): out[m][k] = x[m][k] / s[k] (fp32, on the GPU)."""
+    torch = _torch()
+    M, K = x.shape
+    out = torch.empty_like(x) if out is None else out
+    _check(lib().mq_fold_acts(_dev_ptr(x, torch.float32, "x"),
+                              _dev_ptr(s, torch.float32, "s", (K,)), M, K,
+                              _dev_ptr(out, torch.float32, "out", (M, K)),
+                              _stream_ptr(stream)), "mq_fold_acts")
+    return out
+
+
+def mq_quantize_act(x, alpha: float, zp: int, bits: int = 8, out=None, stream=None):
+    """Static per-tensor quantizer (Section 4.2, Eq.(4)), signed storage."""
+    torch = _torch()
+    out = torch.empty(x.shape, dtype=_act_dtype(bits), device=x.device) if out is None else out
+    _check(lib().mq_quantize_act(_dev_ptr(x, torch.float32, "x"), x.numel(), float(alpha),
+                                 int(zp), int(bits),
+                                 _dev_ptr(out, _act_dtype(bits), "out", x.shape),
+                                 _stream_ptr(stream)), "mq_quantize_act")
+    return out
+
+
+def mq_pack_weights(w, bits: int = 8, w_q=None, w_scale=None, w_colsum=None, stream=None):
+    """Per-output-channel symmetric weight codes, scales and column sums."""
+    torch = _torch()
+    N, K = w.shape
+    dev = w.device
+    if bits == 8:
+        w_q = torch.empty((N, K), dtype=torch.int8, device=dev) if w_q is None else w_q
+        wq_dtype, wq_shape = torch.int8, (N, K)
+    elif bits == 4:
+        w_q = torch.empty((N, K // 2), dtype=torch.uint8, device=dev) if w_q is None else w_q
+        wq_dtype, wq_shape = torch.uint8, (N, K // 2)
+    else:
+        raise ValueError("bits must be 8 or 4")
+    w_scale = torch.empty(N, dtype=torch.float32, device=dev) if w_scale is None else w_scale
+    w_colsum = torch.empty(N, dtype=torch.int32, device=dev) if w_colsum is None else w_colsum
+    _check(lib().mq_pack_weights(_dev_ptr(w, torch.float32, "w"), N, K, int(bits),
+                                 _dev_ptr(w_q, wq_dtype, "w_q", wq_shape),
+                                 _dev_ptr(w_scale, torch.float32, "w_scale", (N,)),
+                                 _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)),
+                                 _stream_ptr(stream)), "mq_pack_weights")
+    return w_q, w_scale, w_colsum
+
+
+def mq_qlinear(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: int,
+               out_scale: float, out_zp: int, out_bits: int = 8, bias=None, out=None,
+               path: int = PATH_AUTO, stream=None):
+    """Integer-only linear layer: int8 A_q [M][K] x W_q -> Y_q [M][N]."""
+    torch = _torch()
+    M, K = a_q.shape
+    N = w_q.shape[0]
+    wq_dtype, wq_shape = (torch.int8, (N, K)) if w_bits == 8 else (torch.uint8, (N, K // 2))
+    out = (torch.empty((M, N), dtype=_act_dtype(out_bits), device=a_q.device)
+           if out is None else out)
+    bptr = None if bias is None else _dev_ptr(bias, torch.float32, "bias", (N,))
+    args = (_dev_ptr(a_q, torch.int8, "a_q"), M, K, N,
+            _dev_ptr(w_q, wq_dtype, "w_q", wq_shape), int(w_bits),
+            _dev_ptr(w_scale, torch.float32, "w_scale", (N,)),
+            _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)),
+            float(a_scale), int(a_zp), float(out_scale), int(out_zp), int(out_bits), bptr,
+            _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)))
+    if path == PATH_AUTO:
+        st = lib().mq_qlinear(*args, _stream_ptr(stream))
+    else:
+        st = lib().mq_qlinear_ex(*args, int(path), _stream_ptr(stream))
+    _check(st, "mq_qlinear")
+    return out
+
+
+def mq_dequant(q, alpha: float, zp: int, out=None, stream=None):
+    """alpha * (q - zp) in fp32 (inverse of Eq.(4))."""
+    torch = _torch()
+    bits = _bits_of(q)
+    if bits is None:
+        raise ValueError("q must be int8 or int16")
+    out = torch.empty(q.shape, dtype=torch.float32, device=q.device) if out is None else out
+    _check(lib().mq_dequant(_dev_ptr(q, q.dtype, "q"), bits, q.numel(), float(alpha), int(zp),
+                            _dev_ptr(out, torch.float32, "out", q.shape), _stream_ptr(stream)),
+           "mq_dequant")
+    return out

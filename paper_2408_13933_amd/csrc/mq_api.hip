@@ -1,0 +1,178 @@
+// Host side of the C ABI declared in include/mq.h: argument validation,
+// the Eq.(2)-(3) activation-format derivation, kernel-path dispatch and HIP
+// error mapping.  Nothing here allocates or synchronises.
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/mq.h"
+#include "mq_internal.h"
+
+namespace {
+
+constexpr int32_t kAbiVersion = 1;
+
+bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
+
+bool zp_ok(int32_t zp, int32_t bits)
+{
+    const int32_t lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
+    return zp >= lo && zp <= hi;
+}
+
+bool act_bits_ok(int32_t bits) { return bits == 8 || bits == 16; }
+
+mq_status from_hip(hipError_t e) { return e == hipSuccess ? MQ_OK : MQ_ERR_HIP; }
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// largest element count the grid-stride kernels index with int64 safely
+constexpr int64_t kMaxElems = (int64_t)1 << 46;
+
+}  // namespace
+
+extern "C" {
+
+const char* mq_status_string(mq_status status)
+{
+    switch (status) {
+    case MQ_OK: return "MQ_OK";
+    case MQ_ERR_INVALID_ARG: return "MQ_ERR_INVALID_ARG: argument rejected by validation";
+    case MQ_ERR_UNSUPPORTED: return "MQ_ERR_UNSUPPORTED: valid but not supported";
+    case MQ_ERR_HIP: return "MQ_ERR_HIP: a HIP launch failed";
+    }
+    return "unknown mq_status";
+}
+
+int32_t mq_version(void) { return kAbiVersion; }
+
+mq_status mq_act_params(float f_min, float f_max, int32_t bits, float* alpha, int32_t* zp)
+{
+    if (!alpha || !zp || !act_bits_ok(bits)) return MQ_ERR_INVALID_ARG;
+    if (!std::isfinite(f_min) || !std::isfinite(f_max) || f_min > f_max) return MQ_ERR_INVALID_ARG;
+    // widen to contain zero, then Eq.(2) q_max and Eq.(3) alpha, beta
+    const double lo = std::fmin((double)f_min, 0.0);
+    const double hi = std::fmax((double)f_max, 0.0);
+    const double qmax = std::ldexp(1.0, bits) - 1.0;
+    const double width = hi - lo;
+    float a = 1.0f;
+    double beta = 0.0;
+    if (width != 0.0) {
+        a = (float)(width / qmax);
+        if (!(a > 0.0f) || !std::isfinite(a)) return MQ_ERR_INVALID_ARG;
+        beta = lo / (double)a;
+    }
+    double z = std::rint(-beta);
+    z = std::fmin(std::fmax(z, 0.0), qmax);
+    *alpha = a;
+    *zp = (int32_t)z - (1 << (bits - 1));
+    return MQ_OK;
+}
+
+mq_status mq_fold_weights(const float* w, const float* s, int64_t N, int64_t K, float* w_hat,
+                          void* stream)
+{
+    if (N < 0 || K < 0 || N > kMaxElems || K > kMaxElems || (K > 0 && N > kMaxElems / K))
+        return MQ_ERR_INVALID_ARG;
+    if (N == 0 || K == 0) return MQ_OK;
+    if (!w || !s || !w_hat) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_fold_weights(w, s, N, K, w_hat, as_stream(stream)));
+}
+
+mq_status mq_fold_acts(const float* x, const float* s, int64_t M, int64_t K, float* x_hat,
+                       void* stream)
+{
+    if (M < 0 || K < 0 || M > kMaxElems || K > kMaxElems || (K > 0 && M > kMaxElems / K))
+        return MQ_ERR_INVALID_ARG;
+    if (M == 0 || K == 0) return MQ_OK;
+    if (!x || !s || !x_hat) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_fold_acts(x, s, M, K, x_hat, as_stream(stream)));
+}
+
+mq_status mq_quantize_act(const float* x, int64_t numel, float alpha, int32_t zp, int32_t bits,
+                          void* x_q, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || !act_bits_ok(bits) || !finite_pos(alpha) ||
+        !zp_ok(zp, bits))
+        return MQ_ERR_INVALID_ARG;
+    if (numel == 0) return MQ_OK;
+    if (!x || !x_q) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_quantize_act(x, numel, alpha, zp, bits, x_q, as_stream(stream)));
+}
+
+mq_status mq_dequant(const void* q, int32_t bits, int64_t numel, float alpha, int32_t zp,
+                     float* y, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || !act_bits_ok(bits) || !finite_pos(alpha) ||
+        !zp_ok(zp, bits))
+        return MQ_ERR_INVALID_ARG;
+    if (numel == 0) return MQ_OK;
+    if (!q || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_dequant(q, bits, numel, alpha, zp, y, as_stream(stream)));
+}
+
+mq_status mq_pack_weights(const float* w, int64_t N, int64_t K, int32_t bits, void* w_q,
+                          float* w_scale, int32_t* w_colsum, void* stream)
+{
+    if (bits != 8 && bits != 4) return MQ_ERR_INVALID_ARG;
+    if (N < 0 || N > 0x7FFFFFFF || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
+    if (bits == 4 && (K % 2) != 0) return MQ_ERR_INVALID_ARG;
+    if (N == 0) return MQ_OK;
+    if (!w || !w_q || !w_scale || !w_colsum) return MQ_ERR_INVALID_ARG;
+    return from_hip(
+        mq::launch_pack_weights(w, N, K, bits, w_q, w_scale, w_colsum, as_stream(stream)));
+}
+
+mq_status mq_qlinear_ex(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
+                        int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
+                        float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                        int32_t out_bits, const float* bias, void* y_q, int32_t path,
+                        void* stream)
+{
+    if (w_bits != 8 && w_bits != 4) return MQ_ERR_INVALID_ARG;
+    if (!act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (M < 0 || N < 0 || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
+    if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || (M > 0 && N > kMaxElems / M)) return MQ_ERR_INVALID_ARG;
+    if (w_bits == 4 && (K % 2) != 0) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(a_scale) || !finite_pos(out_scale)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(a_zp, 8) || !zp_ok(out_zp, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (path < MQ_PATH_AUTO || path > MQ_PATH_GENERIC) return MQ_ERR_INVALID_ARG;
+    if (path == MQ_PATH_DECODE && M > 16) return MQ_ERR_INVALID_ARG;
+    if (M == 0 || N == 0) return MQ_OK;
+    if (!a_q || !w_q || !w_scale || !w_colsum || !y_q) return MQ_ERR_INVALID_ARG;
+
+    mq::QLinearArgs p;
+    p.a = a_q;
+    p.w = w_q;
+    p.w_scale = w_scale;
+    p.colsum = w_colsum;
+    p.bias = bias;
+    p.y = y_q;
+    p.M = M;
+    p.K = K;
+    p.N = N;
+    p.a_scale = a_scale;
+    p.out_scale = out_scale;
+    p.a_zp = a_zp;
+    p.out_zp = out_zp;
+    p.w_bits = w_bits;
+    p.out_bits = out_bits;
+
+    hipStream_t s = as_stream(stream);
+    if (path == MQ_PATH_AUTO) path = M <= 16 ? MQ_PATH_DECODE : MQ_PATH_PREFILL;
+    if (path == MQ_PATH_DECODE && mq::decode_supported(p))
+        return from_hip(mq::launch_qlinear_decode(p, s));
+    if (path == MQ_PATH_PREFILL && mq::prefill_supported(p))
+        return from_hip(mq::launch_qlinear_prefill(p, s));
+    return from_hip(mq::launch_qlinear_generic(p, s));
+}
+
+mq_status mq_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
+                     int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
+                     float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                     int32_t out_bits, const float* bias, void* y_q, void* stream)
+{
+    return mq_qlinear_ex(a_q, M, K, N, w_q, w_bits, w_scale, w_colsum, a_scale, a_zp, out_scale,
+                         out_zp, out_bits, bias, y_q, MQ_PATH_AUTO, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,46 @@
+// Internal declarations shared by the host entry points and the kernel
+// translation units of libmq.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mq {
+
+// Scalars every qlinear kernel needs besides its buffers.
+struct QLinearArgs {
+    const int8_t* a;        // [M][K]
+    const void* w;          // [N][K] int8 or [N][K/2] packed int4
+    const float* w_scale;   // [N]
+    const int32_t* colsum;  // [N]
+    const float* bias;      // [N] or nullptr
+    void* y;                // [M][N] int8 or int16
+    int64_t M, K, N;
+    float a_scale;
+    float out_scale;
+    int32_t a_zp;
+    int32_t out_zp;
+    int32_t w_bits;         // 8 or 4
+    int32_t out_bits;       // 8 or 16
+};
+
+hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t zp,
+                               int32_t bits, void* q, hipStream_t s);
+hipError_t launch_dequant(const void* q, int32_t bits, int64_t n, float alpha,
+                          int32_t zp, float* y, hipStream_t s);
+hipError_t launch_fold_weights(const float* w, const float* sv, int64_t N, int64_t K,
+                               float* out, hipStream_t s);
+hipError_t launch_fold_acts(const float* x, const float* sv, int64_t M, int64_t K,
+                            float* out, hipStream_t s);
+hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int32_t bits,
+                               void* wq, float* scale, int32_t* colsum, hipStream_t s);
+
+hipError_t launch_qlinear_generic(const QLinearArgs& p, hipStream_t s);
+hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);
+hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s);
+
+// Shape/alignment rules of the tuned kernels.
+bool decode_supported(const QLinearArgs& p);
+bool prefill_supported(const QLinearArgs& p);
+
+}  // namespace mq

@@ -1,0 +1,85 @@
+// Device-side requantization shared by every qlinear kernel: the per-column
+// fixed-point parameters and the per-element epilogue
+//   c = sat_int32(acc + off[n]),  off[n] = bias_q[n] - a_zp * colsum[n]
+//   r = floor((c * M0[n] + 2^(sh[n]-1)) / 2^sh[n])
+//   y = clamp(r + out_zp, qmin, qmax)
+// (the integer-only rescale between layers; the paper requires fixed-point
+// integer arithmetic throughout, Section 1 and Section 3.1).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mq {
+
+struct ColParams {
+    int32_t off;  // bias_q - a_zp * colsum, saturated to int32
+    int32_t m0;   // Q31 multiplier in [2^30, 2^31), or 0
+    int32_t sh;   // right shift; >= 63 means r = 0, <= 0 means saturate
+};
+
+// Fixed-point form of M = (a_scale * w_scale) / out_scale and the bias in
+// accumulator units.  fp64 throughout: the product of two fp32 values is
+// exact in fp64, the division is one correctly rounded operation, and
+// frexp/ldexp/rint are exact, so the integers do not depend on the device.
+__device__ inline ColParams derive_col_params(float a_scale, float w_scale, float out_scale,
+                                              const float* bias_n, int32_t colsum,
+                                              int32_t a_zp)
+{
+#pragma clang fp contract(off)
+    ColParams p;
+    const double prod = (double)a_scale * (double)w_scale;
+    const double M = prod / (double)out_scale;
+    if (!(M > 0.0)) {
+        p.m0 = 0;
+        p.sh = 31;
+    } else if (__builtin_isinf(M)) {
+        p.m0 = 1 << 30;
+        p.sh = 0;
+    } else {
+        int e = 0;
+        const double f = frexp(M, &e);
+        long long m0 = (long long)rint(ldexp(f, 31));
+        if (m0 == (1LL << 31)) {
+            m0 = 1LL << 30;
+            e += 1;
+        }
+        p.m0 = (int32_t)m0;
+        p.sh = 31 - e;
+    }
+    long long bq = 0;
+    if (bias_n != nullptr) {
+        double t = (double)(*bias_n) / prod;
+        t = fmin(fmax(t, -1073741824.0), 1073741824.0);
+        bq = (long long)rint(t);
+    }
+    long long off = bq - (long long)a_zp * (long long)colsum;
+    off = off < INT32_MIN ? INT32_MIN : (off > INT32_MAX ? INT32_MAX : off);
+    p.off = (int32_t)off;
+    return p;
+}
+
+// r for one corrected accumulator c (int32).
+__device__ inline int32_t requant_round(int32_t c, int32_t m0, int32_t sh)
+{
+    if (sh >= 63) return 0;
+    if (sh >= 1) {
+        const long long prod = (long long)c * (long long)m0 + (1LL << (sh - 1));
+        const long long r = prod >> sh;  // arithmetic shift = floor division
+        // |r| <= 2^31 here; anything beyond int16 saturates later anyway
+        return (int32_t)(r < -(1LL << 30) ? -(1LL << 30) : (r > (1LL << 30) ? (1LL << 30) : r));
+    }
+    return c > 0 ? (1 << 30) : (c < 0 ? -(1 << 30) : 0);
+}
+
+__device__ inline int32_t requant_out(int32_t acc, const ColParams& p, int32_t out_zp,
+                                      int32_t qmin, int32_t qmax)
+{
+    const int32_t c = __builtin_elementwise_add_sat(acc, p.off);
+    const int32_t r = requant_round(c, p.m0, p.sh);
+    int32_t y = r + out_zp;  // |r| <= 2^30, |out_zp| <= 2^15: no overflow
+    y = y < qmin ? qmin : (y > qmax ? qmax : y);
+    return y;
+}
+
+}  // namespace mq

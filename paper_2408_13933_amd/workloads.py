@@ -131,10 +131,10 @@ def gen_activations(M: int, K: int, act: str, seed_key) -> np.ndarray:
     rng = _rng("act", *seed_key)
     x = rng.standard_normal((M, K), dtype=np.float32)
     if act == "outlier":
-        ch = rng.choice(K, 4, replace=False)
+        ch = rng.choice(K, min(4, K), replace=False)
         x[:, ch] *= np.float32(20.0)
     elif act == "student_t":
-        n_ch = max(4, int(round(0.01 * K)))
+        n_ch = min(K, max(4, int(round(0.01 * K))))
         ch = rng.choice(K, n_ch, replace=False)
         x[:, ch] = rng.standard_t(3.0, size=(M, n_ch)).astype(np.float32)
     else:

@@ -1,0 +1,99 @@
+"""The two pipelines the parity tests compare, step for step.
+
+``gpu_layer`` drives libmq.so through its Python binding (every step a HIP
+kernel); ``oracle_layer`` drives the CPU oracle.  Both start from the same
+seeded fp32 tensors and static float ranges (paper_2408_13933_amd.workloads)
+and derive every scale, zero-point and integer on their own side.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+import oracle
+from paper_2408_13933_amd.workloads import LayerData
+
+
+@dataclasses.dataclass
+class LayerResult:
+    a_scale: float
+    a_zp: int
+    out_scale: float
+    out_zp: int
+    a_q: np.ndarray
+    w_q: np.ndarray
+    w_scale: np.ndarray
+    w_colsum: np.ndarray
+    w_hat: Optional[np.ndarray]
+    y_q: np.ndarray
+    y: np.ndarray
+
+
+def oracle_layer(ld: LayerData, rows=None, nthreads=None) -> LayerResult:
+    L = ld.layer
+    w_hat = oracle.fold_weights(ld.w, ld.s) if ld.s is not None else None
+    wq, ws, cs = oracle.pack_weights(w_hat if w_hat is not None else ld.w, L.w_bits)
+    a_scale, a_zp = oracle.act_params(*ld.act_range, 8)
+    out_scale, out_zp = oracle.act_params(*ld.out_range, L.out_bits)
+    x = ld.x if rows is None else ld.x[rows]
+    a_q = oracle.quantize_act(x, a_scale, a_zp, 8)
+    y_q = oracle.qlinear(a_q, wq, L.w_bits, ws, a_scale, a_zp, out_scale, out_zp, L.out_bits,
+                         bias=ld.bias, nthreads=nthreads)
+    y = oracle.dequant(y_q, out_scale, out_zp)
+    return LayerResult(a_scale, a_zp, out_scale, out_zp, a_q, wq, ws, cs, w_hat, y_q, y)
+
+
+def gpu_layer(ld: LayerData, path: int = 0, keep_device=False):
+    import torch
+    import paper_2408_13933_amd as mq
+
+    L = ld.layer
+    dev = torch.device("cuda", 0)
+    x = torch.from_numpy(ld.x).to(dev)
+    w = torch.from_numpy(ld.w).to(dev)
+    w_hat = None
+    if ld.s is not None:
+        s = torch.from_numpy(ld.s).to(dev)
+        w_hat = mq.mq_fold_weights(w, s)
+    bias = torch.from_numpy(ld.bias).to(dev) if ld.bias is not None else None
+    a_scale, a_zp = mq.mq_act_params(*ld.act_range, 8)
+    out_scale, out_zp = mq.mq_act_params(*ld.out_range, L.out_bits)
+    a_q = mq.mq_quantize_act(x, a_scale, a_zp, 8)
+    wq, ws, cs = mq.mq_pack_weights(w_hat if w_hat is not None else w, L.w_bits)
+    y_q = mq.mq_qlinear(a_q, wq, L.w_bits, ws, cs, a_scale, a_zp, out_scale, out_zp,
+                        L.out_bits, bias=bias, path=path)
+    y = mq.mq_dequant(y_q, out_scale, out_zp)
+    torch.cuda.synchronize()
+    res = LayerResult(a_scale, a_zp, out_scale, out_zp, a_q.cpu().numpy(), wq.cpu().numpy(),
+                      ws.cpu().numpy(), cs.cpu().numpy(),
+                      None if w_hat is None else w_hat.cpu().numpy(), y_q.cpu().numpy(),
+                      y.cpu().numpy())
+    if keep_device:
+        return res, dict(a_q=a_q, w_q=wq, w_scale=ws, w_colsum=cs, bias=bias, a_scale=a_scale,
+                         a_zp=a_zp, out_scale=out_scale, out_zp=out_zp)
+    return res
+
+
+def assert_same(g: LayerResult, o: LayerResult, rows=None, check_weights=True):
+    """Bit-exact integer parity, exact scales; dequant within 1e-6 relative."""
+    assert (g.a_scale, g.a_zp) == (o.a_scale, o.a_zp), "activation format differs"
+    assert (g.out_scale, g.out_zp) == (o.out_scale, o.out_zp), "output format differs"
+    if check_weights:
+        if o.w_hat is not None:
+            assert np.array_equal(g.w_hat.view(np.uint32), o.w_hat.view(np.uint32)), "fold differs"
+        assert np.array_equal(g.w_scale.view(np.uint32), o.w_scale.view(np.uint32)), "w_scale"
+        assert np.array_equal(g.w_q, o.w_q), "packed weights differ"
+        assert np.array_equal(g.w_colsum, o.w_colsum), "column sums differ"
+    ga = g.a_q if rows is None else g.a_q[rows]
+    assert np.array_equal(ga, o.a_q), "quantized activations differ"
+    gy = g.y_q if rows is None else g.y_q[rows]
+    if not np.array_equal(gy, o.y_q):
+        bad = np.argwhere(gy != o.y_q)
+        m, n = bad[0]
+        raise AssertionError(f"{len(bad)} outputs differ; first at ({m},{n}): "
+                             f"gpu {gy[m, n]} oracle {o.y_q[m, n]}")
+    gf = g.y if rows is None else g.y[rows]
+    denom = np.maximum(np.abs(o.y), np.float32(1e-30))
+    assert np.all(np.abs(gf - o.y) <= 1e-6 * denom), "dequantized outputs differ"

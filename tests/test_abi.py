@@ -1,0 +1,127 @@
+"""CPU-side checks of the C ABI: the library loads, exports every entry point
+declared in include/mq.h, and rejects invalid arguments before touching a
+device.  The Eq.(2)-(3) host arithmetic is compared with the oracle here too.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2408_13933_amd as mq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mq.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mq_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("mq_quantize_act", "mq_pack_weights", "mq_qlinear", "mq_dequant",
+                     "mq_act_params", "mq_fold_weights", "mq_fold_acts"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = mq.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), f"{name} declared in mq.h but not exported"
+
+
+def test_status_strings_and_version():
+    L = mq.lib()
+    assert L.mq_status_string(0) == b"MQ_OK"
+    for s in (1, 2, 3):
+        assert L.mq_status_string(s).startswith(b"MQ_ERR_")
+    assert mq.mq_version() == 1
+
+
+P = ctypes.c_void_p
+NZ = P(16)  # never dereferenced: every call below fails validation first
+
+
+def qlin(**kw):
+    a = dict(a_q=NZ, M=4, K=64, N=8, w_q=NZ, w_bits=8, w_scale=NZ, w_colsum=NZ, a_scale=0.1,
+             a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None, y_q=NZ, path=0,
+             stream=None)
+    a.update(kw)
+    return mq.lib().mq_qlinear_ex(a["a_q"], a["M"], a["K"], a["N"], a["w_q"], a["w_bits"],
+                                  a["w_scale"], a["w_colsum"], a["a_scale"], a["a_zp"],
+                                  a["out_scale"], a["out_zp"], a["out_bits"], a["bias"],
+                                  a["y_q"], a["path"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(a_q=None), dict(w_q=None), dict(w_scale=None), dict(w_colsum=None), dict(y_q=None),
+    dict(M=-1), dict(N=-1), dict(K=0), dict(K=-5), dict(K=65537),
+    dict(w_bits=2), dict(w_bits=16), dict(w_bits=4, K=63), dict(out_bits=4), dict(out_bits=32),
+    dict(a_scale=0.0), dict(a_scale=-1.0), dict(a_scale=float("nan")), dict(a_scale=float("inf")),
+    dict(out_scale=0.0), dict(out_scale=float("nan")),
+    dict(a_zp=128), dict(a_zp=-129), dict(out_zp=128), dict(out_bits=16, out_zp=40000),
+    dict(path=7), dict(path=-1), dict(path=1, M=17),
+])
+def test_qlinear_rejects_invalid_arguments(kw):
+    assert qlin(**kw) == 1
+
+
+def test_qlinear_empty_shapes_are_noops():
+    # M = 0 or N = 0: nothing to compute, no device touched
+    assert qlin(M=0) == 0
+    assert qlin(N=0) == 0
+    assert qlin(M=0, a_q=None, y_q=None) == 0
+
+
+@pytest.mark.parametrize("call", [
+    lambda L: L.mq_quantize_act(NZ, 10, 0.0, 0, 8, NZ, None),
+    lambda L: L.mq_quantize_act(NZ, 10, 0.1, 200, 8, NZ, None),
+    lambda L: L.mq_quantize_act(NZ, 10, 0.1, 0, 12, NZ, None),
+    lambda L: L.mq_quantize_act(None, 10, 0.1, 0, 8, NZ, None),
+    lambda L: L.mq_quantize_act(NZ, -1, 0.1, 0, 8, NZ, None),
+    lambda L: L.mq_dequant(NZ, 8, 10, float("inf"), 0, NZ, None),
+    lambda L: L.mq_dequant(NZ, 16, 10, 1.0, 40000, NZ, None),
+    lambda L: L.mq_dequant(None, 8, 10, 1.0, 0, NZ, None),
+    lambda L: L.mq_pack_weights(NZ, 4, 63, 4, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights(NZ, 4, 0, 8, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights(NZ, 4, 65537, 8, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights(NZ, 4, 64, 3, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights(NZ, 4, 64, 8, NZ, None, NZ, None),
+    lambda L: L.mq_fold_weights(NZ, None, 4, 4, NZ, None),
+    lambda L: L.mq_fold_acts(NZ, NZ, -1, 4, NZ, None),
+])
+def test_other_entry_points_reject_invalid_arguments(call):
+    assert call(mq.lib()) == 1
+
+
+def test_zero_sized_elementwise_calls_are_noops():
+    L = mq.lib()
+    assert L.mq_quantize_act(None, 0, 0.1, 0, 8, None, None) == 0
+    assert L.mq_dequant(None, 16, 0, 0.1, 0, None, None) == 0
+    assert L.mq_pack_weights(None, 0, 64, 8, None, None, None, None) == 0
+    assert L.mq_fold_weights(None, None, 0, 7, None, None) == 0
+
+
+def test_act_params_matches_oracle():
+    rng = np.random.default_rng(21)
+    cases = [(-64.0, 191.0), (-10.0, 117.5), (5.0, 255.0), (-7.0, -1.0), (0.0, 0.0),
+             (-1e-30, 1e-30), (-3e38, 3e38), (-1.0, 0.0)]
+    for _ in range(2000):
+        lo, hi = sorted(rng.standard_normal(2) * 10 ** rng.uniform(-6, 6, 2))
+        cases.append((float(np.float32(lo)), float(np.float32(hi))))
+    for lo, hi in cases:
+        for bits in (8, 16):
+            assert mq.mq_act_params(lo, hi, bits) == oracle.act_params(lo, hi, bits), (lo, hi)
+
+
+@pytest.mark.parametrize("lo,hi,bits", [(1.0, 0.0, 8), (float("nan"), 1.0, 8),
+                                        (0.0, float("inf"), 8), (0.0, 1.0, 4)])
+def test_act_params_rejects(lo, hi, bits):
+    with pytest.raises(mq.MQError):
+        mq.mq_act_params(lo, hi, bits)
