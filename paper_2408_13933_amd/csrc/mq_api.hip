@@ -4,7 +4,7 @@
 #include <cmath>
 #include <cstdint>
 
-#include "../../include/mq.h"
+#include "mq.h"
 #include "mq_internal.h"
 
 namespace {

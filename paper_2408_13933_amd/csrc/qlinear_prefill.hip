@@ -3,31 +3,51 @@
 //
 // Prompt encoding is compute-bound (Section 5.6) and int8 x int8 is the
 // fastest integer product (Section 3.1), so the inner loop is
-// v_mfma_i32_16x16x64_i8.  The weight matrix is the MFMA "A" operand (rows =
-// output channels) and the activations the "B" operand (columns = tokens):
-// every lane then ends with four consecutive output channels of one token,
-// which become one 4-byte (int8) or 8-byte (int16) store.
+// v_mfma_i32_32x32x32_i8 (measured on MI355X: one wave per SIMD issuing it
+// back to back reaches ~92% of the int8 peak, the 16x16x64 form ~52%).  The
+// weight matrix is the MFMA "A" operand (rows = output channels) and the
+// activations the "B" operand (columns = tokens): every lane then ends with
+// runs of four consecutive output channels of one token, which become one
+// 4-byte (int8) or 8-byte (int16) store.
 //
-// Tiles of both operands are staged through LDS (double buffered, one
-// barrier per K tile); rows are padded so the 16-row operand reads hit
-// distinct banks.  int4 weights stay packed in LDS (half the bytes) and
-// are unpacked into registers right before the MFMA as 16*w, which the
-// epilogue removes with an exact shift.  Block ids are remapped so the
-// blocks that share weight tiles run on the same XCD (each XCD has its
-// own L2).
+// Data movement (gfx950):
+// - Operand tiles go HBM/L2 -> LDS with buffer_load_dwordx4 ... lds (LDS DMA:
+//   no VGPR staging, no ds_write).  A wave's load fills 1 KiB of LDS; which
+//   16-byte chunk each lane fetches decides the LDS layout, so 16-byte chunks
+//   are XOR-swizzled per row to keep the 16-row MFMA operand reads on
+//   distinct banks.
+// - The buffer descriptor of each tile covers only its valid rows, and a
+//   K-tail chunk gets an out-of-range offset: the hardware returns zeros, so
+//   ragged M, N and K need no branches in the inner loop.
+// - STAGES-deep ring of LDS buffers, one barrier per K step, waits on the
+//   vector-memory counter so STAGES-1 tiles stay in flight.
+// - int4 weights stay packed in LDS (half the bytes) and are unpacked into
+//   registers right before the MFMA as 16*w; the epilogue removes the 16 with
+//   an exact shift.
+// - Block ids are remapped so blocks that share weight tiles run on the same
+//   XCD (each XCD has its own L2).
+#include <cstdlib>
+#include <type_traits>
+
 #include "mq_internal.h"
 #include "requant.h"
+
+#define MQ_LDS __attribute__((address_space(3)))
 
 namespace mq {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr uint32_t kOOB = 0x80000000u;  // any offset past num_records reads zero
 
 __device__ inline v4i unpack_int4_x16(uint32_t x0, uint32_t x1)
 {
     const uint32_t l0 = (x0 << 4) & 0xF0F0F0F0u, h0 = x0 & 0xF0F0F0F0u;
     const uint32_t l1 = (x1 << 4) & 0xF0F0F0F0u, h1 = x1 & 0xF0F0F0F0u;
     v4i r;
+    // v_perm_b32: selector bytes 0-3 pick from the second source, 4-7 from the first
     r[0] = (int)__builtin_amdgcn_perm(h0, l0, 0x05010400u);
     r[1] = (int)__builtin_amdgcn_perm(h0, l0, 0x07030602u);
     r[2] = (int)__builtin_amdgcn_perm(h1, l1, 0x05010400u);
@@ -35,48 +55,76 @@ __device__ inline v4i unpack_int4_x16(uint32_t x0, uint32_t x1)
     return r;
 }
 
-template <int WBITS_, int OBITS_, int TN_, int TM_, int WN_, int WM_, int BK_>
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ inline void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int WBITS_, int OBITS_, int TM_, int TN_, int WM_, int WN_, int BK_, int STAGES_,
+          int SWZ_>
 struct Cfg {
     static constexpr int WBITS = WBITS_, OBITS = OBITS_;
-    static constexpr int TN = TN_, TM = TM_, WN = WN_, WM = WM_, BK = BK_;
-    static constexpr int THREADS = 64 * WN * WM;
-    static constexpr int FN = TN / (WN * 16);        // 16-row fragments per wave (channels)
-    static constexpr int FM = TM / (WM * 16);        // 16-col fragments per wave (tokens)
+    static constexpr int TM = TM_, TN = TN_, WM = WM_, WN = WN_, BK = BK_;
+    static constexpr int STAGES = STAGES_, SWZ = SWZ_;
+    static constexpr int NWAVES = WM * WN;
+    static constexpr int THREADS = 64 * NWAVES;
+    static constexpr int FM = TM / (WM * 32);   // 32-token fragments per wave
+    static constexpr int FN = TN / (WN * 32);   // 32-channel fragments per wave
     static constexpr int BKW = WBITS == 8 ? BK : BK / 2;  // weight bytes per row per stage
-    static constexpr int PADW = WBITS == 8 ? 16 : 8;
-    static constexpr int LDW = BKW + PADW;           // LDS row stride, weights
-    static constexpr int LDA = BK + 16;              // LDS row stride, activations
-    static constexpr int W_STAGE = TN * LDW;
-    static constexpr int A_STAGE = TM * LDA;
-    static constexpr int STAGE = W_STAGE + A_STAGE;
-    static constexpr int W_CHUNKS = TN * BKW / 16;   // 16-byte global chunks per stage
-    static constexpr int A_CHUNKS = TM * BK / 16;
-    static constexpr int W_PER_T = W_CHUNKS / THREADS;
-    static constexpr int A_PER_T = A_CHUNKS / THREADS;
-    static_assert(W_CHUNKS % THREADS == 0 && A_CHUNKS % THREADS == 0, "staging split");
+    static constexpr int CA = BK / 16;          // 16-byte chunks per activation row
+    static constexpr int CW = BKW / 16;         // 16-byte chunks per weight row
+    static constexpr int A_WLOADS = TM * CA / 64;  // 1 KiB wave loads per stage
+    static constexpr int W_WLOADS = TN * CW / 64;
+    static constexpr int A_PER_WAVE = (A_WLOADS + NWAVES - 1) / NWAVES;
+    static constexpr int W_PER_WAVE = (W_WLOADS + NWAVES - 1) / NWAVES;
+    static constexpr int LOADS = A_PER_WAVE + W_PER_WAVE;  // per thread per stage
+    static constexpr int A_BYTES = A_PER_WAVE * NWAVES * 1024;
+    static constexpr int W_BYTES = W_PER_WAVE * NWAVES * 1024;
+    static constexpr int STAGE = A_BYTES + W_BYTES;
+    static constexpr int LDS = STAGES * STAGE + TN * 16;  // + per-column epilogue constants
+    static_assert(TM % (WM * 32) == 0 && TN % (WN * 32) == 0, "wave grid");
+    static_assert((TM * CA) % 64 == 0 && (TN * CW) % 64 == 0, "whole wave loads");
     static_assert(BK % 64 == 0, "BK is a multiple of the MFMA depth");
-    static_assert(FN >= 1 && FM >= 1, "tile too small for the wave grid");
+    static_assert(STAGES >= 2 && STAGES <= 4, "pipeline depth");
+    static_assert((BK / 32) % 2 == 0, "even number of 32-deep steps per stage");
+    static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
+    static_assert(LDS <= 160 * 1024, "LDS per CU");
 };
 
+template <int SWZ>
+__device__ inline int swz(int row, int nchunks)
+{
+    if constexpr (SWZ == 0) return row & (nchunks - 1);
+    else if constexpr (SWZ == 1) return (row >> 1) & (nchunks - 1);
+    else return 0;
+}
+
 template <class C>
-__global__ __launch_bounds__(C::THREADS) void qlinear_prefill_kernel(QLinearArgs p, int tiles_n,
-                                                                    int tiles_m)
+__global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearArgs p,
+                                                                       int tiles_n, int tiles_m)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
     constexpr int32_t qmax = (1 << (C::OBITS - 1)) - 1;
-    extern __shared__ __align__(16) int8_t smem[];
-    ColParams* params = reinterpret_cast<ColParams*>(smem + 2 * C::STAGE);
+    constexpr int KS = C::BK / 32;  // 32-deep MFMA steps per stage
+    extern __shared__ __align__(1024) int8_t smem[];
+    // per-column epilogue constants, structure of arrays after the stages
+    int32_t* e_off = reinterpret_cast<int32_t*>(smem + C::STAGES * C::STAGE);
+    int32_t* e_m0 = e_off + C::TN;
+    int32_t* e_rnd = e_m0 + C::TN;
+    int32_t* e_sp = e_rnd + C::TN;  // shr | pre << 8
 
-    // ---- tile id: blocks that land on one XCD (block id mod 8) get a
-    // contiguous run of tiles, so they share weight tiles in that XCD's L2
+    // ---- tile id: the blocks of one XCD (block id mod 8) take a contiguous
+    // run of tiles, so they share weight tiles in that XCD's L2
     const int total = tiles_n * tiles_m;
     int b = blockIdx.x;
     {
         const int per = total / 8, rem = total % 8;
         const int xcd = b % 8, idx = b / 8;
-        // xcd x owns tiles [start(x), start(x) + per + (x < rem))
-        const int start = xcd * per + (xcd < rem ? xcd : rem);
-        b = start + idx;
+        b = xcd * per + (xcd < rem ? xcd : rem) + idx;
     }
     const int tn = b / tiles_m;
     const int tm = b % tiles_m;
@@ -85,163 +133,307 @@ __global__ __launch_bounds__(C::THREADS) void qlinear_prefill_kernel(QLinearArgs
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep it scalar
     const int wn = wave / C::WM;
     const int wm = wave % C::WM;
-    const int r16 = lane & 15;
-    const int kg = lane >> 4;
+    const int r32 = lane & 31;  // operand row / output token within a fragment
+    const int hk = lane >> 5;   // which 16-byte half of a 32-byte k step
 
-    // ---- per-column requant parameters of this tile
+    // ---- buffer descriptors covering only this tile's valid rows
+    const int64_t K = p.K;
+    const int64_t wrow = C::WBITS == 8 ? K : K / 2;
+    const int rows_a = (int)((p.M - m_tile) < C::TM ? (p.M - m_tile) : C::TM);
+    const int rows_w = (int)((p.N - n_tile) < C::TN ? (p.N - n_tile) : C::TN);
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.a + m_tile * K), (short)0, (int)(rows_a * K), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(static_cast<const int8_t*>(p.w) + n_tile * wrow), (short)0, (int)(rows_w * wrow),
+        0x00020000);
+
+    // Source offsets of this lane's chunks at k = 0; a stage adds kt*BK.  A
+    // chunk past the end of its row (K tail) is pushed out of range.
+    // Source offset of each of this lane's chunks at k = 0 (a stage adds
+    // kt*BK).  Chunks of padding wave loads get an out-of-range offset.
+    uint32_t a_off[C::A_PER_WAVE], w_off[C::W_PER_WAVE];
+    auto a_kb = [&](int i) {  // k byte of the chunk within a stage
+        const int q = (wave + i * C::NWAVES) * 64 + lane;
+        return ((q % C::CA) ^ swz<C::SWZ>(q / C::CA, C::CA)) * 16;
+    };
+    auto w_kb = [&](int i) {
+        const int q = (wave + i * C::NWAVES) * 64 + lane;
+        return ((q % C::CW) ^ swz<C::SWZ>(q / C::CW, C::CW)) * 16;
+    };
+#pragma unroll
+    for (int i = 0; i < C::A_PER_WAVE; ++i) {
+        const int row = ((wave + i * C::NWAVES) * 64 + lane) / C::CA;
+        a_off[i] = wave + i * C::NWAVES < C::A_WLOADS ? (uint32_t)(row * (int)K + a_kb(i)) : kOOB;
+    }
+#pragma unroll
+    for (int i = 0; i < C::W_PER_WAVE; ++i) {
+        const int row = ((wave + i * C::NWAVES) * 64 + lane) / C::CW;
+        w_off[i] = wave + i * C::NWAVES < C::W_WLOADS ? (uint32_t)(row * (int)wrow + w_kb(i))
+                                                      : kOOB;
+    }
+    const int KT = (int)((K + C::BK - 1) / C::BK);
+    // DMA of stage kt into LDS buffer buf.  Every call issues the same number
+    // of loads; a stage past the end (or a chunk past K) reads out of range,
+    // which writes zeros and touches no memory, so the vector-memory counter
+    // advances identically every step.
+    auto issue = [&](int kt, int buf) {
+        MQ_LDS int8_t* base = (MQ_LDS int8_t*)smem + buf * C::STAGE;
+        const int k0 = kt * C::BK, k0w = kt * C::BKW;
+#pragma unroll
+        for (int i = 0; i < C::A_PER_WAVE; ++i) {
+            const int wl = wave + i * C::NWAVES;
+            const uint32_t voff = (k0 + a_kb(i) < (int)K) ? a_off[i] + (uint32_t)k0 : kOOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (MQ_LDS void*)(base + wl * 1024), 16,
+                                                     voff, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < C::W_PER_WAVE; ++i) {
+            const int wl = wave + i * C::NWAVES;
+            const uint32_t voff = (k0w + w_kb(i) < (int)wrow) ? w_off[i] + (uint32_t)k0w : kOOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rw, (MQ_LDS void*)(base + C::A_BYTES + wl * 1024), 16, voff, 0, 0, 0);
+        }
+    };
+
+    // ---- start the pipeline, then derive the per-column constants while
+    // the first tiles are in flight
+#pragma unroll
+    for (int s = 0; s < C::STAGES - 1; ++s) issue(s, s);
+
+    int col_pre0 = 1, col_fold = 1;
     if (tid < C::TN) {
         int64_t n = n_tile + tid;
         if (n >= p.N) n = p.N - 1;
-        params[tid] = derive_col_params(p.a_scale, p.w_scale[n], p.out_scale,
-                                        p.bias ? p.bias + n : nullptr, p.colsum[n], p.a_zp);
+        const ColParams cp = derive_col_params(p.a_scale, p.w_scale[n], p.out_scale,
+                                               p.bias ? p.bias + n : nullptr, p.colsum[n], p.a_zp);
+        const EpiInt ei = epi_int_params(cp);
+        e_off[tid] = cp.off;
+        e_m0[tid] = ei.m0;
+        e_rnd[tid] = ei.rnd;
+        e_sp[tid] = ei.shr | (ei.pre << 8);
+        col_pre0 = ei.pre == 0;
+        // out_zp * 2^shr can join the rounding constant when the sum stays
+        // at most 2^30 (then mul_hi + it cannot overflow int32)
+        const int64_t zabs = p.out_zp < 0 ? -(int64_t)p.out_zp : (int64_t)p.out_zp;
+        col_fold = (int64_t)ei.rnd + (zabs << ei.shr) <= ((int64_t)1 << 30);
     }
+    // Whole-tile epilogue form.  The fences of these barriers also drain
+    // the prologue loads, so stage 0 is in LDS afterwards.
+    const bool all_pre0 = __syncthreads_and(col_pre0) != 0;
+    const bool zp_fold = __syncthreads_and(col_fold) != 0;
+    if (zp_fold && tid < C::TN) e_rnd[tid] += p.out_zp * (1 << (e_sp[tid] & 0xFF));
+    issue(C::STAGES - 1, C::STAGES - 1);
 
-    const int64_t wrow_bytes = C::WBITS == 8 ? p.K : p.K / 2;
-    const int8_t* wbase = static_cast<const int8_t*>(p.w);
-    const int KT = (int)((p.K + C::BK - 1) / C::BK);
-
-    // ---- global -> register staging
-    v4i wreg[C::W_PER_T], areg[C::A_PER_T];
-    auto load_tile = [&](int kt) {
-#pragma unroll
-        for (int i = 0; i < C::W_PER_T; ++i) {
-            const int c = tid + i * C::THREADS;
-            const int row = c / (C::BKW / 16), col = c % (C::BKW / 16);
-            int64_t n = n_tile + row;
-            if (n >= p.N) n = p.N - 1;
-            const int64_t kb = (int64_t)kt * C::BKW + col * 16;
-            v4i v = {0, 0, 0, 0};
-            if (kb < wrow_bytes) v = *reinterpret_cast<const v4i*>(wbase + n * wrow_bytes + kb);
-            wreg[i] = v;
-        }
-#pragma unroll
-        for (int i = 0; i < C::A_PER_T; ++i) {
-            const int c = tid + i * C::THREADS;
-            const int row = c / (C::BK / 16), col = c % (C::BK / 16);
-            int64_t m = m_tile + row;
-            if (m >= p.M) m = p.M - 1;
-            const int64_t kb = (int64_t)kt * C::BK + col * 16;
-            v4i v = {0, 0, 0, 0};
-            if (kb < p.K) v = *reinterpret_cast<const v4i*>(p.a + m * p.K + kb);
-            areg[i] = v;
-        }
-    };
-    auto store_tile = [&](int buf) {
-        int8_t* sw = smem + buf * C::STAGE;
-        int8_t* sa = sw + C::W_STAGE;
-#pragma unroll
-        for (int i = 0; i < C::W_PER_T; ++i) {
-            const int c = tid + i * C::THREADS;
-            const int row = c / (C::BKW / 16), col = c % (C::BKW / 16);
-            int8_t* dst = sw + row * C::LDW + col * 16;
-            if constexpr (C::WBITS == 8) {
-                *reinterpret_cast<v4i*>(dst) = wreg[i];
-            } else {
-                // 72-byte rows are only 8-byte aligned
-                reinterpret_cast<int2*>(dst)[0] = make_int2(wreg[i][0], wreg[i][1]);
-                reinterpret_cast<int2*>(dst)[1] = make_int2(wreg[i][2], wreg[i][3]);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < C::A_PER_T; ++i) {
-            const int c = tid + i * C::THREADS;
-            const int row = c / (C::BK / 16), col = c % (C::BK / 16);
-            *reinterpret_cast<v4i*>(sa + row * C::LDA + col * 16) = areg[i];
-        }
-    };
-
-    v4i acc[C::FN][C::FM];
+    // ---- main loop.  Fragments of the next 32-deep step are read from LDS
+    // while the MFMAs of the current one run; at the last step of a stage
+    // the stage switch (wait, barrier, next DMA, first fragments of the next
+    // stage) sits between the two halves of the step's MFMAs.  The steady
+    // state has no branches, so every wait count is a compile-time constant.
+    v16i acc[C::FN][C::FM];
 #pragma unroll
     for (int i = 0; i < C::FN; ++i)
 #pragma unroll
-        for (int j = 0; j < C::FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+        for (int j = 0; j < C::FM; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
 
-    load_tile(0);
-    store_tile(0);
-    __syncthreads();
-
-    for (int kt = 0; kt < KT; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < KT) load_tile(kt + 1);
-        const int8_t* sw = smem + buf * C::STAGE;
-        const int8_t* sa = sw + C::W_STAGE;
-#pragma unroll
-        for (int ks = 0; ks < C::BK / 64; ++ks) {
-            v4i wf[C::FN], af[C::FM];
-#pragma unroll
-            for (int i = 0; i < C::FN; ++i) {
-                const int row = wn * (C::TN / C::WN) + i * 16 + r16;
-                if constexpr (C::WBITS == 8) {
-                    wf[i] = *reinterpret_cast<const v4i*>(sw + row * C::LDW + ks * 64 + kg * 16);
-                } else {
-                    const uint2 pk =
-                        *reinterpret_cast<const uint2*>(sw + row * C::LDW + ks * 32 + kg * 8);
-                    wf[i] = unpack_int4_x16(pk.x, pk.y);
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < C::FM; ++j) {
-                const int row = wm * (C::TM / C::WM) + j * 16 + r16;
-                af[j] = *reinterpret_cast<const v4i*>(sa + row * C::LDA + ks * 64 + kg * 16);
-            }
-#pragma unroll
-            for (int i = 0; i < C::FN; ++i)
-#pragma unroll
-                for (int j = 0; j < C::FM; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
-        }
-        if (kt + 1 < KT) store_tile(buf ^ 1);
-        __syncthreads();
-    }
-
-    // ---- epilogue: lane holds channels 4*kg + {0..3} of token r16 in each fragment
-#pragma unroll
-    for (int i = 0; i < C::FN; ++i) {
-        const int nl = wn * (C::TN / C::WN) + i * 16 + 4 * kg;
-        const int64_t nb = n_tile + nl;
-        ColParams cp[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) cp[r] = params[nl + r];
+    auto load_frags = [&](int buf, int ks, v4i* wf, v4i* af) {
+        const int8_t* sa = smem + buf * C::STAGE;
+        const int8_t* sw = sa + C::A_BYTES;
 #pragma unroll
         for (int j = 0; j < C::FM; ++j) {
-            const int64_t m = m_tile + wm * (C::TM / C::WM) + j * 16 + r16;
-            if (m >= p.M || nb >= p.N) continue;
-            int32_t out[4];
+            const int row = wm * (C::TM / C::WM) + j * 32 + r32;
+            const int phys = (ks * 2 + hk) ^ swz<C::SWZ>(row, C::CA);
+            af[j] = *reinterpret_cast<const v4i*>(sa + row * C::BK + phys * 16);
+        }
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                int32_t a32 = acc[i][j][r];
-                if constexpr (C::WBITS == 4) a32 >>= 4;
-                out[r] = requant_out(a32, cp[r], p.out_zp, qmin, qmax);
-            }
-            const int64_t base = m * p.N + nb;
-            if (nb + 3 < p.N && (p.N % 4) == 0) {
-                if constexpr (C::OBITS == 8) {
-                    const uint32_t v = ((uint32_t)out[0] & 0xFFu) |
-                                       (((uint32_t)out[1] & 0xFFu) << 8) |
-                                       (((uint32_t)out[2] & 0xFFu) << 16) |
-                                       ((uint32_t)out[3] << 24);
-                    *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(p.y) + base) = v;
-                } else {
-                    const uint2 v =
-                        make_uint2(((uint32_t)out[0] & 0xFFFFu) | ((uint32_t)out[1] << 16),
-                                   ((uint32_t)out[2] & 0xFFFFu) | ((uint32_t)out[3] << 16));
-                    *reinterpret_cast<uint2*>(static_cast<int16_t*>(p.y) + base) = v;
-                }
+        for (int i = 0; i < C::FN; ++i) {
+            const int row = wn * (C::TN / C::WN) + i * 32 + r32;
+            if constexpr (C::WBITS == 8) {
+                const int phys = (ks * 2 + hk) ^ swz<C::SWZ>(row, C::CW);
+                wf[i] = *reinterpret_cast<const v4i*>(sw + row * C::BKW + phys * 16);
             } else {
+                // the 32 weights of this k step are one packed 16-byte chunk
+                const int phys = ks ^ swz<C::SWZ>(row, C::CW);
+                const uint2 pk =
+                    *reinterpret_cast<const uint2*>(sw + row * C::BKW + phys * 16 + hk * 8);
+                wf[i] = unpack_int4_x16(pk.x, pk.y);
+            }
+        }
+    };
+    auto mfma_rows = [&](const v4i* wf, const v4i* af, int i0, int i1) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    if (nb + r >= p.N) break;
-                    if constexpr (C::OBITS == 8)
-                        static_cast<int8_t*>(p.y)[base + r] = (int8_t)out[r];
-                    else
-                        static_cast<int16_t*>(p.y)[base + r] = (int16_t)out[r];
-                }
+        for (int i = i0; i < i1; ++i)
+#pragma unroll
+            for (int j = 0; j < C::FM; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
+    };
+
+    // Instruction interleave (sched_group_barrier masks: 0x008 MFMA, 0x100
+    // LDS read, 0x020 global/buffer load).  Spreading the next step's LDS
+    // reads between this step's MFMAs keeps both pipes busy: measured on
+    // MI355X, one wave per SIMD reaches ~83% of the int8 MFMA peak with one
+    // LDS read per two MFMAs, against ~60-77% with the reads bunched.
+    constexpr int NRD = C::FN + C::FM;         // LDS fragment reads per step
+    constexpr int NMF = C::FN * C::FM;         // MFMAs per step
+    auto interleave_step = [&]() {
+#pragma unroll
+        for (int r = 0; r < NRD; ++r) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, NMF / NRD, 0);
+        }
+        if constexpr (NMF % NRD != 0) __builtin_amdgcn_sched_group_barrier(0x008, NMF % NRD, 0);
+    };
+    auto interleave_switch = [&]() {
+        // the step after a stage switch: next-stage reads, this step's
+        // MFMAs and the DMA of a later stage, evenly mixed
+#pragma unroll
+        for (int r = 0; r < NRD; ++r) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, NMF / NRD, 0);
+            if (r < C::LOADS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        }
+        if constexpr (NMF % NRD != 0) __builtin_amdgcn_sched_group_barrier(0x008, NMF % NRD, 0);
+        if constexpr (C::LOADS > NRD) __builtin_amdgcn_sched_group_barrier(0x020, C::LOADS - NRD, 0);
+    };
+
+    v4i wf0[C::FN], af0[C::FM], wf1[C::FN], af1[C::FM];
+    load_frags(0, 0, wf0, af0);
+    for (int kt = 0; kt < KT - 1; ++kt) {
+        const int buf = kt % C::STAGES;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            v4i* wc = (ks & 1) ? wf1 : wf0;
+            v4i* ac = (ks & 1) ? af1 : af0;
+            v4i* wx = (ks & 1) ? wf0 : wf1;
+            v4i* ax = (ks & 1) ? af0 : af1;
+            if (ks + 1 < KS) {
+                load_frags(buf, ks + 1, wx, ax);
+                mfma_rows(wc, ac, 0, C::FN);
+                interleave_step();
+            } else {
+                // Stage switch at the start of the stage's last step: this
+                // step's fragments are already in registers, so buffer `buf`
+                // is no longer read by this wave once lgkmcnt reaches 0.
+                // Stage kt+1 is complete when only the STAGES-2 stages
+                // issued after it are in flight.
+                wait_vmcnt<(C::STAGES - 2) * C::LOADS>();
+                // Raw barrier: __syncthreads() adds a workgroup release
+                // fence that drains every outstanding load.
+                __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
+                __builtin_amdgcn_s_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+                load_frags((kt + 1) % C::STAGES, 0, wx, ax);
+                mfma_rows(wc, ac, 0, C::FN);
+                issue(kt + C::STAGES, buf);
+                interleave_switch();
             }
         }
     }
+    {  // last stage: no switch
+        const int buf = (KT - 1) % C::STAGES;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            v4i* wc = (ks & 1) ? wf1 : wf0;
+            v4i* ac = (ks & 1) ? af1 : af0;
+            v4i* wx = (ks & 1) ? wf0 : wf1;
+            v4i* ax = (ks & 1) ? af0 : af1;
+            if (ks + 1 < KS) {
+                load_frags(buf, ks + 1, wx, ax);
+                mfma_rows(wc, ac, 0, C::FN);
+                interleave_step();
+            } else {
+                mfma_rows(wc, ac, 0, C::FN);
+            }
+        }
+    }
+
+    // ---- epilogue, straight from the accumulators.  32x32 layout: lane
+    // holds token r32 and, in register group g, the four consecutive
+    // channels 8g + 4hk + {0..3}: one 4-byte (int8) or 8-byte (int16) store.
+    // Stores go through a descriptor covering the tile's valid rows, so rows
+    // past M are dropped by the hardware; channel groups past N get an
+    // out-of-range offset.  The requant is the integer form (mul_hi): on
+    // gfx950 that is cheaper than fp64 conversions.  A tile whose columns
+    // need no pre-shift and whose output zero-point folds into the rounding
+    // constant takes the short form: sat-add, mul_hi, add, shift, clamp.
+    wait_vmcnt<0>();  // the out-of-range DMA of the last steps is retired
+    __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
+    __builtin_amdgcn_s_barrier();  // e_rnd update visible even when KT == 1
+    constexpr int OB = C::OBITS / 8;
+    const int64_t row_bytes = p.N * OB;
+    const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(static_cast<int8_t*>(p.y) + m_tile * row_bytes), (short)0,
+        (int)(rows_a * row_bytes), 0x00020000);
+    const bool n_vec = (p.N % 4) == 0;
+    auto store4 = [&](int row, int nl, const int32_t* y) {
+        const int64_t n = n_tile + nl;
+        if (n_vec) {
+            const uint32_t voff = n < p.N ? (uint32_t)(row * row_bytes + n * OB) : kOOB;
+            if constexpr (C::OBITS == 8) {
+                const uint32_t lo = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x0c0c0400u);
+                const uint32_t hi = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x04000c0cu);
+                __builtin_amdgcn_raw_buffer_store_b32(lo | hi, ry, voff, 0, 0);
+            } else {
+                typedef unsigned v2u __attribute__((ext_vector_type(2)));
+                v2u v;
+                v[0] = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x05040100u);
+                v[1] = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x05040100u);
+                __builtin_amdgcn_raw_buffer_store_b64(v, ry, voff, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t voff =
+                    n + r < p.N ? (uint32_t)(row * row_bytes + (n + r) * OB) : kOOB;
+                if constexpr (C::OBITS == 8)
+                    __builtin_amdgcn_raw_buffer_store_b8((unsigned char)y[r], ry, voff, 0, 0);
+                else
+                    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)y[r], ry, voff, 0, 0);
+            }
+        }
+    };
+    auto epilogue = [&](auto fast) {
+        constexpr bool FAST = decltype(fast)::value;
+#pragma unroll
+        for (int i = 0; i < C::FN; ++i) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int nl = wn * (C::TN / C::WN) + i * 32 + 8 * g + 4 * hk;
+                const v4i off = *reinterpret_cast<const v4i*>(e_off + nl);
+                const v4i m0 = *reinterpret_cast<const v4i*>(e_m0 + nl);
+                const v4i rnd = *reinterpret_cast<const v4i*>(e_rnd + nl);
+                const v4i sp = *reinterpret_cast<const v4i*>(e_sp + nl);
+#pragma unroll
+                for (int j = 0; j < C::FM; ++j) {
+                    const int row = wm * (C::TM / C::WM) + j * 32 + r32;
+                    int32_t y[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        int32_t a32 = acc[i][j][4 * g + r];
+                        if constexpr (C::WBITS == 4) a32 >>= 4;  // exact: a multiple of 16
+                        int32_t c = __builtin_elementwise_add_sat(a32, off[r]);
+                        const int shr = sp[r] & 0xFF;
+                        if constexpr (!FAST) {
+                            const int pre = sp[r] >> 8;
+                            const int32_t bnd = pre ? (1 << (30 - pre)) : 0x7FFFFFFF;
+                            c = max(min(c, bnd), -bnd);
+                            c = (int32_t)((uint32_t)c << pre);
+                        }
+                        int32_t v = (__mulhi(c, m0[r]) + rnd[r]) >> shr;
+                        if (!FAST && !zp_fold) v += p.out_zp;
+                        y[r] = max(min(v, qmax), qmin);
+                    }
+                    store4(row, nl, y);
+                }
+            }
+        }
+    };
+    if (all_pre0 && zp_fold) epilogue(std::true_type{});
+    else epilogue(std::false_type{});
 }
 
 template <class C>
@@ -251,29 +443,70 @@ hipError_t launch_cfg(const QLinearArgs& p, hipStream_t s)
     const int64_t tiles_m = (p.M + C::TM - 1) / C::TM;
     const int64_t total = tiles_n * tiles_m;
     if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-    const size_t lds = 2 * C::STAGE + C::TN * sizeof(ColParams);
     // more than 64 KiB of dynamic LDS must be opted into once per kernel
     static const hipError_t attr = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&qlinear_prefill_kernel<C>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (attr != hipSuccess) return attr;
-    qlinear_prefill_kernel<C><<<dim3((unsigned)total), dim3(C::THREADS), lds, s>>>(
+    qlinear_prefill_kernel<C><<<dim3((unsigned)total), dim3(C::THREADS), C::LDS, s>>>(
         p, (int)tiles_n, (int)tiles_m);
     return hipGetLastError();
+}
+
+// Tile shapes, largest first.  (tokens x channels, wave grid, K bytes per
+// stage, stages, swizzle)
+template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 1>;
+template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 0>;
+template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 0>;
+
+struct TileChoice {
+    int tm, tn;
+    double eff;  // relative per-tile efficiency
+};
+
+int choose_tile(const QLinearArgs& p)
+{
+    if (const char* e = std::getenv("MQ_PREFILL_TILE")) {
+        const int v = std::atoi(e);
+        if (v >= 0 && v <= 2) return v;
+    }
+    static const TileChoice choices[] = {{256, 256, 1.0}, {256, 128, 0.85}, {128, 128, 0.6}};
+    const int cus = 256;
+    int best = 0;
+    double best_t = 1e300;
+    for (int c = 0; c < 3; ++c) {
+        const int64_t tiles =
+            ((p.M + choices[c].tm - 1) / choices[c].tm) * ((p.N + choices[c].tn - 1) / choices[c].tn);
+        const int64_t rounds = (tiles + cus - 1) / cus;
+        const double t = (double)rounds * choices[c].tm * choices[c].tn / choices[c].eff;
+        if (t < best_t) {
+            best_t = t;
+            best = c;
+        }
+    }
+    return best;
 }
 
 template <int WB, int OB>
 hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 {
-    return launch_cfg<Cfg<WB, OB, 128, 128, 2, 2, 128>>(p, s);
+    switch (choose_tile(p)) {
+    case 0: return launch_cfg<T256x256<WB, OB>>(p, s);
+    case 1: return launch_cfg<T256x128<WB, OB>>(p, s);
+    default: return launch_cfg<T128x128<WB, OB>>(p, s);
+    }
 }
 
 }  // namespace
 
 bool prefill_supported(const QLinearArgs& p)
 {
+    // whole 16-byte chunks per row (packed int4 rows too), 16-byte aligned
+    // bases, and per-tile buffer ranges below 2^31 bytes
     const bool kok = p.w_bits == 8 ? (p.K % 16 == 0) : (p.K % 32 == 0);
-    return kok && ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
+    // byte offsets inside one 256-row tile must fit the 32-bit buffer offset
+    const bool nok = 256 * p.N * (p.out_bits / 8) < ((int64_t)1 << 31);
+    return kok && nok && ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
            ((uintptr_t)p.y % 8) == 0;
 }
 

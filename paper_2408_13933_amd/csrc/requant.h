@@ -82,4 +82,47 @@ __device__ inline int32_t requant_out(int32_t acc, const ColParams& p, int32_t o
     return y;
 }
 
+// ---------------------------------------------------------------------------
+// Branch-free integer form for the tiled kernels; it computes exactly the
+// value of requant_out.
+//
+// integer form: r = floor((c*M0 + 2^(sh-1)) / 2^sh) is rewritten with an
+// effective shift s >= 33, where it equals (mulhi(c, M0) + 2^(s-33)) >> (s-32)
+// (the low 32 bits of the product cannot carry into the rounding).  For
+// 3 <= sh <= 32 the accumulator is first limited to +-2^(sh-3), which cannot
+// change the saturated result, and shifted left by 33 - sh without overflow;
+// for sh <= 2 every non-zero c saturates and c is limited to +-1 and shifted
+// by 30.
+struct EpiInt {
+    int32_t m0, rnd, shr, pre, bnd;
+};
+
+__device__ inline EpiInt epi_int_params(const ColParams& cp)
+{
+    EpiInt e;
+    e.m0 = cp.m0;
+    if (cp.m0 == 0) {  // r = 0 for every c
+        e.rnd = 1; e.shr = 1; e.pre = 0; e.bnd = 0x7FFFFFFF;
+    } else if (cp.sh >= 33) {
+        const int s = cp.sh < 63 ? cp.sh : 63;
+        e.rnd = 1 << (s - 33); e.shr = s - 32; e.pre = 0; e.bnd = 0x7FFFFFFF;
+    } else if (cp.sh >= 3) {
+        e.rnd = 1; e.shr = 1; e.pre = 33 - cp.sh; e.bnd = 1 << (cp.sh - 3);
+    } else {
+        e.rnd = 1; e.shr = 1; e.pre = 30; e.bnd = 1;
+    }
+    return e;
+}
+
+__device__ inline int32_t requant_int(int32_t acc, int32_t off, const EpiInt& e, int32_t zp,
+                                      int32_t qmin, int32_t qmax)
+{
+    int32_t c = __builtin_elementwise_add_sat(acc, off);
+    c = max(min(c, e.bnd), -e.bnd);  // v_med3_i32
+    c = (int32_t)((uint32_t)c << e.pre);
+    const int32_t h = __mulhi(c, e.m0);
+    const int32_t r = (h + e.rnd) >> e.shr;
+    return max(min(r + zp, qmax), qmin);  // v_med3_i32
+}
+
 }  // namespace mq
