@@ -103,6 +103,103 @@ __device__ inline int swz(int row, int nchunks)
     else return 0;
 }
 
+struct EpiCtx {
+    const int32_t* e_off;
+    const int32_t* e_m0;
+    const int32_t* e_rnd;
+    const int32_t* e_sp;
+    int32_t row_bytes;     // bytes per output row
+    int32_t lane_row_off;  // byte offset of this lane's first token row in the tile
+    int32_t col0;          // this lane's first channel inside the tile
+    int32_t n_left;        // channels of the tile that exist (N - n_tile)
+    int32_t n_tile;
+    int32_t out_zp;        // 0 when folded into the rounding constants
+    __amdgpu_buffer_rsrc_t ry;  // output rows of this tile
+};
+
+// Requant and store one tile's accumulators.  32x32 accumulator layout:
+// lane holds token r32 and, in register group g, the four consecutive
+// channels 8g + 4hk + {0..3}: one 4-byte (int8) or 8-byte (int16) store.
+// Rows past M fall outside the descriptor and are dropped by the hardware;
+// channel groups past N get an out-of-range offset.  The requant is the
+// integer form with one mul_hi per output (cheaper on gfx950 than fp64
+// conversions).  FAST: no column needs the pre-shift, the output zero-point
+// is folded into the rounding constants and N % 4 == 0, leaving
+// sat-add, mul_hi, add, shift, clamp per output.
+template <class C, bool FAST, class Acc>
+__device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
+{
+    constexpr int32_t qmin = -(1 << (C::OBITS - 1));
+    constexpr int32_t qmax = (1 << (C::OBITS - 1)) - 1;
+    constexpr int OB = C::OBITS / 8;
+#pragma unroll
+    for (int i = 0; i < C::FN; ++i) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int nl = x.col0 + i * 32 + 8 * g;  // tile-local channel
+            const v4i off = *reinterpret_cast<const v4i*>(x.e_off + nl);
+            const v4i m0 = *reinterpret_cast<const v4i*>(x.e_m0 + nl);
+            const v4i rnd = *reinterpret_cast<const v4i*>(x.e_rnd + nl);
+            const v4i sp = *reinterpret_cast<const v4i*>(x.e_sp + nl);
+            const int32_t col_off = (x.n_tile + nl) * OB;
+            const bool col_ok = nl < x.n_left;
+            int32_t shr[4], pre[4], bnd[4];  // per column, hoisted out of the token loop
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                shr[r] = sp[r] & 0xFF;
+                pre[r] = sp[r] >> 8;
+                bnd[r] = pre[r] ? (1 << (30 - pre[r])) : 0x7FFFFFFF;
+            }
+#pragma unroll
+            for (int j = 0; j < C::FM; ++j) {
+                int32_t y[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    int32_t a32 = acc[i][j][4 * g + r];
+                    if constexpr (C::WBITS == 4) a32 >>= 4;  // exact: a multiple of 16
+                    int32_t c = __builtin_elementwise_add_sat(a32, off[r]);
+                    if constexpr (!FAST) {
+                        c = max(min(c, bnd[r]), -bnd[r]);
+                        c = (int32_t)((uint32_t)c << pre[r]);
+                    }
+                    int32_t v = (__mulhi(c, m0[r]) + rnd[r]) >> shr[r];
+                    if constexpr (!FAST) v += x.out_zp;
+                    y[r] = max(min(v, qmax), qmin);
+                }
+                const int32_t row_off = x.lane_row_off + j * 32 * x.row_bytes;
+                if (FAST || (x.n_left & 3) == 0 || nl + 3 < x.n_left) {
+                    const uint32_t voff = col_ok ? (uint32_t)(row_off + col_off) : kOOB;
+                    if constexpr (C::OBITS == 8) {
+                        const uint32_t lo =
+                            __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x0c0c0400u);
+                        const uint32_t hi =
+                            __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x04000c0cu);
+                        __builtin_amdgcn_raw_buffer_store_b32(lo | hi, x.ry, voff, 0, 0);
+                    } else {
+                        typedef unsigned v2u __attribute__((ext_vector_type(2)));
+                        v2u v;
+                        v[0] = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x05040100u);
+                        v[1] = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x05040100u);
+                        __builtin_amdgcn_raw_buffer_store_b64(v, x.ry, voff, 0, 0);
+                    }
+                } else {
+                    // a channel group straddling N (N % 4 != 0): element stores
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const uint32_t voff =
+                            nl + r < x.n_left ? (uint32_t)(row_off + col_off + r * OB) : kOOB;
+                        if constexpr (C::OBITS == 8)
+                            __builtin_amdgcn_raw_buffer_store_b8((unsigned char)y[r], x.ry, voff, 0, 0);
+                        else
+                            __builtin_amdgcn_raw_buffer_store_b16((unsigned short)y[r], x.ry, voff,
+                                                                  0, 0);
+                    }
+                }
+            }
+        }
+    }
+}
+
 template <class C>
 __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearArgs p,
                                                                        int tiles_n, int tiles_m)
@@ -351,89 +448,26 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         }
     }
 
-    // ---- epilogue, straight from the accumulators.  32x32 layout: lane
-    // holds token r32 and, in register group g, the four consecutive
-    // channels 8g + 4hk + {0..3}: one 4-byte (int8) or 8-byte (int16) store.
-    // Stores go through a descriptor covering the tile's valid rows, so rows
-    // past M are dropped by the hardware; channel groups past N get an
-    // out-of-range offset.  The requant is the integer form (mul_hi): on
-    // gfx950 that is cheaper than fp64 conversions.  A tile whose columns
-    // need no pre-shift and whose output zero-point folds into the rounding
-    // constant takes the short form: sat-add, mul_hi, add, shift, clamp.
+    // ---- epilogue, straight from the accumulators (see prefill_epilogue)
     wait_vmcnt<0>();  // the out-of-range DMA of the last steps is retired
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
     __builtin_amdgcn_s_barrier();  // e_rnd update visible even when KT == 1
-    constexpr int OB = C::OBITS / 8;
-    const int64_t row_bytes = p.N * OB;
-    const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(static_cast<int8_t*>(p.y) + m_tile * row_bytes), (short)0,
-        (int)(rows_a * row_bytes), 0x00020000);
-    const bool n_vec = (p.N % 4) == 0;
-    auto store4 = [&](int row, int nl, const int32_t* y) {
-        const int64_t n = n_tile + nl;
-        if (n_vec) {
-            const uint32_t voff = n < p.N ? (uint32_t)(row * row_bytes + n * OB) : kOOB;
-            if constexpr (C::OBITS == 8) {
-                const uint32_t lo = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x0c0c0400u);
-                const uint32_t hi = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x04000c0cu);
-                __builtin_amdgcn_raw_buffer_store_b32(lo | hi, ry, voff, 0, 0);
-            } else {
-                typedef unsigned v2u __attribute__((ext_vector_type(2)));
-                v2u v;
-                v[0] = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x05040100u);
-                v[1] = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x05040100u);
-                __builtin_amdgcn_raw_buffer_store_b64(v, ry, voff, 0, 0);
-            }
-        } else {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const uint32_t voff =
-                    n + r < p.N ? (uint32_t)(row * row_bytes + (n + r) * OB) : kOOB;
-                if constexpr (C::OBITS == 8)
-                    __builtin_amdgcn_raw_buffer_store_b8((unsigned char)y[r], ry, voff, 0, 0);
-                else
-                    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)y[r], ry, voff, 0, 0);
-            }
-        }
-    };
-    auto epilogue = [&](auto fast) {
-        constexpr bool FAST = decltype(fast)::value;
-#pragma unroll
-        for (int i = 0; i < C::FN; ++i) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int nl = wn * (C::TN / C::WN) + i * 32 + 8 * g + 4 * hk;
-                const v4i off = *reinterpret_cast<const v4i*>(e_off + nl);
-                const v4i m0 = *reinterpret_cast<const v4i*>(e_m0 + nl);
-                const v4i rnd = *reinterpret_cast<const v4i*>(e_rnd + nl);
-                const v4i sp = *reinterpret_cast<const v4i*>(e_sp + nl);
-#pragma unroll
-                for (int j = 0; j < C::FM; ++j) {
-                    const int row = wm * (C::TM / C::WM) + j * 32 + r32;
-                    int32_t y[4];
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        int32_t a32 = acc[i][j][4 * g + r];
-                        if constexpr (C::WBITS == 4) a32 >>= 4;  // exact: a multiple of 16
-                        int32_t c = __builtin_elementwise_add_sat(a32, off[r]);
-                        const int shr = sp[r] & 0xFF;
-                        if constexpr (!FAST) {
-                            const int pre = sp[r] >> 8;
-                            const int32_t bnd = pre ? (1 << (30 - pre)) : 0x7FFFFFFF;
-                            c = max(min(c, bnd), -bnd);
-                            c = (int32_t)((uint32_t)c << pre);
-                        }
-                        int32_t v = (__mulhi(c, m0[r]) + rnd[r]) >> shr;
-                        if (!FAST && !zp_fold) v += p.out_zp;
-                        y[r] = max(min(v, qmax), qmin);
-                    }
-                    store4(row, nl, y);
-                }
-            }
-        }
-    };
-    if (all_pre0 && zp_fold) epilogue(std::true_type{});
-    else epilogue(std::false_type{});
+    EpiCtx ctx;
+    ctx.e_off = e_off;
+    ctx.e_m0 = e_m0;
+    ctx.e_rnd = e_rnd;
+    ctx.e_sp = e_sp;
+    ctx.row_bytes = (int32_t)(p.N * (C::OBITS / 8));
+    ctx.lane_row_off = (wm * (C::TM / C::WM) + r32) * ctx.row_bytes;
+    ctx.col0 = wn * (C::TN / C::WN) + 4 * hk;
+    ctx.n_left = (int32_t)(p.N - n_tile);
+    ctx.n_tile = (int32_t)n_tile;
+    ctx.out_zp = zp_fold ? 0 : p.out_zp;
+    ctx.ry = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(static_cast<int8_t*>(p.y) + m_tile * (int64_t)ctx.row_bytes), (short)0,
+        (int)(rows_a * ctx.row_bytes), 0x00020000);
+    if (all_pre0 && zp_fold && (p.N % 4) == 0) prefill_epilogue<C, true>(acc, ctx);
+    else prefill_epilogue<C, false>(acc, ctx);
 }
 
 template <class C>
