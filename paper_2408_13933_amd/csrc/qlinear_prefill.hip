@@ -85,13 +85,14 @@ struct Cfg {
     static constexpr int A_BYTES = A_PER_WAVE * NWAVES * 1024;
     static constexpr int W_BYTES = W_PER_WAVE * NWAVES * 1024;
     static constexpr int STAGE = A_BYTES + W_BYTES;
-    static constexpr int LDS = STAGES * STAGE + TN * 16;  // + per-column epilogue constants
+    // + per-column epilogue constants + one flag word per wave
+    static constexpr int LDS = STAGES * STAGE + TN * 16 + NWAVES * 4;
     static_assert(TM % (WM * 32) == 0 && TN % (WN * 32) == 0, "wave grid");
     static_assert((TM * CA) % 64 == 0 && (TN * CW) % 64 == 0, "whole wave loads");
     static_assert(BK % 64 == 0, "BK is a multiple of the MFMA depth");
     static_assert(STAGES >= 2 && STAGES <= 4, "pipeline depth");
     static_assert((BK / 32) % 2 == 0, "even number of 32-deep steps per stage");
-    static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
+    static_assert(LOADS * (STAGES - 1) < 64, "vmcnt range");
     static_assert(LDS <= 160 * 1024, "LDS per CU");
 };
 
@@ -100,7 +101,13 @@ __device__ inline int swz(int row, int nchunks)
 {
     if constexpr (SWZ == 0) return row & (nchunks - 1);
     else if constexpr (SWZ == 1) return (row >> 1) & (nchunks - 1);
-    else return 0;
+    else if constexpr (SWZ == 2) {
+        // 64 banks x 4 bytes: 256 / (16 * nchunks) rows share one bank row,
+        // so the row index above that is the XOR key; 16 consecutive rows
+        // then cover all 16 groups of four banks
+        const int per = 16 / nchunks;  // rows per 256 bytes
+        return (row / per) & (nchunks - 1);
+    } else return 0;
 }
 
 struct EpiCtx {
@@ -114,7 +121,34 @@ struct EpiCtx {
     int32_t n_left;        // channels of the tile that exist (N - n_tile)
     int32_t n_tile;
     int32_t out_zp;        // 0 when folded into the rounding constants
+    int32_t r32;           // this lane's token row within a 32-row fragment
+    int32_t wave_row0;     // first token row of this wave's sub-tile (tile-local)
+    int32_t wave_col0;     // first channel of this wave's sub-tile (tile-local)
+    MQ_LDS int8_t* stage;  // this wave's LDS staging area (staged stores)
     __amdgpu_buffer_rsrc_t ry;  // output rows of this tile
+};
+
+// Staged stores: a wave's outputs go through its own LDS area, PB bytes of
+// each sub-tile row per pass, and leave as 16-byte stores that cover whole
+// row segments.  Direct stores from the accumulator layout write 4 or 8
+// bytes into each of 32 rows per instruction, which measured ~2x slower
+// for the whole epilogue on MI355X.
+template <class C>
+struct Staging {
+    static constexpr int OB = C::OBITS / 8;
+    static constexpr int WR = C::TM / C::WM;  // sub-tile rows
+    static constexpr int WC = C::TN / C::WN;  // sub-tile channels
+    static constexpr int PASS_COLS = WC * OB > 128 ? 128 / OB : WC;
+    static constexpr int PASSES = WC / PASS_COLS;
+    static constexpr int FNP = C::FN / PASSES;  // 32-channel fragments per pass
+    static constexpr int PB = PASS_COLS * OB;   // staged bytes per row
+    static constexpr int PITCH = PB + 16;       // padding spreads rows over banks
+    static constexpr int CPR = PB / 16;         // 16-byte chunks per row
+    static constexpr int RPI = 64 / CPR;        // rows per wave-wide 16-byte store
+    static constexpr int BYTES = WR * PITCH;    // per wave
+    static_assert(PASS_COLS % 32 == 0 && C::FN % PASSES == 0, "whole fragments per pass");
+    static_assert(WR % RPI == 0, "whole stores per sub-tile");
+    static_assert(C::NWAVES * BYTES <= C::STAGES * C::STAGE, "staging fits the stage ring");
 };
 
 // Requant and store one tile's accumulators.  32x32 accumulator layout:
@@ -126,14 +160,20 @@ struct EpiCtx {
 // conversions).  FAST: no column needs the pre-shift, the output zero-point
 // is folded into the rounding constants and N % 4 == 0, leaving
 // sat-add, mul_hi, add, shift, clamp per output.
-template <class C, bool FAST, class Acc>
+template <class C, bool FAST, bool STAGED, class Acc>
 __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
     constexpr int32_t qmax = (1 << (C::OBITS - 1)) - 1;
     constexpr int OB = C::OBITS / 8;
+    using S = Staging<C>;
+    static_assert(!STAGED || FAST, "staged stores assume whole 4-channel groups");
+    constexpr int PASSES = STAGED ? S::PASSES : 1;
+    constexpr int FNP = C::FN / PASSES;
 #pragma unroll
-    for (int i = 0; i < C::FN; ++i) {
+    for (int pass = 0; pass < PASSES; ++pass) {
+#pragma unroll
+    for (int i = pass * FNP; i < (pass + 1) * FNP; ++i) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int nl = x.col0 + i * 32 + 8 * g;  // tile-local channel
@@ -165,6 +205,26 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
                     int32_t v = (__mulhi(c, m0[r]) + rnd[r]) >> shr[r];
                     if constexpr (!FAST) v += x.out_zp;
                     y[r] = max(min(v, qmax), qmin);
+                }
+                if constexpr (STAGED) {
+                    // tile-local row j*32 + r32, pass-local channel nl - first
+                    const int lrow = j * 32 + x.r32;
+                    MQ_LDS int8_t* dst = x.stage + lrow * S::PITCH +
+                                         (nl - x.wave_col0 - pass * S::PASS_COLS) * OB;
+                    if constexpr (C::OBITS == 8) {
+                        const uint32_t lo =
+                            __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x0c0c0400u);
+                        const uint32_t hi =
+                            __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x04000c0cu);
+                        *reinterpret_cast<MQ_LDS uint32_t*>(dst) = lo | hi;
+                    } else {
+                        typedef unsigned v2u __attribute__((ext_vector_type(2)));
+                        v2u v;
+                        v[0] = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x05040100u);
+                        v[1] = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x05040100u);
+                        *reinterpret_cast<MQ_LDS v2u*>(dst) = v;
+                    }
+                    continue;
                 }
                 const int32_t row_off = x.lane_row_off + j * 32 * x.row_bytes;
                 if (FAST || (x.n_left & 3) == 0 || nl + 3 < x.n_left) {
@@ -198,6 +258,20 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
             }
         }
     }
+    if constexpr (STAGED) {
+        // read back whole 16-byte row chunks and store them
+        const int lane = threadIdx.x & 63;
+        const int ch = lane % S::CPR;
+        const int32_t col_byte = (x.n_tile + x.wave_col0 + pass * S::PASS_COLS) * OB + ch * 16;
+#pragma unroll
+        for (int t = 0; t < S::WR / S::RPI; ++t) {
+            const int lrow = t * S::RPI + lane / S::CPR;
+            const v4i v = *reinterpret_cast<MQ_LDS const v4i*>(x.stage + lrow * S::PITCH + ch * 16);
+            const uint32_t voff = (uint32_t)((x.wave_row0 + lrow) * x.row_bytes + col_byte);
+            __builtin_amdgcn_raw_buffer_store_b128(v, x.ry, voff, 0, 0);
+        }
+    }
+    }
 }
 
 template <class C>
@@ -213,6 +287,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     int32_t* e_m0 = e_off + C::TN;
     int32_t* e_rnd = e_m0 + C::TN;
     int32_t* e_sp = e_rnd + C::TN;  // shr | pre << 8
+    int32_t* e_flag = e_sp + C::TN;  // per wave: bit 0 all pre == 0, bit 1 zp foldable
 
     // ---- tile id: the blocks of one XCD (block id mod 8) take a contiguous
     // run of tiles, so they share weight tiles in that XCD's L2
@@ -295,17 +370,27 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         }
     };
 
-    // ---- start the pipeline, then derive the per-column constants while
-    // the first tiles are in flight
-#pragma unroll
-    for (int s = 0; s < C::STAGES - 1; ++s) issue(s, s);
-
-    int col_pre0 = 1, col_fold = 1;
+    // ---- per-column inputs first: the vector-memory counter retires in
+    // issue order, so these loads are back before the stage DMA behind them
+    // and the constants are derived while the first tiles are in flight
+    float col_ws = 1.0f, col_bias = 0.0f;
+    int32_t col_cs = 0;
     if (tid < C::TN) {
         int64_t n = n_tile + tid;
         if (n >= p.N) n = p.N - 1;
-        const ColParams cp = derive_col_params(p.a_scale, p.w_scale[n], p.out_scale,
-                                               p.bias ? p.bias + n : nullptr, p.colsum[n], p.a_zp);
+        col_ws = p.w_scale[n];
+        col_cs = p.colsum[n];
+        col_bias = (p.bias ? p.bias : p.w_scale)[n];  // branch-free; unused without bias
+    }
+#pragma unroll
+    for (int s = 0; s < C::STAGES - 1; ++s) issue(s, s);
+    // keep every use of the loaded values behind the DMA issue
+    asm volatile("" : "+v"(col_ws), "+v"(col_cs), "+v"(col_bias));
+
+    int col_pre0 = 1, col_fold = 1;
+    if (tid < C::TN) {
+        const ColParams cp = derive_col_params_v(p.a_scale, col_ws, p.out_scale, p.bias != nullptr,
+                                                 col_bias, col_cs, p.a_zp);
         const EpiInt ei = epi_int_params(cp);
         e_off[tid] = cp.off;
         e_m0[tid] = ei.m0;
@@ -317,12 +402,29 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         const int64_t zabs = p.out_zp < 0 ? -(int64_t)p.out_zp : (int64_t)p.out_zp;
         col_fold = (int64_t)ei.rnd + (zabs << ei.shr) <= ((int64_t)1 << 30);
     }
-    // Whole-tile epilogue form.  The fences of these barriers also drain
-    // the prologue loads, so stage 0 is in LDS afterwards.
-    const bool all_pre0 = __syncthreads_and(col_pre0) != 0;
-    const bool zp_fold = __syncthreads_and(col_fold) != 0;
+    // Whole-tile epilogue form: AND of the column flags over the block, by
+    // ballot per wave and one LDS word per wave.  A raw barrier, since
+    // __syncthreads() would also drain the stage DMA.
+    {
+        const bool w_pre0 = __ballot(col_pre0) == ~0ull;
+        const bool w_fold = __ballot(col_fold) == ~0ull;
+        if (lane == 0) e_flag[wave] = (w_pre0 ? 1 : 0) | (w_fold ? 2 : 0);
+    }
+    __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    int flags = 3;
+#pragma unroll
+    for (int w = 0; w < C::NWAVES; ++w) flags &= e_flag[w];
+    flags = __builtin_amdgcn_readfirstlane(flags);
+    const bool all_pre0 = (flags & 1) != 0;
+    const bool zp_fold = (flags & 2) != 0;
     if (zp_fold && tid < C::TN) e_rnd[tid] += p.out_zp * (1 << (e_sp[tid] & 0xFF));
     issue(C::STAGES - 1, C::STAGES - 1);
+    // stage 0 is complete when only the STAGES-1 stages behind it are in
+    // flight, in every wave
+    wait_vmcnt<(C::STAGES - 1) * C::LOADS>();
+    __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
+    __builtin_amdgcn_s_barrier();
 
     // ---- main loop.  Fragments of the next 32-deep step are read from LDS
     // while the MFMAs of the current one run; at the last step of a stage
@@ -355,9 +457,10 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
             } else {
                 // the 32 weights of this k step are one packed 16-byte chunk
                 const int phys = ks ^ swz<C::SWZ>(row, C::CW);
-                const uint2 pk =
-                    *reinterpret_cast<const uint2*>(sw + row * C::BKW + phys * 16 + hk * 8);
-                wf[i] = unpack_int4_x16(pk.x, pk.y);
+                typedef unsigned v2u __attribute__((ext_vector_type(2)));
+                const v2u pk =
+                    *reinterpret_cast<const v2u*>(sw + row * C::BKW + phys * 16 + hk * 8);
+                wf[i] = unpack_int4_x16(pk[0], pk[1]);
             }
         }
     };
@@ -463,11 +566,20 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     ctx.n_left = (int32_t)(p.N - n_tile);
     ctx.n_tile = (int32_t)n_tile;
     ctx.out_zp = zp_fold ? 0 : p.out_zp;
+    ctx.r32 = r32;
+    ctx.wave_row0 = wm * (C::TM / C::WM);
+    ctx.wave_col0 = wn * (C::TN / C::WN);
+    ctx.stage = (MQ_LDS int8_t*)smem + wave * Staging<C>::BYTES;
     ctx.ry = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(static_cast<int8_t*>(p.y) + m_tile * (int64_t)ctx.row_bytes), (short)0,
         (int)(rows_a * ctx.row_bytes), 0x00020000);
-    if (all_pre0 && zp_fold && (p.N % 4) == 0) prefill_epilogue<C, true>(acc, ctx);
-    else prefill_epilogue<C, false>(acc, ctx);
+    const bool fast = all_pre0 && zp_fold && (p.N % 4) == 0;
+    // staged stores need the tile's channels inside N and 16-byte row chunks
+    const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
+                        ((uintptr_t)p.y % 16) == 0;
+    if (staged) prefill_epilogue<C, true, true>(acc, ctx);
+    else if (fast) prefill_epilogue<C, true, false>(acc, ctx);
+    else prefill_epilogue<C, false, false>(acc, ctx);
 }
 
 template <class C>
@@ -489,9 +601,9 @@ hipError_t launch_cfg(const QLinearArgs& p, hipStream_t s)
 
 // Tile shapes, largest first.  (tokens x channels, wave grid, K bytes per
 // stage, stages, swizzle)
-template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 1>;
-template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 0>;
-template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 0>;
+template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2>;
+template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2>;
+template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2>;
 
 struct TileChoice {
     int tm, tn;

@@ -22,9 +22,9 @@ struct ColParams {
 // accumulator units.  fp64 throughout: the product of two fp32 values is
 // exact in fp64, the division is one correctly rounded operation, and
 // frexp/ldexp/rint are exact, so the integers do not depend on the device.
-__device__ inline ColParams derive_col_params(float a_scale, float w_scale, float out_scale,
-                                              const float* bias_n, int32_t colsum,
-                                              int32_t a_zp)
+__device__ inline ColParams derive_col_params_v(float a_scale, float w_scale, float out_scale,
+                                                bool has_bias, float bias_n, int32_t colsum,
+                                                int32_t a_zp)
 {
 #pragma clang fp contract(off)
     ColParams p;
@@ -48,8 +48,8 @@ __device__ inline ColParams derive_col_params(float a_scale, float w_scale, floa
         p.sh = 31 - e;
     }
     long long bq = 0;
-    if (bias_n != nullptr) {
-        double t = (double)(*bias_n) / prod;
+    if (has_bias) {
+        double t = (double)bias_n / prod;
         t = fmin(fmax(t, -1073741824.0), 1073741824.0);
         bq = (long long)rint(t);
     }
@@ -57,6 +57,14 @@ __device__ inline ColParams derive_col_params(float a_scale, float w_scale, floa
     off = off < INT32_MIN ? INT32_MIN : (off > INT32_MAX ? INT32_MAX : off);
     p.off = (int32_t)off;
     return p;
+}
+
+__device__ inline ColParams derive_col_params(float a_scale, float w_scale, float out_scale,
+                                              const float* bias_n, int32_t colsum,
+                                              int32_t a_zp)
+{
+    return derive_col_params_v(a_scale, w_scale, out_scale, bias_n != nullptr,
+                               bias_n != nullptr ? *bias_n : 0.0f, colsum, a_zp);
 }
 
 // r for one corrected accumulator c (int32).
