@@ -2,7 +2,7 @@
 //
 // Generation is bound by weight traffic (the paper finds autoregressive
 // decoding partly memory-bound, Section 5.6, and 4-bit weights help it most,
-// appendix).  Each block owns 16 output channels; its waves split K and each
+// appendix).  Each block owns 16 (or 8) output channels; its waves split K and each
 // lane streams 16 weights of one channel per step with a 16-byte (int8) or
 // 8-byte (int4) load, so one wave-wide load covers 64 contiguous bytes of 16
 // rows.  The 16 x 16 x 64 int8 MFMA multiplies those weights with up to 16
@@ -34,52 +34,112 @@ __device__ inline v4i unpack_int4_x16(uint32_t x0, uint32_t x1)
     return r;
 }
 
-template <int WBITS, int OBITS, int NWAVES>
+// R output channels per block (16, or 8 for narrow layers so the weight
+// stream spreads over more CUs; rows R..15 of the MFMA then load nothing).
+template <int WBITS, int OBITS, int NWAVES, int R>
 __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs p)
 {
-    constexpr int U = 4;  // steps in flight per wave
+    constexpr int U = 8;  // 64-wide k steps per load round (one round covers most layers)
     constexpr int32_t qmin = -(1 << (OBITS - 1));
     constexpr int32_t qmax = (1 << (OBITS - 1)) - 1;
     __shared__ v4i red[NWAVES][64];
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar loop
     const int r16 = lane & 15;  // weight row in the group / token row
     const int kg = lane >> 4;   // 16-wide k group inside a 64-wide step
-    const int64_t n0 = (int64_t)blockIdx.x * 16;
-    int64_t nrow = n0 + r16;
-    if (nrow >= p.N) nrow = p.N - 1;  // duplicate a valid row; never stored
+    const int64_t n0 = (int64_t)blockIdx.x * R;
+    // Buffer descriptors over this block's weight rows and the M token rows:
+    // a load past a valid row (channel >= N, token >= M, k >= K, or a step
+    // beyond this wave's range) returns zeros without touching memory, so
+    // every load is unconditional.
+    constexpr uint32_t kOOB = 0x80000000u;
+    const int64_t wrow_bytes = WBITS == 8 ? p.K : p.K / 2;
+    const int rows_w = (int)(p.N - n0 < R ? p.N - n0 : R);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(static_cast<const int8_t*>(p.w) + n0 * wrow_bytes), (short)0,
+        (int)(rows_w * wrow_bytes), 0x00020000);
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)p.a, (short)0, (int)(p.M * p.K), 0x00020000);
     const bool has_a = r16 < p.M;
-    const int8_t* arow = p.a + (has_a ? (int64_t)r16 * p.K : 0);
+
+    // Per-channel inputs of the epilogue (channels n0 + 4*kg + r), loaded by
+    // the epilogue wave before the weight stream so both share one memory
+    // latency.
+    float col_ws[4] = {1.0f, 1.0f, 1.0f, 1.0f}, col_b[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    int32_t col_cs[4] = {0, 0, 0, 0};
+    if (wave == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            int64_t n = n0 + 4 * kg + r;
+            if (n >= p.N) n = p.N - 1;
+            col_ws[r] = p.w_scale[n];
+            col_cs[r] = p.colsum[n];
+            col_b[r] = (p.bias ? p.bias : p.w_scale)[n];  // branch-free; unused without bias
+        }
+    }
 
     const int64_t steps = (p.K + 63) / 64;
     const int64_t s_begin = steps * wave / NWAVES;
     const int64_t s_end = steps * (wave + 1) / NWAVES;
 
-    v4i acc = {0, 0, 0, 0};
-    for (int64_t s = s_begin; s < s_end; s += U) {
-        v4i wv[U], av[U];
+    // offsets stay below 2^21 (16 rows of at most 65536 bytes), so setting
+    // bit 31 pushes a load out of range without a branch
+    const int K32 = (int)p.K;
+    const int s_end32 = (int)s_end;
+    const uint32_t a_dead = has_a ? 0u : kOOB;
+    auto load = [&](int64_t s, v4i* wv, v4i* av) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t k = (s + u) * 64 + kg * 16;
-            const bool ok = (s + u < s_end) && (k < p.K);
-            v4i w = {0, 0, 0, 0}, a = {0, 0, 0, 0};
-            if (ok) {
-                if constexpr (WBITS == 8) {
-                    w = *reinterpret_cast<const v4i*>(static_cast<const int8_t*>(p.w) +
-                                                       nrow * p.K + k);
-                } else {
-                    const uint2 pk = *reinterpret_cast<const uint2*>(
-                        static_cast<const uint8_t*>(p.w) + nrow * (p.K / 2) + k / 2);
-                    w = unpack_int4_x16(pk.x, pk.y);
-                }
-                if (has_a) a = *reinterpret_cast<const v4i*>(arow + k);
+            const int su = (int)s + u;
+            const int k = su * 64 + kg * 16;
+            const uint32_t dead = (uint32_t)((su >= s_end32) | (k >= K32)) << 31;
+            if constexpr (WBITS == 8) {
+                wv[u] = __builtin_amdgcn_raw_buffer_load_b128(rw, (uint32_t)(r16 * K32 + k) | dead,
+                                                              0, 0);
+            } else {
+                // packed nibbles stay packed until the MFMA needs them, so
+                // the next load round is issued before this one lands
+                typedef unsigned v2u __attribute__((ext_vector_type(2)));
+                const v2u pk = __builtin_amdgcn_raw_buffer_load_b64(
+                    rw, (uint32_t)(r16 * (K32 / 2) + k / 2) | dead, 0, 0);
+                wv[u] = v4i{(int)pk[0], (int)pk[1], 0, 0};
             }
-            wv[u] = w;
-            av[u] = a;
+            av[u] = __builtin_amdgcn_raw_buffer_load_b128(ra, (uint32_t)(r16 * K32 + k) | dead | a_dead,
+                                                          0, 0);
         }
+    };
+    v4i acc = {0, 0, 0, 0};
+    auto mfma = [&](const v4i* wv, const v4i* av) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[u], av[u], acc, 0, 0, 0);
+        for (int u = 0; u < U; ++u) {
+            v4i w = wv[u];
+            if constexpr (WBITS == 4) w = unpack_int4_x16((uint32_t)w[0], (uint32_t)w[1]);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(w, av[u], acc, 0, 0, 0);
+        }
+    };
+    // The launch picks the wave count so one round covers a wave's K range
+    // whenever K <= 16 * 8 * 64; longer rows take several rounds.  Steps
+    // past the range load zeros and touch no memory.  The epilogue wave
+    // derives its fixed-point constants while the first round is in flight
+    // (the per-channel loads were issued before it and return first).
+    v4i wv[U], av[U];
+    load(s_begin, wv, av);
+    // every use of the per-channel inputs stays behind the weight loads
+    asm volatile("" : "+v"(col_ws[0]), "+v"(col_ws[1]), "+v"(col_ws[2]), "+v"(col_ws[3]),
+                 "+v"(col_cs[0]), "+v"(col_cs[1]), "+v"(col_cs[2]), "+v"(col_cs[3]),
+                 "+v"(col_b[0]), "+v"(col_b[1]), "+v"(col_b[2]), "+v"(col_b[3]));
+    ColParams cps[4] = {};
+    if (wave == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            cps[r] = derive_col_params_v(p.a_scale, col_ws[r], p.out_scale, p.bias != nullptr,
+                                         col_b[r], col_cs[r], p.a_zp);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    for (int64_t s = s_begin; s < s_end; s += U) {
+        if (s != s_begin) load(s, wv, av);
+        mfma(wv, av);
     }
 
     if constexpr (NWAVES > 1) {
@@ -92,17 +152,13 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
 
     // lane holds acc for token m = r16 and channels n0 + 4*kg + {0,1,2,3}
     const int64_t m = r16;
-    if (m >= p.M) return;
+    if (m >= p.M || 4 * kg >= R) return;
     int32_t out[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        int64_t n = n0 + 4 * kg + r;
-        if (n >= p.N) n = p.N - 1;
         int32_t a32 = acc[r];
         if constexpr (WBITS == 4) a32 >>= 4;  // exact: the sum is a multiple of 16
-        const ColParams cp = derive_col_params(p.a_scale, p.w_scale[n], p.out_scale,
-                                               p.bias ? p.bias + n : nullptr, p.colsum[n], p.a_zp);
-        out[r] = requant_out(a32, cp, p.out_zp, qmin, qmax);
+        out[r] = requant_out(a32, cps[r], p.out_zp, qmin, qmax);
     }
     const int64_t nb = n0 + 4 * kg;
     const int64_t base = m * p.N + nb;
@@ -128,24 +184,36 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     }
 }
 
+template <int WBITS, int OBITS, int R>
+hipError_t launch_r(const QLinearArgs& p, hipStream_t s)
+{
+    const int64_t blocks = (p.N + R - 1) / R;
+    const int64_t steps = (p.K + 63) / 64;
+    // Waves per block: enough that one 8-step load round covers each wave's
+    // share of K (every weight byte of the block is requested at once), at
+    // least 4 when there are few channel groups so more loads are in flight.
+    int nw = 1;
+    while (nw < 16 && nw * 8 < steps) nw *= 2;
+    if (blocks < 2048) {
+        while (nw < 4 && nw < steps) nw *= 2;
+    }
+    const dim3 g((unsigned)blocks);
+    switch (nw) {
+    case 16: qlinear_decode_kernel<WBITS, OBITS, 16, R><<<g, 16 * 64, 0, s>>>(p); break;
+    case 8: qlinear_decode_kernel<WBITS, OBITS, 8, R><<<g, 8 * 64, 0, s>>>(p); break;
+    case 4: qlinear_decode_kernel<WBITS, OBITS, 4, R><<<g, 4 * 64, 0, s>>>(p); break;
+    case 2: qlinear_decode_kernel<WBITS, OBITS, 2, R><<<g, 2 * 64, 0, s>>>(p); break;
+    default: qlinear_decode_kernel<WBITS, OBITS, 1, R><<<g, 64, 0, s>>>(p); break;
+    }
+    return hipGetLastError();
+}
+
 template <int WBITS, int OBITS>
 hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 {
-    const int64_t blocks = (p.N + 15) / 16;
-    const int64_t steps = (p.K + 63) / 64;
-    // enough waves in flight to cover HBM latency: split K further when there
-    // are few channel groups
-    int nw = blocks >= 2048 ? 4 : (blocks >= 256 ? 8 : 16);
-    while (nw > 1 && steps < nw) nw /= 2;
-    const dim3 g((unsigned)blocks);
-    switch (nw) {
-    case 16: qlinear_decode_kernel<WBITS, OBITS, 16><<<g, 16 * 64, 0, s>>>(p); break;
-    case 8: qlinear_decode_kernel<WBITS, OBITS, 8><<<g, 8 * 64, 0, s>>>(p); break;
-    case 4: qlinear_decode_kernel<WBITS, OBITS, 4><<<g, 4 * 64, 0, s>>>(p); break;
-    case 2: qlinear_decode_kernel<WBITS, OBITS, 2><<<g, 2 * 64, 0, s>>>(p); break;
-    default: qlinear_decode_kernel<WBITS, OBITS, 1><<<g, 64, 0, s>>>(p); break;
-    }
-    return hipGetLastError();
+    // narrow layers: 8 channels per block so at least 256 blocks stream
+    if ((p.N + 15) / 16 < 256) return launch_r<WBITS, OBITS, 8>(p, s);
+    return launch_r<WBITS, OBITS, 16>(p, s);
 }
 
 }  // namespace

@@ -88,6 +88,20 @@ def test_decode_prefill_generic_agree(w_bits, out_bits, M):
     assert np.array_equal(outs[0], oracle_layer(ld).y_q)
 
 
+@pytest.mark.parametrize("w_bits,out_bits", [(8, 8), (4, 16)])
+@pytest.mark.parametrize("M,K,N", [(1, 5632, 48), (16, 4096, 40), (3, 16384, 33), (2, 1088, 20)])
+def test_decode_multi_round_k(w_bits, out_bits, M, K, N):
+    """Decode waves that stream several load rounds each (long K, few
+    channel groups), against the generic path and the oracle."""
+    mq = _mq()
+    layer = wl.Layer("x", M, K, N, w_bits=w_bits, out_bits=out_bits)
+    ld = wl.make_layer("decode_rounds", layer)
+    d = gpu_layer(ld, path=mq.PATH_DECODE).y_q
+    g = gpu_layer(ld, path=mq.PATH_GENERIC).y_q
+    assert np.array_equal(g, oracle_layer(ld).y_q)
+    assert np.array_equal(d, g)
+
+
 @pytest.mark.parametrize("w_bits", [8, 4])
 def test_prefill_equals_generic_ragged(w_bits):
     mq = _mq()
