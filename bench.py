@@ -17,6 +17,8 @@ the CPU oracle's rate on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -32,6 +34,13 @@ METRIC = "qlinear int8 TOPS (prefill, % MFMA peak) + decode GB/s (% HBM peak), b
 PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
 DEFAULT_WORKLOAD = "prefill_w8a8_tinyllama_m2048"
+# HBM traffic of the dominant kernel, from two rocprofv3 --pmc passes
+# (FETCH_SIZE, WRITE_SIZE) summarised by --pmc-summary; valid only while the
+# kernel sources hash to the value recorded with it
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "qlinear_prefill_gate_up_tinyllama_m2048_hbm_traffic.txt")
+KERNEL_SOURCES = ("paper_2408_13933_amd/csrc/qlinear_prefill.hip",
+                  "paper_2408_13933_amd/csrc/requant.h",
+                  "paper_2408_13933_amd/csrc/mq_internal.h")
 
 
 def parse():
@@ -45,7 +54,76 @@ def parse():
                     help="also time the step replayed from a captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, stream this many MiB through a plain elementwise kernel "
+                         "three times (one read and one write of that size: the calibration "
+                         "kernel of the HBM byte counters)")
+    ap.add_argument("--decode-sweep", action="store_true",
+                    help="time the decode-shaped layers (M <= 16) cold: each launch reads a "
+                         "different copy of the weights, >= 512 MB per sweep; prints one JSON "
+                         "line per layer (run under rocprofv3 --kernel-trace for kernel-only "
+                         "durations) and exits")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE "
+                         "and WRITE_SIZE passes over a run with --calib-copy-mib) and exit")
     return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _pmc_rows(path, counter):
+    """(kernel name, grid size, value) per dispatch of one counter."""
+    out = []
+    with open(path, newline="") as f:
+        for row in csv.DictReader(f):
+            if row["Counter_Name"] == counter:
+                out.append((row["Kernel_Name"], int(row["Grid_Size"]), float(row["Counter_Value"])))
+    return out
+
+
+def pmc_summary(fetch_csv, write_csv, copy_mib):
+    """HBM bytes per launch of the dominant prefill kernel, each counter scaled
+    by what it reads for the plain copy of known size in the same run."""
+    from paper_2408_13933_amd import workloads as wl
+
+    L = wl.WORKLOADS[DEFAULT_WORKLOAD].layers[0]
+    grid = ((L.M + 255) // 256) * ((L.N + 255) // 256) * 256  # 256x256 tiles, 256 threads
+    res = {}
+    for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        rows = _pmc_rows(path, counter)
+        k = [v for n, g, v in rows if "qlinear_prefill_kernel" in n and g == grid]
+        c = [v for n, g, v in rows if "bitwise_not" in n]
+        copy_kib = copy_mib * 1024.0  # the copy reads and writes copy_mib each
+        if not k or not c:
+            raise SystemExit(f"{counter}: kernel dispatches {len(k)}, copy dispatches {len(c)}")
+        kib = sum(k) / len(k)
+        factor = copy_kib / (sum(c) / len(c))
+        res[key] = {"kib_per_launch": kib, "launches": len(k), "copy_kib": sum(c) / len(c),
+                    "factor": factor, "bytes_per_launch": kib * 1024.0 * factor}
+    total = res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"]
+    return {"kernel": f"qlinear_prefill {L.name} M={L.M} K={L.K} N={L.N} w{L.w_bits}/o{L.out_bits}",
+            "grid": grid, "source_hash": kernel_source_hash(), "copy_mib": copy_mib,
+            "fetch": res["fetch"], "write": res["write"], "hbm_bytes_per_launch": total,
+            "alg_bytes_per_launch": L.alg_bytes()}
+
+
+def read_traffic():
+    """Calibrated HBM bytes per launch, or None when absent or stale."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            line = [l for l in f if l.startswith("{")][-1]
+        rec = json.loads(line)
+    except (OSError, IndexError, ValueError):
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec
 
 
 class Prepared:
@@ -156,8 +234,95 @@ def cpu_baseline(prep: Prepared, target_s: float):
                       f"threads"}
 
 
+DECODE_LAYERS = (("decode_w8a8_m16", "linear"), ("w4a8_down_tinyllama", "down_proj_m1"),
+                 ("gemma2b_w8a8", "lm_head_m1"))
+
+
+def decode_sweep(launches_per_layer=400):
+    """Cold decode launches.  Weight codes are random (the kernel's time does
+    not depend on their values); shapes, formats and bias follow the
+    workload's layer.  Two timings per layer: HIP events around the launch
+    loop (bounded below by host launch overhead for kernels of a few us) and
+    one captured sweep replayed as a HIP graph."""
+    import torch
+
+    import paper_2408_13933_amd as mq
+    from paper_2408_13933_amd import workloads as wl
+
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    for wname, lname in DECODE_LAYERS:
+        L = next(l for l in wl.WORKLOADS[wname].layers if l.name == lname)
+        kb = L.K * L.w_bits // 8
+        wbytes = L.N * kb
+        copies = max(2, -(-512 * 10**6 // wbytes))
+        ws = [torch.randint(0, 256, (L.N, kb), dtype=torch.uint8, device=dev, generator=g)
+              for _ in range(copies)]
+        if L.w_bits == 8:
+            ws = [w.view(torch.int8) for w in ws]
+        scale = torch.rand(L.N, device=dev, generator=g) * 1e-3 + 1e-4
+        cs = torch.randint(-50000, 50000, (L.N,), dtype=torch.int32, device=dev, generator=g)
+        bias = torch.randn(L.N, device=dev, generator=g) * 0.01 if L.bias else None
+        a = torch.randint(-128, 128, (L.M, L.K), dtype=torch.int8, device=dev, generator=g)
+        y = torch.empty((L.M, L.N), dtype=torch.int8 if L.out_bits == 8 else torch.int16,
+                        device=dev)
+
+        def launch(w):
+            mq.mq_qlinear(a, w, L.w_bits, scale, cs, 0.05, 3, 0.02, -2, L.out_bits, bias=bias,
+                          out=y)
+
+        for w in ws:
+            launch(w)
+        torch.cuda.synchronize()
+        reps = max(1, launches_per_layer // copies)
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for _ in range(reps):
+            for w in ws:
+                launch(w)
+        s1.record()
+        torch.cuda.synchronize()
+        event_us = s0.elapsed_time(s1) * 1e3 / (reps * copies)
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(graph, stream=cap):
+                for w in ws:
+                    launch(w)
+        torch.cuda.current_stream().wait_stream(cap)
+        graph.replay()
+        torch.cuda.synchronize()
+        s0.record()
+        for _ in range(reps):
+            graph.replay()
+        s1.record()
+        torch.cuda.synchronize()
+        graph_us = s0.elapsed_time(s1) * 1e3 / (reps * copies)
+        alg = L.alg_bytes()
+        print(json.dumps({"layer": f"{wname}/{lname}", "M": L.M, "K": L.K, "N": L.N,
+                          "w_bits": L.w_bits, "out_bits": L.out_bits, "weight_copies": copies,
+                          "launches": 2 * reps * copies + copies, "alg_bytes": alg,
+                          "event_us_per_launch": event_us, "graph_us_per_launch": graph_us,
+                          "graph_GBps": alg / (graph_us * 1e-6) / 1e9,
+                          "graph_frac_hbm": alg / (graph_us * 1e-6) / 1e9 / PEAK_HBM_GBS}),
+              flush=True)
+        del ws, graph
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
+    if args.decode_sweep:
+        decode_sweep()
+        return
+    if args.pmc_summary:
+        if args.calib_copy_mib <= 0:
+            raise SystemExit("--pmc-summary needs the --calib-copy-mib size of the profiled run")
+        print(json.dumps(pmc_summary(args.pmc_summary[0], args.pmc_summary[1],
+                                     args.calib_copy_mib)))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))
         sys.exit(2)
@@ -213,6 +378,15 @@ def main():
         ge.record()
         torch.cuda.synchronize()
         graph_ms = gs.elapsed_time(ge) / args.steps
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20)
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.bitwise_not(src, out=dst)  # one streaming read and write of n bytes
+        torch.cuda.synchronize()
+        del src, dst
+
     L = layers[dom[0]]
     if L.M <= 16:
         achieved = L.alg_bytes() / (k_avg_ms * 1e-3) / 1e9
@@ -222,6 +396,13 @@ def main():
         achieved = L.ops / (k_avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                 "frac": achieved / PEAK_INT8_TOPS, "traffic": None}
+        tr = read_traffic() if args.workload == DEFAULT_WORKLOAD else None
+        if tr is not None:
+            roof["traffic"] = tr["hbm_bytes_per_launch"]
+            roof["traffic_detail"] = {"unit": "bytes per launch",
+                                      "fetch": tr["fetch"]["bytes_per_launch"],
+                                      "write": tr["write"]["bytes_per_launch"],
+                                      "algorithmic": tr["alg_bytes_per_launch"]}
     roof.update({"kernel": f"qlinear_prefill {L.name} M={L.M} K={L.K} N={L.N} "
                            f"w{L.w_bits}/o{L.out_bits}" if L.M > 16 else
                            f"qlinear_decode {L.name} M={L.M} K={L.K} N={L.N}",
