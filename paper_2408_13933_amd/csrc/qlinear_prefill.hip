@@ -65,7 +65,7 @@ __device__ inline void wait_vmcnt()
 }
 
 template <int WBITS_, int OBITS_, int TM_, int TN_, int WM_, int WN_, int BK_, int STAGES_,
-          int SWZ_>
+          int SWZ_, int SPREAD_>
 struct Cfg {
     static constexpr int WBITS = WBITS_, OBITS = OBITS_;
     static constexpr int TM = TM_, TN = TN_, WM = WM_, WN = WN_, BK = BK_;
@@ -82,6 +82,20 @@ struct Cfg {
     static constexpr int A_PER_WAVE = (A_WLOADS + NWAVES - 1) / NWAVES;
     static constexpr int W_PER_WAVE = (W_WLOADS + NWAVES - 1) / NWAVES;
     static constexpr int LOADS = A_PER_WAVE + W_PER_WAVE;  // per thread per stage
+    static constexpr int KS = BK / 32;                       // 32-deep steps per stage
+    static constexpr int NRD = FN + FM;                      // fragment reads per step
+    // DMA of a stage spread over the groups of SPREAD steps after its switch
+    static constexpr int SPREAD = SPREAD_;
+    // group slot of DMA d of a stage among the SPREAD*NRD groups after its switch
+    static constexpr int dma_slot(int d) { return d * SPREAD * NRD / LOADS; }
+    // DMAs issued in the stage switch step itself
+    static constexpr int nsw()
+    {
+        int n = 0;
+        for (int d = 0; d < LOADS; ++d) n += dma_slot(d) < NRD ? 1 : 0;
+        return n;
+    }
+    static constexpr int NSW = nsw();
     static constexpr int A_BYTES = A_PER_WAVE * NWAVES * 1024;
     static constexpr int W_BYTES = W_PER_WAVE * NWAVES * 1024;
     static constexpr int STAGE = A_BYTES + W_BYTES;
@@ -93,6 +107,7 @@ struct Cfg {
     static_assert(STAGES >= 2 && STAGES <= 4, "pipeline depth");
     static_assert((BK / 32) % 2 == 0, "even number of 32-deep steps per stage");
     static_assert(LOADS * (STAGES - 1) < 64, "vmcnt range");
+    static_assert(SPREAD >= 1 && SPREAD <= KS, "the DMA spread stays within one stage");
     static_assert(LDS <= 160 * 1024, "LDS per CU");
 };
 
@@ -351,23 +366,25 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // of loads; a stage past the end (or a chunk past K) reads out of range,
     // which writes zeros and touches no memory, so the vector-memory counter
     // advances identically every step.
-    auto issue = [&](int kt, int buf) {
+    auto issue_one = [&](int kt, int buf, int idx) {  // idx < LOADS, compile-time
         MQ_LDS int8_t* base = (MQ_LDS int8_t*)smem + buf * C::STAGE;
-        const int k0 = kt * C::BK, k0w = kt * C::BKW;
-#pragma unroll
-        for (int i = 0; i < C::A_PER_WAVE; ++i) {
+        if (idx < C::A_PER_WAVE) {
+            const int i = idx, k0 = kt * C::BK;
             const int wl = wave + i * C::NWAVES;
             const uint32_t voff = (k0 + a_kb(i) < (int)K) ? a_off[i] + (uint32_t)k0 : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (MQ_LDS void*)(base + wl * 1024), 16,
                                                      voff, 0, 0, 0);
-        }
-#pragma unroll
-        for (int i = 0; i < C::W_PER_WAVE; ++i) {
+        } else {
+            const int i = idx - C::A_PER_WAVE, k0w = kt * C::BKW;
             const int wl = wave + i * C::NWAVES;
             const uint32_t voff = (k0w + w_kb(i) < (int)wrow) ? w_off[i] + (uint32_t)k0w : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rw, (MQ_LDS void*)(base + C::A_BYTES + wl * 1024), 16, voff, 0, 0, 0);
         }
+    };
+    auto issue = [&](int kt, int buf) {
+#pragma unroll
+        for (int idx = 0; idx < C::LOADS; ++idx) issue_one(kt, buf, idx);
     };
 
     // ---- per-column inputs first: the vector-memory counter retires in
@@ -419,10 +436,14 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     const bool all_pre0 = (flags & 1) != 0;
     const bool zp_fold = (flags & 2) != 0;
     if (zp_fold && tid < C::TN) e_rnd[tid] += p.out_zp * (1 << (e_sp[tid] & 0xFF));
-    issue(C::STAGES - 1, C::STAGES - 1);
-    // stage 0 is complete when only the STAGES-1 stages behind it are in
+    // stage STAGES-1: the part the stage switch step would issue; the rest
+    // goes out during the first stage's steps, as for every later stage
+#pragma unroll
+    for (int d = 0; d < C::LOADS; ++d)
+        if (C::dma_slot(d) < C::NRD) issue_one(C::STAGES - 1, C::STAGES - 1, d);
+    // stage 0 is complete when only the loads issued after it are in
     // flight, in every wave
-    wait_vmcnt<(C::STAGES - 1) * C::LOADS>();
+    wait_vmcnt<(C::STAGES - 2) * C::LOADS + C::NSW>();
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
     __builtin_amdgcn_s_barrier();
 
@@ -439,17 +460,16 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
 
-    auto load_frags = [&](int buf, int ks, v4i* wf, v4i* af) {
+    // fragment g of a 32-deep step: g < FM activation rows, then weight rows
+    auto load_frag = [&](int buf, int ks, int g, v4i* wf, v4i* af) {
         const int8_t* sa = smem + buf * C::STAGE;
         const int8_t* sw = sa + C::A_BYTES;
-#pragma unroll
-        for (int j = 0; j < C::FM; ++j) {
-            const int row = wm * (C::TM / C::WM) + j * 32 + r32;
+        if (g < C::FM) {
+            const int row = wm * (C::TM / C::WM) + g * 32 + r32;
             const int phys = (ks * 2 + hk) ^ swz<C::SWZ>(row, C::CA);
-            af[j] = *reinterpret_cast<const v4i*>(sa + row * C::BK + phys * 16);
-        }
-#pragma unroll
-        for (int i = 0; i < C::FN; ++i) {
+            af[g] = *reinterpret_cast<const v4i*>(sa + row * C::BK + phys * 16);
+        } else {
+            const int i = g - C::FM;
             const int row = wn * (C::TN / C::WN) + i * 32 + r32;
             if constexpr (C::WBITS == 8) {
                 const int phys = (ks * 2 + hk) ^ swz<C::SWZ>(row, C::CW);
@@ -464,44 +484,46 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
             }
         }
     };
-    auto mfma_rows = [&](const v4i* wf, const v4i* af, int i0, int i1) {
+    // MFMA t of a step: channel fragment t / FM, token fragment t % FM
+    auto mfma_range = [&](const v4i* wf, const v4i* af, int t0, int t1) {
 #pragma unroll
-        for (int i = i0; i < i1; ++i)
-#pragma unroll
-            for (int j = 0; j < C::FM; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
+        for (int t = t0; t < t1; ++t) {
+            const int i = t / C::FM, j = t % C::FM;
+            acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
+        }
     };
 
-    // Instruction interleave (sched_group_barrier masks: 0x008 MFMA, 0x100
-    // LDS read, 0x020 global/buffer load).  Spreading the next step's LDS
-    // reads between this step's MFMAs keeps both pipes busy: measured on
-    // MI355X, one wave per SIMD reaches ~83% of the int8 MFMA peak with one
-    // LDS read per two MFMAs, against ~60-77% with the reads bunched.
-    constexpr int NRD = C::FN + C::FM;         // LDS fragment reads per step
-    constexpr int NMF = C::FN * C::FM;         // MFMAs per step
-    auto interleave_step = [&]() {
+    // One 32-deep step in NRD groups, each: one LDS read of the next step's
+    // fragments, this step's share of MFMAs, and (at a stage switch) one DMA
+    // of a later stage.  sched_barrier fences keep the groups in this order:
+    // a wave stalled on a full load queue (DMA issue) or on an LDS read
+    // would otherwise stop feeding its MFMA pipe for the whole bunch.
+    // Measured on MI355X: one wave per SIMD reaches ~83% of the int8 MFMA
+    // peak with one LDS read per two MFMAs, against ~60-77% with the reads
+    // bunched.
+    // The DMA of a stage is spread evenly over the KS*NRD groups that follow
+    // the barrier which frees its buffer: the stage switch step (slots
+    // 0..NRD-1) and the first KS-1 steps of the next stage.
+    constexpr int NRD = C::FN + C::FM;  // LDS fragment reads per step
+    constexpr int NMF = C::FN * C::FM;  // MFMAs per step
+    auto step = [&](const v4i* wc, const v4i* ac, bool read, int rbuf, int rks, v4i* wx,
+                    v4i* ax, bool dma, int dkt, int dbuf, int slot_step) {
 #pragma unroll
-        for (int r = 0; r < NRD; ++r) {
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, NMF / NRD, 0);
-        }
-        if constexpr (NMF % NRD != 0) __builtin_amdgcn_sched_group_barrier(0x008, NMF % NRD, 0);
-    };
-    auto interleave_switch = [&]() {
-        // the step after a stage switch: next-stage reads, this step's
-        // MFMAs and the DMA of a later stage, evenly mixed
+        for (int g = 0; g < NRD; ++g) {
+            if (read) load_frag(rbuf, rks, g, wx, ax);
+            mfma_range(wc, ac, g * NMF / NRD, (g + 1) * NMF / NRD);
+            if (dma) {
 #pragma unroll
-        for (int r = 0; r < NRD; ++r) {
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, NMF / NRD, 0);
-            if (r < C::LOADS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                for (int d = 0; d < C::LOADS; ++d)
+                    if (C::dma_slot(d) == slot_step * NRD + g) issue_one(dkt, dbuf, d);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
-        if constexpr (NMF % NRD != 0) __builtin_amdgcn_sched_group_barrier(0x008, NMF % NRD, 0);
-        if constexpr (C::LOADS > NRD) __builtin_amdgcn_sched_group_barrier(0x020, C::LOADS - NRD, 0);
     };
 
     v4i wf0[C::FN], af0[C::FM], wf1[C::FN], af1[C::FM];
-    load_frags(0, 0, wf0, af0);
+#pragma unroll
+    for (int g = 0; g < NRD; ++g) load_frag(0, 0, g, wf0, af0);
     for (int kt = 0; kt < KT - 1; ++kt) {
         const int buf = kt % C::STAGES;
 #pragma unroll
@@ -511,9 +533,10 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
             v4i* wx = (ks & 1) ? wf0 : wf1;
             v4i* ax = (ks & 1) ? af0 : af1;
             if (ks + 1 < KS) {
-                load_frags(buf, ks + 1, wx, ax);
-                mfma_rows(wc, ac, 0, C::FN);
-                interleave_step();
+                // the rest of the DMA of stage kt+STAGES-1 (its buffer was
+                // freed by the previous stage switch)
+                step(wc, ac, true, buf, ks + 1, wx, ax, true, kt + C::STAGES - 1,
+                     (kt + C::STAGES - 1) % C::STAGES, ks + 1);
             } else {
                 // Stage switch at the start of the stage's last step: this
                 // step's fragments are already in registers, so buffer `buf`
@@ -526,10 +549,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
                 __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
                 __builtin_amdgcn_s_barrier();
                 __builtin_amdgcn_sched_barrier(0);
-                load_frags((kt + 1) % C::STAGES, 0, wx, ax);
-                mfma_rows(wc, ac, 0, C::FN);
-                issue(kt + C::STAGES, buf);
-                interleave_switch();
+                step(wc, ac, true, (kt + 1) % C::STAGES, 0, wx, ax, true, kt + C::STAGES, buf, 0);
             }
         }
     }
@@ -541,13 +561,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
             v4i* ac = (ks & 1) ? af1 : af0;
             v4i* wx = (ks & 1) ? wf0 : wf1;
             v4i* ax = (ks & 1) ? af0 : af1;
-            if (ks + 1 < KS) {
-                load_frags(buf, ks + 1, wx, ax);
-                mfma_rows(wc, ac, 0, C::FN);
-                interleave_step();
-            } else {
-                mfma_rows(wc, ac, 0, C::FN);
-            }
+            step(wc, ac, ks + 1 < KS, buf, ks + 1, wx, ax, false, 0, 0, 0);
         }
     }
 
@@ -600,10 +614,12 @@ hipError_t launch_cfg(const QLinearArgs& p, hipStream_t s)
 }
 
 // Tile shapes, largest first.  (tokens x channels, wave grid, K bytes per
-// stage, stages, swizzle)
-template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2>;
-template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2>;
-template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2>;
+// stage, stages, swizzle, steps the DMA of a stage is spread over; measured:
+// the 256x256 K loop is fastest with all DMA in the switch step, the
+// 128-deep tiles with it spread over the whole stage)
+template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2, 1>;
+template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2, 4>;
+template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
 
 struct TileChoice {
     int tm, tn;
