@@ -192,7 +192,8 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int nl = x.col0 + i * 32 + 8 * g;  // tile-local channel
-            const v4i off = *reinterpret_cast<const v4i*>(x.e_off + nl);
+            v4i off = {0, 0, 0, 0};
+            if constexpr (!FAST) off = *reinterpret_cast<const v4i*>(x.e_off + nl);
             const v4i m0 = *reinterpret_cast<const v4i*>(x.e_m0 + nl);
             const v4i rnd = *reinterpret_cast<const v4i*>(x.e_rnd + nl);
             const v4i sp = *reinterpret_cast<const v4i*>(x.e_sp + nl);
@@ -212,8 +213,9 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
                 for (int r = 0; r < 4; ++r) {
                     int32_t a32 = acc[i][j][4 * g + r];
                     if constexpr (C::WBITS == 4) a32 >>= 4;  // exact: a multiple of 16
-                    int32_t c = __builtin_elementwise_add_sat(a32, off[r]);
+                    int32_t c = a32;  // fast form: off is already in the accumulator
                     if constexpr (!FAST) {
+                        c = __builtin_elementwise_add_sat(a32, off[r]);
                         c = max(min(c, bnd[r]), -bnd[r]);
                         c = (int32_t)((uint32_t)c << pre[r]);
                     }
@@ -404,7 +406,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // keep every use of the loaded values behind the DMA issue
     asm volatile("" : "+v"(col_ws), "+v"(col_cs), "+v"(col_bias));
 
-    int col_pre0 = 1, col_fold = 1;
+    int col_pre0 = 1, col_fold = 1, col_offin = 1;
     if (tid < C::TN) {
         const ColParams cp = derive_col_params_v(p.a_scale, col_ws, p.out_scale, p.bias != nullptr,
                                                  col_bias, col_cs, p.a_zp);
@@ -418,6 +420,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         // at most 2^30 (then mul_hi + it cannot overflow int32)
         const int64_t zabs = p.out_zp < 0 ? -(int64_t)p.out_zp : (int64_t)p.out_zp;
         col_fold = (int64_t)ei.rnd + (zabs << ei.shr) <= ((int64_t)1 << 30);
+        // off can start the accumulator (scaled by 16 for int4 weights)
+        // when no partial sum can leave int32: |acc| <= K * 128 * 127 <
+        // K * 2^14, so the saturating add of the epilogue never saturates
+        const int64_t offa = (cp.off < 0 ? -(int64_t)cp.off : (int64_t)cp.off) *
+                             (C::WBITS == 4 ? 16 : 1);
+        col_offin = offa + (K << 14) < ((int64_t)1 << 31);
     }
     // Whole-tile epilogue form: AND of the column flags over the block, by
     // ballot per wave and one LDS word per wave.  A raw barrier, since
@@ -425,16 +433,19 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     {
         const bool w_pre0 = __ballot(col_pre0) == ~0ull;
         const bool w_fold = __ballot(col_fold) == ~0ull;
-        if (lane == 0) e_flag[wave] = (w_pre0 ? 1 : 0) | (w_fold ? 2 : 0);
+        const bool w_offin = __ballot(col_offin) == ~0ull;
+        if (lane == 0) e_flag[wave] = (w_pre0 ? 1 : 0) | (w_fold ? 2 : 0) | (w_offin ? 4 : 0);
     }
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));  // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
-    int flags = 3;
+    int flags = 7;
 #pragma unroll
     for (int w = 0; w < C::NWAVES; ++w) flags &= e_flag[w];
     flags = __builtin_amdgcn_readfirstlane(flags);
-    const bool all_pre0 = (flags & 1) != 0;
     const bool zp_fold = (flags & 2) != 0;
+    // the fast epilogue form: one mul_hi per output, zero-point in the
+    // rounding constant, off in the accumulator's start value
+    const bool fast = (flags == 7) && (p.N % 4) == 0;
     if (zp_fold && tid < C::TN) e_rnd[tid] += p.out_zp * (1 << (e_sp[tid] & 0xFF));
     // stage STAGES-1: the part the stage switch step would issue; the rest
     // goes out during the first stage's steps, as for every later stage
@@ -452,13 +463,24 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // the stage switch (wait, barrier, next DMA, first fragments of the next
     // stage) sits between the two halves of the step's MFMAs.  The steady
     // state has no branches, so every wait count is a compile-time constant.
+    // Accumulator layout: lane holds channels col0 + 32i + 8g + 4hk + r
+    // (register 4g + r) of tokens 32j + r32.  In the fast form each starts
+    // at its channel's off.
     v16i acc[C::FN][C::FM];
+    const int col0 = wn * (C::TN / C::WN) + 4 * hk;
 #pragma unroll
-    for (int i = 0; i < C::FN; ++i)
+    for (int i = 0; i < C::FN; ++i) {
+        v16i start;
 #pragma unroll
-        for (int j = 0; j < C::FM; ++j)
+        for (int g = 0; g < 4; ++g) {
+            v4i o = *reinterpret_cast<const v4i*>(e_off + col0 + i * 32 + 8 * g);
+            if constexpr (C::WBITS == 4) o *= 16;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+            for (int r = 0; r < 4; ++r) start[4 * g + r] = fast ? o[r] : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < C::FM; ++j) acc[i][j] = start;
+    }
 
     // fragment g of a 32-deep step: g < FM activation rows, then weight rows
     auto load_frag = [&](int buf, int ks, int g, v4i* wf, v4i* af) {
@@ -587,7 +609,6 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     ctx.ry = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(static_cast<int8_t*>(p.y) + m_tile * (int64_t)ctx.row_bytes), (short)0,
         (int)(rows_a * ctx.row_bytes), 0x00020000);
-    const bool fast = all_pre0 && zp_fold && (p.N % 4) == 0;
     // staged stores need the tile's channels inside N and 16-byte row chunks
     const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
                         ((uintptr_t)p.y % 16) == 0;
