@@ -2,8 +2,9 @@
 // activation quantizer (Section 4.2, Eq.(4)), its inverse, the fold of the
 // smoothing vector (Section 3.2, Eq.(1)) and the per-channel weight packer.
 //
-// All of them stream HBM: 16-byte vector loads, grid-stride loops sized to
-// the 256 CUs, and scalar code only for ragged tails and unaligned buffers.
+// All of them stream HBM: 16-byte vector loads on consecutive lanes,
+// grid-stride loops sized to the 256 CUs, and scalar code only for ragged
+// tails and unaligned buffers.
 // Floating point is IEEE: correctly rounded fp32 division, rint = round
 // half to even, no contraction.
 #include "mq_internal.h"
@@ -36,36 +37,81 @@ __device__ inline int32_t quant1(float x, float alpha, int32_t zp)
     return v < qmin ? qmin : (v > qmax ? qmax : v);
 }
 
-// 8 elements per thread per step: two float4 loads, one 8- or 16-byte store.
+// x / alpha as far as rint() can tell.  The product with the rounded
+// reciprocal is within 2.5 ulp of the quotient (reciprocal error 0.5 ulp,
+// product rounding 0.5 ulp, quotient rounding 0.5 ulp, relative to |t|), so
+// where it lies more than 4 ulp (|t| * 2^-21) from every half-integer,
+// rounding it to an integer gives the same result as rounding the correctly
+// rounded quotient.  Other lanes (and NaN, infinities, |t| >= 2^20) take
+// the correctly rounded division, behind a wave-uniform branch so the
+// division is not evaluated speculatively on every lane.
+__device__ inline bool product_decides_rint(float t)
+{
+#pragma clang fp contract(off)
+    const float d = fabsf(t - rintf(t));  // exact for |t| < 2^23
+    return fabsf(0.5f - d) > fabsf(t) * 0x1p-21f;
+}
+
+template <int BITS>
+__device__ inline int32_t code_from_quotient(float t, int32_t zp)
+{
+    constexpr int32_t qmin = -(1 << (BITS - 1));
+    constexpr int32_t qmax = (1 << (BITS - 1)) - 1;
+    t = fminf(fmaxf(t, -1048576.0f), 1048576.0f);
+    int32_t v = (int32_t)rintf(t) + zp;
+    return v < qmin ? qmin : (v > qmax ? qmax : v);
+}
+
+// One float4 -> 4 codes per thread and step, lanes on consecutive float4s
+// (every load and store instruction covers a contiguous span); two steps
+// per loop trip keep two loads in flight.
+template <int BITS>
+__device__ inline void quant_store4(const float4 a, float alpha, float inv, int32_t zp, void* q,
+                                    int64_t i)
+{
+#pragma clang fp contract(off)
+    const float xs[4] = {a.x, a.y, a.z, a.w};
+    float t[4];
+    bool ok = true;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        t[k] = xs[k] * inv;
+        ok = ok && product_decides_rint(t[k]);
+    }
+    if (__builtin_expect(__ballot(!ok) != 0, 0)) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (!product_decides_rint(xs[k] * inv)) t[k] = xs[k] / alpha;
+    }
+    const int32_t v0 = code_from_quotient<BITS>(t[0], zp);
+    const int32_t v1 = code_from_quotient<BITS>(t[1], zp);
+    const int32_t v2 = code_from_quotient<BITS>(t[2], zp);
+    const int32_t v3 = code_from_quotient<BITS>(t[3], zp);
+    if constexpr (BITS == 8) {
+        reinterpret_cast<uint32_t*>(q)[i] = ((uint32_t)v0 & 0xFFu) | (((uint32_t)v1 & 0xFFu) << 8) |
+                                            (((uint32_t)v2 & 0xFFu) << 16) | ((uint32_t)v3 << 24);
+    } else {
+        reinterpret_cast<uint2*>(q)[i] =
+            make_uint2(((uint32_t)v0 & 0xFFFFu) | ((uint32_t)v1 << 16),
+                       ((uint32_t)v2 & 0xFFFFu) | ((uint32_t)v3 << 16));
+    }
+}
+
 template <int BITS>
 __global__ __launch_bounds__(kThreads) void quantize_act_vec(const float4* __restrict__ x,
-                                                             int64_t groups, float alpha,
-                                                             int32_t zp, void* __restrict__ q)
+                                                             int64_t n4, float alpha,
+                                                             float inv_alpha, int32_t zp,
+                                                             void* __restrict__ q)
 {
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < groups; g += stride) {
-        const float4 a = x[2 * g];
-        const float4 b = x[2 * g + 1];
-        int32_t v[8] = {quant1<BITS>(a.x, alpha, zp), quant1<BITS>(a.y, alpha, zp),
-                        quant1<BITS>(a.z, alpha, zp), quant1<BITS>(a.w, alpha, zp),
-                        quant1<BITS>(b.x, alpha, zp), quant1<BITS>(b.y, alpha, zp),
-                        quant1<BITS>(b.z, alpha, zp), quant1<BITS>(b.w, alpha, zp)};
-        if constexpr (BITS == 8) {
-            uint32_t lo = 0, hi = 0;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                lo |= ((uint32_t)v[i] & 0xFFu) << (8 * i);
-                hi |= ((uint32_t)v[4 + i] & 0xFFu) << (8 * i);
-            }
-            reinterpret_cast<uint2*>(q)[g] = make_uint2(lo, hi);
-        } else {
-            uint32_t w[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                w[i] = ((uint32_t)v[2 * i] & 0xFFFFu) | (((uint32_t)v[2 * i + 1] & 0xFFFFu) << 16);
-            reinterpret_cast<uint4*>(q)[g] = make_uint4(w[0], w[1], w[2], w[3]);
-        }
+    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    for (; i + stride < n4; i += 2 * stride) {
+        const float4 a = x[i];
+        const float4 b = x[i + stride];
+        quant_store4<BITS>(a, alpha, inv_alpha, zp, q, i);
+        quant_store4<BITS>(b, alpha, inv_alpha, zp, q, i + stride);
     }
+    if (i < n4) quant_store4<BITS>(x[i], alpha, inv_alpha, zp, q, i);
 }
 
 template <int BITS>
@@ -92,34 +138,38 @@ __device__ inline float deq1(int32_t q, float alpha, int32_t zp)
 }
 
 template <int BITS>
-__global__ __launch_bounds__(kThreads) void dequant_vec(const void* __restrict__ q, int64_t groups,
+__device__ inline void deq_store4(const void* __restrict__ q, float alpha, int32_t zp,
+                                  float4* __restrict__ y, int64_t i)
+{
+    int32_t v[4];
+    if constexpr (BITS == 8) {
+        const uint32_t p = reinterpret_cast<const uint32_t*>(q)[i];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = (int32_t)(int8_t)(p >> (8 * k));
+    } else {
+        const uint2 p = reinterpret_cast<const uint2*>(q)[i];
+        v[0] = (int32_t)(int16_t)(p.x & 0xFFFFu);
+        v[1] = (int32_t)(int16_t)(p.x >> 16);
+        v[2] = (int32_t)(int16_t)(p.y & 0xFFFFu);
+        v[3] = (int32_t)(int16_t)(p.y >> 16);
+    }
+    y[i] = make_float4(deq1<BITS>(v[0], alpha, zp), deq1<BITS>(v[1], alpha, zp),
+                       deq1<BITS>(v[2], alpha, zp), deq1<BITS>(v[3], alpha, zp));
+}
+
+// 4 codes -> one float4 per thread and step, lanes on consecutive groups
+template <int BITS>
+__global__ __launch_bounds__(kThreads) void dequant_vec(const void* __restrict__ q, int64_t n4,
                                                         float alpha, int32_t zp,
                                                         float4* __restrict__ y)
 {
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < groups; g += stride) {
-        int32_t v[8];
-        if constexpr (BITS == 8) {
-            const uint2 p = reinterpret_cast<const uint2*>(q)[g];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                v[i] = (int32_t)(int8_t)(p.x >> (8 * i));
-                v[4 + i] = (int32_t)(int8_t)(p.y >> (8 * i));
-            }
-        } else {
-            const uint4 p = reinterpret_cast<const uint4*>(q)[g];
-            const uint32_t w[4] = {p.x, p.y, p.z, p.w};
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                v[2 * i] = (int32_t)(int16_t)(w[i] & 0xFFFFu);
-                v[2 * i + 1] = (int32_t)(int16_t)(w[i] >> 16);
-            }
-        }
-        y[2 * g] = make_float4(deq1<BITS>(v[0], alpha, zp), deq1<BITS>(v[1], alpha, zp),
-                               deq1<BITS>(v[2], alpha, zp), deq1<BITS>(v[3], alpha, zp));
-        y[2 * g + 1] = make_float4(deq1<BITS>(v[4], alpha, zp), deq1<BITS>(v[5], alpha, zp),
-                                   deq1<BITS>(v[6], alpha, zp), deq1<BITS>(v[7], alpha, zp));
+    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    for (; i + stride < n4; i += 2 * stride) {
+        deq_store4<BITS>(q, alpha, zp, y, i);
+        deq_store4<BITS>(q, alpha, zp, y, i + stride);
     }
+    if (i < n4) deq_store4<BITS>(q, alpha, zp, y, i);
 }
 
 template <int BITS>
@@ -216,19 +266,23 @@ __global__ __launch_bounds__(kThreads) void pack_weights_kernel(const float* __r
 hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t zp, int32_t bits,
                                void* q, hipStream_t st)
 {
-    int64_t vec_groups = 0;
-    const uintptr_t qalign = bits == 8 ? 8 : 16;
-    if (aligned(x, 16) && aligned(q, qalign)) vec_groups = n / 8;
-    if (vec_groups > 0) {
-        const int g = grid_for(vec_groups, kThreads);
+    int64_t n4 = 0;
+    const uintptr_t qalign = bits == 8 ? 4 : 8;
+    if (aligned(x, 16) && aligned(q, qalign)) n4 = n / 4;
+    if (n4 > 0) {
+        const int g = grid_for(n4, 2 * kThreads);
+        // rounded reciprocal (see quotient_for_rint); for alpha >= 2^126 it
+        // would be subnormal and too coarse, and NaN sends every lane to the
+        // division
+        const float inv = alpha < 0x1p126f ? 1.0f / alpha : __builtin_nanf("");
         if (bits == 8)
-            quantize_act_vec<8><<<g, kThreads, 0, st>>>(reinterpret_cast<const float4*>(x),
-                                                        vec_groups, alpha, zp, q);
+            quantize_act_vec<8><<<g, kThreads, 0, st>>>(reinterpret_cast<const float4*>(x), n4,
+                                                        alpha, inv, zp, q);
         else
-            quantize_act_vec<16><<<g, kThreads, 0, st>>>(reinterpret_cast<const float4*>(x),
-                                                         vec_groups, alpha, zp, q);
+            quantize_act_vec<16><<<g, kThreads, 0, st>>>(reinterpret_cast<const float4*>(x), n4,
+                                                         alpha, inv, zp, q);
     }
-    const int64_t begin = vec_groups * 8;
+    const int64_t begin = n4 * 4;
     if (begin < n) {
         const int g = grid_for(n - begin, kThreads);
         if (bits == 8)
@@ -242,19 +296,17 @@ hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t z
 hipError_t launch_dequant(const void* q, int32_t bits, int64_t n, float alpha, int32_t zp,
                           float* y, hipStream_t st)
 {
-    int64_t vec_groups = 0;
-    const uintptr_t qalign = bits == 8 ? 8 : 16;
-    if (aligned(y, 16) && aligned(q, qalign)) vec_groups = n / 8;
-    if (vec_groups > 0) {
-        const int g = grid_for(vec_groups, kThreads);
+    int64_t n4 = 0;
+    const uintptr_t qalign = bits == 8 ? 4 : 8;
+    if (aligned(y, 16) && aligned(q, qalign)) n4 = n / 4;
+    if (n4 > 0) {
+        const int g = grid_for(n4, 2 * kThreads);
         if (bits == 8)
-            dequant_vec<8><<<g, kThreads, 0, st>>>(q, vec_groups, alpha, zp,
-                                                   reinterpret_cast<float4*>(y));
+            dequant_vec<8><<<g, kThreads, 0, st>>>(q, n4, alpha, zp, reinterpret_cast<float4*>(y));
         else
-            dequant_vec<16><<<g, kThreads, 0, st>>>(q, vec_groups, alpha, zp,
-                                                    reinterpret_cast<float4*>(y));
+            dequant_vec<16><<<g, kThreads, 0, st>>>(q, n4, alpha, zp, reinterpret_cast<float4*>(y));
     }
-    const int64_t begin = vec_groups * 8;
+    const int64_t begin = n4 * 4;
     if (begin < n) {
         const int g = grid_for(n - begin, kThreads);
         if (bits == 8)

@@ -272,6 +272,31 @@ def test_quantize_dequant_ragged(n, bits):
     assert np.array_equal(q2, q)
 
 
+@pytest.mark.parametrize("bits", [8, 16])
+@pytest.mark.parametrize("alpha", [0.1, 0.0373, 0.5, 3.0e-3, 1.7e-30, 2.5e37])
+def test_quantize_near_rounding_ties(bits, alpha):
+    """Inputs within a few ulp of (n + 1/2) * alpha, where the quotient's
+    rounding decides the code: every lane must match the correctly rounded
+    division, including the lanes that fall back to it, and an alpha whose
+    reciprocal would be subnormal."""
+    mq, torch = _mq(), _torch()
+    alpha = np.float32(alpha)
+    qmax = (1 << (bits - 1)) - 1
+    n = np.arange(-qmax - 3, qmax + 3, max(1, (2 * qmax) // 509), dtype=np.float64)
+    with np.errstate(over="ignore"):  # the largest alpha overflows to +-inf at the ends
+        centers = ((n + 0.5) * np.float64(alpha)).astype(np.float32)
+    xs = [centers]
+    for direction in (np.inf, -np.inf):
+        cur = centers
+        for _ in range(8):
+            cur = np.nextafter(cur, np.float32(direction))
+            xs.append(cur)
+    x = np.concatenate(xs).astype(np.float32)
+    zp = 3
+    got = mq.mq_quantize_act(torch.from_numpy(x).cuda(), float(alpha), zp, bits).cpu().numpy()
+    assert np.array_equal(got, oracle.quantize_act(x, float(alpha), zp, bits))
+
+
 def test_fold_acts_matches_oracle():
     mq, torch = _mq(), _torch()
     rng = np.random.default_rng(41)
