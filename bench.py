@@ -173,6 +173,14 @@ class Prepared:
         self.deq = torch.empty(last["y"].shape, dtype=torch.float32, device=dev)
         torch.cuda.synchronize()
 
+    def launch_layer(self, i):
+        """One qlinear launch of layer i on its already quantized input."""
+        e = self.layers[i]
+        L = e["layer"]
+        self.mq.mq_qlinear(self.inputs[e["key"]]["q"], e["w_q"], L.w_bits, e["w_scale"],
+                           e["w_colsum"], e["a_scale"], e["a_zp"], e["out_scale"], e["out_zp"],
+                           L.out_bits, bias=e["bias"], out=e["y"])
+
     def step(self, events=None, dom=()):
         """One pass of the hot path.  `events` = (start, end) recorded around
         the consecutive run of dominant-kernel launches listed in `dom`."""
@@ -357,6 +365,31 @@ def main():
     ms = start.elapsed_time(end) / args.steps
     k_avg_ms = float(np.mean([a.elapsed_time(b) for a, b in evs])) / len(dom)
 
+    # Cross-check of the dominant kernel's duration, outside the timed
+    # region: its launches replayed back to back from a HIP graph (no host
+    # launch gaps), the same steady state a kernel trace of this replay sees.
+    reps = 10
+    gk = torch.cuda.CUDAGraph()
+    s_k = torch.cuda.Stream()
+    s_k.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s_k):
+        with torch.cuda.graph(gk, stream=s_k):
+            for _ in range(reps):
+                for i in dom:
+                    prep.launch_layer(i)
+    torch.cuda.current_stream().wait_stream(s_k)
+    gk.replay()
+    torch.cuda.synchronize()
+    k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_replay = 5
+    k0.record()
+    for _ in range(n_replay):
+        gk.replay()
+    k1.record()
+    torch.cuda.synchronize()
+    k_graph_ms = k0.elapsed_time(k1) / (n_replay * reps * len(dom))
+    del gk
+
     graph_ms = None
     if args.graph:
         # the same step captured once into a HIP graph and replayed: no
@@ -406,7 +439,8 @@ def main():
     roof.update({"kernel": f"qlinear_prefill {L.name} M={L.M} K={L.K} N={L.N} "
                            f"w{L.w_bits}/o{L.out_bits}" if L.M > 16 else
                            f"qlinear_decode {L.name} M={L.M} K={L.K} N={L.N}",
-                 "kernel_us": k_avg_ms * 1e3})
+                 "kernel_us": k_avg_ms * 1e3,
+                 "kernel_us_graph_replay": k_graph_ms * 1e3})
 
     value = ops_step / (ms * 1e-3) / 1e12
     line = {

@@ -11,6 +11,7 @@ from __future__ import annotations
 import concurrent.futures as cf
 import glob
 import os
+import re
 import subprocess
 import sys
 
@@ -43,19 +44,43 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+# per-kernel resource report of the device pass; a kernel that spills
+# registers to scratch memory fails the build (a spill in the tiled GEMM
+# writes kilobytes per lane to HBM and hides behind an unchanged result)
+RESOURCE_REMARKS = "-Rpass-analysis=kernel-resource-usage"
+
+
+def _scratch_kernels(log: str) -> list[tuple[str, int]]:
+    bad, name = [], None
+    for line in log.splitlines():
+        m = re.search(r"remark: Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"remark:\s+ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            bad.append((name, int(m.group(1))))
+    return bad
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CXXFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CXXFLAGS, RESOURCE_REMARKS, "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
         raise RuntimeError(f"hipcc failed on {src}")
-    # the host pass does not know the packed-fp32 feature; that warning is noise
-    noise = "is not a recognized feature for this target"
-    rest = "\n".join(l for l in (r.stdout + r.stderr).splitlines() if noise not in l
-                     and "(ignoring feature)" not in l)
+    log = r.stdout + r.stderr
+    spills = _scratch_kernels(log)
+    if spills:
+        raise RuntimeError(f"{os.path.basename(src)}: kernels use scratch memory: {spills}")
+    # the host pass does not know the packed-fp32 feature; that warning is
+    # noise, and so are the resource remarks once checked
+    noise = ("is not a recognized feature for this target", "(ignoring feature)",
+             "kernel-resource-usage")
+    rest = "\n".join(l for l in log.splitlines() if not any(n in l for n in noise))
     if rest.strip() and verbose:
         sys.stderr.write(rest + "\n")
     return obj

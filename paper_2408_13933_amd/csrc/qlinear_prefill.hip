@@ -467,19 +467,25 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // (register 4g + r) of tokens 32j + r32.  In the fast form each starts
     // at its channel's off.
     v16i acc[C::FN][C::FM];
-    const int col0 = wn * (C::TN / C::WN) + 4 * hk;
 #pragma unroll
-    for (int i = 0; i < C::FN; ++i) {
-        v16i start;
+    for (int i = 0; i < C::FN; ++i)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            v4i o = *reinterpret_cast<const v4i*>(e_off + col0 + i * 32 + 8 * g);
-            if constexpr (C::WBITS == 4) o *= 16;
+        for (int j = 0; j < C::FM; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) start[4 * g + r] = fast ? o[r] : 0;
-        }
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+    if (fast) {  // block-uniform
+        const int col0 = wn * (C::TN / C::WN) + 4 * hk;
 #pragma unroll
-        for (int j = 0; j < C::FM; ++j) acc[i][j] = start;
+        for (int i = 0; i < C::FN; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                v4i o = *reinterpret_cast<const v4i*>(e_off + col0 + i * 32 + 8 * g);
+                if constexpr (C::WBITS == 4) o *= 16;
+#pragma unroll
+                for (int j = 0; j < C::FM; ++j)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[i][j][4 * g + r] = o[r];
+            }
     }
 
     // fragment g of a 32-deep step: g < FM activation rows, then weight rows
