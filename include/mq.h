@@ -181,6 +181,36 @@ mq_status mq_qlinear_ex(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
                         const float* bias, void* y_q, int32_t path, void* stream);
 
 /*
+ * mq_qlinear_workspace_bytes -- device workspace mq_qlinear_ws can use for
+ * this shape to split the reduction over K across several work-groups per
+ * output tile (for layers with few output tiles and a long K, e.g. the
+ * down projections).  0: the shape is not split.  -1: invalid arguments
+ * (negative sizes, K outside [1, MQ_MAX_K], bits other than 8/4 and 8/16).
+ * The result depends only on the shape and bit widths.
+ */
+int64_t mq_qlinear_workspace_bytes(int64_t M, int64_t K, int64_t N, int32_t w_bits,
+                                   int32_t out_bits);
+
+/*
+ * mq_qlinear_ws -- mq_qlinear_ex with a workspace for the K split.  Results
+ * are bit-identical to mq_qlinear_ex: the slices' int32 partial sums are
+ * added exactly before the requant.
+ *   workspace        device memory owned by the caller, 256-byte aligned,
+ *                    zero-filled once before its first use with this
+ *                    library; every call leaves its counters at zero again.
+ *                    NULL (or workspace_bytes below
+ *                    mq_qlinear_workspace_bytes) -> no split.  Calls that may
+ *                    run concurrently must not share a workspace.
+ *   workspace_bytes  >= 0
+ */
+mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                        const void* w_q, int32_t w_bits, const float* w_scale,
+                        const int32_t* w_colsum, float a_scale, int32_t a_zp,
+                        float out_scale, int32_t out_zp, int32_t out_bits,
+                        const float* bias, void* y_q, void* workspace,
+                        int64_t workspace_bytes, int32_t path, void* stream);
+
+/*
  * mq_dequant -- inverse of Eq.(4): y = alpha * (float)(q - zp), one exact
  * integer subtraction and one fp32 multiply.
  *   q      device int8 (bits 8) or int16 (bits 16) [numel]

@@ -64,9 +64,13 @@ def lib():
                              c_i32, c_i32, c_p, c_p, c_p]
     L.mq_qlinear_ex.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32,
                                 c_f, c_i32, c_i32, c_p, c_p, c_i32, c_p]
+    L.mq_qlinear_ws.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32,
+                                c_f, c_i32, c_i32, c_p, c_p, c_p, c_i64, c_i32, c_p]
+    L.mq_qlinear_workspace_bytes.argtypes = [c_i64, c_i64, c_i64, c_i32, c_i32]
+    L.mq_qlinear_workspace_bytes.restype = c_i64
     L.mq_dequant.argtypes = [c_p, c_i32, c_i64, c_f, c_i32, c_p, c_p]
     for name in ("mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
-                 "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_dequant"):
+                 "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -192,10 +196,22 @@ def mq_pack_weights(w, bits: int = 8, w_q=None, w_scale=None, w_colsum=None, str
     return w_q, w_scale, w_colsum
 
 
+def mq_qlinear_workspace_bytes(M: int, K: int, N: int, w_bits: int = 8, out_bits: int = 8) -> int:
+    """Workspace bytes mq_qlinear can use to split K for this shape (0: none)."""
+    n = lib().mq_qlinear_workspace_bytes(int(M), int(K), int(N), int(w_bits), int(out_bits))
+    if n < 0:
+        raise MQError(f"mq_qlinear_workspace_bytes: invalid shape {(M, K, N, w_bits, out_bits)}")
+    return n
+
+
 def mq_qlinear(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: int,
                out_scale: float, out_zp: int, out_bits: int = 8, bias=None, out=None,
-               path: int = PATH_AUTO, stream=None):
-    """Integer-only linear layer: int8 A_q [M][K] x W_q -> Y_q [M][N]."""
+               path: int = PATH_AUTO, stream=None, workspace=None):
+    """Integer-only linear layer: int8 A_q [M][K] x W_q -> Y_q [M][N].
+
+    `workspace`: an optional zero-filled uint8 device tensor of at least
+    mq_qlinear_workspace_bytes(...) bytes, kept by the caller across calls
+    (the K split leaves it zero-filled again)."""
     torch = _torch()
     M, K = a_q.shape
     N = w_q.shape[0]
@@ -209,7 +225,13 @@ def mq_qlinear(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: i
             _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)),
             float(a_scale), int(a_zp), float(out_scale), int(out_zp), int(out_bits), bptr,
             _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)))
-    if path == PATH_AUTO:
+    if workspace is not None:
+        if workspace.dtype != torch.uint8 or workspace.device.type != "cuda" or \
+                not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous uint8 device tensor")
+        st = lib().mq_qlinear_ws(*args, ctypes.c_void_p(workspace.data_ptr()),
+                                 int(workspace.numel()), int(path), _stream_ptr(stream))
+    elif path == PATH_AUTO:
         st = lib().mq_qlinear(*args, _stream_ptr(stream))
     else:
         st = lib().mq_qlinear_ex(*args, int(path), _stream_ptr(stream))

@@ -122,12 +122,41 @@ mq_status mq_pack_weights(const float* w, int64_t N, int64_t K, int32_t bits, vo
         mq::launch_pack_weights(w, N, K, bits, w_q, w_scale, w_colsum, as_stream(stream)));
 }
 
+int64_t mq_qlinear_workspace_bytes(int64_t M, int64_t K, int64_t N, int32_t w_bits,
+                                   int32_t out_bits)
+{
+    if (w_bits != 8 && w_bits != 4) return -1;
+    if (!act_bits_ok(out_bits)) return -1;
+    if (M < 0 || N < 0 || K < 1 || K > MQ_MAX_K) return -1;
+    if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || (M > 0 && N > kMaxElems / M)) return -1;
+    if (M <= 16 || N == 0) return 0;  // decode path or nothing to do
+    mq::QLinearArgs p;
+    p.M = M;
+    p.K = K;
+    p.N = N;
+    p.w_bits = w_bits;
+    p.out_bits = out_bits;
+    return mq::prefill_workspace_bytes(p);
+}
+
 mq_status mq_qlinear_ex(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
                         int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
                         float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
                         int32_t out_bits, const float* bias, void* y_q, int32_t path,
                         void* stream)
 {
+    return mq_qlinear_ws(a_q, M, K, N, w_q, w_bits, w_scale, w_colsum, a_scale, a_zp, out_scale,
+                         out_zp, out_bits, bias, y_q, nullptr, 0, path, stream);
+}
+
+mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
+                        int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
+                        float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                        int32_t out_bits, const float* bias, void* y_q, void* workspace,
+                        int64_t workspace_bytes, int32_t path, void* stream)
+{
+    if (workspace_bytes < 0) return MQ_ERR_INVALID_ARG;
+    if (workspace && ((uintptr_t)workspace % 256) != 0) return MQ_ERR_INVALID_ARG;
     if (w_bits != 8 && w_bits != 4) return MQ_ERR_INVALID_ARG;
     if (!act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
     if (M < 0 || N < 0 || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
@@ -156,6 +185,8 @@ mq_status mq_qlinear_ex(const int8_t* a_q, int64_t M, int64_t K, int64_t N, cons
     p.out_zp = out_zp;
     p.w_bits = w_bits;
     p.out_bits = out_bits;
+    p.ws = workspace;
+    p.ws_bytes = workspace ? workspace_bytes : 0;
 
     hipStream_t s = as_stream(stream);
     if (path == MQ_PATH_AUTO) path = M <= 16 ? MQ_PATH_DECODE : MQ_PATH_PREFILL;

@@ -22,6 +22,8 @@ struct QLinearArgs {
     int32_t out_zp;
     int32_t w_bits;         // 8 or 4
     int32_t out_bits;       // 8 or 16
+    void* ws = nullptr;     // split-K workspace (zero-filled once by its owner) or nullptr
+    int64_t ws_bytes = 0;
 };
 
 hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t zp,
@@ -38,6 +40,10 @@ hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int32_t bit
 hipError_t launch_qlinear_generic(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s);
+
+// Workspace bytes the prefill kernel would use to split K for this shape
+// (0 when it would not split).
+int64_t prefill_workspace_bytes(const QLinearArgs& p);
 
 // Shape/alignment rules of the tuned kernels.
 bool decode_supported(const QLinearArgs& p);

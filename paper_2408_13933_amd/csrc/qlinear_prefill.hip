@@ -42,6 +42,13 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr uint32_t kOOB = 0x80000000u;  // any offset past num_records reads zero
 
+// Split-K workspace: one int32 arrival counter per tile (rounded up to 256
+// bytes), then the int32 partial sums of every (tile, slice) block.
+__host__ __device__ inline int64_t split_counter_bytes(int64_t tiles)
+{
+    return (tiles * 4 + 255) / 256 * 256;
+}
+
 __device__ inline v4i unpack_int4_x16(uint32_t x0, uint32_t x1)
 {
     const uint32_t l0 = (x0 << 4) & 0xF0F0F0F0u, h0 = x0 & 0xF0F0F0F0u;
@@ -96,6 +103,9 @@ struct Cfg {
         return n;
     }
     static constexpr int NSW = nsw();
+    // K slices (split-K) for the smaller tiles; the 256x256 tile has no
+    // registers to spare for the slice bookkeeping
+    static constexpr bool SPLITK = TM * TN < 256 * 256;
     static constexpr int A_BYTES = A_PER_WAVE * NWAVES * 1024;
     static constexpr int W_BYTES = W_PER_WAVE * NWAVES * 1024;
     static constexpr int STAGE = A_BYTES + W_BYTES;
@@ -293,7 +303,9 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
 
 template <class C>
 __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearArgs p,
-                                                                       int tiles_n, int tiles_m)
+                                                                       int tiles_n, int tiles_m,
+                                                                       int splits,
+                                                                       int kt_per_split)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
     constexpr int32_t qmax = (1 << (C::OBITS - 1)) - 1;
@@ -306,17 +318,21 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     int32_t* e_sp = e_rnd + C::TN;  // shr | pre << 8
     int32_t* e_flag = e_sp + C::TN;  // per wave: bit 0 all pre == 0, bit 1 zp foldable
 
-    // ---- tile id: the blocks of one XCD (block id mod 8) take a contiguous
-    // run of tiles, so they share weight tiles in that XCD's L2
+    // ---- tile and K slice: the blocks of one XCD (block id mod 8) take a
+    // contiguous run of work items, so they share operand tiles in that
+    // XCD's L2; item = slice * tiles + tile
     const int total = tiles_n * tiles_m;
     int b = blockIdx.x;
     {
-        const int per = total / 8, rem = total % 8;
+        const int items = total * splits;
+        const int per = items / 8, rem = items % 8;
         const int xcd = b % 8, idx = b / 8;
         b = xcd * per + (xcd < rem ? xcd : rem) + idx;
     }
-    const int tn = b / tiles_m;
-    const int tm = b % tiles_m;
+    const int split = C::SPLITK ? b / total : 0;
+    const int tile = C::SPLITK ? b % total : b;
+    const int tn = tile / tiles_m;
+    const int tm = tile % tiles_m;
     const int64_t n_tile = (int64_t)tn * C::TN;
     const int64_t m_tile = (int64_t)tm * C::TM;
 
@@ -328,16 +344,23 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     const int r32 = lane & 31;  // operand row / output token within a fragment
     const int hk = lane >> 5;   // which 16-byte half of a 32-byte k step
 
-    // ---- buffer descriptors covering only this tile's valid rows
+    // ---- buffer descriptors covering only this tile's valid rows, from the
+    // first K byte of this block's slice; KL = the slice's length in K
     const int64_t K = p.K;
     const int64_t wrow = C::WBITS == 8 ? K : K / 2;
+    const int64_t k_begin = C::SPLITK ? (int64_t)split * kt_per_split * C::BK : 0;
+    const int64_t KL = !C::SPLITK ? K
+                       : (K - k_begin) < (int64_t)kt_per_split * C::BK
+                           ? (K - k_begin) : (int64_t)kt_per_split * C::BK;
+    const int64_t k_begin_w = C::WBITS == 8 ? k_begin : k_begin / 2;
+    const int64_t KLw = C::WBITS == 8 ? KL : KL / 2;
     const int rows_a = (int)((p.M - m_tile) < C::TM ? (p.M - m_tile) : C::TM);
     const int rows_w = (int)((p.N - n_tile) < C::TN ? (p.N - n_tile) : C::TN);
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.a + m_tile * K), (short)0, (int)(rows_a * K), 0x00020000);
+        (void*)(p.a + m_tile * K + k_begin), (short)0, (int)(rows_a * K - k_begin), 0x00020000);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(static_cast<const int8_t*>(p.w) + n_tile * wrow), (short)0, (int)(rows_w * wrow),
-        0x00020000);
+        (void*)(static_cast<const int8_t*>(p.w) + n_tile * wrow + k_begin_w), (short)0,
+        (int)(rows_w * wrow - k_begin_w), 0x00020000);
 
     // Source offsets of this lane's chunks at k = 0; a stage adds kt*BK.  A
     // chunk past the end of its row (K tail) is pushed out of range.
@@ -363,7 +386,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         w_off[i] = wave + i * C::NWAVES < C::W_WLOADS ? (uint32_t)(row * (int)wrow + w_kb(i))
                                                       : kOOB;
     }
-    const int KT = (int)((K + C::BK - 1) / C::BK);
+    const int KT = (int)((KL + C::BK - 1) / C::BK);  // stages of this slice
     // DMA of stage kt into LDS buffer buf.  Every call issues the same number
     // of loads; a stage past the end (or a chunk past K) reads out of range,
     // which writes zeros and touches no memory, so the vector-memory counter
@@ -373,13 +396,13 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         if (idx < C::A_PER_WAVE) {
             const int i = idx, k0 = kt * C::BK;
             const int wl = wave + i * C::NWAVES;
-            const uint32_t voff = (k0 + a_kb(i) < (int)K) ? a_off[i] + (uint32_t)k0 : kOOB;
+            const uint32_t voff = (k0 + a_kb(i) < (int)KL) ? a_off[i] + (uint32_t)k0 : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (MQ_LDS void*)(base + wl * 1024), 16,
                                                      voff, 0, 0, 0);
         } else {
             const int i = idx - C::A_PER_WAVE, k0w = kt * C::BKW;
             const int wl = wave + i * C::NWAVES;
-            const uint32_t voff = (k0w + w_kb(i) < (int)wrow) ? w_off[i] + (uint32_t)k0w : kOOB;
+            const uint32_t voff = (k0w + w_kb(i) < (int)KLw) ? w_off[i] + (uint32_t)k0w : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rw, (MQ_LDS void*)(base + C::A_BYTES + wl * 1024), 16, voff, 0, 0, 0);
         }
@@ -473,7 +496,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         for (int j = 0; j < C::FM; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
-    if (fast) {  // block-uniform
+    if (fast && split == 0) {  // block-uniform; off joins the sum once
         const int col0 = wn * (C::TN / C::WN) + 4 * hk;
 #pragma unroll
         for (int i = 0; i < C::FN; ++i)
@@ -593,8 +616,73 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         }
     }
 
-    // ---- epilogue, straight from the accumulators (see prefill_epilogue)
+    // ---- K slices: every block stores its partial sums (int32, in the
+    // accumulator register layout, so each lane's 16-byte chunks are
+    // contiguous across the block) and counts itself in at its tile's
+    // counter; the last block to arrive adds the other slices (exact integer
+    // sums), returns the counter to zero for the next call and runs the
+    // epilogue.  Nobody waits for anybody, so no schedule can deadlock.
+    // The slices of a tile may run on different XCDs (separate L2s): the
+    // partial sums are written through to memory and read around the caches
+    // (sc0 sc1), and the counter is a system-scope atomic, which keeps the
+    // exchange coherent without writing back or invalidating whole L2s.
     wait_vmcnt<0>();  // the out-of-range DMA of the last steps is retired
+    if (C::SPLITK && splits > 1) {
+        constexpr int CHUNKS = C::FN * C::FM * 4;  // 16-byte chunks per lane
+        constexpr int kCoherent = 1 | 16;          // cache policy sc0 | sc1
+        int32_t* counters = static_cast<int32_t*>(p.ws);
+        const int64_t part_bytes = (int64_t)CHUNKS * C::THREADS * 16;  // one block's slice
+        const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+            static_cast<int8_t*>(p.ws) + split_counter_bytes(total) +
+                (int64_t)tile * splits * part_bytes,
+            (short)0, (int)(splits * part_bytes), 0x00020000);
+        auto chunk_off = [&](int s, int i, int j, int g) {
+            return (uint32_t)(s * part_bytes +
+                              ((int64_t)((i * C::FM + j) * 4 + g) * C::THREADS + tid) * 16);
+        };
+#pragma unroll
+        for (int i = 0; i < C::FN; ++i)
+#pragma unroll
+            for (int j = 0; j < C::FM; ++j) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const v4i v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                   acc[i][j][4 * g + 3]};
+                    __builtin_amdgcn_raw_buffer_store_b128(v, rp, chunk_off(split, i, j, g), 0,
+                                                           kCoherent);
+                }
+                __builtin_amdgcn_sched_barrier(0);  // one fragment at a time: bounded registers
+            }
+        wait_vmcnt<0>();  // this wave's partial sums have reached memory
+        __syncthreads();
+        if (tid == 0)
+            e_flag[0] = __hip_atomic_fetch_add(counters + tile, 1, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_SYSTEM);
+        __syncthreads();
+        const int arrived = e_flag[0];
+        __syncthreads();  // everybody has read the count before e_flag is reused
+        if (arrived != splits - 1) return;
+        for (int s = 0; s < splits; ++s) {
+            if (s == split) continue;
+#pragma unroll
+            for (int i = 0; i < C::FN; ++i)
+#pragma unroll
+                for (int j = 0; j < C::FM; ++j) {
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const v4i v = __builtin_amdgcn_raw_buffer_load_b128(
+                            rp, chunk_off(s, i, j, g), 0, kCoherent);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) acc[i][j][4 * g + r] += v[r];
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+        }
+        if (tid == 0)
+            __hip_atomic_exchange(counters + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+
+    // ---- epilogue, straight from the accumulators (see prefill_epilogue)
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
     __builtin_amdgcn_s_barrier();  // e_rnd update visible even when KT == 1
     EpiCtx ctx;
@@ -624,19 +712,22 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
 }
 
 template <class C>
-hipError_t launch_cfg(const QLinearArgs& p, hipStream_t s)
+hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
 {
     const int64_t tiles_n = (p.N + C::TN - 1) / C::TN;
     const int64_t tiles_m = (p.M + C::TM - 1) / C::TM;
     const int64_t total = tiles_n * tiles_m;
-    if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const int64_t kt = (p.K + C::BK - 1) / C::BK;
+    const int64_t kt_per_split = (kt + splits - 1) / splits;
+    splits = (int)((kt + kt_per_split - 1) / kt_per_split);  // every slice non-empty
+    if (total * splits > 0x7FFFFFFF) return hipErrorInvalidValue;
     // more than 64 KiB of dynamic LDS must be opted into once per kernel
     static const hipError_t attr = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&qlinear_prefill_kernel<C>),
         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (attr != hipSuccess) return attr;
-    qlinear_prefill_kernel<C><<<dim3((unsigned)total), dim3(C::THREADS), C::LDS, s>>>(
-        p, (int)tiles_n, (int)tiles_m);
+    qlinear_prefill_kernel<C><<<dim3((unsigned)(total * splits)), dim3(C::THREADS), C::LDS, s>>>(
+        p, (int)tiles_n, (int)tiles_m, splits, (int)kt_per_split);
     return hipGetLastError();
 }
 
@@ -648,41 +739,74 @@ template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2,
 template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2, 4>;
 template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
 
-struct TileChoice {
-    int tm, tn;
-    double eff;  // relative per-tile efficiency
+// Per-block cycle model of each tile shape on MI355X (phase timings of the
+// kernel): fixed prologue + K-loop cycles per stage + epilogue, and for a
+// K split the store of one partial tile plus, on the last block, the reads
+// of the others (int32 tile / ~64 B per cycle).
+struct TileModel {
+    int tm, tn, bk;
+    double prologue, per_stage, epilogue, partial;
+};
+constexpr TileModel kTiles[] = {
+    {256, 256, 64, 6500, 1450, 9800, 4096},
+    {256, 128, 128, 6000, 1500, 6000, 2048},
+    {128, 128, 128, 5300, 980, 3300, 1024},
+};
+constexpr int kCUs = 256;
+constexpr int kMaxSplits = 8;
+
+struct Choice {
+    int tile, splits;
 };
 
-int choose_tile(const QLinearArgs& p)
+Choice choose(const QLinearArgs& p, bool can_split)
 {
+    Choice best{0, 1};
+    double best_t = 1e300;
+    int only = -1;
     if (const char* e = std::getenv("MQ_PREFILL_TILE")) {
         const int v = std::atoi(e);
-        if (v >= 0 && v <= 2) return v;
+        if (v >= 0 && v <= 2) only = v;
     }
-    static const TileChoice choices[] = {{256, 256, 1.0}, {256, 128, 0.85}, {128, 128, 0.6}};
-    const int cus = 256;
-    int best = 0;
-    double best_t = 1e300;
     for (int c = 0; c < 3; ++c) {
-        const int64_t tiles =
-            ((p.M + choices[c].tm - 1) / choices[c].tm) * ((p.N + choices[c].tn - 1) / choices[c].tn);
-        const int64_t rounds = (tiles + cus - 1) / cus;
-        const double t = (double)rounds * choices[c].tm * choices[c].tn / choices[c].eff;
-        if (t < best_t) {
-            best_t = t;
-            best = c;
+        if (only >= 0 && c != only) continue;
+        const TileModel& t = kTiles[c];
+        const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn);
+        const int64_t kt = (p.K + t.bk - 1) / t.bk;
+        const bool tile_splits = t.tm * t.tn < 256 * 256;  // Cfg::SPLITK
+        for (int sp = 1; sp <= (can_split && tile_splits ? kMaxSplits : 1); sp *= 2) {
+            const int64_t per = (kt + sp - 1) / sp;
+            if (sp > 1 && per < 4) break;  // slices too thin to pipeline
+            const int64_t rounds = (tiles * sp + kCUs - 1) / kCUs;
+            const double t_blk = t.prologue + t.per_stage * (double)per + t.epilogue +
+                                 (sp > 1 ? t.partial * sp : 0.0);
+            const double tt = (double)rounds * t_blk;
+            if (tt < best_t * 0.97) {  // a split has to win clearly
+                best_t = tt;
+                best = {c, sp};
+            }
         }
     }
     return best;
 }
 
+int64_t workspace_for(const QLinearArgs& p, const Choice& ch)
+{
+    if (ch.splits <= 1) return 0;
+    const TileModel& t = kTiles[ch.tile];
+    const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn);
+    return split_counter_bytes(tiles) + tiles * ch.splits * (int64_t)t.tm * t.tn * 4;
+}
+
 template <int WB, int OB>
 hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 {
-    switch (choose_tile(p)) {
-    case 0: return launch_cfg<T256x256<WB, OB>>(p, s);
-    case 1: return launch_cfg<T256x128<WB, OB>>(p, s);
-    default: return launch_cfg<T128x128<WB, OB>>(p, s);
+    Choice ch = choose(p, p.ws != nullptr);
+    if (ch.splits > 1 && workspace_for(p, ch) > p.ws_bytes) ch = choose(p, false);
+    switch (ch.tile) {
+    case 0: return launch_cfg<T256x256<WB, OB>>(p, ch.splits, s);
+    case 1: return launch_cfg<T256x128<WB, OB>>(p, ch.splits, s);
+    default: return launch_cfg<T128x128<WB, OB>>(p, ch.splits, s);
     }
 }
 
@@ -697,6 +821,11 @@ bool prefill_supported(const QLinearArgs& p)
     const bool nok = 256 * p.N * (p.out_bits / 8) < ((int64_t)1 << 31);
     return kok && nok && ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
            ((uintptr_t)p.y % 8) == 0;
+}
+
+int64_t prefill_workspace_bytes(const QLinearArgs& p)
+{
+    return workspace_for(p, choose(p, true));
 }
 
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s)

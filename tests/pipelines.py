@@ -45,7 +45,7 @@ def oracle_layer(ld: LayerData, rows=None, nthreads=None) -> LayerResult:
     return LayerResult(a_scale, a_zp, out_scale, out_zp, a_q, wq, ws, cs, w_hat, y_q, y)
 
 
-def gpu_layer(ld: LayerData, path: int = 0, keep_device=False):
+def gpu_layer(ld: LayerData, path: int = 0, keep_device=False, workspace=None):
     import torch
     import paper_2408_13933_amd as mq
 
@@ -63,7 +63,7 @@ def gpu_layer(ld: LayerData, path: int = 0, keep_device=False):
     a_q = mq.mq_quantize_act(x, a_scale, a_zp, 8)
     wq, ws, cs = mq.mq_pack_weights(w_hat if w_hat is not None else w, L.w_bits)
     y_q = mq.mq_qlinear(a_q, wq, L.w_bits, ws, cs, a_scale, a_zp, out_scale, out_zp,
-                        L.out_bits, bias=bias, path=path)
+                        L.out_bits, bias=bias, path=path, workspace=workspace)
     y = mq.mq_dequant(y_q, out_scale, out_zp)
     torch.cuda.synchronize()
     res = LayerResult(a_scale, a_zp, out_scale, out_zp, a_q.cpu().numpy(), wq.cpu().numpy(),

@@ -72,6 +72,42 @@ def test_qlinear_rejects_invalid_arguments(kw):
     assert qlin(**kw) == 1
 
 
+def qlin_ws(workspace, workspace_bytes, **kw):
+    a = dict(a_q=NZ, M=64, K=4096, N=64, w_q=NZ, w_bits=8, w_scale=NZ, w_colsum=NZ, a_scale=0.1,
+             a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None, y_q=NZ, path=0,
+             stream=None)
+    a.update(kw)
+    return mq.lib().mq_qlinear_ws(a["a_q"], a["M"], a["K"], a["N"], a["w_q"], a["w_bits"],
+                                  a["w_scale"], a["w_colsum"], a["a_scale"], a["a_zp"],
+                                  a["out_scale"], a["out_zp"], a["out_bits"], a["bias"],
+                                  a["y_q"], workspace, workspace_bytes, a["path"], a["stream"])
+
+
+def test_qlinear_ws_rejects_invalid_workspace():
+    assert qlin_ws(P(256), -1) == 1            # negative size
+    assert qlin_ws(P(256 + 16), 4096) == 1     # not 256-byte aligned
+    assert qlin_ws(P(256), 4096, K=0) == 1     # the usual validation applies too
+    assert qlin_ws(P(256), 4096, M=0) == 0     # empty: nothing enqueued
+    assert qlin_ws(None, 0, M=0) == 0
+
+
+def test_workspace_bytes_query():
+    f = mq.lib().mq_qlinear_workspace_bytes
+    assert f(-1, 64, 64, 8, 8) == -1
+    assert f(64, 0, 64, 8, 8) == -1
+    assert f(64, 65537, 64, 8, 8) == -1
+    assert f(64, 64, 64, 3, 8) == -1
+    assert f(64, 64, 64, 8, 12) == -1
+    assert f(16, 65536, 64, 8, 8) == 0      # decode-shaped: never split
+    assert f(2048, 2048, 5632, 8, 8) == 0   # enough output tiles
+    # few output tiles, long K: split, and the size covers one int32 tile per
+    # slice (at least two slices of a 128x128 tile) plus the counters
+    n = f(512, 16384, 2048, 8, 16)
+    assert n >= 2 * 128 * 128 * 4 * ((512 // 128) * (2048 // 128))
+    assert n % 256 == 0
+    assert mq.mq_qlinear_workspace_bytes(512, 16384, 2048, 8, 16) == n
+
+
 def test_qlinear_empty_shapes_are_noops():
     # M = 0 or N = 0: nothing to compute, no device touched
     assert qlin(M=0) == 0

@@ -13,13 +13,16 @@ from paper_2408_13933_amd import workloads as wl
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("M,w_bits,out_bits", [(300, 8, 8), (16, 8, 16), (130, 4, 16)])
-def test_graph_replay_matches_eager(M, w_bits, out_bits):
+@pytest.mark.parametrize("M,K,w_bits,out_bits", [(300, 1024, 8, 8), (16, 1024, 8, 16),
+                                                 (130, 1024, 4, 16), (130, 8192, 8, 8)])
+def test_graph_replay_matches_eager(M, K, w_bits, out_bits):
+    """The last case splits K through a workspace: its arrival counters
+    return to zero inside the kernel, so replays need no memset."""
     import torch
 
     import paper_2408_13933_amd as mq
 
-    layer = wl.Layer("g", M, 1024, 384, w_bits=w_bits, out_bits=out_bits)
+    layer = wl.Layer("g", M, K, 384, w_bits=w_bits, out_bits=out_bits)
     ld = wl.make_layer("graph", layer)
     dev = torch.device("cuda", 0)
     x = torch.from_numpy(ld.x).to(dev)
@@ -31,11 +34,15 @@ def test_graph_replay_matches_eager(M, w_bits, out_bits):
     a_q = torch.empty(x.shape, dtype=torch.int8, device=dev)
     y = torch.empty((M, 384), dtype=torch.int8 if out_bits == 8 else torch.int16, device=dev)
     deq = torch.empty((M, 384), dtype=torch.float32, device=dev)
+    nws = mq.mq_qlinear_workspace_bytes(M, K, 384, w_bits, out_bits)
+    work = torch.zeros(nws, dtype=torch.uint8, device=dev) if nws else None
+    if K > 1024:
+        assert nws > 0
 
     def step():
         mq.mq_quantize_act(x, a_scale, a_zp, 8, out=a_q)
         mq.mq_qlinear(a_q, wq, w_bits, ws, cs, a_scale, a_zp, o_scale, o_zp, out_bits,
-                      bias=bias, out=y)
+                      bias=bias, out=y, workspace=work)
         mq.mq_dequant(y, o_scale, o_zp, out=deq)
 
     step()  # eager, also performs any one-time kernel set-up before capture

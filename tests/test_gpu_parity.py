@@ -102,6 +102,34 @@ def test_decode_multi_round_k(w_bits, out_bits, M, K, N):
     assert np.array_equal(d, g)
 
 
+SPLIT_CASES = [
+    # M, K, N, w_bits, out_bits, bias: few output tiles, long K
+    (130, 8192, 300, 8, 8, True),
+    (200, 5632, 300, 4, 16, False),
+    (64, 16384, 160, 8, 16, False),
+    (257, 4128, 130, 8, 8, True),   # ragged M and N, K tail, uneven last slice
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: "x".join(map(str, c[:5])))
+def test_split_k_parity(case):
+    """K split across work-groups (workspace path): bit-identical to the
+    oracle, twice in a row on one workspace, which ends zero-filled."""
+    mq, torch = _mq(), _torch()
+    M, K, N, wb, ob, has_bias = case
+    nbytes = mq.mq_qlinear_workspace_bytes(M, K, N, wb, ob)
+    assert nbytes > 0, "the shape is expected to split"
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    layer = wl.Layer("x", M, K, N, w_bits=wb, out_bits=ob, bias=has_bias)
+    ld = wl.make_layer("splitk", layer)
+    o = oracle_layer(ld)
+    for _ in range(2):
+        assert_same(gpu_layer(ld, workspace=ws), o)
+    assert int(ws[:256].count_nonzero()) == 0, "arrival counters not returned to zero"
+    # without a workspace the same call does not split and gives the same bits
+    assert np.array_equal(gpu_layer(ld).y_q, o.y_q)
+
+
 @pytest.mark.parametrize("w_bits", [8, 4])
 def test_prefill_equals_generic_ragged(w_bits):
     mq = _mq()
@@ -316,7 +344,12 @@ FULL = [(w.name, l.name) for w in wl.WORKLOADS.values() for l in w.layers]
 def test_full_size_parity(case):
     workload, name = case
     ld = _full_layer(workload, name)
-    g = gpu_layer(ld)
+    L = ld.layer
+    ws = None
+    nbytes = _mq().mq_qlinear_workspace_bytes(L.M, L.K, L.N, L.w_bits, L.out_bits)
+    if nbytes:  # the layer splits K when given a workspace: take that path
+        ws = _torch().zeros(nbytes, dtype=_torch().uint8, device="cuda")
+    g = gpu_layer(ld, workspace=ws)
     M = ld.layer.M
     rows = None if M * ld.layer.N * ld.layer.K <= 2 ** 31 else _rows(M)
     o = oracle_layer(ld, rows=rows)
