@@ -662,21 +662,32 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         const int arrived = e_flag[0];
         __syncthreads();  // everybody has read the count before e_flag is reused
         if (arrived != splits - 1) return;
+        // the other slices, 16 chunks (64 registers) in flight per batch: each
+        // batch costs one memory round trip, not one per chunk
+        constexpr int IB = 16 / (C::FM * 4) > 0 ? 16 / (C::FM * 4) : 1;  // fragment rows per batch
         for (int s = 0; s < splits; ++s) {
             if (s == split) continue;
 #pragma unroll
-            for (int i = 0; i < C::FN; ++i)
+            for (int i0 = 0; i0 < C::FN; i0 += IB) {
+                v4i tmp[IB][C::FM][4];
 #pragma unroll
-                for (int j = 0; j < C::FM; ++j) {
+                for (int i = 0; i < IB; ++i)
 #pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const v4i v = __builtin_amdgcn_raw_buffer_load_b128(
-                            rp, chunk_off(s, i, j, g), 0, kCoherent);
+                    for (int j = 0; j < C::FM; ++j)
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) acc[i][j][4 * g + r] += v[r];
-                    }
-                    __builtin_amdgcn_sched_barrier(0);
-                }
+                        for (int g = 0; g < 4; ++g)
+                            tmp[i][j][g] = __builtin_amdgcn_raw_buffer_load_b128(
+                                rp, chunk_off(s, i0 + i, j, g), 0, kCoherent);
+#pragma unroll
+                for (int i = 0; i < IB; ++i)
+#pragma unroll
+                    for (int j = 0; j < C::FM; ++j)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) acc[i0 + i][j][4 * g + r] += tmp[i][j][g][r];
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
         if (tid == 0)
             __hip_atomic_exchange(counters + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -740,18 +751,24 @@ template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2
 template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
 
 // Per-block cycle model of each tile shape on MI355X (phase timings of the
-// kernel): fixed prologue + K-loop cycles per stage + epilogue, and for a
-// K split the store of one partial tile plus, on the last block, the reads
-// of the others (int32 tile / ~64 B per cycle).
+// kernel): fixed prologue + K-loop cycles per stage + epilogue.
 struct TileModel {
     int tm, tn, bk;
-    double prologue, per_stage, epilogue, partial;
+    double prologue, per_stage, epilogue;
 };
 constexpr TileModel kTiles[] = {
-    {256, 256, 64, 6500, 1450, 9800, 4096},
-    {256, 128, 128, 6000, 1500, 6000, 2048},
-    {128, 128, 128, 5300, 980, 3300, 1024},
+    {256, 256, 64, 6500, 1450, 9800},
+    {256, 128, 128, 6000, 1500, 6000},
+    {128, 128, 128, 5300, 980, 3300},
 };
+// A split adds round trips to memory (partial stores, the counter, the
+// partial loads) and moves every slice's int32 tile through memory and back
+// (write-through, read around the caches): ~4 TB/s, about 2 KB per cycle
+// for the whole chip.  Measured on MI355X: a split pays from K ~ 4096 on.
+constexpr double kSplitFixed = 9000;
+// int4 weights: the in-register unpack makes a K-loop stage ~1.35x longer
+constexpr double kInt4StageFactor = 1.35;
+constexpr double kExchangeBytesPerCycle = 2048;
 constexpr int kCUs = 256;
 constexpr int kMaxSplits = 8;
 
@@ -778,9 +795,13 @@ Choice choose(const QLinearArgs& p, bool can_split)
             const int64_t per = (kt + sp - 1) / sp;
             if (sp > 1 && per < 4) break;  // slices too thin to pipeline
             const int64_t rounds = (tiles * sp + kCUs - 1) / kCUs;
-            const double t_blk = t.prologue + t.per_stage * (double)per + t.epilogue +
-                                 (sp > 1 ? t.partial * sp : 0.0);
-            const double tt = (double)rounds * t_blk;
+            const double stage = t.per_stage * (p.w_bits == 4 ? kInt4StageFactor : 1.0);
+            const double t_blk = t.prologue + stage * (double)per + t.epilogue;
+            const double exchange =
+                sp > 1 ? kSplitFixed + (double)tiles * (2 * sp - 1) * t.tm * t.tn * 4 /
+                                           kExchangeBytesPerCycle
+                       : 0.0;
+            const double tt = (double)rounds * t_blk + exchange;
             if (tt < best_t * 0.97) {  // a split has to win clearly
                 best_t = tt;
                 best = {c, sp};
