@@ -13,9 +13,13 @@ Functions and the passages they follow (arXiv 2408.13933):
 * ``dequant``         -- inverse of Eq.(4)
 * ``fold_weights`` / ``fold_acts`` -- Section 3.2, Eq.(1) (S W and X S^-1)
 * ``pack_weights``    -- Section 5.1 / appendix: symmetric per-channel W8, W4
+* ``pack_weights_asym`` -- Section 5.1: asymmetric per-channel W8, W4 (the
+  quantizer of Eq.(2)-(4) applied per output row)
+* ``act_rowsum``      -- sum_k A_q[m][k] (the zero-point cross term)
 * ``requant_params`` / ``requant_value`` -- fixed-point rescale to the next
   layer's integer format (Section 1, Section 3.1: integer-only arithmetic)
-* ``qlinear``         -- the integer-only linear layer end to end
+* ``qlinear``         -- the integer-only linear layer end to end, with
+  optional per-channel weight zero-points
 * ``int_matmul``      -- the raw integer product, for pinning the accumulate
 
 Parity status: every function is pinned by ``tests/test_oracle_pins.py``
@@ -66,6 +70,11 @@ def _load():
     lib.oracle_pack_weights.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                         _vp, _f32p, _i32p]
     lib.oracle_pack_weights.restype = None
+    lib.oracle_pack_weights_asym.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64,
+                                             ctypes.c_int, _vp, _f32p, _i32p, _i32p]
+    lib.oracle_pack_weights_asym.restype = None
+    lib.oracle_act_rowsum.argtypes = [_i8p, ctypes.c_int64, ctypes.c_int64, _i32p]
+    lib.oracle_act_rowsum.restype = None
     lib.oracle_requant_params.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                           ctypes.POINTER(ctypes.c_float),
                                           ctypes.POINTER(ctypes.c_int64),
@@ -82,6 +91,11 @@ def _load():
                                    ctypes.c_float, ctypes.c_int32, ctypes.c_int, _vp, _vp,
                                    ctypes.c_int]
     lib.oracle_qlinear.restype = None
+    lib.oracle_qlinear_asym.argtypes = [_i8p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                        _vp, ctypes.c_int, _f32p, _vp, ctypes.c_float,
+                                        ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
+                                        ctypes.c_int, _vp, _vp, ctypes.c_int]
+    lib.oracle_qlinear_asym.restype = None
     lib.oracle_int_matmul.argtypes = [_i8p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                       _vp, ctypes.c_int, _i64p]
     lib.oracle_int_matmul.restype = None
@@ -178,6 +192,42 @@ def pack_weights(w: np.ndarray, bits: int):
     return wq, scale, colsum
 
 
+def _packed_weight_buffer(N: int, K: int, bits: int) -> np.ndarray:
+    if bits == 8:
+        return np.empty((N, K), dtype=np.int8)
+    if bits == 4:
+        if K % 2:
+            raise ValueError("int4 packing needs an even K")
+        return np.empty((N, K // 2), dtype=np.uint8)
+    raise ValueError("bits must be 8 or 4")
+
+
+def pack_weights_asym(w: np.ndarray, bits: int):
+    """Asymmetric per-output-channel quantizer and packer (Section 5.1).
+
+    Returns (w_q, w_scale, w_zp, colsum); codes are signed (the unsigned
+    Eq.(4) code minus 2^(bits-1)), w_zp is the signed zero-point, colsum
+    the row sum of the stored codes.
+    """
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    N, K = w.shape
+    wq = _packed_weight_buffer(N, K, bits)
+    scale = np.empty(N, dtype=np.float32)
+    zp = np.empty(N, dtype=np.int32)
+    colsum = np.empty(N, dtype=np.int32)
+    _load().oracle_pack_weights_asym(w, N, K, bits, _ptr(wq), scale, zp, colsum)
+    return wq, scale, zp, colsum
+
+
+def act_rowsum(a_q: np.ndarray) -> np.ndarray:
+    """sum_k A_q[m][k] as int32 [M]."""
+    a_q = np.ascontiguousarray(a_q, dtype=np.int8)
+    M, K = a_q.shape
+    out = np.empty(M, dtype=np.int32)
+    _load().oracle_act_rowsum(a_q, M, K, out)
+    return out
+
+
 def requant_params(alpha_a: float, w_scale: float, alpha_y: float, bias=None):
     """(M0, sh, bias_q) for one output channel."""
     M0 = ctypes.c_int64()
@@ -201,8 +251,12 @@ def requant_value(c: int, M0: int, sh: int, zp_y: int, bits_y: int) -> int:
 
 def qlinear(a_q: np.ndarray, w_q: np.ndarray, bits: int, w_scale: np.ndarray,
             alpha_a: float, zp_a: int, alpha_y: float, zp_y: int, bits_y: int,
-            bias=None, nthreads: int | None = None) -> np.ndarray:
-    """Integer-only linear layer: Y_q[m][n] from A_q[M][K] and W_q."""
+            bias=None, nthreads: int | None = None, w_zp=None) -> np.ndarray:
+    """Integer-only linear layer: Y_q[m][n] from A_q[M][K] and W_q.
+
+    ``w_zp`` (int32 [N]) gives per-channel weight zero-points; None means
+    symmetric weights.
+    """
     a_q = np.ascontiguousarray(a_q, dtype=np.int8)
     M, K = a_q.shape
     w_q = np.ascontiguousarray(w_q)
@@ -220,12 +274,17 @@ def qlinear(a_q: np.ndarray, w_q: np.ndarray, bits: int, w_scale: np.ndarray,
         bias = np.ascontiguousarray(bias, dtype=np.float32)
         assert bias.shape == (N,)
         bptr = _ptr(bias)
+    zptr = None
+    if w_zp is not None:
+        w_zp = np.ascontiguousarray(w_zp, dtype=np.int32)
+        assert w_zp.shape == (N,)
+        zptr = _ptr(w_zp)
     y = np.empty((M, N), dtype=_act_dtype(bits_y))
     if M == 0 or N == 0:
         return y
-    _load().oracle_qlinear(a_q, M, K, N, _ptr(w_q), bits, w_scale, alpha_a, zp_a,
-                           alpha_y, zp_y, bits_y, bptr, _ptr(y),
-                           nthreads or default_threads())
+    _load().oracle_qlinear_asym(a_q, M, K, N, _ptr(w_q), bits, w_scale, zptr, alpha_a,
+                                zp_a, alpha_y, zp_y, bits_y, bptr, _ptr(y),
+                                nthreads or default_threads())
     return y
 
 

@@ -182,6 +182,84 @@ void oracle_pack_weights(const float* w, int64_t N, int64_t K, int bits,
     free(tmp);
 }
 
+/* ------------------------------------------------------------------ */
+/* Asymmetric per-channel weights (Section 5.1: both the W8A8 and the W4A8
+ * settings quantize weights asymmetrically, using the full range of the
+ * format).  Each output row n is quantized like an activation tensor with
+ * the quantizer of Eq.(2)-(4) at bits 8 or 4: the range is the row's
+ * [min, max] over its finite values, widened to contain 0;
+ *   alpha_n = (hi - lo) / (2^bits - 1)   (in fp64, then to fp32)
+ *   beta_n  = lo / alpha_n,  zp_n = clamp(rint(-beta_n), 0, 2^bits - 1)
+ *                                   - 2^(bits-1)              (signed)
+ *   q = clamp(rint(w / alpha_n) + zp_n, -2^(bits-1), 2^(bits-1) - 1)
+ * with w / alpha_n one fp32 division limited to +-2^20 (NaN -> the low
+ * end) as in the activation quantizer.  A zero-width range (or one whose
+ * alpha_n would not be a positive finite fp32) takes alpha_n = 1 and
+ * beta_n = 0, so an all-zero row stores zp_n = -2^(bits-1) everywhere.
+ * colsum[n] = sum_k q[n][k]; int4 packs two codes per byte, low nibble =
+ * even k.                                                              */
+/* ------------------------------------------------------------------ */
+void oracle_pack_weights_asym(const float* w, int64_t N, int64_t K, int bits,
+                              void* w_q, float* w_scale, int32_t* w_zp,
+                              int32_t* colsum)
+{
+    const double q_max = (double)(((int64_t)1 << bits) - 1);   /* Eq.(2) */
+    const int64_t qlo = qmin_of(bits), qhi = qmax_of(bits);
+    const float lim = 1048576.0f; /* 2^20 */
+    int8_t* tmp = (int8_t*)malloc((size_t)K);
+    for (int64_t n = 0; n < N; ++n) {
+        const float* row = w + n * K;
+        double lo = 0.0, hi = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            if (!isfinite(row[k])) continue;
+            if (row[k] < lo) lo = row[k];
+            if (row[k] > hi) hi = row[k];
+        }
+        float alpha = 1.0f;
+        double beta = 0.0;
+        if (hi - lo != 0.0) {
+            float a = (float)((hi - lo) / q_max);                  /* Eq.(3) */
+            if (a > 0.0f && isfinite(a)) {
+                alpha = a;
+                beta = lo / (double)alpha;                         /* Eq.(3) */
+            }
+        }
+        double zu = rint(-beta);
+        if (zu < 0.0) zu = 0.0;
+        if (zu > q_max) zu = q_max;
+        const int32_t zp = (int32_t)((int64_t)zu - ((int64_t)1 << (bits - 1)));
+        int64_t sum = 0;
+        for (int64_t k = 0; k < K; ++k) {
+            float t = row[k] / alpha;                              /* Eq.(4) */
+            t = fminf(fmaxf(t, -lim), lim);
+            tmp[k] = (int8_t)clamp_i64((int64_t)rintf(t) + zp, qlo, qhi);
+            sum += tmp[k];
+        }
+        w_scale[n] = alpha;
+        w_zp[n] = zp;
+        colsum[n] = (int32_t)sum;
+        if (bits == 8) {
+            memcpy((int8_t*)w_q + n * K, tmp, (size_t)K);
+        } else {
+            uint8_t* dst = (uint8_t*)w_q + n * (K / 2);
+            for (int64_t j = 0; j < K / 2; ++j)
+                dst[j] = (uint8_t)(((unsigned)tmp[2 * j] & 0xFu) |
+                                   (((unsigned)tmp[2 * j + 1] & 0xFu) << 4));
+        }
+    }
+    free(tmp);
+}
+
+/* Row sums of the quantized activations, sum_k A_q[m][k].              */
+void oracle_act_rowsum(const int8_t* a_q, int64_t M, int64_t K, int32_t* rowsum)
+{
+    for (int64_t m = 0; m < M; ++m) {
+        int64_t s = 0;
+        for (int64_t k = 0; k < K; ++k) s += a_q[m * K + k];
+        rowsum[m] = (int32_t)s;
+    }
+}
+
 /* Weight code of row n, input channel k, read from the stored layout.
  * int4: the nibble is a two's-complement 4-bit integer.               */
 static int64_t weight_at(const void* w_q, int bits, int64_t K, int64_t n,
@@ -266,10 +344,12 @@ int64_t oracle_requant_value(int64_t c, int64_t M0, int32_t sh, int32_t zp_y,
 
 /* ------------------------------------------------------------------ */
 /* Integer-only linear layer (the hot path):
- *   c[m][n] = sat_int32( sum_k (A_q[m][k] - zp_a) * W_q[n][k] + bias_q[n] )
+ *   c[m][n] = sat_int32( sum_k (A_q[m][k] - zp_a) * (W_q[n][k] - zp_w[n])
+ *                        + bias_q[n] )
  *   Y_q[m][n] = requant(c[m][n])
- * The sum is the plain definition, accumulated exactly in int64 (integer
- * MACs with a wide accumulator: Section 1, Section 3.1).               */
+ * zp_w = 0 for symmetric weights.  The sum is the plain definition,
+ * accumulated exactly in int64 (integer MACs with a wide accumulator:
+ * Section 1, Section 3.1).                                              */
 /* ------------------------------------------------------------------ */
 typedef struct {
     const int8_t* a;
@@ -277,6 +357,7 @@ typedef struct {
     const void* w_q;
     int bits;
     const float* w_scale;
+    const int32_t* w_zp;
     float alpha_a;
     int32_t zp_a;
     float alpha_y;
@@ -296,10 +377,11 @@ static void* qlinear_rows(void* arg)
     for (int64_t m = j->row_begin; m < j->row_end; ++m) {
         const int8_t* arow = j->a + m * j->K;
         for (int64_t n = 0; n < j->N; ++n) {
+            const int64_t zw = j->w_zp ? j->w_zp[n] : 0;
             int64_t acc = 0;
             for (int64_t k = 0; k < j->K; ++k)
                 acc += ((int64_t)arow[k] - j->zp_a) *
-                       weight_at(j->w_q, j->bits, j->K, n, k);
+                       (weight_at(j->w_q, j->bits, j->K, n, k) - zw);
             int64_t c = clamp_i64(acc + j->bq[n], INT32_MIN, INT32_MAX);
             int64_t v = oracle_requant_value(c, j->M0[n], j->sh[n], j->zp_y,
                                              j->bits_y);
@@ -309,10 +391,11 @@ static void* qlinear_rows(void* arg)
     return NULL;
 }
 
-void oracle_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
-                    const void* w_q, int bits, const float* w_scale,
-                    float alpha_a, int32_t zp_a, float alpha_y, int32_t zp_y,
-                    int bits_y, const float* bias, void* y_q, int nthreads)
+void oracle_qlinear_asym(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                         const void* w_q, int bits, const float* w_scale,
+                         const int32_t* w_zp, float alpha_a, int32_t zp_a,
+                         float alpha_y, int32_t zp_y, int bits_y,
+                         const float* bias, void* y_q, int nthreads)
 {
     int64_t* M0 = (int64_t*)malloc(sizeof(int64_t) * (size_t)N);
     int32_t* sh = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
@@ -325,7 +408,7 @@ void oracle_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
     pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
     qlinear_job* jobs = (qlinear_job*)malloc(sizeof(qlinear_job) * (size_t)nthreads);
     for (int t = 0; t < nthreads; ++t) {
-        qlinear_job j = {a_q, M, K, N, w_q, bits, w_scale, alpha_a, zp_a,
+        qlinear_job j = {a_q, M, K, N, w_q, bits, w_scale, w_zp, alpha_a, zp_a,
                          alpha_y, zp_y, bits_y, bias, y_q,
                          M * t / nthreads, M * (t + 1) / nthreads, M0, sh, bq};
         jobs[t] = j;
@@ -337,6 +420,16 @@ void oracle_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
     free(M0);
     free(sh);
     free(bq);
+}
+
+/* Symmetric weights: zp_w = 0.                                         */
+void oracle_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                    const void* w_q, int bits, const float* w_scale,
+                    float alpha_a, int32_t zp_a, float alpha_y, int32_t zp_y,
+                    int bits_y, const float* bias, void* y_q, int nthreads)
+{
+    oracle_qlinear_asym(a_q, M, K, N, w_q, bits, w_scale, NULL, alpha_a, zp_a,
+                        alpha_y, zp_y, bits_y, bias, y_q, nthreads);
 }
 
 /* The raw integer product sum_k A_q[m][k] * W_q[n][k] (no zero-point, no

@@ -25,13 +25,15 @@ def sat(v: int, bits: int) -> int:
     return max(lo, min(hi, v))
 
 
-def qlinear_exact(A, W, zp_a, bias_q, M0, sh, zp_y, out_bits):
-    """Y from nested lists: A [M][K], W [N][K], per-column bias_q/M0/sh."""
+def qlinear_exact(A, W, zp_a, bias_q, M0, sh, zp_y, out_bits, zp_w=None):
+    """Y from nested lists: A [M][K], W [N][K], per-column bias_q/M0/sh and
+    optional per-column weight zero-points zp_w."""
     M, N = len(A), len(W)
     Y = [[0] * N for _ in range(M)]
     for m in range(M):
         for n in range(N):
-            c = sum((A[m][k] - zp_a) * W[n][k] for k in range(len(A[m])))
+            zw = 0 if zp_w is None else zp_w[n]
+            c = sum((A[m][k] - zp_a) * (W[n][k] - zw) for k in range(len(A[m])))
             c = sat(c + bias_q[n], 32)
             r = requant_exact(c, M0[n], sh[n])
             Y[m][n] = sat(r + zp_y, out_bits)

@@ -209,6 +209,109 @@ def test_int4_qlinear_reads_all_256_bytes():
 
 
 # ---------------------------------------------------------------------------
+# Section 5.1: asymmetric per-channel weights
+# ---------------------------------------------------------------------------
+def _asym_rows():
+    rng = np.random.default_rng(21)
+    N, K = 44, 96
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    w[3] = 0.0                                   # all zero
+    w[4] = np.abs(w[4]) + 0.01                   # all positive: range widened to 0
+    w[5] = -np.abs(w[5]) - 0.01                  # all negative
+    w[6] = 0.37                                  # constant
+    w[7, 9], w[7, 10], w[7, 11] = np.inf, np.nan, -np.inf   # ignored by the range
+    w[8] += 0.015                                # skewed: zero-point far from the middle
+    w[9, :] = np.linspace(-1e-3, 9e-3, K)        # evenly spread, skewed
+    w[10, :2] = [-3.0, 5.0]                      # outliers set the range
+    return w
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_asym_weight_quantizer_properties(bits):
+    w = _asym_rows()
+    N, K = w.shape
+    wq, scale, zp, colsum = oracle.pack_weights_asym(w, bits)
+    q_max = 2 ** bits - 1
+    qlo, qhi = -(2 ** (bits - 1)), 2 ** (bits - 1) - 1
+    q = wq.astype(np.int64) if bits == 8 else _unpack_nibbles(wq)
+    assert q.shape == (N, K) and q.min() >= qlo and q.max() <= qhi
+    assert np.array_equal(colsum.astype(np.int64), q.sum(axis=1))
+    for n in range(N):
+        fin = np.isfinite(w[n])
+        lo = min(float(w[n][fin].min()), 0.0)
+        hi = max(float(w[n][fin].max()), 0.0)
+        if hi == lo:
+            # degenerate range: unit scale, unsigned zero-point 0
+            assert scale[n] == 1.0 and zp[n] == qlo and np.all(q[n] == qlo), n
+            continue
+        # Eq.(3) alpha from the exact range width, rounded to fp32
+        alpha = np.float32(float((Fraction(hi) - Fraction(lo)) / q_max))
+        assert scale[n] == alpha, n
+        # Eq.(3) beta = f_min / alpha; the unsigned zero-point is -beta rounded
+        zu = int(zp[n]) - qlo
+        assert 0 <= zu <= q_max
+        assert abs(Fraction(zu) + Fraction(lo) / Fraction(float(alpha))) <= Fraction(1, 2) + Fraction(1, 10 ** 9)
+        # Eq.(4) codes: one IEEE fp32 division (numpy's), half-to-even, clamp
+        x = w[n][fin]
+        ref = np.clip(np.rint(x / np.float32(alpha)).astype(np.int64) + zp[n], qlo, qhi)
+        assert np.array_equal(q[n][fin], ref), n
+        # zero is exactly representable and the range ends land on the grid ends
+        if lo < 0:
+            assert q[n][fin][np.argmin(x)] <= qlo + 1
+        if hi > 0:
+            assert q[n][fin][np.argmax(x)] >= qhi - 1
+        # reconstruction error within half a step over the whole range; at
+        # the top end the fp32 rounding of alpha can add q_max * 2^-24 steps
+        # when both ends round outwards (a tie at each end)
+        err = np.abs(x.astype(np.float64) - float(alpha) * (q[n][fin] - zp[n]))
+        assert np.max(err) <= float(alpha) * (0.5 + q_max * 2.0 ** -22), n
+    # a zero weight stores the zero-point
+    z = np.zeros((3, 8), np.float32)
+    z[:, 0] = [-1.0, 0.5, 2.0]
+    zq, _, zzp, _ = oracle.pack_weights_asym(z, bits)
+    zqi = zq.astype(np.int64) if bits == 8 else _unpack_nibbles(zq)
+    assert np.array_equal(zqi[:, 1:], np.repeat(zzp.astype(np.int64)[:, None], 7, axis=1))
+    # non-finite entries: +inf -> top of the grid, -inf and NaN -> bottom
+    assert q[7, 9] == qhi and q[7, 10] == qlo and q[7, 11] == qlo
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_asym_step_never_exceeds_the_symmetric_one(bits):
+    # (max - min)/(2^b - 1) <= 2 max|w| / (2^b - 1) < max|w| / (2^(b-1) - 1)
+    w = _asym_rows()
+    w = np.where(np.isfinite(w), w, 0.0).astype(np.float32)
+    _, s_asym, _, _ = oracle.pack_weights_asym(w, bits)
+    _, s_sym, _ = oracle.pack_weights(w, bits)
+    nz = np.abs(w).max(axis=1) > 0
+    assert np.all(s_asym[nz] < s_sym[nz])
+
+
+def test_asym_int8_rows_match_the_activation_quantizer():
+    # Section 5.1 applies the Eq.(2)-(4) quantizer per weight row: at 8 bits
+    # each row equals the (separately pinned) per-tensor activation
+    # quantizer run on that row's range
+    w = _asym_rows()
+    w = np.where(np.isfinite(w), w, 0.0).astype(np.float32)
+    wq, scale, zp, _ = oracle.pack_weights_asym(w, 8)
+    for n in range(w.shape[0]):
+        if w[n].min() == w[n].max() == 0.0:
+            continue
+        a, z = oracle.act_params(float(w[n].min()), float(w[n].max()), 8)
+        assert (scale[n], zp[n]) == (a, z)
+        assert np.array_equal(oracle.quantize_act(w[n], a, z, 8), wq[n])
+
+
+def test_act_rowsum_matches_numpy():
+    rng = np.random.default_rng(22)
+    for M, K in [(1, 1), (3, 7), (17, 300), (5, 65536)]:
+        a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+        assert np.array_equal(oracle.act_rowsum(a).astype(np.int64), a.astype(np.int64).sum(axis=1))
+    a = np.full((2, 65536), -128, np.int8)
+    a[1] = 127
+    assert oracle.act_rowsum(a).tolist() == [-128 * 65536, 127 * 65536]
+
+
+# ---------------------------------------------------------------------------
 # Integer accumulation and fixed-point requantization
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("shape", [(1, 1, 1), (3, 5, 2), (16, 64, 33), (67, 130, 96)])
@@ -383,6 +486,102 @@ def test_qlinear_bruteforce_tiny(bits, out_bits):
                 ref = bf.qlinear_exact(a.astype(int).tolist(), wv.tolist(), zp_a, bq, M0, sh,
                                        zp_y, out_bits)
                 assert y.astype(int).tolist() == ref, (M, N, K)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("out_bits", [8, 16])
+def test_qlinear_asym_bruteforce_tiny(bits, out_bits):
+    rng = np.random.default_rng(30 + bits + out_bits)
+    sizes = [1, 2, 3, 6]
+    qlo, qhi = -(2 ** (bits - 1)), 2 ** (bits - 1) - 1
+    for M in sizes:
+        for N in sizes:
+            for K in sizes:
+                if bits == 4 and K % 2:
+                    continue
+                a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+                wv = rng.integers(qlo, qhi + 1, (N, K))
+                wv[0, 0] = qlo
+                zw = rng.integers(qlo, qhi + 1, N).astype(np.int32)
+                zw[0] = qhi
+                if bits == 8:
+                    wq = wv.astype(np.int8)
+                else:
+                    wq = ((wv[:, 0::2] & 0xF) | ((wv[:, 1::2] & 0xF) << 4)).astype(np.uint8)
+                w_scale = rng.uniform(1e-3, 3e-2, N).astype(np.float32)
+                bias = rng.normal(0, 0.05, N).astype(np.float32) if N % 2 else None
+                alpha_a = float(np.float32(rng.uniform(0.01, 0.5)))
+                zp_a = int(rng.choice([-128, -3, 0, 40, 127]))
+                alpha_y = float(np.float32(rng.uniform(0.001, 0.2) * (1e-2 if out_bits == 16 else 1)))
+                zp_y = int(rng.integers(-100, 100))
+                y = oracle.qlinear(a, wq, bits, w_scale, alpha_a, zp_a, alpha_y, zp_y, out_bits,
+                                   bias=bias, nthreads=2, w_zp=zw)
+                M0, sh, bq = _exact_params(alpha_a, w_scale, alpha_y, bias)
+                ref = bf.qlinear_exact(a.astype(int).tolist(), wv.tolist(), zp_a, bq, M0, sh,
+                                       zp_y, out_bits, zp_w=zw.tolist())
+                assert y.astype(int).tolist() == ref, (M, N, K)
+
+
+def test_qlinear_asym_textbook_reduction_and_decomposition():
+    # unit rescale: the layer is (A - zp_a)(W - zp_w)^T + zp_y, numpy int64;
+    # the same value expands into the four terms a kernel can evaluate:
+    # A W^T - zp_a colsum - zp_w rowsum + K zp_a zp_w
+    rng = np.random.default_rng(31)
+    M, K, N = 29, 300, 37
+    a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    w = rng.integers(-128, 128, (N, K)).astype(np.int8)
+    zw = rng.integers(-128, 128, N).astype(np.int32)
+    zp_a, zp_y = -21, 7
+    y = oracle.qlinear(a, w, 8, np.full(N, 0.25, np.float32), 0.5, zp_a, 0.125, zp_y, 16,
+                       w_zp=zw)
+    c = (a.astype(np.int64) - zp_a) @ (w.astype(np.int64) - zw.astype(np.int64)[:, None]).T
+    assert np.array_equal(y.astype(np.int64), np.clip(c + zp_y, -32768, 32767))
+    rowsum = oracle.act_rowsum(a).astype(np.int64)
+    colsum = w.astype(np.int64).sum(axis=1)
+    terms = (oracle.int_matmul(a, w, 8) - zp_a * colsum[None, :] - zw[None, :] * rowsum[:, None]
+             + K * zp_a * zw[None, :].astype(np.int64))
+    assert np.array_equal(terms, c)
+
+
+def test_qlinear_zero_weight_zero_points_reduce_to_symmetric():
+    rng = np.random.default_rng(32)
+    M, K, N = 11, 64, 19
+    a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    w = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    ws = rng.uniform(0.001, 0.01, N).astype(np.float32)
+    b = rng.normal(0, 0.1, N).astype(np.float32)
+    args = (a, w, 8, ws, 0.07, 5, 0.02, -3, 8)
+    assert np.array_equal(oracle.qlinear(*args, bias=b, w_zp=np.zeros(N, np.int32)),
+                          oracle.qlinear(*args, bias=b))
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_qlinear_asym_dequantized_output_tracks_the_layer(bits):
+    # the integer pipeline computes dequant(A) dequant(W)^T + b, with
+    # dequant(W) = w_scale (W_q - zp_w), exactly up to the output rounding
+    # and the rounding of the bias to accumulator units
+    rng = np.random.default_rng(33 + bits)
+    M, K, N = 16, 256, 48
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    w = (rng.standard_normal((N, K)) * 0.02 + 0.01).astype(np.float32)
+    b = (rng.standard_normal(N) * 0.01).astype(np.float32)
+    alpha_a, zp_a = oracle.act_params(float(x.min()), float(x.max()), 8)
+    a = oracle.quantize_act(x, alpha_a, zp_a, 8)
+    wq, ws, zw, _ = oracle.pack_weights_asym(w, bits)
+    q = wq.astype(np.float64) if bits == 8 else _unpack_nibbles(wq).astype(np.float64)
+    w_deq = ws[:, None].astype(np.float64) * (q - zw[:, None])
+    a_deq = alpha_a * (a.astype(np.float64) - zp_a)
+    pipe = a_deq @ w_deq.T + b
+    alpha_y, zp_y = oracle.act_params(float(pipe.min()) * 1.1, float(pipe.max()) * 1.1, 16)
+    y = oracle.qlinear(a, wq, bits, ws, alpha_a, zp_a, alpha_y, zp_y, 16, bias=b, w_zp=zw)
+    deq = oracle.dequant(y, alpha_y, zp_y).astype(np.float64)
+    assert np.max(np.abs(deq - pipe)) <= alpha_y * 0.5 + alpha_a * ws.max() * 0.5 + 1e-6
+    # the asymmetric grid beats the symmetric one on these shifted weights
+    wq_s, ws_s, _ = oracle.pack_weights(w, bits)
+    qs = wq_s.astype(np.float64) if bits == 8 else _unpack_nibbles(wq_s).astype(np.float64)
+    err_asym = np.abs(w_deq - w).mean()
+    err_sym = np.abs(ws_s[:, None] * qs - w).mean()
+    assert err_asym < err_sym
 
 
 def test_qlinear_textbook_reduction():
