@@ -13,8 +13,8 @@ Functions and the passages they follow (arXiv 2408.13933):
 * ``dequant``         -- inverse of Eq.(4)
 * ``fold_weights`` / ``fold_acts`` -- Section 3.2, Eq.(1) (S W and X S^-1)
 * ``pack_weights``    -- Section 5.1 / appendix: symmetric per-channel W8, W4
-* ``pack_weights_asym`` -- Section 5.1: asymmetric per-channel W8, W4 (the
-  quantizer of Eq.(2)-(4) applied per output row)
+* ``pack_weights_asym`` -- Section 5.1: asymmetric W8, W4 (the quantizer of
+  Eq.(2)-(4) over each output row's range, or the whole matrix's)
 * ``act_rowsum``      -- sum_k A_q[m][k] (the zero-point cross term)
 * ``requant_params`` / ``requant_value`` -- fixed-point rescale to the next
   layer's integer format (Section 1, Section 3.1: integer-only arithmetic)
@@ -71,7 +71,8 @@ def _load():
                                         _vp, _f32p, _i32p]
     lib.oracle_pack_weights.restype = None
     lib.oracle_pack_weights_asym.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64,
-                                             ctypes.c_int, _vp, _f32p, _i32p, _i32p]
+                                             ctypes.c_int, ctypes.c_int, _vp, _f32p, _i32p,
+                                             _i32p]
     lib.oracle_pack_weights_asym.restype = None
     lib.oracle_act_rowsum.argtypes = [_i8p, ctypes.c_int64, ctypes.c_int64, _i32p]
     lib.oracle_act_rowsum.restype = None
@@ -202,12 +203,13 @@ def _packed_weight_buffer(N: int, K: int, bits: int) -> np.ndarray:
     raise ValueError("bits must be 8 or 4")
 
 
-def pack_weights_asym(w: np.ndarray, bits: int):
-    """Asymmetric per-output-channel quantizer and packer (Section 5.1).
+def pack_weights_asym(w: np.ndarray, bits: int, per_tensor: bool = False):
+    """Asymmetric weight quantizer and packer (Section 5.1), one range per
+    output channel or (per_tensor) one for the whole matrix.
 
-    Returns (w_q, w_scale, w_zp, colsum); codes are signed (the unsigned
-    Eq.(4) code minus 2^(bits-1)), w_zp is the signed zero-point, colsum
-    the row sum of the stored codes.
+    Returns (w_q, w_scale, w_zp, colsum), all per output row; codes are
+    signed (the unsigned Eq.(4) code minus 2^(bits-1)), w_zp is the signed
+    zero-point, colsum the row sum of the stored codes.
     """
     w = np.ascontiguousarray(w, dtype=np.float32)
     N, K = w.shape
@@ -215,7 +217,8 @@ def pack_weights_asym(w: np.ndarray, bits: int):
     scale = np.empty(N, dtype=np.float32)
     zp = np.empty(N, dtype=np.int32)
     colsum = np.empty(N, dtype=np.int32)
-    _load().oracle_pack_weights_asym(w, N, K, bits, _ptr(wq), scale, zp, colsum)
+    _load().oracle_pack_weights_asym(w, N, K, bits, int(bool(per_tensor)), _ptr(wq), scale, zp,
+                                     colsum)
     return wq, scale, zp, colsum
 
 

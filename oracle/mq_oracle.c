@@ -183,51 +183,75 @@ void oracle_pack_weights(const float* w, int64_t N, int64_t K, int bits,
 }
 
 /* ------------------------------------------------------------------ */
-/* Asymmetric per-channel weights (Section 5.1: both the W8A8 and the W4A8
- * settings quantize weights asymmetrically, using the full range of the
- * format).  Each output row n is quantized like an activation tensor with
- * the quantizer of Eq.(2)-(4) at bits 8 or 4: the range is the row's
- * [min, max] over its finite values, widened to contain 0;
- *   alpha_n = (hi - lo) / (2^bits - 1)   (in fp64, then to fp32)
- *   beta_n  = lo / alpha_n,  zp_n = clamp(rint(-beta_n), 0, 2^bits - 1)
- *                                   - 2^(bits-1)              (signed)
- *   q = clamp(rint(w / alpha_n) + zp_n, -2^(bits-1), 2^(bits-1) - 1)
- * with w / alpha_n one fp32 division limited to +-2^20 (NaN -> the low
+/* Asymmetric weights (Section 5.1: both the W8A8 and the W4A8 settings
+ * quantize weights asymmetrically, using the full range of the format;
+ * W8A8 takes one range per tensor except for the MLP down projection,
+ * W4A8 one range per output channel).  The weights are quantized like an
+ * activation tensor with the quantizer of Eq.(2)-(4) at bits 8 or 4, over
+ * the range [min, max] of the finite values of a row (per channel) or of
+ * the whole matrix (per tensor), widened to contain 0:
+ *   alpha = (hi - lo) / (2^bits - 1)   (in fp64, then to fp32)
+ *   beta  = lo / alpha,  zp = clamp(rint(-beta), 0, 2^bits - 1)
+ *                             - 2^(bits-1)                     (signed)
+ *   q = clamp(rint(w / alpha) + zp, -2^(bits-1), 2^(bits-1) - 1)
+ * with w / alpha one fp32 division limited to +-2^20 (NaN -> the low
  * end) as in the activation quantizer.  A zero-width range (or one whose
- * alpha_n would not be a positive finite fp32) takes alpha_n = 1 and
- * beta_n = 0, so an all-zero row stores zp_n = -2^(bits-1) everywhere.
+ * alpha would not be a positive finite fp32) takes alpha = 1 and beta = 0,
+ * so an all-zero range stores zp = -2^(bits-1) everywhere.  The per-row
+ * outputs w_scale[n], w_zp[n] repeat the tensor's values per tensor.
  * colsum[n] = sum_k q[n][k]; int4 packs two codes per byte, low nibble =
  * even k.                                                              */
 /* ------------------------------------------------------------------ */
-void oracle_pack_weights_asym(const float* w, int64_t N, int64_t K, int bits,
-                              void* w_q, float* w_scale, int32_t* w_zp,
-                              int32_t* colsum)
+static void finite_range(const float* v, int64_t n, double* lo, double* hi)
+{
+    *lo = 0.0;
+    *hi = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        if (!isfinite(v[i])) continue;
+        if (v[i] < *lo) *lo = v[i];
+        if (v[i] > *hi) *hi = v[i];
+    }
+}
+
+static void asym_format(double lo, double hi, int bits, float* alpha_out, int32_t* zp_out)
 {
     const double q_max = (double)(((int64_t)1 << bits) - 1);   /* Eq.(2) */
+    float alpha = 1.0f;
+    double beta = 0.0;
+    if (hi - lo != 0.0) {
+        float a = (float)((hi - lo) / q_max);                  /* Eq.(3) */
+        if (a > 0.0f && isfinite(a)) {
+            alpha = a;
+            beta = lo / (double)alpha;                         /* Eq.(3) */
+        }
+    }
+    double zu = rint(-beta);
+    if (zu < 0.0) zu = 0.0;
+    if (zu > q_max) zu = q_max;
+    *alpha_out = alpha;
+    *zp_out = (int32_t)((int64_t)zu - ((int64_t)1 << (bits - 1)));
+}
+
+void oracle_pack_weights_asym(const float* w, int64_t N, int64_t K, int bits,
+                              int per_tensor, void* w_q, float* w_scale,
+                              int32_t* w_zp, int32_t* colsum)
+{
     const int64_t qlo = qmin_of(bits), qhi = qmax_of(bits);
     const float lim = 1048576.0f; /* 2^20 */
+    double lo, hi;
+    float alpha = 1.0f;
+    int32_t zp = 0;
+    if (per_tensor) {
+        finite_range(w, N * K, &lo, &hi);
+        asym_format(lo, hi, bits, &alpha, &zp);
+    }
     int8_t* tmp = (int8_t*)malloc((size_t)K);
     for (int64_t n = 0; n < N; ++n) {
         const float* row = w + n * K;
-        double lo = 0.0, hi = 0.0;
-        for (int64_t k = 0; k < K; ++k) {
-            if (!isfinite(row[k])) continue;
-            if (row[k] < lo) lo = row[k];
-            if (row[k] > hi) hi = row[k];
+        if (!per_tensor) {
+            finite_range(row, K, &lo, &hi);
+            asym_format(lo, hi, bits, &alpha, &zp);
         }
-        float alpha = 1.0f;
-        double beta = 0.0;
-        if (hi - lo != 0.0) {
-            float a = (float)((hi - lo) / q_max);                  /* Eq.(3) */
-            if (a > 0.0f && isfinite(a)) {
-                alpha = a;
-                beta = lo / (double)alpha;                         /* Eq.(3) */
-            }
-        }
-        double zu = rint(-beta);
-        if (zu < 0.0) zu = 0.0;
-        if (zu > q_max) zu = q_max;
-        const int32_t zp = (int32_t)((int64_t)zu - ((int64_t)1 << (bits - 1)));
         int64_t sum = 0;
         for (int64_t k = 0; k < K; ++k) {
             float t = row[k] / alpha;                              /* Eq.(4) */

@@ -301,6 +301,45 @@ def test_asym_int8_rows_match_the_activation_quantizer():
         assert np.array_equal(oracle.quantize_act(w[n], a, z, 8), wq[n])
 
 
+@pytest.mark.parametrize("bits", [8, 4])
+def test_asym_per_tensor_weights(bits):
+    # Section 5.1 W8A8: one range for the whole matrix.  Every row then
+    # carries the same (alpha, zp), derived from the exact range of all
+    # finite entries, and the codes are Eq.(4) with those.
+    w = _asym_rows()
+    N, K = w.shape
+    wq, scale, zp, colsum = oracle.pack_weights_asym(w, bits, per_tensor=True)
+    fin = np.isfinite(w)
+    lo, hi = min(float(w[fin].min()), 0.0), max(float(w[fin].max()), 0.0)
+    q_max = 2 ** bits - 1
+    qlo, qhi = -(2 ** (bits - 1)), 2 ** (bits - 1) - 1
+    alpha = np.float32(float((Fraction(hi) - Fraction(lo)) / q_max))
+    assert np.all(scale == alpha) and np.all(zp == zp[0])
+    zu = int(zp[0]) - qlo
+    assert abs(Fraction(zu) + Fraction(lo) / Fraction(float(alpha))) <= Fraction(1, 2) + Fraction(1, 10 ** 9)
+    q = wq.astype(np.int64) if bits == 8 else _unpack_nibbles(wq)
+    ref = np.clip(np.rint(np.where(fin, w, 0) / alpha).astype(np.int64) + zp[0], qlo, qhi)
+    assert np.array_equal(q[fin], ref[fin])
+    assert np.array_equal(colsum.astype(np.int64), q.sum(axis=1))
+    # the per-tensor step is at least the largest per-channel step (rows
+    # with a zero-width range take the unit step and are left out)
+    _, s_ch, _, _ = oracle.pack_weights_asym(w, bits)
+    live = np.array([np.ptp(np.append(r[np.isfinite(r)], 0.0)) > 0 for r in w])
+    assert alpha >= s_ch[live].max()
+    # the extremes in the first and the last row set the range
+    e = (np.random.default_rng(23).standard_normal((5, 8)) * 0.1).astype(np.float32)
+    e[0, 0], e[-1, -1] = -2.0, 3.0
+    _, es, ez, _ = oracle.pack_weights_asym(e, bits, per_tensor=True)
+    assert np.all(es == np.float32(5.0 / q_max))
+    assert np.all(ez == int(round(2.0 / float(np.float32(5.0 / q_max)))) + qlo)
+    if bits == 8:
+        # and it is the per-tensor activation quantizer on the flattened matrix
+        wf = np.where(fin, w, 0).astype(np.float32)
+        a, z = oracle.act_params(float(wf.min()), float(wf.max()), 8)
+        assert (float(alpha), int(zp[0])) == (a, z)
+        assert np.array_equal(oracle.quantize_act(wf, a, z, 8)[fin], wq[fin])
+
+
 def test_act_rowsum_matches_numpy():
     rng = np.random.default_rng(22)
     for M, K in [(1, 1), (3, 7), (17, 300), (5, 65536)]:
