@@ -149,11 +149,16 @@ class Prepared:
             w = torch.from_numpy(ld.w).to(dev)
             if ld.s is not None:
                 w = mq.mq_fold_weights(w, torch.from_numpy(ld.s).to(dev))
-            w_q, w_scale, w_colsum = mq.mq_pack_weights(w, layer.w_bits)
+            w_zp = None
+            if layer.asym:
+                w_q, w_scale, w_zp, w_colsum = mq.mq_pack_weights_asym(
+                    w, layer.w_bits, per_tensor=layer.per_tensor)
+            else:
+                w_q, w_scale, w_colsum = mq.mq_pack_weights(w, layer.w_bits)
             del w
             a_scale, a_zp = mq.mq_act_params(*ld.act_range, 8)
             out_scale, out_zp = mq.mq_act_params(*ld.out_range, layer.out_bits)
-            entry = dict(layer=layer, data=ld, key=key, w_q=w_q, w_scale=w_scale,
+            entry = dict(layer=layer, data=ld, key=key, w_q=w_q, w_scale=w_scale, w_zp=w_zp,
                          w_colsum=w_colsum, a_scale=a_scale, a_zp=a_zp, out_scale=out_scale,
                          out_zp=out_zp,
                          bias=None if ld.bias is None else torch.from_numpy(ld.bias).to(dev))
@@ -166,7 +171,11 @@ class Prepared:
                 x = torch.from_numpy(e["data"].x).to(dev)
                 self.inputs[e["key"]] = dict(x=x, q=torch.empty(x.shape, dtype=torch.int8,
                                                                 device=dev),
-                                             scale=e["a_scale"], zp=e["a_zp"])
+                                             scale=e["a_scale"], zp=e["a_zp"], rs=None)
+            if e["layer"].asym and self.inputs[e["key"]]["rs"] is None:
+                # asymmetric weights read the row sums of their quantized input
+                self.inputs[e["key"]]["rs"] = torch.empty(e["layer"].M, dtype=torch.int32,
+                                                          device=dev)
         for e in self.layers:
             L = e["layer"]
             e["y"] = torch.empty((L.M, L.N), dtype=torch.int8 if L.out_bits == 8 else torch.int16,
@@ -182,13 +191,25 @@ class Prepared:
         self.deq = torch.empty(last["y"].shape, dtype=torch.float32, device=dev)
         torch.cuda.synchronize()
 
+    def qlinear(self, e, w_q=None, workspace=None):
+        """One qlinear launch of layer entry e on its already quantized input
+        (and, for asymmetric weights, its row sums)."""
+        L = e["layer"]
+        inp = self.inputs[e["key"]]
+        w_q = e["w_q"] if w_q is None else w_q
+        if L.asym:
+            self.mq.mq_qlinear_asym(inp["q"], inp["rs"], w_q, L.w_bits, e["w_scale"], e["w_zp"],
+                                    e["w_colsum"], e["a_scale"], e["a_zp"], e["out_scale"],
+                                    e["out_zp"], L.out_bits, bias=e["bias"], out=e["y"],
+                                    workspace=workspace)
+        else:
+            self.mq.mq_qlinear(inp["q"], w_q, L.w_bits, e["w_scale"], e["w_colsum"],
+                               e["a_scale"], e["a_zp"], e["out_scale"], e["out_zp"], L.out_bits,
+                               bias=e["bias"], out=e["y"], workspace=workspace)
+
     def launch_layer(self, i):
         """One qlinear launch of layer i on its already quantized input."""
-        e = self.layers[i]
-        L = e["layer"]
-        self.mq.mq_qlinear(self.inputs[e["key"]]["q"], e["w_q"], L.w_bits, e["w_scale"],
-                           e["w_colsum"], e["a_scale"], e["a_zp"], e["out_scale"], e["out_zp"],
-                           L.out_bits, bias=e["bias"], out=e["y"], workspace=self.workspace)
+        self.qlinear(self.layers[i], workspace=self.workspace)
 
     def step(self, events=None, dom=()):
         """One pass of the hot path.  `events` = (start, end) recorded around
@@ -196,14 +217,12 @@ class Prepared:
         mq = self.mq
         for inp in self.inputs.values():
             mq.mq_quantize_act(inp["x"], inp["scale"], inp["zp"], 8, out=inp["q"])
+            if inp["rs"] is not None:
+                mq.mq_act_rowsum(inp["q"], out=inp["rs"])
         for i, e in enumerate(self.layers):
-            L = e["layer"]
-            a = self.inputs[e["key"]]["q"]
             if events is not None and dom and i == dom[0]:
                 events[0].record()
-            mq.mq_qlinear(a, e["w_q"], L.w_bits, e["w_scale"], e["w_colsum"], e["a_scale"],
-                          e["a_zp"], e["out_scale"], e["out_zp"], L.out_bits, bias=e["bias"],
-                          out=e["y"], workspace=self.workspace)
+            self.qlinear(e, workspace=self.workspace)
             if events is not None and dom and i == dom[-1]:
                 events[1].record()
         last = self.layers[-1]
@@ -223,11 +242,9 @@ def cold_graph_us(prep: Prepared, i: int, min_bytes: int = 512 * 10**6, replays:
     wbytes = e["w_q"].numel()
     copies = max(2, -(-min_bytes // wbytes))
     ws = [e["w_q"]] + [e["w_q"].clone() for _ in range(copies - 1)]
-    a = prep.inputs[e["key"]]["q"]
 
     def launch(w):
-        prep.mq.mq_qlinear(a, w, L.w_bits, e["w_scale"], e["w_colsum"], e["a_scale"], e["a_zp"],
-                           e["out_scale"], e["out_zp"], L.out_bits, bias=e["bias"], out=e["y"])
+        prep.qlinear(e, w_q=w)
 
     for w in ws:
         launch(w)
@@ -261,17 +278,18 @@ def cpu_baseline(prep: Prepared, target_s: float):
     w_host = []
     for e in prep.layers:
         w_host.append((e["w_q"].cpu().numpy(), e["w_scale"].cpu().numpy(),
-                       None if e["bias"] is None else e["bias"].cpu().numpy()))
+                       None if e["bias"] is None else e["bias"].cpu().numpy(),
+                       None if e["w_zp"] is None else e["w_zp"].cpu().numpy()))
 
     def run(rows):
         ops = 0
         t0 = time.perf_counter()
-        for e, (wq, ws, b) in zip(prep.layers, w_host):
+        for e, (wq, ws, b, zw) in zip(prep.layers, w_host):
             L = e["layer"]
             x = e["data"].x[:rows]
             a = oracle.quantize_act(x, e["a_scale"], e["a_zp"], 8)
             oracle.qlinear(a, wq, L.w_bits, ws, e["a_scale"], e["a_zp"], e["out_scale"],
-                           e["out_zp"], L.out_bits, bias=b, nthreads=nthreads)
+                           e["out_zp"], L.out_bits, bias=b, nthreads=nthreads, w_zp=zw)
             ops += 2 * rows * L.N * L.K
         return ops, time.perf_counter() - t0
 

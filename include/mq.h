@@ -211,6 +211,68 @@ mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
                         int64_t workspace_bytes, int32_t path, void* stream);
 
 /*
+ * mq_pack_weights_asym -- asymmetric weight quantizer and packer (Section
+ * 5.1: the W8A8 and W4A8 settings quantize weights asymmetrically over the
+ * full integer range; W8A8 with one range per tensor except the MLP down
+ * projection, W4A8 per output channel).  The Eq.(2)-(4) quantizer runs
+ * over the range lo = min(0, min w), hi = max(0, max w) of the finite
+ * entries of row n (per_tensor = 0) or of the whole matrix (per_tensor = 1):
+ *   w_scale[n] = (float)((hi - lo) / (2^bits - 1))       (fp64, then fp32)
+ *   w_zp[n]    = clamp(rint(-lo / w_scale[n]), 0, 2^bits - 1) - 2^(bits-1)
+ *   q[n][k]    = clamp(rint(w[n][k] / w_scale[n]) + w_zp[n],
+ *                      -2^(bits-1), 2^(bits-1) - 1)
+ * with one IEEE fp32 division limited to +-2^20 (NaN ends at the low end).
+ * A zero-width range gives w_scale 1 and w_zp -2^(bits-1).  Per tensor,
+ * every row repeats the tensor's scale and zero-point, so the layer call
+ * is the same for both granularities.
+ *   w         device fp32 [N][K]
+ *   bits      8 -> w_q int8 [N][K];  4 -> w_q uint8 [N][K/2] (K even,
+ *             low nibble = even k)
+ *   per_tensor  0 or 1
+ *   w_scale   device fp32 [N]     w_zp  device int32 [N] (per tensor both
+ *             also hold the per-row ranges between the launches of the call)
+ *   w_colsum  device int32 [N], sum_k q[n][k]
+ *   1 <= K <= MQ_MAX_K.
+ */
+mq_status mq_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bits,
+                               int32_t per_tensor, void* w_q, float* w_scale,
+                               int32_t* w_zp, int32_t* w_colsum, void* stream);
+
+/*
+ * mq_act_rowsum -- rowsum[m] = sum_k a_q[m][k] (int32), the per-token
+ * term the weight zero-points of mq_qlinear_asym multiply.  Compute it once
+ * per quantized activation and share it among the layers that read it.
+ *   a_q     device int8 [M][K]     rowsum  device int32 [M]
+ *   M >= 0 (0 -> nothing to do), 1 <= K <= MQ_MAX_K.
+ */
+mq_status mq_act_rowsum(const int8_t* a_q, int64_t M, int64_t K, int32_t* rowsum,
+                        void* stream);
+
+/*
+ * mq_qlinear_asym -- mq_qlinear_ws for asymmetric per-channel weights
+ * (Section 5.1).  For every token m and output channel n:
+ *   c = sat_int32( sum_k (A_q[m][k] - a_zp) * (W_q[n][k] - w_zp[n])
+ *                  + bias_q[n] )
+ * (the sum exact), then the requant of mq_qlinear.  The kernels evaluate
+ * it as acc - a_zp * w_colsum[n] - w_zp[n] * (a_rowsum[m] - K * a_zp)
+ * + bias_q[n].
+ *   a_rowsum  device int32 [M], sum_k A_q[m][k] as written by
+ *             mq_act_rowsum for this a_q (not checked: other values give
+ *             other results)
+ *   w_q, w_scale, w_zp, w_colsum  as written by mq_pack_weights_asym
+ *             (w_zp device int32 [N], within the signed range of w_bits)
+ *   everything else as in mq_qlinear_ws (same workspace rules; the split
+ *   decision does not depend on the zero-points).
+ */
+mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M,
+                          int64_t K, int64_t N, const void* w_q, int32_t w_bits,
+                          const float* w_scale, const int32_t* w_zp,
+                          const int32_t* w_colsum, float a_scale, int32_t a_zp,
+                          float out_scale, int32_t out_zp, int32_t out_bits,
+                          const float* bias, void* y_q, void* workspace,
+                          int64_t workspace_bytes, int32_t path, void* stream);
+
+/*
  * mq_dequant -- inverse of Eq.(4): y = alpha * (float)(q - zp), one exact
  * integer subtraction and one fp32 multiply.
  *   q      device int8 (bits 8) or int16 (bits 16) [numel]

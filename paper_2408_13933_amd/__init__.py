@@ -15,6 +15,7 @@ import os
 __all__ = [
     "MQError", "lib", "lib_path", "mq_version", "mq_act_params", "mq_fold_weights",
     "mq_fold_acts", "mq_quantize_act", "mq_pack_weights", "mq_qlinear", "mq_dequant",
+    "mq_pack_weights_asym", "mq_act_rowsum", "mq_qlinear_asym", "mq_qlinear_workspace_bytes",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
 ]
 
@@ -69,8 +70,15 @@ def lib():
     L.mq_qlinear_workspace_bytes.argtypes = [c_i64, c_i64, c_i64, c_i32, c_i32]
     L.mq_qlinear_workspace_bytes.restype = c_i64
     L.mq_dequant.argtypes = [c_p, c_i32, c_i64, c_f, c_i32, c_p, c_p]
+    L.mq_pack_weights_asym.argtypes = [c_p, c_i64, c_i64, c_i32, c_i32, c_p, c_p, c_p, c_p,
+                                       c_p]
+    L.mq_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_p, c_p]
+    L.mq_qlinear_asym.argtypes = [c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_p,
+                                  c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p, c_p, c_i64, c_i32,
+                                  c_p]
     for name in ("mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
-                 "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant"):
+                 "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
+                 "mq_pack_weights_asym", "mq_act_rowsum", "mq_qlinear_asym"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -178,14 +186,7 @@ def mq_pack_weights(w, bits: int = 8, w_q=None, w_scale=None, w_colsum=None, str
     torch = _torch()
     N, K = w.shape
     dev = w.device
-    if bits == 8:
-        w_q = torch.empty((N, K), dtype=torch.int8, device=dev) if w_q is None else w_q
-        wq_dtype, wq_shape = torch.int8, (N, K)
-    elif bits == 4:
-        w_q = torch.empty((N, K // 2), dtype=torch.uint8, device=dev) if w_q is None else w_q
-        wq_dtype, wq_shape = torch.uint8, (N, K // 2)
-    else:
-        raise ValueError("bits must be 8 or 4")
+    w_q, wq_dtype, wq_shape = _packed_weights(N, K, bits, dev, w_q)
     w_scale = torch.empty(N, dtype=torch.float32, device=dev) if w_scale is None else w_scale
     w_colsum = torch.empty(N, dtype=torch.int32, device=dev) if w_colsum is None else w_colsum
     _check(lib().mq_pack_weights(_dev_ptr(w, torch.float32, "w"), N, K, int(bits),
@@ -196,11 +197,88 @@ def mq_pack_weights(w, bits: int = 8, w_q=None, w_scale=None, w_colsum=None, str
     return w_q, w_scale, w_colsum
 
 
+def _packed_weights(N, K, bits, dev, w_q):
+    torch = _torch()
+    if bits == 8:
+        w_q = torch.empty((N, K), dtype=torch.int8, device=dev) if w_q is None else w_q
+        return w_q, torch.int8, (N, K)
+    if bits == 4:
+        w_q = torch.empty((N, K // 2), dtype=torch.uint8, device=dev) if w_q is None else w_q
+        return w_q, torch.uint8, (N, K // 2)
+    raise ValueError("bits must be 8 or 4")
+
+
+def mq_pack_weights_asym(w, bits: int = 8, per_tensor: bool = False, w_q=None, w_scale=None,
+                         w_zp=None, w_colsum=None, stream=None):
+    """Asymmetric weight codes, per-row scales, zero-points and code sums
+    (Section 5.1); one range per output channel or per tensor."""
+    torch = _torch()
+    N, K = w.shape
+    dev = w.device
+    w_q, wq_dtype, wq_shape = _packed_weights(N, K, bits, dev, w_q)
+    w_scale = torch.empty(N, dtype=torch.float32, device=dev) if w_scale is None else w_scale
+    w_zp = torch.empty(N, dtype=torch.int32, device=dev) if w_zp is None else w_zp
+    w_colsum = torch.empty(N, dtype=torch.int32, device=dev) if w_colsum is None else w_colsum
+    _check(lib().mq_pack_weights_asym(_dev_ptr(w, torch.float32, "w"), N, K, int(bits),
+                                      int(bool(per_tensor)),
+                                      _dev_ptr(w_q, wq_dtype, "w_q", wq_shape),
+                                      _dev_ptr(w_scale, torch.float32, "w_scale", (N,)),
+                                      _dev_ptr(w_zp, torch.int32, "w_zp", (N,)),
+                                      _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)),
+                                      _stream_ptr(stream)), "mq_pack_weights_asym")
+    return w_q, w_scale, w_zp, w_colsum
+
+
+def mq_act_rowsum(a_q, out=None, stream=None):
+    """sum_k a_q[m][k] as int32 [M]."""
+    torch = _torch()
+    M, K = a_q.shape
+    out = torch.empty(M, dtype=torch.int32, device=a_q.device) if out is None else out
+    _check(lib().mq_act_rowsum(_dev_ptr(a_q, torch.int8, "a_q"), M, K,
+                               _dev_ptr(out, torch.int32, "out", (M,)), _stream_ptr(stream)),
+           "mq_act_rowsum")
+    return out
+
+
+def _workspace_args(workspace):
+    torch = _torch()
+    if workspace is None:
+        return None, 0
+    if workspace.dtype != torch.uint8 or workspace.device.type != "cuda" or \
+            not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 device tensor")
+    return ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel())
+
+
+def mq_qlinear_asym(a_q, a_rowsum, w_q, w_bits: int, w_scale, w_zp, w_colsum, a_scale: float,
+                    a_zp: int, out_scale: float, out_zp: int, out_bits: int = 8, bias=None,
+                    out=None, path: int = PATH_AUTO, stream=None, workspace=None):
+    """Integer-only linear layer with asymmetric per-channel weights."""
+    torch = _torch()
+    M, K = a_q.shape
+    N = w_q.shape[0]
+    wq_dtype, wq_shape = (torch.int8, (N, K)) if w_bits == 8 else (torch.uint8, (N, K // 2))
+    out = (torch.empty((M, N), dtype=_act_dtype(out_bits), device=a_q.device)
+           if out is None else out)
+    bptr = None if bias is None else _dev_ptr(bias, torch.float32, "bias", (N,))
+    ws, ws_bytes = _workspace_args(workspace)
+    _check(lib().mq_qlinear_asym(
+        _dev_ptr(a_q, torch.int8, "a_q"), _dev_ptr(a_rowsum, torch.int32, "a_rowsum", (M,)),
+        M, K, N, _dev_ptr(w_q, wq_dtype, "w_q", wq_shape), int(w_bits),
+        _dev_ptr(w_scale, torch.float32, "w_scale", (N,)),
+        _dev_ptr(w_zp, torch.int32, "w_zp", (N,)),
+        _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)),
+        float(a_scale), int(a_zp), float(out_scale), int(out_zp), int(out_bits), bptr,
+        _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), ws, ws_bytes, int(path),
+        _stream_ptr(stream)), "mq_qlinear_asym")
+    return out
+
+
 def mq_qlinear_workspace_bytes(M: int, K: int, N: int, w_bits: int = 8, out_bits: int = 8) -> int:
     """Workspace bytes mq_qlinear can use to split K for this shape (0: none)."""
     n = lib().mq_qlinear_workspace_bytes(int(M), int(K), int(N), int(w_bits), int(out_bits))
     if n < 0:
-        raise MQError(f"mq_qlinear_workspace_bytes: invalid shape {(M, K, N, w_bits, out_bits)}")
+        raise ValueError(f"mq_qlinear_workspace_bytes: invalid shape {(M, K, N, w_bits, out_bits)}")
     return n
 
 
@@ -226,11 +304,8 @@ def mq_qlinear(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: i
             float(a_scale), int(a_zp), float(out_scale), int(out_zp), int(out_bits), bptr,
             _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)))
     if workspace is not None:
-        if workspace.dtype != torch.uint8 or workspace.device.type != "cuda" or \
-                not workspace.is_contiguous():
-            raise ValueError("workspace must be a contiguous uint8 device tensor")
-        st = lib().mq_qlinear_ws(*args, ctypes.c_void_p(workspace.data_ptr()),
-                                 int(workspace.numel()), int(path), _stream_ptr(stream))
+        ws, ws_bytes = _workspace_args(workspace)
+        st = lib().mq_qlinear_ws(*args, ws, ws_bytes, int(path), _stream_ptr(stream))
     elif path == PATH_AUTO:
         st = lib().mq_qlinear(*args, _stream_ptr(stream))
     else:

@@ -261,6 +261,215 @@ __global__ __launch_bounds__(kThreads) void pack_weights_kernel(const float* __r
     }
 }
 
+// Asymmetric weights (Section 5.1): the Eq.(2)-(4) quantizer over a range
+// [lo, hi] that contains 0 -- the finite values of one row (per channel)
+// or of the whole matrix (per tensor).  alpha = (hi - lo)/(2^bits - 1) in
+// fp64, rounded to fp32; the unsigned zero-point rint(-lo/alpha) clamped to
+// the grid; codes clamp(rint(w/alpha) + zp) with one correctly rounded fp32
+// division.  A zero-width range takes alpha = 1 and zero-point -2^(bits-1).
+template <int BITS>
+__device__ inline void asym_format(float lo, float hi, float* alpha_out, int32_t* zp_out)
+{
+#pragma clang fp contract(off)
+    constexpr double QMAX = (double)((1 << BITS) - 1);
+    float alpha = 1.0f;
+    double beta = 0.0;
+    const double width = (double)hi - (double)lo;
+    if (width != 0.0) {
+        const float a = (float)(width / QMAX);
+        if (a > 0.0f && __builtin_isfinite(a)) {
+            alpha = a;
+            beta = (double)lo / (double)alpha;
+        }
+    }
+    const double zu = fmin(fmax(rint(-beta), 0.0), QMAX);
+    *alpha_out = alpha;
+    *zp_out = (int32_t)zu - (1 << (BITS - 1));
+}
+
+// [min, max] of the finite values of v[0..n), widened to contain 0, for the
+// whole block (every thread gets the result).
+__device__ inline void block_finite_range(const float* v, int64_t n, float* lo_out, float* hi_out)
+{
+    __shared__ float red_lo[kThreads / 64], red_hi[kThreads / 64];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    float lo = 0.0f, hi = 0.0f;
+    for (int64_t k = threadIdx.x; k < n; k += kThreads) {
+        const float x = v[k];
+        if (__builtin_isfinite(x)) {
+            lo = fminf(lo, x);
+            hi = fmaxf(hi, x);
+        }
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = fminf(lo, __shfl_xor(lo, o));
+        hi = fmaxf(hi, __shfl_xor(hi, o));
+    }
+    if (lane == 0) {
+        red_lo[wave] = lo;
+        red_hi[wave] = hi;
+    }
+    __syncthreads();
+    lo = red_lo[0];
+    hi = red_hi[0];
+#pragma unroll
+    for (int i = 1; i < kThreads / 64; ++i) {
+        lo = fminf(lo, red_lo[i]);
+        hi = fmaxf(hi, red_hi[i]);
+    }
+    *lo_out = lo;
+    *hi_out = hi;
+}
+
+// Per-tensor range, step 1: each row's range into lo[n], hi[n].
+__global__ __launch_bounds__(kThreads) void row_range_kernel(const float* __restrict__ w,
+                                                             int64_t K, float* __restrict__ lo,
+                                                             float* __restrict__ hi)
+{
+    float l, h;
+    block_finite_range(w + (int64_t)blockIdx.x * K, K, &l, &h);
+    if (threadIdx.x == 0) {
+        lo[blockIdx.x] = l;
+        hi[blockIdx.x] = h;
+    }
+}
+
+// Per-tensor range, step 2 (one block): the rows' ranges -> the tensor's
+// alpha and zero-point, written to scale[0] and zp[0].  lo/hi alias
+// scale/zp (the host passes the output arrays as the scratch of step 1).
+template <int BITS>
+__global__ __launch_bounds__(kThreads) void tensor_format_kernel(int64_t N, float* scale,
+                                                                 int32_t* zp)
+{
+    __shared__ float red_lo[kThreads / 64], red_hi[kThreads / 64];
+    const float* lo_in = scale;
+    const float* hi_in = reinterpret_cast<const float*>(zp);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    float lo = 0.0f, hi = 0.0f;
+    for (int64_t n = threadIdx.x; n < N; n += kThreads) {
+        lo = fminf(lo, lo_in[n]);
+        hi = fmaxf(hi, hi_in[n]);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = fminf(lo, __shfl_xor(lo, o));
+        hi = fmaxf(hi, __shfl_xor(hi, o));
+    }
+    if (lane == 0) {
+        red_lo[wave] = lo;
+        red_hi[wave] = hi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int i = 1; i < kThreads / 64; ++i) {  // lo, hi already hold wave 0's
+            lo = fminf(lo, red_lo[i]);
+            hi = fmaxf(hi, red_hi[i]);
+        }
+        float a;
+        int32_t z;
+        asym_format<BITS>(lo, hi, &a, &z);
+        scale[0] = a;
+        zp[0] = z;
+    }
+}
+
+// Codes, code sums and (per channel) the row's own format.  PER_TENSOR:
+// the format comes from scale[0], zp[0] (written by tensor_format_kernel);
+// row 0 leaves them in place and every other row copies them.
+template <int BITS, bool PER_TENSOR>
+__global__ __launch_bounds__(kThreads) void pack_weights_asym_kernel(
+    const float* __restrict__ w, int64_t K, void* __restrict__ wq, float* scale_out,
+    int32_t* zp_out, int32_t* __restrict__ colsum)
+{
+#pragma clang fp contract(off)
+    constexpr int QLO = -(1 << (BITS - 1)), QHI = (1 << (BITS - 1)) - 1;
+    constexpr float LIM = 1048576.0f;  // 2^20: the quotient converts to an integer
+    __shared__ int32_t red_i[kThreads / 64];
+    const int64_t n = blockIdx.x;
+    const float* row = w + n * K;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+
+    float alpha;
+    int32_t zp;
+    if constexpr (PER_TENSOR) {
+        alpha = scale_out[0];
+        zp = zp_out[0];
+    } else {
+        float lo, hi;
+        block_finite_range(row, K, &lo, &hi);
+        asym_format<BITS>(lo, hi, &alpha, &zp);
+    }
+
+    auto code = [&](float v) {
+        const float t = fminf(fmaxf(v / alpha, -LIM), LIM);
+        const int32_t q = (int32_t)rintf(t) + zp;
+        return q < QLO ? QLO : (q > QHI ? QHI : q);
+    };
+    int32_t sum = 0;
+    if constexpr (BITS == 8) {
+        int8_t* dst = static_cast<int8_t*>(wq) + n * K;
+        for (int64_t k = threadIdx.x; k < K; k += kThreads) {
+            const int32_t v = code(row[k]);
+            dst[k] = (int8_t)v;
+            sum += v;
+        }
+    } else {
+        uint8_t* dst = static_cast<uint8_t*>(wq) + n * (K / 2);
+        for (int64_t j = threadIdx.x; j < K / 2; j += kThreads) {
+            const int32_t v0 = code(row[2 * j]);
+            const int32_t v1 = code(row[2 * j + 1]);
+            dst[j] = (uint8_t)(((uint32_t)v0 & 0xFu) | (((uint32_t)v1 & 0xFu) << 4));
+            sum += v0 + v1;
+        }
+    }
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    if (lane == 0) red_i[wave] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t t = 0;
+#pragma unroll
+        for (int i = 0; i < kThreads / 64; ++i) t += red_i[i];
+        colsum[n] = t;
+        if (!PER_TENSOR || n != 0) {
+            scale_out[n] = alpha;
+            zp_out[n] = zp;
+        }
+    }
+}
+
+// Row sums of int8 activations, one wave per row: 16-byte loads folded with
+// dot4 against ones when the rows are 16-byte aligned, bytes otherwise.
+// |sum| <= 128 * K fits int32 for every accepted K.
+__global__ __launch_bounds__(kThreads) void act_rowsum_kernel(const int8_t* __restrict__ a,
+                                                              int64_t M, int64_t K,
+                                                              int32_t* __restrict__ rowsum)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t m = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+    if (m >= M) return;
+    const int8_t* row = a + m * K;
+    int32_t sum = 0;
+    int64_t k0 = 0;
+    if (((uintptr_t)row % 16) == 0) {
+        const int64_t n16 = K / 16;
+        const int4* r16 = reinterpret_cast<const int4*>(row);
+        for (int64_t i = lane; i < n16; i += 64) {
+            const int4 v = r16[i];
+            sum = __builtin_amdgcn_sdot4(v.x, 0x01010101, sum, false);
+            sum = __builtin_amdgcn_sdot4(v.y, 0x01010101, sum, false);
+            sum = __builtin_amdgcn_sdot4(v.z, 0x01010101, sum, false);
+            sum = __builtin_amdgcn_sdot4(v.w, 0x01010101, sum, false);
+        }
+        k0 = n16 * 16;
+    }
+    for (int64_t k = k0 + lane; k < K; k += 64) sum += row[k];
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    if (lane == 0) rowsum[m] = sum;
+}
+
 }  // namespace
 
 hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t zp, int32_t bits,
@@ -340,6 +549,39 @@ hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int32_t bit
         pack_weights_kernel<8><<<(unsigned)N, kThreads, 0, st>>>(w, K, wq, scale, colsum);
     else
         pack_weights_kernel<4><<<(unsigned)N, kThreads, 0, st>>>(w, K, wq, scale, colsum);
+    return hipGetLastError();
+}
+
+template <int BITS>
+hipError_t pack_asym_t(const float* w, int64_t N, int64_t K, bool per_tensor, void* wq,
+                       float* scale, int32_t* zp, int32_t* colsum, hipStream_t st)
+{
+    const unsigned g = (unsigned)N;
+    if (!per_tensor) {
+        pack_weights_asym_kernel<BITS, false><<<g, kThreads, 0, st>>>(w, K, wq, scale, zp, colsum);
+        return hipGetLastError();
+    }
+    // the output arrays hold the per-row ranges between the first two steps
+    row_range_kernel<<<g, kThreads, 0, st>>>(w, K, scale, reinterpret_cast<float*>(zp));
+    tensor_format_kernel<BITS><<<1, kThreads, 0, st>>>(N, scale, zp);
+    pack_weights_asym_kernel<BITS, true><<<g, kThreads, 0, st>>>(w, K, wq, scale, zp, colsum);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bits,
+                                    bool per_tensor, void* wq, float* scale, int32_t* zp,
+                                    int32_t* colsum, hipStream_t st)
+{
+    if (bits == 8) return pack_asym_t<8>(w, N, K, per_tensor, wq, scale, zp, colsum, st);
+    return pack_asym_t<4>(w, N, K, per_tensor, wq, scale, zp, colsum, st);
+}
+
+hipError_t launch_act_rowsum(const int8_t* a, int64_t M, int64_t K, int32_t* rowsum,
+                             hipStream_t st)
+{
+    // four rows per block; M <= 2^31 - 1 (host validation) keeps the grid in range
+    const int64_t blocks = (M + kThreads / 64 - 1) / (kThreads / 64);
+    act_rowsum_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(a, M, K, rowsum);
     return hipGetLastError();
 }
 

@@ -122,6 +122,28 @@ mq_status mq_pack_weights(const float* w, int64_t N, int64_t K, int32_t bits, vo
         mq::launch_pack_weights(w, N, K, bits, w_q, w_scale, w_colsum, as_stream(stream)));
 }
 
+mq_status mq_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bits,
+                               int32_t per_tensor, void* w_q, float* w_scale, int32_t* w_zp,
+                               int32_t* w_colsum, void* stream)
+{
+    if (bits != 8 && bits != 4) return MQ_ERR_INVALID_ARG;
+    if (per_tensor != 0 && per_tensor != 1) return MQ_ERR_INVALID_ARG;
+    if (N < 0 || N > 0x7FFFFFFF || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
+    if (bits == 4 && (K % 2) != 0) return MQ_ERR_INVALID_ARG;
+    if (N == 0) return MQ_OK;
+    if (!w || !w_q || !w_scale || !w_zp || !w_colsum) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_pack_weights_asym(w, N, K, bits, per_tensor != 0, w_q, w_scale,
+                                                 w_zp, w_colsum, as_stream(stream)));
+}
+
+mq_status mq_act_rowsum(const int8_t* a_q, int64_t M, int64_t K, int32_t* rowsum, void* stream)
+{
+    if (M < 0 || M > 0x7FFFFFFF || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
+    if (M == 0) return MQ_OK;
+    if (!a_q || !rowsum) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_act_rowsum(a_q, M, K, rowsum, as_stream(stream)));
+}
+
 int64_t mq_qlinear_workspace_bytes(int64_t M, int64_t K, int64_t N, int32_t w_bits,
                                    int32_t out_bits)
 {
@@ -149,11 +171,18 @@ mq_status mq_qlinear_ex(const int8_t* a_q, int64_t M, int64_t K, int64_t N, cons
                          out_zp, out_bits, bias, y_q, nullptr, 0, path, stream);
 }
 
-mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
-                        int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
-                        float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
-                        int32_t out_bits, const float* bias, void* y_q, void* workspace,
-                        int64_t workspace_bytes, int32_t path, void* stream)
+}  // extern "C"
+
+namespace {
+
+// Validation and dispatch shared by the symmetric and asymmetric entry
+// points; w_zp and a_rowsum are both null (symmetric) or both set.
+mq_status qlinear_impl(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
+                       int64_t N, const void* w_q, int32_t w_bits, const float* w_scale,
+                       const int32_t* w_zp, const int32_t* w_colsum, float a_scale, int32_t a_zp,
+                       float out_scale, int32_t out_zp, int32_t out_bits, const float* bias,
+                       void* y_q, void* workspace, int64_t workspace_bytes, int32_t path,
+                       void* stream)
 {
     if (workspace_bytes < 0) return MQ_ERR_INVALID_ARG;
     if (workspace && ((uintptr_t)workspace % 256) != 0) return MQ_ERR_INVALID_ARG;
@@ -168,6 +197,7 @@ mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N, cons
     if (path == MQ_PATH_DECODE && M > 16) return MQ_ERR_INVALID_ARG;
     if (M == 0 || N == 0) return MQ_OK;
     if (!a_q || !w_q || !w_scale || !w_colsum || !y_q) return MQ_ERR_INVALID_ARG;
+    if ((w_zp == nullptr) != (a_rowsum == nullptr)) return MQ_ERR_INVALID_ARG;
 
     mq::QLinearArgs p;
     p.a = a_q;
@@ -187,6 +217,8 @@ mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N, cons
     p.out_bits = out_bits;
     p.ws = workspace;
     p.ws_bytes = workspace ? workspace_bytes : 0;
+    p.w_zp = w_zp;
+    p.a_rowsum = a_rowsum;
 
     hipStream_t s = as_stream(stream);
     if (path == MQ_PATH_AUTO) path = M <= 16 ? MQ_PATH_DECODE : MQ_PATH_PREFILL;
@@ -195,6 +227,34 @@ mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N, cons
     if (path == MQ_PATH_PREFILL && mq::prefill_supported(p))
         return from_hip(mq::launch_qlinear_prefill(p, s));
     return from_hip(mq::launch_qlinear_generic(p, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
+                        int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
+                        float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                        int32_t out_bits, const float* bias, void* y_q, void* workspace,
+                        int64_t workspace_bytes, int32_t path, void* stream)
+{
+    return qlinear_impl(a_q, nullptr, M, K, N, w_q, w_bits, w_scale, nullptr, w_colsum, a_scale,
+                        a_zp, out_scale, out_zp, out_bits, bias, y_q, workspace, workspace_bytes,
+                        path, stream);
+}
+
+mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
+                          int64_t N, const void* w_q, int32_t w_bits, const float* w_scale,
+                          const int32_t* w_zp, const int32_t* w_colsum, float a_scale,
+                          int32_t a_zp, float out_scale, int32_t out_zp, int32_t out_bits,
+                          const float* bias, void* y_q, void* workspace, int64_t workspace_bytes,
+                          int32_t path, void* stream)
+{
+    if (M > 0 && N > 0 && (!a_rowsum || !w_zp)) return MQ_ERR_INVALID_ARG;
+    return qlinear_impl(a_q, a_rowsum, M, K, N, w_q, w_bits, w_scale, w_zp, w_colsum, a_scale,
+                        a_zp, out_scale, out_zp, out_bits, bias, y_q, workspace, workspace_bytes,
+                        path, stream);
 }
 
 mq_status mq_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,

@@ -24,6 +24,10 @@ struct QLinearArgs {
     int32_t out_bits;       // 8 or 16
     void* ws = nullptr;     // split-K workspace (zero-filled once by its owner) or nullptr
     int64_t ws_bytes = 0;
+    // asymmetric per-channel weights: zero-points [N] and the activation
+    // row sums [M] (sum_k a[m][k]); both nullptr for symmetric weights
+    const int32_t* w_zp = nullptr;
+    const int32_t* a_rowsum = nullptr;
 };
 
 hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t zp,
@@ -36,6 +40,11 @@ hipError_t launch_fold_acts(const float* x, const float* sv, int64_t M, int64_t 
                             float* out, hipStream_t s);
 hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int32_t bits,
                                void* wq, float* scale, int32_t* colsum, hipStream_t s);
+hipError_t launch_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bits,
+                                    bool per_tensor, void* wq, float* scale, int32_t* zp,
+                                    int32_t* colsum, hipStream_t s);
+hipError_t launch_act_rowsum(const int8_t* a, int64_t M, int64_t K, int32_t* rowsum,
+                             hipStream_t s);
 
 hipError_t launch_qlinear_generic(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);

@@ -36,7 +36,9 @@ __device__ inline v4i unpack_int4_x16(uint32_t x0, uint32_t x1)
 
 // R output channels per block (16, or 8 for narrow layers so the weight
 // stream spreads over more CUs; rows R..15 of the MFMA then load nothing).
-template <int WBITS, int OBITS, int NWAVES, int R>
+// ASYM: asymmetric weights, the zero-point term is added in the epilogue
+// (exact int64 form, four outputs per lane).
+template <int WBITS, int OBITS, int NWAVES, int R, bool ASYM>
 __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs p)
 {
     constexpr int U = 8;  // 64-wide k steps per load round (one round covers most layers)
@@ -67,7 +69,7 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     // the epilogue wave before the weight stream so both share one memory
     // latency.
     float col_ws[4] = {1.0f, 1.0f, 1.0f, 1.0f}, col_b[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    int32_t col_cs[4] = {0, 0, 0, 0};
+    int32_t col_cs[4] = {0, 0, 0, 0}, col_zw[4] = {0, 0, 0, 0}, row_sum = 0;
     if (wave == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -76,7 +78,9 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
             col_ws[r] = p.w_scale[n];
             col_cs[r] = p.colsum[n];
             col_b[r] = (p.bias ? p.bias : p.w_scale)[n];  // branch-free; unused without bias
+            if constexpr (ASYM) col_zw[r] = p.w_zp[n];
         }
+        if constexpr (ASYM) row_sum = p.a_rowsum[r16 < p.M ? r16 : p.M - 1];
     }
 
     const int64_t steps = (p.K + 63) / 64;
@@ -129,6 +133,9 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     asm volatile("" : "+v"(col_ws[0]), "+v"(col_ws[1]), "+v"(col_ws[2]), "+v"(col_ws[3]),
                  "+v"(col_cs[0]), "+v"(col_cs[1]), "+v"(col_cs[2]), "+v"(col_cs[3]),
                  "+v"(col_b[0]), "+v"(col_b[1]), "+v"(col_b[2]), "+v"(col_b[3]));
+    if constexpr (ASYM)
+        asm volatile("" : "+v"(col_zw[0]), "+v"(col_zw[1]), "+v"(col_zw[2]), "+v"(col_zw[3]),
+                     "+v"(row_sum));
     ColParams cps[4] = {};
     if (wave == 0) {
 #pragma unroll
@@ -154,11 +161,16 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     const int64_t m = r16;
     if (m >= p.M || 4 * kg >= R) return;
     int32_t out[4];
+    const int32_t rs = row_sum - (int32_t)p.K * p.a_zp;  // sum_k (a - a_zp), ASYM only
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         int32_t a32 = acc[r];
         if constexpr (WBITS == 4) a32 >>= 4;  // exact: the sum is a multiple of 16
-        out[r] = requant_out(a32, cps[r], p.out_zp, qmin, qmax);
+        if constexpr (ASYM)
+            out[r] = requant_c(corrected_acc_asym(a32, cps[r].off, -col_zw[r], rs), cps[r],
+                               p.out_zp, qmin, qmax);
+        else
+            out[r] = requant_out(a32, cps[r], p.out_zp, qmin, qmax);
     }
     const int64_t nb = n0 + 4 * kg;
     const int64_t base = m * p.N + nb;
@@ -184,7 +196,7 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     }
 }
 
-template <int WBITS, int OBITS, int R>
+template <int WBITS, int OBITS, int R, bool ASYM>
 hipError_t launch_r(const QLinearArgs& p, hipStream_t s)
 {
     const int64_t blocks = (p.N + R - 1) / R;
@@ -199,21 +211,27 @@ hipError_t launch_r(const QLinearArgs& p, hipStream_t s)
     }
     const dim3 g((unsigned)blocks);
     switch (nw) {
-    case 16: qlinear_decode_kernel<WBITS, OBITS, 16, R><<<g, 16 * 64, 0, s>>>(p); break;
-    case 8: qlinear_decode_kernel<WBITS, OBITS, 8, R><<<g, 8 * 64, 0, s>>>(p); break;
-    case 4: qlinear_decode_kernel<WBITS, OBITS, 4, R><<<g, 4 * 64, 0, s>>>(p); break;
-    case 2: qlinear_decode_kernel<WBITS, OBITS, 2, R><<<g, 2 * 64, 0, s>>>(p); break;
-    default: qlinear_decode_kernel<WBITS, OBITS, 1, R><<<g, 64, 0, s>>>(p); break;
+    case 16: qlinear_decode_kernel<WBITS, OBITS, 16, R, ASYM><<<g, 16 * 64, 0, s>>>(p); break;
+    case 8: qlinear_decode_kernel<WBITS, OBITS, 8, R, ASYM><<<g, 8 * 64, 0, s>>>(p); break;
+    case 4: qlinear_decode_kernel<WBITS, OBITS, 4, R, ASYM><<<g, 4 * 64, 0, s>>>(p); break;
+    case 2: qlinear_decode_kernel<WBITS, OBITS, 2, R, ASYM><<<g, 2 * 64, 0, s>>>(p); break;
+    default: qlinear_decode_kernel<WBITS, OBITS, 1, R, ASYM><<<g, 64, 0, s>>>(p); break;
     }
     return hipGetLastError();
+}
+
+template <int WBITS, int OBITS, bool ASYM>
+hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
+{
+    // narrow layers: 8 channels per block so at least 256 blocks stream
+    if ((p.N + 15) / 16 < 256) return launch_r<WBITS, OBITS, 8, ASYM>(p, s);
+    return launch_r<WBITS, OBITS, 16, ASYM>(p, s);
 }
 
 template <int WBITS, int OBITS>
 hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 {
-    // narrow layers: 8 channels per block so at least 256 blocks stream
-    if ((p.N + 15) / 16 < 256) return launch_r<WBITS, OBITS, 8>(p, s);
-    return launch_r<WBITS, OBITS, 16>(p, s);
+    return p.w_zp ? launch_a<WBITS, OBITS, true>(p, s) : launch_a<WBITS, OBITS, false>(p, s);
 }
 
 }  // namespace

@@ -33,7 +33,14 @@ __global__ __launch_bounds__(256) void qlinear_generic_kernel(QLinearArgs p)
         }
         const ColParams cp = derive_col_params(p.a_scale, p.w_scale[n], p.out_scale,
                                                p.bias ? p.bias + n : nullptr, p.colsum[n], p.a_zp);
-        const int32_t y = requant_out(acc, cp, p.out_zp, qmin, qmax);
+        int32_t y;
+        if (p.w_zp) {
+            const int32_t rs = p.a_rowsum[m] - (int32_t)p.K * p.a_zp;
+            y = requant_c(corrected_acc_asym(acc, cp.off, -p.w_zp[n], rs), cp, p.out_zp, qmin,
+                          qmax);
+        } else {
+            y = requant_out(acc, cp, p.out_zp, qmin, qmax);
+        }
         if constexpr (OBITS == 8)
             static_cast<int8_t*>(p.y)[idx] = (int8_t)y;
         else

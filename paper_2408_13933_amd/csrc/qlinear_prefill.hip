@@ -111,6 +111,8 @@ struct Cfg {
     static constexpr int STAGE = A_BYTES + W_BYTES;
     // + per-column epilogue constants + one flag word per wave
     static constexpr int LDS = STAGES * STAGE + TN * 16 + NWAVES * 4;
+    // asymmetric weights add per channel -w_zp and per token row sum
+    static constexpr int LDS_ASYM = LDS + (TN + TM) * 4;
     static_assert(TM % (WM * 32) == 0 && TN % (WN * 32) == 0, "wave grid");
     static_assert((TM * CA) % 64 == 0 && (TN * CW) % 64 == 0, "whole wave loads");
     static_assert(BK % 64 == 0, "BK is a multiple of the MFMA depth");
@@ -118,7 +120,7 @@ struct Cfg {
     static_assert((BK / 32) % 2 == 0, "even number of 32-deep steps per stage");
     static_assert(LOADS * (STAGES - 1) < 64, "vmcnt range");
     static_assert(SPREAD >= 1 && SPREAD <= KS, "the DMA spread stays within one stage");
-    static_assert(LDS <= 160 * 1024, "LDS per CU");
+    static_assert(LDS_ASYM <= 160 * 1024, "LDS per CU");
 };
 
 template <int SWZ>
@@ -136,6 +138,8 @@ __device__ inline int swz(int row, int nchunks)
 }
 
 struct EpiCtx {
+    const int32_t* e_nzw;  // asymmetric weights: -w_zp per tile channel
+    const int32_t* e_rs;   // asymmetric weights: sum_k (a - a_zp) per tile token row
     const int32_t* e_off;
     const int32_t* e_m0;
     const int32_t* e_rnd;
@@ -185,7 +189,10 @@ struct Staging {
 // conversions).  FAST: no column needs the pre-shift, the output zero-point
 // is folded into the rounding constants and N % 4 == 0, leaving
 // sat-add, mul_hi, add, shift, clamp per output.
-template <class C, bool FAST, bool STAGED, class Acc>
+// ASYM (asymmetric weights) adds -w_zp[n] * rs[m]: the fast form has it in
+// the accumulator's start value already, the other adds it exactly in
+// int64 before the saturation.
+template <class C, bool ASYM, bool FAST, bool STAGED, class Acc>
 __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
@@ -195,6 +202,10 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
     static_assert(!STAGED || FAST, "staged stores assume whole 4-channel groups");
     constexpr int PASSES = STAGED ? S::PASSES : 1;
     constexpr int FNP = C::FN / PASSES;
+    int32_t rs[C::FM];  // this lane's token rows
+#pragma unroll
+    for (int j = 0; j < C::FM; ++j)
+        rs[j] = ASYM && !FAST ? x.e_rs[x.wave_row0 + j * 32 + x.r32] : 0;
 #pragma unroll
     for (int pass = 0; pass < PASSES; ++pass) {
 #pragma unroll
@@ -202,8 +213,9 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int nl = x.col0 + i * 32 + 8 * g;  // tile-local channel
-            v4i off = {0, 0, 0, 0};
+            v4i off = {0, 0, 0, 0}, nzw = {0, 0, 0, 0};
             if constexpr (!FAST) off = *reinterpret_cast<const v4i*>(x.e_off + nl);
+            if constexpr (ASYM && !FAST) nzw = *reinterpret_cast<const v4i*>(x.e_nzw + nl);
             const v4i m0 = *reinterpret_cast<const v4i*>(x.e_m0 + nl);
             const v4i rnd = *reinterpret_cast<const v4i*>(x.e_rnd + nl);
             const v4i sp = *reinterpret_cast<const v4i*>(x.e_sp + nl);
@@ -225,7 +237,10 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
                     if constexpr (C::WBITS == 4) a32 >>= 4;  // exact: a multiple of 16
                     int32_t c = a32;  // fast form: off is already in the accumulator
                     if constexpr (!FAST) {
-                        c = __builtin_elementwise_add_sat(a32, off[r]);
+                        if constexpr (ASYM)
+                            c = corrected_acc_asym(a32, off[r], nzw[r], rs[j]);
+                        else
+                            c = __builtin_elementwise_add_sat(a32, off[r]);
                         c = max(min(c, bnd[r]), -bnd[r]);
                         c = (int32_t)((uint32_t)c << pre[r]);
                     }
@@ -301,7 +316,7 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
     }
 }
 
-template <class C>
+template <class C, bool ASYM>
 __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearArgs p,
                                                                        int tiles_n, int tiles_m,
                                                                        int splits,
@@ -317,6 +332,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     int32_t* e_rnd = e_m0 + C::TN;
     int32_t* e_sp = e_rnd + C::TN;  // shr | pre << 8
     int32_t* e_flag = e_sp + C::TN;  // per wave: bit 0 all pre == 0, bit 1 zp foldable
+    int32_t* e_nzw = e_flag + C::NWAVES;  // asymmetric weights only
+    int32_t* e_rs = e_nzw + C::TN;
 
     // ---- tile and K slice: the blocks of one XCD (block id mod 8) take a
     // contiguous run of work items, so they share operand tiles in that
@@ -416,18 +433,22 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // issue order, so these loads are back before the stage DMA behind them
     // and the constants are derived while the first tiles are in flight
     float col_ws = 1.0f, col_bias = 0.0f;
-    int32_t col_cs = 0;
+    int32_t col_cs = 0, col_zw = 0, row_sum = 0;
     if (tid < C::TN) {
         int64_t n = n_tile + tid;
         if (n >= p.N) n = p.N - 1;
         col_ws = p.w_scale[n];
         col_cs = p.colsum[n];
         col_bias = (p.bias ? p.bias : p.w_scale)[n];  // branch-free; unused without bias
+        if constexpr (ASYM) col_zw = p.w_zp[n];
     }
+    if (ASYM && tid < C::TM) row_sum = p.a_rowsum[tid < rows_a ? m_tile + tid : m_tile];
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s) issue(s, s);
     // keep every use of the loaded values behind the DMA issue
     asm volatile("" : "+v"(col_ws), "+v"(col_cs), "+v"(col_bias));
+    if constexpr (ASYM) asm volatile("" : "+v"(col_zw), "+v"(row_sum));
+    if (ASYM && tid < C::TM) e_rs[tid] = row_sum - (int32_t)K * p.a_zp;
 
     int col_pre0 = 1, col_fold = 1, col_offin = 1;
     if (tid < C::TN) {
@@ -444,11 +465,19 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         const int64_t zabs = p.out_zp < 0 ? -(int64_t)p.out_zp : (int64_t)p.out_zp;
         col_fold = (int64_t)ei.rnd + (zabs << ei.shr) <= ((int64_t)1 << 30);
         // off can start the accumulator (scaled by 16 for int4 weights)
-        // when no partial sum can leave int32: |acc| <= K * 128 * 127 <
-        // K * 2^14, so the saturating add of the epilogue never saturates
-        const int64_t offa = (cp.off < 0 ? -(int64_t)cp.off : (int64_t)cp.off) *
-                             (C::WBITS == 4 ? 16 : 1);
-        col_offin = offa + (K << 14) < ((int64_t)1 << 31);
+        // when no partial sum can leave int32: |acc| <= K * 128 * 128 =
+        // K * 2^14, so the saturating add of the epilogue never saturates.
+        // With asymmetric weights the start value also holds the zero-point
+        // term -w_zp * rs, |rs| <= 255 K, formed by a 24-bit multiply
+        // (|rs| < 2^23).
+        int64_t offa = cp.off < 0 ? -(int64_t)cp.off : (int64_t)cp.off;
+        if constexpr (ASYM) {
+            e_nzw[tid] = -col_zw;
+            offa += (col_zw < 0 ? -(int64_t)col_zw : (int64_t)col_zw) * 255 * K;
+        }
+        offa *= C::WBITS == 4 ? 16 : 1;
+        col_offin = offa + (K << 14) < ((int64_t)1 << 31) &&
+                    (!ASYM || 255 * K < ((int64_t)1 << 23));
     }
     // Whole-tile epilogue form: AND of the column flags over the block, by
     // ballot per wave and one LDS word per wave.  A raw barrier, since
@@ -481,14 +510,11 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
     __builtin_amdgcn_s_barrier();
 
-    // ---- main loop.  Fragments of the next 32-deep step are read from LDS
-    // while the MFMAs of the current one run; at the last step of a stage
-    // the stage switch (wait, barrier, next DMA, first fragments of the next
-    // stage) sits between the two halves of the step's MFMAs.  The steady
-    // state has no branches, so every wait count is a compile-time constant.
-    // Accumulator layout: lane holds channels col0 + 32i + 8g + 4hk + r
-    // (register 4g + r) of tokens 32j + r32.  In the fast form each starts
-    // at its channel's off.
+    // ---- accumulators.  Layout:
+    // lane holds channels col0 + 32i + 8g + 4hk + r (register 4g + r) of
+    // tokens 32j + r32.  In the fast form each starts at its channel's off
+    // (plus, for asymmetric weights, -w_zp[n] * rs[m]), scaled by 16 for
+    // int4 weights like the products.
     v16i acc[C::FN][C::FM];
 #pragma unroll
     for (int i = 0; i < C::FN; ++i)
@@ -498,18 +524,34 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
     if (fast && split == 0) {  // block-uniform; off joins the sum once
         const int col0 = wn * (C::TN / C::WN) + 4 * hk;
+        int32_t rs[C::FM];
+#pragma unroll
+        for (int j = 0; j < C::FM; ++j)
+            rs[j] = ASYM ? e_rs[wm * (C::TM / C::WM) + j * 32 + r32] : 0;
 #pragma unroll
         for (int i = 0; i < C::FN; ++i)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                v4i o = *reinterpret_cast<const v4i*>(e_off + col0 + i * 32 + 8 * g);
-                if constexpr (C::WBITS == 4) o *= 16;
+                const v4i o = *reinterpret_cast<const v4i*>(e_off + col0 + i * 32 + 8 * g);
+                v4i z = {0, 0, 0, 0};
+                if constexpr (ASYM) z = *reinterpret_cast<const v4i*>(e_nzw + col0 + i * 32 + 8 * g);
 #pragma unroll
                 for (int j = 0; j < C::FM; ++j)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) acc[i][j][4 * g + r] = o[r];
+                    for (int r = 0; r < 4; ++r) {
+                        int32_t v = o[r];
+                        if constexpr (ASYM) v += __mul24(z[r], rs[j]);
+                        if constexpr (C::WBITS == 4) v *= 16;
+                        acc[i][j][4 * g + r] = v;
+                    }
             }
     }
+
+    // ---- main loop.  Fragments of the next 32-deep step are read from LDS
+    // while the MFMAs of the current one run; at the last step of a stage
+    // the stage switch (wait, barrier, next DMA, first fragments of the next
+    // stage) sits between the two halves of the step's MFMAs.  The steady
+    // state has no branches, so every wait count is a compile-time constant.
 
     // fragment g of a 32-deep step: g < FM activation rows, then weight rows
     auto load_frag = [&](int buf, int ks, int g, v4i* wf, v4i* af) {
@@ -697,6 +739,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
     __builtin_amdgcn_s_barrier();  // e_rnd update visible even when KT == 1
     EpiCtx ctx;
+    ctx.e_nzw = e_nzw;
+    ctx.e_rs = e_rs;
     ctx.e_off = e_off;
     ctx.e_m0 = e_m0;
     ctx.e_rnd = e_rnd;
@@ -717,12 +761,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // staged stores need the tile's channels inside N and 16-byte row chunks
     const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
                         ((uintptr_t)p.y % 16) == 0;
-    if (staged) prefill_epilogue<C, true, true>(acc, ctx);
-    else if (fast) prefill_epilogue<C, true, false>(acc, ctx);
-    else prefill_epilogue<C, false, false>(acc, ctx);
+    if (staged) prefill_epilogue<C, ASYM, true, true>(acc, ctx);
+    else if (fast) prefill_epilogue<C, ASYM, true, false>(acc, ctx);
+    else prefill_epilogue<C, ASYM, false, false>(acc, ctx);
 }
 
-template <class C>
+template <class C, bool ASYM>
 hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
 {
     const int64_t tiles_n = (p.N + C::TN - 1) / C::TN;
@@ -733,11 +777,12 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
     splits = (int)((kt + kt_per_split - 1) / kt_per_split);  // every slice non-empty
     if (total * splits > 0x7FFFFFFF) return hipErrorInvalidValue;
     // more than 64 KiB of dynamic LDS must be opted into once per kernel
+    constexpr int lds = ASYM ? C::LDS_ASYM : C::LDS;
     static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&qlinear_prefill_kernel<C>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+        reinterpret_cast<const void*>(&qlinear_prefill_kernel<C, ASYM>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (attr != hipSuccess) return attr;
-    qlinear_prefill_kernel<C><<<dim3((unsigned)(total * splits)), dim3(C::THREADS), C::LDS, s>>>(
+    qlinear_prefill_kernel<C, ASYM><<<dim3((unsigned)(total * splits)), dim3(C::THREADS), lds, s>>>(
         p, (int)tiles_n, (int)tiles_m, splits, (int)kt_per_split);
     return hipGetLastError();
 }
@@ -819,16 +864,22 @@ int64_t workspace_for(const QLinearArgs& p, const Choice& ch)
     return split_counter_bytes(tiles) + tiles * ch.splits * (int64_t)t.tm * t.tn * 4;
 }
 
-template <int WB, int OB>
-hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
+template <int WB, int OB, bool ASYM>
+hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
 {
     Choice ch = choose(p, p.ws != nullptr);
     if (ch.splits > 1 && workspace_for(p, ch) > p.ws_bytes) ch = choose(p, false);
     switch (ch.tile) {
-    case 0: return launch_cfg<T256x256<WB, OB>>(p, ch.splits, s);
-    case 1: return launch_cfg<T256x128<WB, OB>>(p, ch.splits, s);
-    default: return launch_cfg<T128x128<WB, OB>>(p, ch.splits, s);
+    case 0: return launch_cfg<T256x256<WB, OB>, ASYM>(p, ch.splits, s);
+    case 1: return launch_cfg<T256x128<WB, OB>, ASYM>(p, ch.splits, s);
+    default: return launch_cfg<T128x128<WB, OB>, ASYM>(p, ch.splits, s);
     }
+}
+
+template <int WB, int OB>
+hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
+{
+    return p.w_zp ? launch_a<WB, OB, true>(p, s) : launch_a<WB, OB, false>(p, s);
 }
 
 }  // namespace

@@ -80,14 +80,30 @@ __device__ inline int32_t requant_round(int32_t c, int32_t m0, int32_t sh)
     return c > 0 ? (1 << 30) : (c < 0 ? -(1 << 30) : 0);
 }
 
-__device__ inline int32_t requant_out(int32_t acc, const ColParams& p, int32_t out_zp,
-                                      int32_t qmin, int32_t qmax)
+// y from the corrected accumulator c.
+__device__ inline int32_t requant_c(int32_t c, const ColParams& p, int32_t out_zp, int32_t qmin,
+                                    int32_t qmax)
 {
-    const int32_t c = __builtin_elementwise_add_sat(acc, p.off);
     const int32_t r = requant_round(c, p.m0, p.sh);
     int32_t y = r + out_zp;  // |r| <= 2^30, |out_zp| <= 2^15: no overflow
     y = y < qmin ? qmin : (y > qmax ? qmax : y);
     return y;
+}
+
+__device__ inline int32_t requant_out(int32_t acc, const ColParams& p, int32_t out_zp,
+                                      int32_t qmin, int32_t qmax)
+{
+    return requant_c(__builtin_elementwise_add_sat(acc, p.off), p, out_zp, qmin, qmax);
+}
+
+// Asymmetric per-channel weights (codes W - w_zp[n]): the zero-point adds
+// the term -w_zp[n] * sum_k (A[m][k] - a_zp) = -w_zp[n] * rs[m], where
+// rs[m] = rowsum[m] - K * a_zp (|rs| <= 255 K).  Exact in int64, then
+//   c = sat_int32(acc + off + nzw * rs),  nzw = -w_zp[n].
+__device__ inline int32_t corrected_acc_asym(int32_t acc, int32_t off, int32_t nzw, int32_t rs)
+{
+    const long long c = (long long)acc + (long long)off + (long long)nzw * (long long)rs;
+    return (int32_t)(c < INT32_MIN ? INT32_MIN : (c > INT32_MAX ? INT32_MAX : c));
 }
 
 // ---------------------------------------------------------------------------

@@ -19,12 +19,17 @@ quantization hard (Section 3.2).
 * weights W [N][K] fp32: N(0, 0.02^2), before folding.
 * smoothing vector s [K] (only where a layer folds one): exp(U(ln 0.5,
   ln 2)); the fold W_hat = W diag(s) is done by the code under test.
+* asymmetric-weight layers (Section 5.1 quantizes weights asymmetrically
+  per channel): each weight row gets its own mean, W[n] += mu_n with mu_n
+  ~ U(-2, 2) * 0.02, so row ranges are off-centre and the zero-points
+  spread over the grid instead of sitting near 0.
 * bias [N] fp32: N(0, 0.01^2) where the layer has one.
 * static activation range: min and max of X_hat (a plain data statistic).
 * static output range: the layer output has standard deviation
   sigma_y = 0.02 * rms_m sqrt(sum_k (X_hat[m,k] s[k])^2) under this recipe;
   the range is [-4.5 sigma_y - 3 sigma_b, 5.5 sigma_y + 3 sigma_b], skewed
-  so the output zero-point is not zero and a few outputs saturate.
+  so the output zero-point is not zero and a few outputs saturate.  With
+  row means mu_n, sigma_y^2 adds mean_n(mu_n^2) * mean_m((sum_k X_hat s)^2).
 """
 from __future__ import annotations
 
@@ -50,6 +55,8 @@ class Layer:
     act: str = "outlier"     # "outlier" | "student_t"
     smooth: Optional[str] = None   # name of the smoothing vector folded in
     smooth_len: int = 0            # length of that vector
+    asym: bool = False             # asymmetric weights
+    per_tensor: bool = False       # one weight range per tensor (asym only)
 
     @property
     def ops(self) -> int:
@@ -61,6 +68,8 @@ class Layer:
         a = self.M * self.K
         y = self.M * self.N * self.out_bits // 8
         params = self.N * (8 + (4 if self.bias else 0))
+        if self.asym:  # weight zero-points and activation row sums
+            params += self.N * 4 + self.M * 4
         return w + a + y + params
 
 
@@ -71,15 +80,18 @@ class Workload:
     layers: tuple
 
 
-def _tinyllama_block(M: int):
-    L = dict(out_bits=16, bias=False)
+def _tinyllama_block(M: int, asym: bool = False):
+    L = dict(out_bits=16, bias=False, asym=asym)
+    # asymmetric (Section 5.1 W8A8): one weight range per tensor except the
+    # MLP down projection, which keeps one per output channel
+    T = dict(per_tensor=asym)
     return (
-        Layer("q_proj", M, 2048, 2048, smooth="attn_norm", smooth_len=2048, **L),
-        Layer("k_proj", M, 2048, 256, smooth="attn_norm", smooth_len=2048, **L),
-        Layer("v_proj", M, 2048, 256, smooth="attn_norm", smooth_len=2048, **L),
-        Layer("o_proj", M, 2048, 2048, smooth="v_to_o", smooth_len=256, **L),
-        Layer("gate_proj", M, 2048, 5632, smooth="mlp_norm", smooth_len=2048, **L),
-        Layer("up_proj", M, 2048, 5632, smooth="mlp_norm", smooth_len=2048, **L),
+        Layer("q_proj", M, 2048, 2048, smooth="attn_norm", smooth_len=2048, **L, **T),
+        Layer("k_proj", M, 2048, 256, smooth="attn_norm", smooth_len=2048, **L, **T),
+        Layer("v_proj", M, 2048, 256, smooth="attn_norm", smooth_len=2048, **L, **T),
+        Layer("o_proj", M, 2048, 2048, smooth="v_to_o", smooth_len=256, **L, **T),
+        Layer("gate_proj", M, 2048, 5632, smooth="mlp_norm", smooth_len=2048, **L, **T),
+        Layer("up_proj", M, 2048, 5632, smooth="mlp_norm", smooth_len=2048, **L, **T),
         Layer("down_proj", M, 5632, 2048, smooth="up_to_down", smooth_len=5632, **L),
     )
 
@@ -108,6 +120,17 @@ WORKLOADS = {
         "intermediate-5632 decoder block at batch 1, seq 1024, W8A8 with "
         "folded smoothing vectors, int8 in, int16 out",
         _tinyllama_block(1024)),
+    "block_w8a8_asym_tinyllama_s1024": Workload(
+        "block_w8a8_asym_tinyllama_s1024",
+        "the same decoder block in the paper's main W8A8 setting: asymmetric "
+        "weights, one range per tensor except per-channel down_proj",
+        _tinyllama_block(1024, asym=True)),
+    "w4a8_asym_down_tinyllama": Workload(
+        "w4a8_asym_down_tinyllama",
+        "the paper's main W4A8 setting on the down-proj K=5632, N=2048: "
+        "asymmetric per-channel int4, int16 out, at M=1 and M=1024",
+        (Layer("down_proj_m1", 1, 5632, 2048, w_bits=4, out_bits=16, asym=True),
+         Layer("down_proj_m1024", 1024, 5632, 2048, w_bits=4, out_bits=16, asym=True))),
     "gemma2b_w8a8": Workload(
         "gemma2b_w8a8",
         "Gemma-2B-shaped W8A8 layers: MLP gate/up K=2048 N=16384 and down "
@@ -149,6 +172,11 @@ def gen_weights(N: int, K: int, seed_key) -> np.ndarray:
     return w
 
 
+def gen_row_means(N: int, seed_key) -> np.ndarray:
+    rng = _rng("mu", *seed_key)
+    return (rng.uniform(-2.0, 2.0, size=N) * W_STD).astype(np.float32)
+
+
 def gen_bias(N: int, seed_key) -> np.ndarray:
     rng = _rng("b", *seed_key)
     return (rng.standard_normal(N, dtype=np.float32) * np.float32(B_STD)).astype(np.float32)
@@ -188,12 +216,16 @@ class LayerData:
     out_range: tuple               # static output range
 
 
-def _output_range(x: np.ndarray, s: Optional[np.ndarray], has_bias: bool):
+def _output_range(x: np.ndarray, s: Optional[np.ndarray], has_bias: bool,
+                  mu: Optional[np.ndarray] = None):
     xs = x.astype(np.float64)
     if s is not None:
         xs = xs * s.astype(np.float64)[None, :]
     row_ss = np.einsum("mk,mk->m", xs, xs)
-    sigma_y = W_STD * float(np.sqrt(np.mean(row_ss)))
+    var_y = W_STD ** 2 * float(np.mean(row_ss))
+    if mu is not None:
+        var_y += float(np.mean(mu.astype(np.float64) ** 2)) * float(np.mean(xs.sum(axis=1) ** 2))
+    sigma_y = float(np.sqrt(var_y))
     sb = 3.0 * B_STD if has_bias else 0.0
     return (float(np.float32(-4.5 * sigma_y - sb)), float(np.float32(5.5 * sigma_y + sb)))
 
@@ -212,10 +244,14 @@ def make_layer(workload: str, layer: Layer, rows: Optional[slice] = None,
         x = gen_activations(_x_rows(workload, layer), layer.K, layer.act, key_x)
     x = np.ascontiguousarray(x[: layer.M])
     w = gen_weights(layer.N, layer.K, (workload, _w_name(layer)))
+    mu = None
+    if layer.asym:
+        mu = gen_row_means(layer.N, (workload, _w_name(layer)))
+        w += mu[:, None]
     s = smoothing_for(layer, workload)
     bias = gen_bias(layer.N, (workload, _w_name(layer))) if layer.bias else None
     act_range = (float(x.min()), float(x.max()))
-    out_range = _output_range(x, s, layer.bias)
+    out_range = _output_range(x, s, layer.bias, mu)
     if rows is not None:
         x = np.ascontiguousarray(x[rows])
     return LayerData(layer, x, w, s, bias, act_range, out_range)

@@ -29,20 +29,28 @@ class LayerResult:
     w_hat: Optional[np.ndarray]
     y_q: np.ndarray
     y: np.ndarray
+    w_zp: Optional[np.ndarray] = None      # asymmetric weights only
+    a_rowsum: Optional[np.ndarray] = None  # asymmetric weights only
 
 
 def oracle_layer(ld: LayerData, rows=None, nthreads=None) -> LayerResult:
     L = ld.layer
     w_hat = oracle.fold_weights(ld.w, ld.s) if ld.s is not None else None
-    wq, ws, cs = oracle.pack_weights(w_hat if w_hat is not None else ld.w, L.w_bits)
+    w_in = w_hat if w_hat is not None else ld.w
+    zw = None
+    if L.asym:
+        wq, ws, zw, cs = oracle.pack_weights_asym(w_in, L.w_bits, per_tensor=L.per_tensor)
+    else:
+        wq, ws, cs = oracle.pack_weights(w_in, L.w_bits)
     a_scale, a_zp = oracle.act_params(*ld.act_range, 8)
     out_scale, out_zp = oracle.act_params(*ld.out_range, L.out_bits)
     x = ld.x if rows is None else ld.x[rows]
     a_q = oracle.quantize_act(x, a_scale, a_zp, 8)
     y_q = oracle.qlinear(a_q, wq, L.w_bits, ws, a_scale, a_zp, out_scale, out_zp, L.out_bits,
-                         bias=ld.bias, nthreads=nthreads)
+                         bias=ld.bias, nthreads=nthreads, w_zp=zw)
     y = oracle.dequant(y_q, out_scale, out_zp)
-    return LayerResult(a_scale, a_zp, out_scale, out_zp, a_q, wq, ws, cs, w_hat, y_q, y)
+    rs = oracle.act_rowsum(a_q) if L.asym else None
+    return LayerResult(a_scale, a_zp, out_scale, out_zp, a_q, wq, ws, cs, w_hat, y_q, y, zw, rs)
 
 
 def gpu_layer(ld: LayerData, path: int = 0, keep_device=False, workspace=None):
@@ -61,18 +69,27 @@ def gpu_layer(ld: LayerData, path: int = 0, keep_device=False, workspace=None):
     a_scale, a_zp = mq.mq_act_params(*ld.act_range, 8)
     out_scale, out_zp = mq.mq_act_params(*ld.out_range, L.out_bits)
     a_q = mq.mq_quantize_act(x, a_scale, a_zp, 8)
-    wq, ws, cs = mq.mq_pack_weights(w_hat if w_hat is not None else w, L.w_bits)
-    y_q = mq.mq_qlinear(a_q, wq, L.w_bits, ws, cs, a_scale, a_zp, out_scale, out_zp,
-                        L.out_bits, bias=bias, path=path, workspace=workspace)
+    w_in = w_hat if w_hat is not None else w
+    zw = rs = None
+    if L.asym:
+        wq, ws, zw, cs = mq.mq_pack_weights_asym(w_in, L.w_bits, per_tensor=L.per_tensor)
+        rs = mq.mq_act_rowsum(a_q)
+        y_q = mq.mq_qlinear_asym(a_q, rs, wq, L.w_bits, ws, zw, cs, a_scale, a_zp, out_scale,
+                                 out_zp, L.out_bits, bias=bias, path=path, workspace=workspace)
+    else:
+        wq, ws, cs = mq.mq_pack_weights(w_in, L.w_bits)
+        y_q = mq.mq_qlinear(a_q, wq, L.w_bits, ws, cs, a_scale, a_zp, out_scale, out_zp,
+                            L.out_bits, bias=bias, path=path, workspace=workspace)
     y = mq.mq_dequant(y_q, out_scale, out_zp)
     torch.cuda.synchronize()
     res = LayerResult(a_scale, a_zp, out_scale, out_zp, a_q.cpu().numpy(), wq.cpu().numpy(),
                       ws.cpu().numpy(), cs.cpu().numpy(),
                       None if w_hat is None else w_hat.cpu().numpy(), y_q.cpu().numpy(),
-                      y.cpu().numpy())
+                      y.cpu().numpy(), None if zw is None else zw.cpu().numpy(),
+                      None if rs is None else rs.cpu().numpy())
     if keep_device:
         return res, dict(a_q=a_q, w_q=wq, w_scale=ws, w_colsum=cs, bias=bias, a_scale=a_scale,
-                         a_zp=a_zp, out_scale=out_scale, out_zp=out_zp)
+                         a_zp=a_zp, out_scale=out_scale, out_zp=out_zp, w_zp=zw, a_rowsum=rs)
     return res
 
 
@@ -86,8 +103,13 @@ def assert_same(g: LayerResult, o: LayerResult, rows=None, check_weights=True):
         assert np.array_equal(g.w_scale.view(np.uint32), o.w_scale.view(np.uint32)), "w_scale"
         assert np.array_equal(g.w_q, o.w_q), "packed weights differ"
         assert np.array_equal(g.w_colsum, o.w_colsum), "column sums differ"
+        if o.w_zp is not None:
+            assert np.array_equal(g.w_zp, o.w_zp), "weight zero-points differ"
     ga = g.a_q if rows is None else g.a_q[rows]
     assert np.array_equal(ga, o.a_q), "quantized activations differ"
+    if o.a_rowsum is not None:
+        gr = g.a_rowsum if rows is None else g.a_rowsum[rows]
+        assert np.array_equal(gr, o.a_rowsum), "activation row sums differ"
     gy = g.y_q if rows is None else g.y_q[rows]
     if not np.array_equal(gy, o.y_q):
         bad = np.argwhere(gy != o.y_q)

@@ -108,6 +108,32 @@ def test_workspace_bytes_query():
     assert mq.mq_qlinear_workspace_bytes(512, 16384, 2048, 8, 16) == n
 
 
+def qlin_asym(**kw):
+    a = dict(a_q=NZ, a_rowsum=NZ, M=4, K=64, N=8, w_q=NZ, w_bits=8, w_scale=NZ, w_zp=NZ,
+             w_colsum=NZ, a_scale=0.1, a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None,
+             y_q=NZ, workspace=None, workspace_bytes=0, path=0, stream=None)
+    a.update(kw)
+    return mq.lib().mq_qlinear_asym(a["a_q"], a["a_rowsum"], a["M"], a["K"], a["N"], a["w_q"],
+                                    a["w_bits"], a["w_scale"], a["w_zp"], a["w_colsum"],
+                                    a["a_scale"], a["a_zp"], a["out_scale"], a["out_zp"],
+                                    a["out_bits"], a["bias"], a["y_q"], a["workspace"],
+                                    a["workspace_bytes"], a["path"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(a_rowsum=None), dict(w_zp=None), dict(a_q=None), dict(w_colsum=None), dict(K=0),
+    dict(K=65537), dict(w_bits=4, K=63), dict(out_bits=12), dict(a_zp=200), dict(path=1, M=17),
+    dict(workspace=P(256 + 16), workspace_bytes=4096), dict(workspace_bytes=-1),
+])
+def test_qlinear_asym_rejects_invalid_arguments(kw):
+    assert qlin_asym(**kw) == 1
+
+
+def test_qlinear_asym_empty_shapes_are_noops():
+    assert qlin_asym(M=0, a_rowsum=None, a_q=None) == 0
+    assert qlin_asym(N=0, w_zp=None) == 0
+
+
 def test_qlinear_empty_shapes_are_noops():
     # M = 0 or N = 0: nothing to compute, no device touched
     assert qlin(M=0) == 0
@@ -129,6 +155,17 @@ def test_qlinear_empty_shapes_are_noops():
     lambda L: L.mq_pack_weights(NZ, 4, 65537, 8, NZ, NZ, NZ, None),
     lambda L: L.mq_pack_weights(NZ, 4, 64, 3, NZ, NZ, NZ, None),
     lambda L: L.mq_pack_weights(NZ, 4, 64, 8, NZ, None, NZ, None),
+    lambda L: L.mq_pack_weights_asym(NZ, 4, 63, 4, 0, NZ, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights_asym(NZ, 4, 0, 8, 0, NZ, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights_asym(NZ, 4, 64, 2, 0, NZ, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights_asym(NZ, 4, 64, 8, 0, NZ, NZ, None, NZ, None),
+    lambda L: L.mq_pack_weights_asym(NZ, -1, 64, 8, 0, NZ, NZ, NZ, NZ, None),
+    lambda L: L.mq_pack_weights_asym(NZ, 4, 64, 8, 2, NZ, NZ, NZ, NZ, None),
+    lambda L: L.mq_act_rowsum(NZ, 4, 0, NZ, None),
+    lambda L: L.mq_act_rowsum(NZ, -1, 4, NZ, None),
+    lambda L: L.mq_act_rowsum(NZ, 4, 65537, NZ, None),
+    lambda L: L.mq_act_rowsum(None, 4, 4, NZ, None),
+    lambda L: L.mq_act_rowsum(NZ, 4, 4, None, None),
     lambda L: L.mq_fold_weights(NZ, None, 4, 4, NZ, None),
     lambda L: L.mq_fold_acts(NZ, NZ, -1, 4, NZ, None),
 ])
@@ -142,6 +179,8 @@ def test_zero_sized_elementwise_calls_are_noops():
     assert L.mq_dequant(None, 16, 0, 0.1, 0, None, None) == 0
     assert L.mq_pack_weights(None, 0, 64, 8, None, None, None, None) == 0
     assert L.mq_fold_weights(None, None, 0, 7, None, None) == 0
+    assert L.mq_pack_weights_asym(None, 0, 64, 4, 1, None, None, None, None, None) == 0
+    assert L.mq_act_rowsum(None, 0, 64, None, None) == 0
 
 
 def test_act_params_matches_oracle():
