@@ -216,9 +216,11 @@ class Prepared:
         the consecutive run of dominant-kernel launches listed in `dom`."""
         mq = self.mq
         for inp in self.inputs.values():
-            mq.mq_quantize_act(inp["x"], inp["scale"], inp["zp"], 8, out=inp["q"])
-            if inp["rs"] is not None:
-                mq.mq_act_rowsum(inp["q"], out=inp["rs"])
+            if inp["rs"] is not None:  # codes and their row sums in one pass
+                mq.mq_quantize_act_rowsum(inp["x"], inp["scale"], inp["zp"], out=inp["q"],
+                                          rowsum=inp["rs"])
+            else:
+                mq.mq_quantize_act(inp["x"], inp["scale"], inp["zp"], 8, out=inp["q"])
         for i, e in enumerate(self.layers):
             if events is not None and dom and i == dom[0]:
                 events[0].record()

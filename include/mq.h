@@ -249,6 +249,19 @@ mq_status mq_act_rowsum(const int8_t* a_q, int64_t M, int64_t K, int32_t* rowsum
                         void* stream);
 
 /*
+ * mq_quantize_act_rowsum -- mq_quantize_act at 8 bits on x [M][K] fused
+ * with mq_act_rowsum of the codes it writes (one pass; the codes are those
+ * of mq_quantize_act bit for bit).  For the activations that feed layers
+ * with asymmetric weights.
+ *   x       device fp32 [M][K]       x_q  device int8 [M][K]
+ *   alpha   finite, > 0              zp   in [-128, 127]
+ *   rowsum  device int32 [M]
+ *   M >= 0 (0 -> nothing to do), 1 <= K <= MQ_MAX_K.
+ */
+mq_status mq_quantize_act_rowsum(const float* x, int64_t M, int64_t K, float alpha,
+                                 int32_t zp, int8_t* x_q, int32_t* rowsum, void* stream);
+
+/*
  * mq_qlinear_asym -- mq_qlinear_ws for asymmetric per-channel weights
  * (Section 5.1).  For every token m and output channel n:
  *   c = sat_int32( sum_k (A_q[m][k] - a_zp) * (W_q[n][k] - w_zp[n])
@@ -257,8 +270,8 @@ mq_status mq_act_rowsum(const int8_t* a_q, int64_t M, int64_t K, int32_t* rowsum
  * it as acc - a_zp * w_colsum[n] - w_zp[n] * (a_rowsum[m] - K * a_zp)
  * + bias_q[n].
  *   a_rowsum  device int32 [M], sum_k A_q[m][k] as written by
- *             mq_act_rowsum for this a_q (not checked: other values give
- *             other results)
+ *             mq_act_rowsum or mq_quantize_act_rowsum for this a_q (not
+ *             checked: other values give other results)
  *   w_q, w_scale, w_zp, w_colsum  as written by mq_pack_weights_asym
  *             (w_zp device int32 [N], within the signed range of w_bits)
  *   everything else as in mq_qlinear_ws (same workspace rules; the split

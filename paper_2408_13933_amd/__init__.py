@@ -15,7 +15,8 @@ import os
 __all__ = [
     "MQError", "lib", "lib_path", "mq_version", "mq_act_params", "mq_fold_weights",
     "mq_fold_acts", "mq_quantize_act", "mq_pack_weights", "mq_qlinear", "mq_dequant",
-    "mq_pack_weights_asym", "mq_act_rowsum", "mq_qlinear_asym", "mq_qlinear_workspace_bytes",
+    "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum", "mq_qlinear_asym",
+    "mq_qlinear_workspace_bytes",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
 ]
 
@@ -73,12 +74,14 @@ def lib():
     L.mq_pack_weights_asym.argtypes = [c_p, c_i64, c_i64, c_i32, c_i32, c_p, c_p, c_p, c_p,
                                        c_p]
     L.mq_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_p, c_p]
+    L.mq_quantize_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_p, c_p, c_p]
     L.mq_qlinear_asym.argtypes = [c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_p,
                                   c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p, c_p, c_i64, c_i32,
                                   c_p]
     for name in ("mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
-                 "mq_pack_weights_asym", "mq_act_rowsum", "mq_qlinear_asym"):
+                 "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
+                 "mq_qlinear_asym"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -238,6 +241,20 @@ def mq_act_rowsum(a_q, out=None, stream=None):
                                _dev_ptr(out, torch.int32, "out", (M,)), _stream_ptr(stream)),
            "mq_act_rowsum")
     return out
+
+
+def mq_quantize_act_rowsum(x, alpha: float, zp: int, out=None, rowsum=None, stream=None):
+    """8-bit Eq.(4) quantizer on x [M][K] and the row sums of its codes, in
+    one pass: returns (x_q, rowsum)."""
+    torch = _torch()
+    M, K = x.shape
+    out = torch.empty((M, K), dtype=torch.int8, device=x.device) if out is None else out
+    rowsum = torch.empty(M, dtype=torch.int32, device=x.device) if rowsum is None else rowsum
+    _check(lib().mq_quantize_act_rowsum(_dev_ptr(x, torch.float32, "x"), M, K, float(alpha),
+                                        int(zp), _dev_ptr(out, torch.int8, "out", (M, K)),
+                                        _dev_ptr(rowsum, torch.int32, "rowsum", (M,)),
+                                        _stream_ptr(stream)), "mq_quantize_act_rowsum")
+    return out, rowsum
 
 
 def _workspace_args(workspace):

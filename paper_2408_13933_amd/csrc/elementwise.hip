@@ -64,10 +64,10 @@ __device__ inline int32_t code_from_quotient(float t, int32_t zp)
 
 // One float4 -> 4 codes per thread and step, lanes on consecutive float4s
 // (every load and store instruction covers a contiguous span); two steps
-// per loop trip keep two loads in flight.
+// per loop trip keep two loads in flight.  Returns the sum of the 4 codes.
 template <int BITS>
-__device__ inline void quant_store4(const float4 a, float alpha, float inv, int32_t zp, void* q,
-                                    int64_t i)
+__device__ inline int32_t quant_store4(const float4 a, float alpha, float inv, int32_t zp, void* q,
+                                       int64_t i)
 {
 #pragma clang fp contract(off)
     const float xs[4] = {a.x, a.y, a.z, a.w};
@@ -95,6 +95,7 @@ __device__ inline void quant_store4(const float4 a, float alpha, float inv, int3
             make_uint2(((uint32_t)v0 & 0xFFFFu) | ((uint32_t)v1 << 16),
                        ((uint32_t)v2 & 0xFFFFu) | ((uint32_t)v3 << 16));
     }
+    return v0 + v1 + v2 + v3;
 }
 
 template <int BITS>
@@ -128,6 +129,61 @@ __global__ __launch_bounds__(kThreads) void quantize_act_scalar(const float* __r
         else
             static_cast<int16_t*>(q)[i] = (int16_t)v;
     }
+}
+
+// Sum over the block of one int32 per thread (every thread gets it).
+__device__ inline int32_t block_sum(int32_t v)
+{
+    __shared__ int32_t red[kThreads / 64];
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    int32_t t = 0;
+#pragma unroll
+    for (int i = 0; i < kThreads / 64; ++i) t += red[i];
+    return t;
+}
+
+// Eq.(4) quantizer on int8 rows fused with their code sums (the term that
+// asymmetric weights multiply): one block per row, the codes are those of
+// quantize_act_vec / quantize_act_scalar, bit for bit.
+__global__ __launch_bounds__(kThreads) void quantize_rowsum_vec(const float4* __restrict__ x,
+                                                                int64_t K4, float alpha,
+                                                                float inv_alpha, int32_t zp,
+                                                                int8_t* __restrict__ q,
+                                                                int32_t* __restrict__ rowsum)
+{
+    const int64_t m = blockIdx.x;
+    const float4* xr = x + m * K4;
+    int8_t* qr = q + m * K4 * 4;
+    int32_t sum = 0;
+    int64_t i = threadIdx.x;
+    for (; i + kThreads < K4; i += 2 * kThreads) {
+        const float4 a = xr[i];
+        const float4 b = xr[i + kThreads];
+        sum += quant_store4<8>(a, alpha, inv_alpha, zp, qr, i);
+        sum += quant_store4<8>(b, alpha, inv_alpha, zp, qr, i + kThreads);
+    }
+    if (i < K4) sum += quant_store4<8>(xr[i], alpha, inv_alpha, zp, qr, i);
+    sum = block_sum(sum);
+    if (threadIdx.x == 0) rowsum[m] = sum;
+}
+
+__global__ __launch_bounds__(kThreads) void quantize_rowsum_scalar(const float* __restrict__ x,
+                                                                   int64_t K, float alpha,
+                                                                   int32_t zp,
+                                                                   int8_t* __restrict__ q,
+                                                                   int32_t* __restrict__ rowsum)
+{
+    const int64_t m = blockIdx.x;
+    int32_t sum = 0;
+    for (int64_t k = threadIdx.x; k < K; k += kThreads) {
+        const int32_t v = quant1<8>(x[m * K + k], alpha, zp);
+        q[m * K + k] = (int8_t)v;
+        sum += v;
+    }
+    sum = block_sum(sum);
+    if (threadIdx.x == 0) rowsum[m] = sum;
 }
 
 template <int BITS>
@@ -574,6 +630,20 @@ hipError_t launch_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_
 {
     if (bits == 8) return pack_asym_t<8>(w, N, K, per_tensor, wq, scale, zp, colsum, st);
     return pack_asym_t<4>(w, N, K, per_tensor, wq, scale, zp, colsum, st);
+}
+
+hipError_t launch_quantize_act_rowsum(const float* x, int64_t M, int64_t K, float alpha,
+                                      int32_t zp, int8_t* q, int32_t* rowsum, hipStream_t st)
+{
+    // one block per row; M <= 2^31 - 1 (host validation)
+    if (K % 4 == 0 && aligned(x, 16) && aligned(q, 4)) {
+        const float inv = alpha < 0x1p126f ? 1.0f / alpha : __builtin_nanf("");
+        quantize_rowsum_vec<<<(unsigned)M, kThreads, 0, st>>>(
+            reinterpret_cast<const float4*>(x), K / 4, alpha, inv, zp, q, rowsum);
+    } else {
+        quantize_rowsum_scalar<<<(unsigned)M, kThreads, 0, st>>>(x, K, alpha, zp, q, rowsum);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_act_rowsum(const int8_t* a, int64_t M, int64_t K, int32_t* rowsum,

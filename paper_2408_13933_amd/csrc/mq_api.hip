@@ -136,6 +136,17 @@ mq_status mq_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bit
                                                  w_zp, w_colsum, as_stream(stream)));
 }
 
+mq_status mq_quantize_act_rowsum(const float* x, int64_t M, int64_t K, float alpha, int32_t zp,
+                                 int8_t* x_q, int32_t* rowsum, void* stream)
+{
+    if (M < 0 || M > 0x7FFFFFFF || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(alpha) || !zp_ok(zp, 8)) return MQ_ERR_INVALID_ARG;
+    if (M == 0) return MQ_OK;
+    if (!x || !x_q || !rowsum) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_quantize_act_rowsum(x, M, K, alpha, zp, x_q, rowsum,
+                                                   as_stream(stream)));
+}
+
 mq_status mq_act_rowsum(const int8_t* a_q, int64_t M, int64_t K, int32_t* rowsum, void* stream)
 {
     if (M < 0 || M > 0x7FFFFFFF || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;

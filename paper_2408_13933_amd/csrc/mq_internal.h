@@ -43,6 +43,8 @@ hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int32_t bit
 hipError_t launch_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bits,
                                     bool per_tensor, void* wq, float* scale, int32_t* zp,
                                     int32_t* colsum, hipStream_t s);
+hipError_t launch_quantize_act_rowsum(const float* x, int64_t M, int64_t K, float alpha,
+                                      int32_t zp, int8_t* q, int32_t* rowsum, hipStream_t s);
 hipError_t launch_act_rowsum(const int8_t* a, int64_t M, int64_t K, int32_t* rowsum,
                              hipStream_t s);
 

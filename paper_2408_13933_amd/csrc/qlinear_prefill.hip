@@ -186,13 +186,16 @@ struct Staging {
 // Rows past M fall outside the descriptor and are dropped by the hardware;
 // channel groups past N get an out-of-range offset.  The requant is the
 // integer form with one mul_hi per output (cheaper on gfx950 than fp64
-// conversions).  FAST: no column needs the pre-shift, the output zero-point
-// is folded into the rounding constants and N % 4 == 0, leaving
-// sat-add, mul_hi, add, shift, clamp per output.
+// conversions).  FAST: off is in the accumulator's start value, the output
+// zero-point is folded into the rounding constants and N % 4 == 0, leaving
+// mul_hi, add, shift, clamp per output; PRE adds the clamp and left shift
+// of the columns whose shift is below 33 (large rescale factors, typical of
+// int16 outputs), which the plain FAST form leaves out when no column of
+// the tile needs them.
 // ASYM (asymmetric weights) adds -w_zp[n] * rs[m]: the fast form has it in
 // the accumulator's start value already, the other adds it exactly in
 // int64 before the saturation.
-template <class C, bool ASYM, bool FAST, bool STAGED, class Acc>
+template <class C, bool ASYM, bool FAST, bool PRE, bool STAGED, class Acc>
 __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
@@ -241,6 +244,8 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
                             c = corrected_acc_asym(a32, off[r], nzw[r], rs[j]);
                         else
                             c = __builtin_elementwise_add_sat(a32, off[r]);
+                    }
+                    if constexpr (!FAST || PRE) {
                         c = max(min(c, bnd[r]), -bnd[r]);
                         c = (int32_t)((uint32_t)c << pre[r]);
                     }
@@ -496,8 +501,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     flags = __builtin_amdgcn_readfirstlane(flags);
     const bool zp_fold = (flags & 2) != 0;
     // the fast epilogue form: one mul_hi per output, zero-point in the
-    // rounding constant, off in the accumulator's start value
-    const bool fast = (flags == 7) && (p.N % 4) == 0;
+    // rounding constant, off in the accumulator's start value; pre0: no
+    // column of the tile needs the pre-shift.  The 256x256 tile has no
+    // registers left for the pre-shift forms.
+    constexpr bool kPreForms = C::TM * C::TN < 256 * 256;
+    const bool pre0 = (flags & 1) != 0;
+    const bool fast = (kPreForms ? (flags & 6) == 6 : flags == 7) && (p.N % 4) == 0;
     if (zp_fold && tid < C::TN) e_rnd[tid] += p.out_zp * (1 << (e_sp[tid] & 0xFF));
     // stage STAGES-1: the part the stage switch step would issue; the rest
     // goes out during the first stage's steps, as for every later stage
@@ -761,9 +770,16 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // staged stores need the tile's channels inside N and 16-byte row chunks
     const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
                         ((uintptr_t)p.y % 16) == 0;
-    if (staged) prefill_epilogue<C, ASYM, true, true>(acc, ctx);
-    else if (fast) prefill_epilogue<C, ASYM, true, false>(acc, ctx);
-    else prefill_epilogue<C, ASYM, false, false>(acc, ctx);
+    if constexpr (kPreForms) {
+        if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true>(acc, ctx);
+        else if (staged) prefill_epilogue<C, ASYM, true, true, true>(acc, ctx);
+        else if (fast) prefill_epilogue<C, ASYM, true, true, false>(acc, ctx);
+        else prefill_epilogue<C, ASYM, false, false, false>(acc, ctx);
+    } else {
+        if (staged) prefill_epilogue<C, ASYM, true, false, true>(acc, ctx);
+        else if (fast) prefill_epilogue<C, ASYM, true, false, false>(acc, ctx);
+        else prefill_epilogue<C, ASYM, false, false, false>(acc, ctx);
+    }
 }
 
 template <class C, bool ASYM>

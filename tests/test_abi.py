@@ -161,6 +161,13 @@ def test_qlinear_empty_shapes_are_noops():
     lambda L: L.mq_pack_weights_asym(NZ, 4, 64, 8, 0, NZ, NZ, None, NZ, None),
     lambda L: L.mq_pack_weights_asym(NZ, -1, 64, 8, 0, NZ, NZ, NZ, NZ, None),
     lambda L: L.mq_pack_weights_asym(NZ, 4, 64, 8, 2, NZ, NZ, NZ, NZ, None),
+    lambda L: L.mq_quantize_act_rowsum(NZ, 4, 0, 0.1, 0, NZ, NZ, None),
+    lambda L: L.mq_quantize_act_rowsum(NZ, -1, 8, 0.1, 0, NZ, NZ, None),
+    lambda L: L.mq_quantize_act_rowsum(NZ, 4, 8, 0.0, 0, NZ, NZ, None),
+    lambda L: L.mq_quantize_act_rowsum(NZ, 4, 8, float("nan"), 0, NZ, NZ, None),
+    lambda L: L.mq_quantize_act_rowsum(NZ, 4, 8, 0.1, 128, NZ, NZ, None),
+    lambda L: L.mq_quantize_act_rowsum(NZ, 4, 8, 0.1, 0, NZ, None, None),
+    lambda L: L.mq_quantize_act_rowsum(None, 4, 8, 0.1, 0, NZ, NZ, None),
     lambda L: L.mq_act_rowsum(NZ, 4, 0, NZ, None),
     lambda L: L.mq_act_rowsum(NZ, -1, 4, NZ, None),
     lambda L: L.mq_act_rowsum(NZ, 4, 65537, NZ, None),
@@ -181,6 +188,7 @@ def test_zero_sized_elementwise_calls_are_noops():
     assert L.mq_fold_weights(None, None, 0, 7, None, None) == 0
     assert L.mq_pack_weights_asym(None, 0, 64, 4, 1, None, None, None, None, None) == 0
     assert L.mq_act_rowsum(None, 0, 64, None, None) == 0
+    assert L.mq_quantize_act_rowsum(None, 0, 64, 0.1, 0, None, None, None) == 0
 
 
 def test_act_params_matches_oracle():

@@ -69,6 +69,31 @@ def test_act_rowsum_parity(M, K, offset):
     assert np.array_equal(rs.cpu().numpy(), oracle.act_rowsum(a))
 
 
+@pytest.mark.parametrize("M,K,offset", [(1, 2048, 0), (7, 5632, 0), (33, 1001, 0), (64, 2048, 1),
+                                        (3, 65536, 0), (1024, 2048, 0), (5, 6, 2)])
+def test_quantize_act_rowsum_parity(M, K, offset):
+    """The fused quantizer + row sum: codes equal the oracle's Eq.(4) codes
+    and the plain quantizer's, row sums the oracle's sums of those codes.
+    offset > 0 puts x off its 16-byte alignment (the scalar path)."""
+    mq, torch = _mq(), _torch()
+    rng = np.random.default_rng(M * 7 + K)
+    x = rng.standard_normal((M, K)).astype(np.float32) * 3
+    x[:, : min(K, 4)] *= 30.0
+    x.reshape(-1)[:3] = [np.nan, np.inf, -np.inf]
+    alpha, zp = mq.mq_act_params(-10.0, 14.0, 8)
+    # values on and next to the rounding ties of the grid
+    ties = ((np.arange(K) % 40 - 20) + 0.5).astype(np.float32) * np.float32(alpha)
+    x[-1] = np.where(np.arange(K) % 2 == 0, ties, np.nextafter(ties, np.float32(np.inf)))
+    buf = torch.empty(M * K + offset, dtype=torch.float32, device="cuda")
+    gx = buf[offset:].view(M, K)
+    gx.copy_(torch.from_numpy(x))
+    q, rs = mq.mq_quantize_act_rowsum(gx, alpha, zp)
+    ref = oracle.quantize_act(x, alpha, zp, 8)
+    assert np.array_equal(q.cpu().numpy(), ref)
+    assert np.array_equal(rs.cpu().numpy(), oracle.act_rowsum(ref))
+    assert np.array_equal(mq.mq_quantize_act(gx, alpha, zp, 8).cpu().numpy(), ref)
+
+
 ASYM_CASES = [
     # M, K, N, w_bits, out_bits, bias, per_tensor -- several tiles, ragged tails
     (1, 2048, 520, 8, 8, True, False),       # decode
