@@ -268,6 +268,45 @@ def test_extreme_accumulators_at_max_k(w_bits):
             assert np.array_equal(y.cpu().numpy(), ref), (M, path, a_zp)
 
 
+@pytest.mark.parametrize("tile", ["0", "1", "2"])
+@pytest.mark.parametrize("asym", [False, True])
+def test_prefill_epilogue_forms(tile, asym, monkeypatch):
+    """Every epilogue form of every prefill tile: per-column rescale factors
+    spread over 8 decades (shifts from 0 to 64 over the output scales, so
+    one tile mixes columns with and without the pre-shift), int8 and int16
+    outputs, N giving staged stores (256), a ragged last tile (260) and
+    N % 4 != 0 (258)."""
+    mq, torch = _mq(), _torch()
+    monkeypatch.setenv("MQ_PREFILL_TILE", tile)
+    dev = torch.device("cuda", 0)
+    rng = np.random.default_rng(int(tile) * 2 + asym)
+    M, K = 300, 512
+    a = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    g_a = torch.from_numpy(a).to(dev)
+    rs = mq.mq_act_rowsum(g_a)
+    for N in (256, 260, 258):
+        codes = rng.integers(-128, 128, (N, K))
+        wq = codes.astype(np.int8)
+        cs = codes.sum(axis=1).astype(np.int32)
+        zw = rng.integers(-128, 128, N).astype(np.int32) if asym else None
+        ws = (10.0 ** rng.uniform(-7, 1, N)).astype(np.float32)
+        bias = (rng.standard_normal(N) * 0.5).astype(np.float32)
+        g = [torch.from_numpy(v).to(dev) for v in (wq, ws, cs, bias)]
+        for out_bits, out_scale, zp in ((8, 0.05, -7), (16, 0.002, 1234), (16, 30.0, -3),
+                                        (16, 1e-10, 0)):
+            if asym:
+                y = mq.mq_qlinear_asym(g_a, rs, g[0], 8, g[1], torch.from_numpy(zw).to(dev), g[2],
+                                       0.02, 5, out_scale, zp, out_bits, bias=g[3],
+                                       path=mq.PATH_PREFILL)
+            else:
+                y = mq.mq_qlinear(g_a, g[0], 8, g[1], g[2], 0.02, 5, out_scale, zp, out_bits,
+                                  bias=g[3], path=mq.PATH_PREFILL)
+            ref = oracle.qlinear(a, wq, 8, ws, 0.02, 5, out_scale, zp, out_bits, bias=bias,
+                                 w_zp=zw)
+            got = y.cpu().numpy()
+            assert np.array_equal(got, ref), (N, out_bits, out_scale, int((got != ref).sum()))
+
+
 def test_empty_shapes():
     mq, torch = _mq(), _torch()
     dev = torch.device("cuda", 0)
