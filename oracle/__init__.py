@@ -97,6 +97,11 @@ def _load():
                                         ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
                                         ctypes.c_int, _vp, _vp, ctypes.c_int]
     lib.oracle_qlinear_asym.restype = None
+    lib.oracle_qlinear_gen.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+                                       ctypes.c_int64, _vp, ctypes.c_int, _f32p, _vp,
+                                       ctypes.c_float, ctypes.c_int32, ctypes.c_float,
+                                       ctypes.c_int32, ctypes.c_int, _vp, _vp, ctypes.c_int]
+    lib.oracle_qlinear_gen.restype = None
     lib.oracle_int_matmul.argtypes = [_i8p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                       _vp, ctypes.c_int, _i64p]
     lib.oracle_int_matmul.restype = None
@@ -257,10 +262,14 @@ def qlinear(a_q: np.ndarray, w_q: np.ndarray, bits: int, w_scale: np.ndarray,
             bias=None, nthreads: int | None = None, w_zp=None) -> np.ndarray:
     """Integer-only linear layer: Y_q[m][n] from A_q[M][K] and W_q.
 
-    ``w_zp`` (int32 [N]) gives per-channel weight zero-points; None means
-    symmetric weights.
+    ``a_q`` is int8, or int16 for 16-bit activations (W8A16).  ``w_zp``
+    (int32 [N]) gives per-channel weight zero-points; None means symmetric
+    weights.
     """
-    a_q = np.ascontiguousarray(a_q, dtype=np.int8)
+    a_q = np.ascontiguousarray(a_q)
+    if a_q.dtype not in (np.int8, np.int16):
+        raise ValueError("a_q must be int8 or int16")
+    a_bits = 8 if a_q.dtype == np.int8 else 16
     M, K = a_q.shape
     w_q = np.ascontiguousarray(w_q)
     N = w_q.shape[0]
@@ -285,9 +294,9 @@ def qlinear(a_q: np.ndarray, w_q: np.ndarray, bits: int, w_scale: np.ndarray,
     y = np.empty((M, N), dtype=_act_dtype(bits_y))
     if M == 0 or N == 0:
         return y
-    _load().oracle_qlinear_asym(a_q, M, K, N, _ptr(w_q), bits, w_scale, zptr, alpha_a,
-                                zp_a, alpha_y, zp_y, bits_y, bptr, _ptr(y),
-                                nthreads or default_threads())
+    _load().oracle_qlinear_gen(_ptr(a_q), a_bits, M, K, N, _ptr(w_q), bits, w_scale, zptr,
+                               alpha_a, zp_a, alpha_y, zp_y, bits_y, bptr, _ptr(y),
+                               nthreads or default_threads())
     return y
 
 

@@ -371,12 +371,14 @@ int64_t oracle_requant_value(int64_t c, int64_t M0, int32_t sh, int32_t zp_y,
  *   c[m][n] = sat_int32( sum_k (A_q[m][k] - zp_a) * (W_q[n][k] - zp_w[n])
  *                        + bias_q[n] )
  *   Y_q[m][n] = requant(c[m][n])
- * zp_w = 0 for symmetric weights.  The sum is the plain definition,
- * accumulated exactly in int64 (integer MACs with a wide accumulator:
- * Section 1, Section 3.1).                                              */
+ * zp_w = 0 for symmetric weights.  A_q holds 8-bit codes, or 16-bit codes
+ * for the W8A16 setting (Section 5.6: 16-bit activations into 8-bit-weight
+ * matmuls).  The sum is the plain definition, accumulated exactly in int64
+ * (integer MACs with a wide accumulator: Section 1, Section 3.1).       */
 /* ------------------------------------------------------------------ */
 typedef struct {
-    const int8_t* a;
+    const void* a;
+    int a_bits;
     int64_t M, K, N;
     const void* w_q;
     int bits;
@@ -399,13 +401,15 @@ static void* qlinear_rows(void* arg)
 {
     qlinear_job* j = (qlinear_job*)arg;
     for (int64_t m = j->row_begin; m < j->row_end; ++m) {
-        const int8_t* arow = j->a + m * j->K;
+        const int8_t* arow8 = (const int8_t*)j->a + m * j->K;
+        const int16_t* arow16 = (const int16_t*)j->a + m * j->K;
         for (int64_t n = 0; n < j->N; ++n) {
             const int64_t zw = j->w_zp ? j->w_zp[n] : 0;
             int64_t acc = 0;
-            for (int64_t k = 0; k < j->K; ++k)
-                acc += ((int64_t)arow[k] - j->zp_a) *
-                       (weight_at(j->w_q, j->bits, j->K, n, k) - zw);
+            for (int64_t k = 0; k < j->K; ++k) {
+                const int64_t a = j->a_bits == 8 ? (int64_t)arow8[k] : (int64_t)arow16[k];
+                acc += (a - j->zp_a) * (weight_at(j->w_q, j->bits, j->K, n, k) - zw);
+            }
             int64_t c = clamp_i64(acc + j->bq[n], INT32_MIN, INT32_MAX);
             int64_t v = oracle_requant_value(c, j->M0[n], j->sh[n], j->zp_y,
                                              j->bits_y);
@@ -415,11 +419,11 @@ static void* qlinear_rows(void* arg)
     return NULL;
 }
 
-void oracle_qlinear_asym(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
-                         const void* w_q, int bits, const float* w_scale,
-                         const int32_t* w_zp, float alpha_a, int32_t zp_a,
-                         float alpha_y, int32_t zp_y, int bits_y,
-                         const float* bias, void* y_q, int nthreads)
+void oracle_qlinear_gen(const void* a_q, int a_bits, int64_t M, int64_t K, int64_t N,
+                        const void* w_q, int bits, const float* w_scale,
+                        const int32_t* w_zp, float alpha_a, int32_t zp_a,
+                        float alpha_y, int32_t zp_y, int bits_y,
+                        const float* bias, void* y_q, int nthreads)
 {
     int64_t* M0 = (int64_t*)malloc(sizeof(int64_t) * (size_t)N);
     int32_t* sh = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
@@ -432,7 +436,7 @@ void oracle_qlinear_asym(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
     pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
     qlinear_job* jobs = (qlinear_job*)malloc(sizeof(qlinear_job) * (size_t)nthreads);
     for (int t = 0; t < nthreads; ++t) {
-        qlinear_job j = {a_q, M, K, N, w_q, bits, w_scale, w_zp, alpha_a, zp_a,
+        qlinear_job j = {a_q, a_bits, M, K, N, w_q, bits, w_scale, w_zp, alpha_a, zp_a,
                          alpha_y, zp_y, bits_y, bias, y_q,
                          M * t / nthreads, M * (t + 1) / nthreads, M0, sh, bq};
         jobs[t] = j;
@@ -444,6 +448,17 @@ void oracle_qlinear_asym(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
     free(M0);
     free(sh);
     free(bq);
+}
+
+/* 8-bit activations.                                                   */
+void oracle_qlinear_asym(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                         const void* w_q, int bits, const float* w_scale,
+                         const int32_t* w_zp, float alpha_a, int32_t zp_a,
+                         float alpha_y, int32_t zp_y, int bits_y,
+                         const float* bias, void* y_q, int nthreads)
+{
+    oracle_qlinear_gen(a_q, 8, M, K, N, w_q, bits, w_scale, w_zp, alpha_a, zp_a,
+                       alpha_y, zp_y, bits_y, bias, y_q, nthreads);
 }
 
 /* Symmetric weights: zp_w = 0.                                         */

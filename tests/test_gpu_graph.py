@@ -67,3 +67,53 @@ def test_graph_replay_matches_eager(M, K, w_bits, out_bits):
         assert np.array_equal(deq.cpu().numpy().view(np.uint32), d_ref.view(np.uint32))
         step()  # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_graph_replay_asymmetric_split():
+    """Asymmetric weights with the fused quantizer + row sums and a K split
+    through a workspace, captured and replayed."""
+    import torch
+
+    import paper_2408_13933_amd as mq
+
+    M, K, N = 130, 8192, 384
+    layer = wl.Layer("g", M, K, N, w_bits=8, out_bits=16, asym=True)
+    ld = wl.make_layer("graph_asym", layer)
+    dev = torch.device("cuda", 0)
+    x = torch.from_numpy(ld.x).to(dev)
+    w = torch.from_numpy(ld.w).to(dev)
+    bias = torch.from_numpy(ld.bias).to(dev)
+    wq, ws, zw, cs = mq.mq_pack_weights_asym(w, 8)
+    a_scale, a_zp = mq.mq_act_params(*ld.act_range, 8)
+    o_scale, o_zp = mq.mq_act_params(*ld.out_range, 16)
+    a_q = torch.empty(x.shape, dtype=torch.int8, device=dev)
+    rs = torch.empty(M, dtype=torch.int32, device=dev)
+    y = torch.empty((M, N), dtype=torch.int16, device=dev)
+    nws = mq.mq_qlinear_workspace_bytes(M, K, N, 8, 16)
+    assert nws > 0
+    work = torch.zeros(nws, dtype=torch.uint8, device=dev)
+
+    def step():
+        mq.mq_quantize_act_rowsum(x, a_scale, a_zp, out=a_q, rowsum=rs)
+        mq.mq_qlinear_asym(a_q, rs, wq, 8, ws, zw, cs, a_scale, a_zp, o_scale, o_zp, 16,
+                           bias=bias, out=y, workspace=work)
+
+    step()
+    torch.cuda.synchronize()
+    y_ref = y.cpu().numpy().copy()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            step()
+    torch.cuda.current_stream().wait_stream(s)
+    for rep in range(4):
+        y.fill_(0)
+        rs.fill_(0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(y.cpu().numpy(), y_ref), f"replay {rep}"
+        step()
+        torch.cuda.synchronize()

@@ -623,6 +623,68 @@ def test_qlinear_asym_dequantized_output_tracks_the_layer(bits):
     assert err_asym < err_sym
 
 
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("out_bits", [8, 16])
+def test_qlinear_a16_bruteforce_tiny(bits, out_bits):
+    # 16-bit activation codes (the W8A16 setting) through the same exact
+    # rational reference
+    rng = np.random.default_rng(40 + bits + out_bits)
+    sizes = [1, 2, 3, 6]
+    Q = 127 if bits == 8 else 7
+    for M in sizes:
+        for N in sizes:
+            for K in sizes:
+                if bits == 4 and K % 2:
+                    continue
+                a = rng.integers(-32768, 32768, (M, K)).astype(np.int16)
+                a[0, 0] = -32768
+                a[-1, -1] = 32767
+                wv = rng.integers(-Q, Q + 1, (N, K))
+                if bits == 8:
+                    wq = wv.astype(np.int8)
+                else:
+                    wq = ((wv[:, 0::2] & 0xF) | ((wv[:, 1::2] & 0xF) << 4)).astype(np.uint8)
+                w_scale = rng.uniform(1e-3, 3e-2, N).astype(np.float32)
+                bias = rng.normal(0, 0.05, N).astype(np.float32) if N % 2 else None
+                alpha_a = float(np.float32(rng.uniform(1e-4, 2e-3)))
+                zp_a = int(rng.choice([-32768, -300, 0, 1234, 32767]))
+                alpha_y = float(np.float32(rng.uniform(0.001, 0.2) * (1e-2 if out_bits == 16 else 1)))
+                zp_y = int(rng.integers(-100, 100))
+                y = oracle.qlinear(a, wq, bits, w_scale, alpha_a, zp_a, alpha_y, zp_y, out_bits,
+                                   bias=bias, nthreads=2)
+                M0, sh, bq = _exact_params(alpha_a, w_scale, alpha_y, bias)
+                ref = bf.qlinear_exact(a.astype(int).tolist(), wv.tolist(), zp_a, bq, M0, sh,
+                                       zp_y, out_bits)
+                assert y.astype(int).tolist() == ref, (M, N, K)
+
+
+def test_qlinear_a16_reductions():
+    rng = np.random.default_rng(41)
+    M, K, N = 17, 300, 23
+    w = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    ws = rng.uniform(1e-3, 1e-2, N).astype(np.float32)
+    # int8-range codes stored as int16 give the int8 layer
+    a8 = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    args = (w, 8, ws, 0.05, 7, 0.02, -3, 16)
+    assert np.array_equal(oracle.qlinear(a8.astype(np.int16), *args), oracle.qlinear(a8, *args))
+    # unit rescale: numpy int64 (A - zp_a) W^T + zp_y
+    a = rng.integers(-32768, 32768, (M, K)).astype(np.int16)
+    y = oracle.qlinear(a, w, 8, np.full(N, 0.25, np.float32), 0.5, -1000, 0.125, 11, 16)
+    c = (a.astype(np.int64) + 1000) @ w.astype(np.int64).T
+    assert np.array_equal(y.astype(np.int64), np.clip(c + 11, -32768, 32767))
+    # the 32-bit accumulator saturates before the rescale: K = 65536 at the
+    # grid ends makes |sum| ~ 2^39, and a tiny rescale then shows the
+    # saturated int32 value, not the true sum
+    K = 65536
+    a = np.full((2, K), 32767, np.int16)
+    a[1] = -32768
+    w = np.full((2, K), 127, np.int8)
+    w[1] = -127
+    y = oracle.qlinear(a, w, 8, np.ones(2, np.float32), 2.0 ** -20, -32768, 1.0, 0, 16)
+    # c = +-(2^31 - 1) or -2^31, times 2^-20 -> +-2048 (round half up)
+    assert y.tolist() == [[2048, -2048], [0, 0]]
+
+
 def test_qlinear_textbook_reduction():
     # alpha_a * w_scale == alpha_y makes the rescale exactly 1: the layer is
     # then the integer matmul with zero-point plus the output zero-point,
