@@ -156,7 +156,7 @@ class Prepared:
             else:
                 w_q, w_scale, w_colsum = mq.mq_pack_weights(w, layer.w_bits)
             del w
-            a_scale, a_zp = mq.mq_act_params(*ld.act_range, 8)
+            a_scale, a_zp = mq.mq_act_params(*ld.act_range, layer.a_bits)
             out_scale, out_zp = mq.mq_act_params(*ld.out_range, layer.out_bits)
             entry = dict(layer=layer, data=ld, key=key, w_q=w_q, w_scale=w_scale, w_zp=w_zp,
                          w_colsum=w_colsum, a_scale=a_scale, a_zp=a_zp, out_scale=out_scale,
@@ -169,9 +169,11 @@ class Prepared:
         for e in self.layers:
             if e["key"] not in self.inputs:
                 x = torch.from_numpy(e["data"].x).to(dev)
-                self.inputs[e["key"]] = dict(x=x, q=torch.empty(x.shape, dtype=torch.int8,
-                                                                device=dev),
-                                             scale=e["a_scale"], zp=e["a_zp"], rs=None)
+                a_bits = e["layer"].a_bits
+                qdt = torch.int8 if a_bits == 8 else torch.int16
+                self.inputs[e["key"]] = dict(x=x, q=torch.empty(x.shape, dtype=qdt, device=dev),
+                                             scale=e["a_scale"], zp=e["a_zp"], rs=None,
+                                             bits=a_bits)
             if e["layer"].asym and self.inputs[e["key"]]["rs"] is None:
                 # asymmetric weights read the row sums of their quantized input
                 self.inputs[e["key"]]["rs"] = torch.empty(e["layer"].M, dtype=torch.int32,
@@ -202,6 +204,10 @@ class Prepared:
                                     e["w_colsum"], e["a_scale"], e["a_zp"], e["out_scale"],
                                     e["out_zp"], L.out_bits, bias=e["bias"], out=e["y"],
                                     workspace=workspace)
+        elif L.a_bits == 16:
+            self.mq.mq_qlinear_a16(inp["q"], w_q, L.w_bits, e["w_scale"], e["w_colsum"],
+                                   e["a_scale"], e["a_zp"], e["out_scale"], e["out_zp"],
+                                   L.out_bits, bias=e["bias"], out=e["y"])
         else:
             self.mq.mq_qlinear(inp["q"], w_q, L.w_bits, e["w_scale"], e["w_colsum"],
                                e["a_scale"], e["a_zp"], e["out_scale"], e["out_zp"], L.out_bits,
@@ -220,7 +226,7 @@ class Prepared:
                 mq.mq_quantize_act_rowsum(inp["x"], inp["scale"], inp["zp"], out=inp["q"],
                                           rowsum=inp["rs"])
             else:
-                mq.mq_quantize_act(inp["x"], inp["scale"], inp["zp"], 8, out=inp["q"])
+                mq.mq_quantize_act(inp["x"], inp["scale"], inp["zp"], inp["bits"], out=inp["q"])
         for i, e in enumerate(self.layers):
             if events is not None and dom and i == dom[0]:
                 events[0].record()
@@ -289,7 +295,7 @@ def cpu_baseline(prep: Prepared, target_s: float):
         for e, (wq, ws, b, zw) in zip(prep.layers, w_host):
             L = e["layer"]
             x = e["data"].x[:rows]
-            a = oracle.quantize_act(x, e["a_scale"], e["a_zp"], 8)
+            a = oracle.quantize_act(x, e["a_scale"], e["a_zp"], L.a_bits)
             oracle.qlinear(a, wq, L.w_bits, ws, e["a_scale"], e["a_zp"], e["out_scale"],
                            e["out_zp"], L.out_bits, bias=b, nthreads=nthreads, w_zp=zw)
             ops += 2 * rows * L.N * L.K

@@ -286,6 +286,26 @@ mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M,
                           int64_t workspace_bytes, int32_t path, void* stream);
 
 /*
+ * mq_qlinear_a16 -- mq_qlinear_ex with 16-bit activation codes (the W8A16
+ * setting of Section 5.6: activations kept at 16 bits, 8-bit weights):
+ *   c = sat_int32( sum_k (A_q[m][k] - a_zp) * W_q[n][k] + bias_q[n] )
+ * with the sum exact, then the requant of mq_qlinear.  The kernels split
+ * each code into its high byte and its low byte - 128 and run two int8
+ * products (exact).
+ *   a_q    device int16 [M][K] (as written by mq_quantize_act with bits 16)
+ *   a_zp   in [-32768, 32767]
+ *   w_q, w_bits, w_scale, w_colsum: symmetric weights as in mq_qlinear
+ *   (the tuned prefill kernel takes w_bits 8; w_bits 4 runs on the decode
+ *   kernel for M <= 16 and on the generic kernel otherwise).
+ *   Everything else as in mq_qlinear_ex.
+ */
+mq_status mq_qlinear_a16(const int16_t* a_q, int64_t M, int64_t K, int64_t N,
+                         const void* w_q, int32_t w_bits, const float* w_scale,
+                         const int32_t* w_colsum, float a_scale, int32_t a_zp,
+                         float out_scale, int32_t out_zp, int32_t out_bits,
+                         const float* bias, void* y_q, int32_t path, void* stream);
+
+/*
  * mq_dequant -- inverse of Eq.(4): y = alpha * (float)(q - zp), one exact
  * integer subtraction and one fp32 multiply.
  *   q      device int8 (bits 8) or int16 (bits 16) [numel]

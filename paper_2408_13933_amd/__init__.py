@@ -16,6 +16,7 @@ __all__ = [
     "MQError", "lib", "lib_path", "mq_version", "mq_act_params", "mq_fold_weights",
     "mq_fold_acts", "mq_quantize_act", "mq_pack_weights", "mq_qlinear", "mq_dequant",
     "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum", "mq_qlinear_asym",
+    "mq_qlinear_a16",
     "mq_qlinear_workspace_bytes",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
 ]
@@ -75,13 +76,15 @@ def lib():
                                        c_p]
     L.mq_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_p, c_p]
     L.mq_quantize_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_p, c_p, c_p]
+    L.mq_qlinear_a16.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32,
+                                 c_f, c_i32, c_i32, c_p, c_p, c_i32, c_p]
     L.mq_qlinear_asym.argtypes = [c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_p,
                                   c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p, c_p, c_i64, c_i32,
                                   c_p]
     for name in ("mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
-                 "mq_qlinear_asym"):
+                 "mq_qlinear_asym", "mq_qlinear_a16"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -288,6 +291,27 @@ def mq_qlinear_asym(a_q, a_rowsum, w_q, w_bits: int, w_scale, w_zp, w_colsum, a_
         float(a_scale), int(a_zp), float(out_scale), int(out_zp), int(out_bits), bptr,
         _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), ws, ws_bytes, int(path),
         _stream_ptr(stream)), "mq_qlinear_asym")
+    return out
+
+
+def mq_qlinear_a16(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: int,
+                   out_scale: float, out_zp: int, out_bits: int = 8, bias=None, out=None,
+                   path: int = PATH_AUTO, stream=None):
+    """Integer-only linear layer on 16-bit activation codes (W8A16)."""
+    torch = _torch()
+    M, K = a_q.shape
+    N = w_q.shape[0]
+    wq_dtype, wq_shape = (torch.int8, (N, K)) if w_bits == 8 else (torch.uint8, (N, K // 2))
+    out = (torch.empty((M, N), dtype=_act_dtype(out_bits), device=a_q.device)
+           if out is None else out)
+    bptr = None if bias is None else _dev_ptr(bias, torch.float32, "bias", (N,))
+    _check(lib().mq_qlinear_a16(
+        _dev_ptr(a_q, torch.int16, "a_q"), M, K, N, _dev_ptr(w_q, wq_dtype, "w_q", wq_shape),
+        int(w_bits), _dev_ptr(w_scale, torch.float32, "w_scale", (N,)),
+        _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)), float(a_scale), int(a_zp),
+        float(out_scale), int(out_zp), int(out_bits), bptr,
+        _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), int(path), _stream_ptr(stream)),
+        "mq_qlinear_a16")
     return out
 
 

@@ -188,12 +188,12 @@ namespace {
 
 // Validation and dispatch shared by the symmetric and asymmetric entry
 // points; w_zp and a_rowsum are both null (symmetric) or both set.
-mq_status qlinear_impl(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
-                       int64_t N, const void* w_q, int32_t w_bits, const float* w_scale,
-                       const int32_t* w_zp, const int32_t* w_colsum, float a_scale, int32_t a_zp,
-                       float out_scale, int32_t out_zp, int32_t out_bits, const float* bias,
-                       void* y_q, void* workspace, int64_t workspace_bytes, int32_t path,
-                       void* stream)
+mq_status qlinear_impl(const void* a_q, int32_t a_bits, const int32_t* a_rowsum, int64_t M,
+                       int64_t K, int64_t N, const void* w_q, int32_t w_bits,
+                       const float* w_scale, const int32_t* w_zp, const int32_t* w_colsum,
+                       float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                       int32_t out_bits, const float* bias, void* y_q, void* workspace,
+                       int64_t workspace_bytes, int32_t path, void* stream)
 {
     if (workspace_bytes < 0) return MQ_ERR_INVALID_ARG;
     if (workspace && ((uintptr_t)workspace % 256) != 0) return MQ_ERR_INVALID_ARG;
@@ -203,7 +203,7 @@ mq_status qlinear_impl(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, in
     if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || (M > 0 && N > kMaxElems / M)) return MQ_ERR_INVALID_ARG;
     if (w_bits == 4 && (K % 2) != 0) return MQ_ERR_INVALID_ARG;
     if (!finite_pos(a_scale) || !finite_pos(out_scale)) return MQ_ERR_INVALID_ARG;
-    if (!zp_ok(a_zp, 8) || !zp_ok(out_zp, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(a_zp, a_bits) || !zp_ok(out_zp, out_bits)) return MQ_ERR_INVALID_ARG;
     if (path < MQ_PATH_AUTO || path > MQ_PATH_GENERIC) return MQ_ERR_INVALID_ARG;
     if (path == MQ_PATH_DECODE && M > 16) return MQ_ERR_INVALID_ARG;
     if (M == 0 || N == 0) return MQ_OK;
@@ -211,7 +211,8 @@ mq_status qlinear_impl(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, in
     if ((w_zp == nullptr) != (a_rowsum == nullptr)) return MQ_ERR_INVALID_ARG;
 
     mq::QLinearArgs p;
-    p.a = a_q;
+    p.a = static_cast<const int8_t*>(a_q);
+    p.a_bits = a_bits;
     p.w = w_q;
     p.w_scale = w_scale;
     p.colsum = w_colsum;
@@ -250,9 +251,20 @@ mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N, cons
                         int32_t out_bits, const float* bias, void* y_q, void* workspace,
                         int64_t workspace_bytes, int32_t path, void* stream)
 {
-    return qlinear_impl(a_q, nullptr, M, K, N, w_q, w_bits, w_scale, nullptr, w_colsum, a_scale,
-                        a_zp, out_scale, out_zp, out_bits, bias, y_q, workspace, workspace_bytes,
-                        path, stream);
+    return qlinear_impl(a_q, 8, nullptr, M, K, N, w_q, w_bits, w_scale, nullptr, w_colsum,
+                        a_scale, a_zp, out_scale, out_zp, out_bits, bias, y_q, workspace,
+                        workspace_bytes, path, stream);
+}
+
+mq_status mq_qlinear_a16(const int16_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
+                         int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
+                         float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                         int32_t out_bits, const float* bias, void* y_q, int32_t path,
+                         void* stream)
+{
+    return qlinear_impl(a_q, 16, nullptr, M, K, N, w_q, w_bits, w_scale, nullptr, w_colsum,
+                        a_scale, a_zp, out_scale, out_zp, out_bits, bias, y_q, nullptr, 0, path,
+                        stream);
 }
 
 mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
@@ -263,9 +275,9 @@ mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M,
                           int32_t path, void* stream)
 {
     if (M > 0 && N > 0 && (!a_rowsum || !w_zp)) return MQ_ERR_INVALID_ARG;
-    return qlinear_impl(a_q, a_rowsum, M, K, N, w_q, w_bits, w_scale, w_zp, w_colsum, a_scale,
-                        a_zp, out_scale, out_zp, out_bits, bias, y_q, workspace, workspace_bytes,
-                        path, stream);
+    return qlinear_impl(a_q, 8, a_rowsum, M, K, N, w_q, w_bits, w_scale, w_zp, w_colsum,
+                        a_scale, a_zp, out_scale, out_zp, out_bits, bias, y_q, workspace,
+                        workspace_bytes, path, stream);
 }
 
 mq_status mq_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,

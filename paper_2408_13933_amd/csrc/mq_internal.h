@@ -9,7 +9,7 @@ namespace mq {
 
 // Scalars every qlinear kernel needs besides its buffers.
 struct QLinearArgs {
-    const int8_t* a;        // [M][K]
+    const int8_t* a;        // [M][K] int8, or int16 when a_bits == 16 (byte pointer)
     const void* w;          // [N][K] int8 or [N][K/2] packed int4
     const float* w_scale;   // [N]
     const int32_t* colsum;  // [N]
@@ -28,6 +28,7 @@ struct QLinearArgs {
     // row sums [M] (sum_k a[m][k]); both nullptr for symmetric weights
     const int32_t* w_zp = nullptr;
     const int32_t* a_rowsum = nullptr;
+    int32_t a_bits = 8;     // 8, or 16 (W8A16: 16-bit activation codes)
 };
 
 hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t zp,

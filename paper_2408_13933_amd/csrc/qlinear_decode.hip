@@ -37,14 +37,18 @@ __device__ inline v4i unpack_int4_x16(uint32_t x0, uint32_t x1)
 // R output channels per block (16, or 8 for narrow layers so the weight
 // stream spreads over more CUs; rows R..15 of the MFMA then load nothing).
 // ASYM: asymmetric weights, the zero-point term is added in the epilogue
-// (exact int64 form, four outputs per lane).
-template <int WBITS, int OBITS, int NWAVES, int R, bool ASYM>
+// (exact int64 form, four outputs per lane).  A16: 16-bit activation codes,
+// each 64-deep step loads 32 bytes of a token row per lane and runs two
+// MFMAs on its high and offset-low byte planes (split_a16), combined
+// exactly in int64 in the epilogue.
+template <int WBITS, int OBITS, int NWAVES, int R, bool ASYM, bool A16>
 __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs p)
 {
     constexpr int U = 8;  // 64-wide k steps per load round (one round covers most layers)
     constexpr int32_t qmin = -(1 << (OBITS - 1));
     constexpr int32_t qmax = (1 << (OBITS - 1)) - 1;
-    __shared__ v4i red[NWAVES][64];
+    constexpr int AB = A16 ? 2 : 1;  // activation bytes per code
+    __shared__ v4i red[NWAVES][64 * AB];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar loop
@@ -62,7 +66,7 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
         (void*)(static_cast<const int8_t*>(p.w) + n0 * wrow_bytes), (short)0,
         (int)(rows_w * wrow_bytes), 0x00020000);
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)p.a, (short)0, (int)(p.M * p.K), 0x00020000);
+        (void*)p.a, (short)0, (int)(p.M * p.K * AB), 0x00020000);
     const bool has_a = r16 < p.M;
 
     // Per-channel inputs of the epilogue (channels n0 + 4*kg + r), loaded by
@@ -87,12 +91,12 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     const int64_t s_begin = steps * wave / NWAVES;
     const int64_t s_end = steps * (wave + 1) / NWAVES;
 
-    // offsets stay below 2^21 (16 rows of at most 65536 bytes), so setting
+    // offsets stay below 2^22 (16 rows of at most 131072 bytes), so setting
     // bit 31 pushes a load out of range without a branch
     const int K32 = (int)p.K;
     const int s_end32 = (int)s_end;
     const uint32_t a_dead = has_a ? 0u : kOOB;
-    auto load = [&](int64_t s, v4i* wv, v4i* av) {
+    auto load = [&](int64_t s, v4i* wv, v4i* av, v4i* av2) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int su = (int)s + u;
@@ -109,17 +113,31 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
                     rw, (uint32_t)(r16 * (K32 / 2) + k / 2) | dead, 0, 0);
                 wv[u] = v4i{(int)pk[0], (int)pk[1], 0, 0};
             }
-            av[u] = __builtin_amdgcn_raw_buffer_load_b128(ra, (uint32_t)(r16 * K32 + k) | dead | a_dead,
-                                                          0, 0);
+            if constexpr (A16) {
+                const uint32_t off = (uint32_t)(r16 * K32 + k) * 2;
+                av[u] = __builtin_amdgcn_raw_buffer_load_b128(ra, off | dead | a_dead, 0, 0);
+                av2[u] = __builtin_amdgcn_raw_buffer_load_b128(ra, (off + 16) | dead | a_dead,
+                                                               0, 0);
+            } else {
+                av[u] = __builtin_amdgcn_raw_buffer_load_b128(
+                    ra, (uint32_t)(r16 * K32 + k) | dead | a_dead, 0, 0);
+            }
         }
     };
-    v4i acc = {0, 0, 0, 0};
-    auto mfma = [&](const v4i* wv, const v4i* av) {
+    v4i acc = {0, 0, 0, 0}, acc2 = {0, 0, 0, 0};  // acc2: A16 low-byte plane
+    auto mfma = [&](const v4i* wv, const v4i* av, const v4i* av2) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             v4i w = wv[u];
             if constexpr (WBITS == 4) w = unpack_int4_x16((uint32_t)w[0], (uint32_t)w[1]);
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(w, av[u], acc, 0, 0, 0);
+            if constexpr (A16) {
+                v4i h, l;
+                split_a16(av[u], av2[u], h, l);
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(w, h, acc, 0, 0, 0);
+                acc2 = __builtin_amdgcn_mfma_i32_16x16x64_i8(w, l, acc2, 0, 0, 0);
+            } else {
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(w, av[u], acc, 0, 0, 0);
+            }
         }
     };
     // The launch picks the wave count so one round covers a wave's K range
@@ -127,8 +145,8 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     // past the range load zeros and touch no memory.  The epilogue wave
     // derives its fixed-point constants while the first round is in flight
     // (the per-channel loads were issued before it and return first).
-    v4i wv[U], av[U];
-    load(s_begin, wv, av);
+    v4i wv[U], av[U], av2[A16 ? U : 1];
+    load(s_begin, wv, av, av2);
     // every use of the per-channel inputs stays behind the weight loads
     asm volatile("" : "+v"(col_ws[0]), "+v"(col_ws[1]), "+v"(col_ws[2]), "+v"(col_ws[3]),
                  "+v"(col_cs[0]), "+v"(col_cs[1]), "+v"(col_cs[2]), "+v"(col_cs[3]),
@@ -145,16 +163,20 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     }
     __builtin_amdgcn_sched_barrier(0);
     for (int64_t s = s_begin; s < s_end; s += U) {
-        if (s != s_begin) load(s, wv, av);
-        mfma(wv, av);
+        if (s != s_begin) load(s, wv, av, av2);
+        mfma(wv, av, av2);
     }
 
     if constexpr (NWAVES > 1) {
         red[wave][lane] = acc;
+        if constexpr (A16) red[wave][64 + lane] = acc2;
         __syncthreads();
         if (wave != 0) return;
 #pragma unroll
-        for (int w = 1; w < NWAVES; ++w) acc += red[w][lane];
+        for (int w = 1; w < NWAVES; ++w) {
+            acc += red[w][lane];
+            if constexpr (A16) acc2 += red[w][64 + lane];
+        }
     }
 
     // lane holds acc for token m = r16 and channels n0 + 4*kg + {0,1,2,3}
@@ -164,6 +186,13 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     const int32_t rs = row_sum - (int32_t)p.K * p.a_zp;  // sum_k (a - a_zp), ASYM only
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
+        if constexpr (A16) {
+            int64_t sum = ((int64_t)acc[r] << 8) + acc2[r];
+            if constexpr (WBITS == 4) sum >>= 4;  // exact: a multiple of 16
+            const int64_t c = sum + a16_offset(cps[r], p.a_zp, col_cs[r]);
+            out[r] = requant_c(sat32(c), cps[r], p.out_zp, qmin, qmax);
+            continue;
+        }
         int32_t a32 = acc[r];
         if constexpr (WBITS == 4) a32 >>= 4;  // exact: the sum is a multiple of 16
         if constexpr (ASYM)
@@ -196,7 +225,7 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     }
 }
 
-template <int WBITS, int OBITS, int R, bool ASYM>
+template <int WBITS, int OBITS, int R, bool ASYM, bool A16>
 hipError_t launch_r(const QLinearArgs& p, hipStream_t s)
 {
     const int64_t blocks = (p.N + R - 1) / R;
@@ -204,34 +233,42 @@ hipError_t launch_r(const QLinearArgs& p, hipStream_t s)
     // Waves per block: enough that one 8-step load round covers each wave's
     // share of K (every weight byte of the block is requested at once), at
     // least 4 when there are few channel groups so more loads are in flight.
+    // 16-bit codes double the activation registers: at most 8 waves (two per
+    // SIMD) so they fit without spilling
+    constexpr int NWMAX = A16 ? 8 : 16;
     int nw = 1;
-    while (nw < 16 && nw * 8 < steps) nw *= 2;
+    while (nw < NWMAX && nw * 8 < steps) nw *= 2;
     if (blocks < 2048) {
         while (nw < 4 && nw < steps) nw *= 2;
     }
     const dim3 g((unsigned)blocks);
     switch (nw) {
-    case 16: qlinear_decode_kernel<WBITS, OBITS, 16, R, ASYM><<<g, 16 * 64, 0, s>>>(p); break;
-    case 8: qlinear_decode_kernel<WBITS, OBITS, 8, R, ASYM><<<g, 8 * 64, 0, s>>>(p); break;
-    case 4: qlinear_decode_kernel<WBITS, OBITS, 4, R, ASYM><<<g, 4 * 64, 0, s>>>(p); break;
-    case 2: qlinear_decode_kernel<WBITS, OBITS, 2, R, ASYM><<<g, 2 * 64, 0, s>>>(p); break;
-    default: qlinear_decode_kernel<WBITS, OBITS, 1, R, ASYM><<<g, 64, 0, s>>>(p); break;
+    case 16:
+        if constexpr (NWMAX >= 16)
+            qlinear_decode_kernel<WBITS, OBITS, 16, R, ASYM, A16><<<g, 16 * 64, 0, s>>>(p);
+        break;
+    case 8: qlinear_decode_kernel<WBITS, OBITS, 8, R, ASYM, A16><<<g, 8 * 64, 0, s>>>(p); break;
+    case 4: qlinear_decode_kernel<WBITS, OBITS, 4, R, ASYM, A16><<<g, 4 * 64, 0, s>>>(p); break;
+    case 2: qlinear_decode_kernel<WBITS, OBITS, 2, R, ASYM, A16><<<g, 2 * 64, 0, s>>>(p); break;
+    default: qlinear_decode_kernel<WBITS, OBITS, 1, R, ASYM, A16><<<g, 64, 0, s>>>(p); break;
     }
     return hipGetLastError();
 }
 
-template <int WBITS, int OBITS, bool ASYM>
+template <int WBITS, int OBITS, bool ASYM, bool A16>
 hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
 {
     // narrow layers: 8 channels per block so at least 256 blocks stream
-    if ((p.N + 15) / 16 < 256) return launch_r<WBITS, OBITS, 8, ASYM>(p, s);
-    return launch_r<WBITS, OBITS, 16, ASYM>(p, s);
+    if ((p.N + 15) / 16 < 256) return launch_r<WBITS, OBITS, 8, ASYM, A16>(p, s);
+    return launch_r<WBITS, OBITS, 16, ASYM, A16>(p, s);
 }
 
 template <int WBITS, int OBITS>
 hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 {
-    return p.w_zp ? launch_a<WBITS, OBITS, true>(p, s) : launch_a<WBITS, OBITS, false>(p, s);
+    if (p.a_bits == 16) return launch_a<WBITS, OBITS, false, true>(p, s);
+    return p.w_zp ? launch_a<WBITS, OBITS, true, false>(p, s)
+                  : launch_a<WBITS, OBITS, false, false>(p, s);
 }
 
 }  // namespace

@@ -72,9 +72,14 @@ __device__ inline void wait_vmcnt()
 }
 
 template <int WBITS_, int OBITS_, int TM_, int TN_, int WM_, int WN_, int BK_, int STAGES_,
-          int SWZ_, int SPREAD_>
+          int SWZ_, int SPREAD_, int ABITS_ = 8>
 struct Cfg {
     static constexpr int WBITS = WBITS_, OBITS = OBITS_;
+    // 16-bit activation codes (W8A16): two byte planes per code, two MFMAs
+    // per fragment pair, a second accumulator set
+    static constexpr int ABITS = ABITS_;
+    static constexpr bool A16 = ABITS == 16;
+    static constexpr int AB = ABITS / 8;  // activation bytes per code
     static constexpr int TM = TM_, TN = TN_, WM = WM_, WN = WN_, BK = BK_;
     static constexpr int STAGES = STAGES_, SWZ = SWZ_;
     static constexpr int NWAVES = WM * WN;
@@ -82,7 +87,8 @@ struct Cfg {
     static constexpr int FM = TM / (WM * 32);   // 32-token fragments per wave
     static constexpr int FN = TN / (WN * 32);   // 32-channel fragments per wave
     static constexpr int BKW = WBITS == 8 ? BK : BK / 2;  // weight bytes per row per stage
-    static constexpr int CA = BK / 16;          // 16-byte chunks per activation row
+    static constexpr int BKA = BK * AB;         // activation bytes per row per stage
+    static constexpr int CA = BKA / 16;         // 16-byte chunks per activation row
     static constexpr int CW = BKW / 16;         // 16-byte chunks per weight row
     static constexpr int A_WLOADS = TM * CA / 64;  // 1 KiB wave loads per stage
     static constexpr int W_WLOADS = TN * CW / 64;
@@ -90,7 +96,7 @@ struct Cfg {
     static constexpr int W_PER_WAVE = (W_WLOADS + NWAVES - 1) / NWAVES;
     static constexpr int LOADS = A_PER_WAVE + W_PER_WAVE;  // per thread per stage
     static constexpr int KS = BK / 32;                       // 32-deep steps per stage
-    static constexpr int NRD = FN + FM;                      // fragment reads per step
+    static constexpr int NRD = FN + FM * AB;                 // fragment reads per step
     // DMA of a stage spread over the groups of SPREAD steps after its switch
     static constexpr int SPREAD = SPREAD_;
     // group slot of DMA d of a stage among the SPREAD*NRD groups after its switch
@@ -105,14 +111,16 @@ struct Cfg {
     static constexpr int NSW = nsw();
     // K slices (split-K) for the smaller tiles; the 256x256 tile has no
     // registers to spare for the slice bookkeeping
-    static constexpr bool SPLITK = TM * TN < 256 * 256;
+    static constexpr bool SPLITK = TM * TN < 256 * 256 && !A16;
     static constexpr int A_BYTES = A_PER_WAVE * NWAVES * 1024;
     static constexpr int W_BYTES = W_PER_WAVE * NWAVES * 1024;
     static constexpr int STAGE = A_BYTES + W_BYTES;
     // + per-column epilogue constants + one flag word per wave
     static constexpr int LDS = STAGES * STAGE + TN * 16 + NWAVES * 4;
-    // asymmetric weights add per channel -w_zp and per token row sum
+    // asymmetric weights add per channel -w_zp and per token row sum; 16-bit
+    // activations use the channel array for the low part of the offset
     static constexpr int LDS_ASYM = LDS + (TN + TM) * 4;
+    static_assert(!A16 || (WBITS == 8 && !SPLITK), "16-bit activations: int8 weights, no split");
     static_assert(TM % (WM * 32) == 0 && TN % (WN * 32) == 0, "wave grid");
     static_assert((TM * CA) % 64 == 0 && (TN * CW) % 64 == 0, "whole wave loads");
     static_assert(BK % 64 == 0, "BK is a multiple of the MFMA depth");
@@ -195,8 +203,8 @@ struct Staging {
 // ASYM (asymmetric weights) adds -w_zp[n] * rs[m]: the fast form has it in
 // the accumulator's start value already, the other adds it exactly in
 // int64 before the saturation.
-template <class C, bool ASYM, bool FAST, bool PRE, bool STAGED, class Acc>
-__device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
+template <class C, bool ASYM, bool FAST, bool PRE, bool STAGED, class Acc, class Acc2>
+__device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const EpiCtx& x)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
     constexpr int32_t qmax = (1 << (C::OBITS - 1)) - 1;
@@ -218,7 +226,8 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
             const int nl = x.col0 + i * 32 + 8 * g;  // tile-local channel
             v4i off = {0, 0, 0, 0}, nzw = {0, 0, 0, 0};
             if constexpr (!FAST) off = *reinterpret_cast<const v4i*>(x.e_off + nl);
-            if constexpr (ASYM && !FAST) nzw = *reinterpret_cast<const v4i*>(x.e_nzw + nl);
+            if constexpr ((ASYM || C::A16) && !FAST)
+                nzw = *reinterpret_cast<const v4i*>(x.e_nzw + nl);  // A16: offset low part
             const v4i m0 = *reinterpret_cast<const v4i*>(x.e_m0 + nl);
             const v4i rnd = *reinterpret_cast<const v4i*>(x.e_rnd + nl);
             const v4i sp = *reinterpret_cast<const v4i*>(x.e_sp + nl);
@@ -239,13 +248,19 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, const EpiCtx& x)
                     int32_t a32 = acc[i][j][4 * g + r];
                     if constexpr (C::WBITS == 4) a32 >>= 4;  // exact: a multiple of 16
                     int32_t c = a32;  // fast form: off is already in the accumulator
-                    if constexpr (!FAST) {
+                    if constexpr (C::A16) {
+                        // high plane * 256 + low plane (+ the offset, split
+                        // the same way, when it is not in the start values)
+                        int64_t c64 = ((int64_t)a32 << 8) + acc2[i][j][4 * g + r];
+                        if constexpr (!FAST) c64 += ((int64_t)off[r] << 8) + nzw[r];
+                        c = sat32(c64);
+                    } else if constexpr (!FAST) {
                         if constexpr (ASYM)
                             c = corrected_acc_asym(a32, off[r], nzw[r], rs[j]);
                         else
                             c = __builtin_elementwise_add_sat(a32, off[r]);
                     }
-                    if constexpr (!FAST || PRE) {
+                    if constexpr (!FAST || PRE || C::A16) {
                         c = max(min(c, bnd[r]), -bnd[r]);
                         c = (int32_t)((uint32_t)c << pre[r]);
                     }
@@ -379,7 +394,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     const int rows_a = (int)((p.M - m_tile) < C::TM ? (p.M - m_tile) : C::TM);
     const int rows_w = (int)((p.N - n_tile) < C::TN ? (p.N - n_tile) : C::TN);
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.a + m_tile * K + k_begin), (short)0, (int)(rows_a * K - k_begin), 0x00020000);
+        (void*)(p.a + (m_tile * K + k_begin) * C::AB), (short)0,
+        (int)((rows_a * K - k_begin) * C::AB), 0x00020000);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(static_cast<const int8_t*>(p.w) + n_tile * wrow + k_begin_w), (short)0,
         (int)(rows_w * wrow - k_begin_w), 0x00020000);
@@ -400,7 +416,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
 #pragma unroll
     for (int i = 0; i < C::A_PER_WAVE; ++i) {
         const int row = ((wave + i * C::NWAVES) * 64 + lane) / C::CA;
-        a_off[i] = wave + i * C::NWAVES < C::A_WLOADS ? (uint32_t)(row * (int)K + a_kb(i)) : kOOB;
+        a_off[i] = wave + i * C::NWAVES < C::A_WLOADS
+                       ? (uint32_t)(row * (int)K * C::AB + a_kb(i)) : kOOB;
     }
 #pragma unroll
     for (int i = 0; i < C::W_PER_WAVE; ++i) {
@@ -416,9 +433,10 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     auto issue_one = [&](int kt, int buf, int idx) {  // idx < LOADS, compile-time
         MQ_LDS int8_t* base = (MQ_LDS int8_t*)smem + buf * C::STAGE;
         if (idx < C::A_PER_WAVE) {
-            const int i = idx, k0 = kt * C::BK;
+            const int i = idx, k0 = kt * C::BKA;  // bytes
             const int wl = wave + i * C::NWAVES;
-            const uint32_t voff = (k0 + a_kb(i) < (int)KL) ? a_off[i] + (uint32_t)k0 : kOOB;
+            const uint32_t voff =
+                (k0 + a_kb(i) < (int)KL * C::AB) ? a_off[i] + (uint32_t)k0 : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (MQ_LDS void*)(base + wl * 1024), 16,
                                                      voff, 0, 0, 0);
         } else {
@@ -483,6 +501,16 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         offa *= C::WBITS == 4 ? 16 : 1;
         col_offin = offa + (K << 14) < ((int64_t)1 << 31) &&
                     (!ASYM || 255 * K < ((int64_t)1 << 23));
+        if constexpr (C::A16) {
+            // the offset bias_q + (128 - a_zp) colsum (int64) split as
+            // 256 hi + lo, lo in [0, 255]; hi starts the high-plane sums
+            // when hi + K * 2^14 stays in int32
+            const int64_t off = a16_offset(cp, p.a_zp, col_cs);
+            const int64_t hi = off >> 8;  // floor
+            e_off[tid] = (int32_t)hi;
+            e_nzw[tid] = (int32_t)(off - hi * 256);
+            col_offin = (hi < 0 ? -hi : hi) + (K << 14) < ((int64_t)1 << 31);
+        }
     }
     // Whole-tile epilogue form: AND of the column flags over the block, by
     // ballot per wave and one LDS word per wave.  A raw barrier, since
@@ -524,13 +552,24 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // tokens 32j + r32.  In the fast form each starts at its channel's off
     // (plus, for asymmetric weights, -w_zp[n] * rs[m]), scaled by 16 for
     // int4 weights like the products.
+    // 16-bit activations: acc holds the high-byte plane, acc2 the low one
+    // (each starting at its part of the offset in the fast form)
     v16i acc[C::FN][C::FM];
+    v16i acc2[C::A16 ? C::FN : 1][C::A16 ? C::FM : 1];
 #pragma unroll
     for (int i = 0; i < C::FN; ++i)
 #pragma unroll
         for (int j = 0; j < C::FM; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+    if constexpr (C::A16) {
+#pragma unroll
+        for (int i = 0; i < C::FN; ++i)
+#pragma unroll
+            for (int j = 0; j < C::FM; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc2[i][j][r] = 0;
+    }
     if (fast && split == 0) {  // block-uniform; off joins the sum once
         const int col0 = wn * (C::TN / C::WN) + 4 * hk;
         int32_t rs[C::FM];
@@ -543,7 +582,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
             for (int g = 0; g < 4; ++g) {
                 const v4i o = *reinterpret_cast<const v4i*>(e_off + col0 + i * 32 + 8 * g);
                 v4i z = {0, 0, 0, 0};
-                if constexpr (ASYM) z = *reinterpret_cast<const v4i*>(e_nzw + col0 + i * 32 + 8 * g);
+                if constexpr (ASYM || C::A16)
+                    z = *reinterpret_cast<const v4i*>(e_nzw + col0 + i * 32 + 8 * g);
 #pragma unroll
                 for (int j = 0; j < C::FM; ++j)
 #pragma unroll
@@ -552,6 +592,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
                         if constexpr (ASYM) v += __mul24(z[r], rs[j]);
                         if constexpr (C::WBITS == 4) v *= 16;
                         acc[i][j][4 * g + r] = v;
+                        if constexpr (C::A16) acc2[i][j][4 * g + r] = z[r];
                     }
             }
     }
@@ -562,16 +603,19 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // stage) sits between the two halves of the step's MFMAs.  The steady
     // state has no branches, so every wait count is a compile-time constant.
 
-    // fragment g of a 32-deep step: g < FM activation rows, then weight rows
+    // fragment read g of a 32-deep step: g < FM*AB activation rows (16-bit
+    // codes: two 16-byte halves per fragment, af[2j] and af[2j+1]), then
+    // weight rows
     auto load_frag = [&](int buf, int ks, int g, v4i* wf, v4i* af) {
         const int8_t* sa = smem + buf * C::STAGE;
         const int8_t* sw = sa + C::A_BYTES;
-        if (g < C::FM) {
-            const int row = wm * (C::TM / C::WM) + g * 32 + r32;
-            const int phys = (ks * 2 + hk) ^ swz<C::SWZ>(row, C::CA);
-            af[g] = *reinterpret_cast<const v4i*>(sa + row * C::BK + phys * 16);
+        if (g < C::FM * C::AB) {
+            const int row = wm * (C::TM / C::WM) + (g / C::AB) * 32 + r32;
+            const int chunk = C::A16 ? ks * 4 + hk * 2 + (g % 2) : ks * 2 + hk;
+            const int phys = chunk ^ swz<C::SWZ>(row, C::CA);
+            af[g] = *reinterpret_cast<const v4i*>(sa + row * C::BKA + phys * 16);
         } else {
-            const int i = g - C::FM;
+            const int i = g - C::FM * C::AB;
             const int row = wn * (C::TN / C::WN) + i * 32 + r32;
             if constexpr (C::WBITS == 8) {
                 const int phys = (ks * 2 + hk) ^ swz<C::SWZ>(row, C::CW);
@@ -586,12 +630,25 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
             }
         }
     };
-    // MFMA t of a step: channel fragment t / FM, token fragment t % FM
+    // MFMA t of a step: channel fragment t / FM, token fragment t % FM; with
+    // 16-bit codes (af = the split planes, high at 2j, low at 2j+1) the
+    // plane is t % 2 and the pair index t / 2
     auto mfma_range = [&](const v4i* wf, const v4i* af, int t0, int t1) {
 #pragma unroll
         for (int t = t0; t < t1; ++t) {
-            const int i = t / C::FM, j = t % C::FM;
-            acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
+            if constexpr (C::A16) {
+                const int q = t / 2, i = q / C::FM, j = q % C::FM;
+                if (t % 2 == 0)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[2 * j], acc[i][j],
+                                                                      0, 0, 0);
+                else
+                    acc2[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[2 * j + 1],
+                                                                       acc2[i][j], 0, 0, 0);
+            } else {
+                const int i = t / C::FM, j = t % C::FM;
+                acc[i][j] =
+                    __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
+            }
         }
     };
 
@@ -606,14 +663,23 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // The DMA of a stage is spread evenly over the KS*NRD groups that follow
     // the barrier which frees its buffer: the stage switch step (slots
     // 0..NRD-1) and the first KS-1 steps of the next stage.
-    constexpr int NRD = C::FN + C::FM;  // LDS fragment reads per step
-    constexpr int NMF = C::FN * C::FM;  // MFMAs per step
+    constexpr int NRD = C::NRD;                  // LDS fragment reads per step
+    constexpr int NMF = C::FN * C::FM * C::AB;   // MFMAs per step
     auto step = [&](const v4i* wc, const v4i* ac, bool read, int rbuf, int rks, v4i* wx,
                     v4i* ax, bool dma, int dkt, int dbuf, int slot_step) {
+        // 16-bit codes: this step's byte planes (its fragments were read
+        // during the previous step)
+        v4i planes[C::A16 ? 2 * C::FM : 1];
+        if constexpr (C::A16) {
+#pragma unroll
+            for (int j = 0; j < C::FM; ++j)
+                split_a16(ac[2 * j], ac[2 * j + 1], planes[2 * j], planes[2 * j + 1]);
+        }
+        const v4i* aop = C::A16 ? planes : ac;
 #pragma unroll
         for (int g = 0; g < NRD; ++g) {
             if (read) load_frag(rbuf, rks, g, wx, ax);
-            mfma_range(wc, ac, g * NMF / NRD, (g + 1) * NMF / NRD);
+            mfma_range(wc, aop, g * NMF / NRD, (g + 1) * NMF / NRD);
             if (dma) {
 #pragma unroll
                 for (int d = 0; d < C::LOADS; ++d)
@@ -623,7 +689,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         }
     };
 
-    v4i wf0[C::FN], af0[C::FM], wf1[C::FN], af1[C::FM];
+    v4i wf0[C::FN], af0[C::FM * C::AB], wf1[C::FN], af1[C::FM * C::AB];
 #pragma unroll
     for (int g = 0; g < NRD; ++g) load_frag(0, 0, g, wf0, af0);
     for (int kt = 0; kt < KT - 1; ++kt) {
@@ -771,14 +837,14 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
                         ((uintptr_t)p.y % 16) == 0;
     if constexpr (kPreForms) {
-        if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true>(acc, ctx);
-        else if (staged) prefill_epilogue<C, ASYM, true, true, true>(acc, ctx);
-        else if (fast) prefill_epilogue<C, ASYM, true, true, false>(acc, ctx);
-        else prefill_epilogue<C, ASYM, false, false, false>(acc, ctx);
+        if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true>(acc, acc2, ctx);
+        else if (staged) prefill_epilogue<C, ASYM, true, true, true>(acc, acc2, ctx);
+        else if (fast) prefill_epilogue<C, ASYM, true, true, false>(acc, acc2, ctx);
+        else prefill_epilogue<C, ASYM, false, false, false>(acc, acc2, ctx);
     } else {
-        if (staged) prefill_epilogue<C, ASYM, true, false, true>(acc, ctx);
-        else if (fast) prefill_epilogue<C, ASYM, true, false, false>(acc, ctx);
-        else prefill_epilogue<C, ASYM, false, false, false>(acc, ctx);
+        if (staged) prefill_epilogue<C, ASYM, true, false, true>(acc, acc2, ctx);
+        else if (fast) prefill_epilogue<C, ASYM, true, false, false>(acc, acc2, ctx);
+        else prefill_epilogue<C, ASYM, false, false, false>(acc, acc2, ctx);
     }
 }
 
@@ -793,7 +859,7 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
     splits = (int)((kt + kt_per_split - 1) / kt_per_split);  // every slice non-empty
     if (total * splits > 0x7FFFFFFF) return hipErrorInvalidValue;
     // more than 64 KiB of dynamic LDS must be opted into once per kernel
-    constexpr int lds = ASYM ? C::LDS_ASYM : C::LDS;
+    constexpr int lds = ASYM || C::A16 ? C::LDS_ASYM : C::LDS;
     static const hipError_t attr = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&qlinear_prefill_kernel<C, ASYM>),
         hipFuncAttributeMaxDynamicSharedMemorySize, lds);
@@ -810,6 +876,9 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
 template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2, 1>;
 template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2, 4>;
 template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
+// 16-bit activation codes: 128x128 tokens x channels, 64 k per stage (128
+// bytes of each activation row), DMA spread over both steps of a stage
+template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16>;
 
 // Per-block cycle model of each tile shape on MI355X (phase timings of the
 // kernel): fixed prologue + K-loop cycles per stage + epilogue.
@@ -907,7 +976,9 @@ bool prefill_supported(const QLinearArgs& p)
     const bool kok = p.w_bits == 8 ? (p.K % 16 == 0) : (p.K % 32 == 0);
     // byte offsets inside one 256-row tile must fit the 32-bit buffer offset
     const bool nok = 256 * p.N * (p.out_bits / 8) < ((int64_t)1 << 31);
-    return kok && nok && ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
+    // 16-bit activation codes: int8 weights only (the W8A16 tile)
+    const bool aok = p.a_bits == 8 || (p.w_bits == 8 && p.w_zp == nullptr);
+    return kok && nok && aok && ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
            ((uintptr_t)p.y % 8) == 0;
 }
 
@@ -918,6 +989,10 @@ int64_t prefill_workspace_bytes(const QLinearArgs& p)
 
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s)
 {
+    if (p.a_bits == 16) {  // one tile shape, no K split
+        if (p.out_bits == 8) return launch_cfg<T128x128A16<8>, false>(p, 1, s);
+        return launch_cfg<T128x128A16<16>, false>(p, 1, s);
+    }
     if (p.w_bits == 8 && p.out_bits == 8) return launch_t<8, 8>(p, s);
     if (p.w_bits == 8) return launch_t<8, 16>(p, s);
     if (p.out_bits == 8) return launch_t<4, 8>(p, s);

@@ -16,6 +16,7 @@ struct ColParams {
     int32_t off;  // bias_q - a_zp * colsum, saturated to int32
     int32_t m0;   // Q31 multiplier in [2^30, 2^31), or 0
     int32_t sh;   // right shift; >= 63 means r = 0, <= 0 means saturate
+    int32_t bq;   // bias_q alone, |bias_q| <= 2^30
 };
 
 // Fixed-point form of M = (a_scale * w_scale) / out_scale and the bias in
@@ -56,6 +57,7 @@ __device__ inline ColParams derive_col_params_v(float a_scale, float w_scale, fl
     long long off = bq - (long long)a_zp * (long long)colsum;
     off = off < INT32_MIN ? INT32_MIN : (off > INT32_MAX ? INT32_MAX : off);
     p.off = (int32_t)off;
+    p.bq = (int32_t)bq;
     return p;
 }
 
@@ -94,6 +96,39 @@ __device__ inline int32_t requant_out(int32_t acc, const ColParams& p, int32_t o
                                       int32_t qmin, int32_t qmax)
 {
     return requant_c(__builtin_elementwise_add_sat(acc, p.off), p, out_zp, qmin, qmax);
+}
+
+// 16-bit activations (W8A16): the kernels split each code a into an int8
+// high part h = a >> 8 and an offset low part l = (a & 255) - 128, so that
+// a = 256 h + l + 128 and
+//   sum_k (a - a_zp) w = 256 sum h w + sum l w + (128 - a_zp) colsum,
+// two exact int8 products.  |(128 - a_zp) colsum| < 2^39: int64.
+__device__ inline int64_t a16_offset(const ColParams& cp, int32_t a_zp, int32_t colsum)
+{
+    return (int64_t)cp.bq + (int64_t)(128 - a_zp) * (int64_t)colsum;
+}
+
+// 16 int16 codes in k order (32 bytes: x0 = codes 0-7, x1 = codes 8-15; a
+// dword holds two codes, the even one in its low half) -> the int8 MFMA
+// operands h (high bytes) and l (low bytes - 128), 16 lanes each in k order.
+// v_perm_b32 selector bytes 0-3 pick from the second source, 4-7 from the
+// first.
+typedef int a16_v4i __attribute__((ext_vector_type(4)));
+__device__ inline void split_a16(const a16_v4i& x0, const a16_v4i& x1, a16_v4i& h, a16_v4i& l)
+{
+    h[0] = (int)__builtin_amdgcn_perm((uint32_t)x0[1], (uint32_t)x0[0], 0x07050301u);
+    h[1] = (int)__builtin_amdgcn_perm((uint32_t)x0[3], (uint32_t)x0[2], 0x07050301u);
+    h[2] = (int)__builtin_amdgcn_perm((uint32_t)x1[1], (uint32_t)x1[0], 0x07050301u);
+    h[3] = (int)__builtin_amdgcn_perm((uint32_t)x1[3], (uint32_t)x1[2], 0x07050301u);
+    l[0] = (int)(__builtin_amdgcn_perm((uint32_t)x0[1], (uint32_t)x0[0], 0x06040200u) ^ 0x80808080u);
+    l[1] = (int)(__builtin_amdgcn_perm((uint32_t)x0[3], (uint32_t)x0[2], 0x06040200u) ^ 0x80808080u);
+    l[2] = (int)(__builtin_amdgcn_perm((uint32_t)x1[1], (uint32_t)x1[0], 0x06040200u) ^ 0x80808080u);
+    l[3] = (int)(__builtin_amdgcn_perm((uint32_t)x1[3], (uint32_t)x1[2], 0x06040200u) ^ 0x80808080u);
+}
+
+__device__ inline int32_t sat32(int64_t c)
+{
+    return (int32_t)(c < INT32_MIN ? INT32_MIN : (c > INT32_MAX ? INT32_MAX : c));
 }
 
 // Asymmetric per-channel weights (codes W - w_zp[n]): the zero-point adds

@@ -57,6 +57,7 @@ class Layer:
     smooth_len: int = 0            # length of that vector
     asym: bool = False             # asymmetric weights
     per_tensor: bool = False       # one weight range per tensor (asym only)
+    a_bits: int = 8                # activation codes: 8, or 16 (W8A16)
 
     @property
     def ops(self) -> int:
@@ -65,7 +66,7 @@ class Layer:
     def alg_bytes(self) -> int:
         """Minimum bytes one qlinear call moves: A, W, Y and per-column params."""
         w = self.N * self.K * self.w_bits // 8
-        a = self.M * self.K
+        a = self.M * self.K * self.a_bits // 8
         y = self.M * self.N * self.out_bits // 8
         params = self.N * (8 + (4 if self.bias else 0))
         if self.asym:  # weight zero-points and activation row sums
@@ -80,8 +81,8 @@ class Workload:
     layers: tuple
 
 
-def _tinyllama_block(M: int, asym: bool = False):
-    L = dict(out_bits=16, bias=False, asym=asym)
+def _tinyllama_block(M: int, asym: bool = False, a_bits: int = 8):
+    L = dict(out_bits=16, bias=False, asym=asym, a_bits=a_bits)
     # asymmetric (Section 5.1 W8A8): one weight range per tensor except the
     # MLP down projection, which keeps one per output channel
     T = dict(per_tensor=asym)
@@ -125,6 +126,11 @@ WORKLOADS = {
         "the same decoder block in the paper's main W8A8 setting: asymmetric "
         "weights, one range per tensor except per-channel down_proj",
         _tinyllama_block(1024, asym=True)),
+    "block_w8a16_tinyllama_s1024": Workload(
+        "block_w8a16_tinyllama_s1024",
+        "the same decoder block in the W8A16 comparison setting (Section 5.6): "
+        "16-bit activation codes into the seven linears, int8 weights",
+        _tinyllama_block(1024, a_bits=16)),
     "w4a8_asym_down_tinyllama": Workload(
         "w4a8_asym_down_tinyllama",
         "the paper's main W4A8 setting on the down-proj K=5632, N=2048: "

@@ -42,10 +42,10 @@ def oracle_layer(ld: LayerData, rows=None, nthreads=None) -> LayerResult:
         wq, ws, zw, cs = oracle.pack_weights_asym(w_in, L.w_bits, per_tensor=L.per_tensor)
     else:
         wq, ws, cs = oracle.pack_weights(w_in, L.w_bits)
-    a_scale, a_zp = oracle.act_params(*ld.act_range, 8)
+    a_scale, a_zp = oracle.act_params(*ld.act_range, L.a_bits)
     out_scale, out_zp = oracle.act_params(*ld.out_range, L.out_bits)
     x = ld.x if rows is None else ld.x[rows]
-    a_q = oracle.quantize_act(x, a_scale, a_zp, 8)
+    a_q = oracle.quantize_act(x, a_scale, a_zp, L.a_bits)
     y_q = oracle.qlinear(a_q, wq, L.w_bits, ws, a_scale, a_zp, out_scale, out_zp, L.out_bits,
                          bias=ld.bias, nthreads=nthreads, w_zp=zw)
     y = oracle.dequant(y_q, out_scale, out_zp)
@@ -66,9 +66,9 @@ def gpu_layer(ld: LayerData, path: int = 0, keep_device=False, workspace=None):
         s = torch.from_numpy(ld.s).to(dev)
         w_hat = mq.mq_fold_weights(w, s)
     bias = torch.from_numpy(ld.bias).to(dev) if ld.bias is not None else None
-    a_scale, a_zp = mq.mq_act_params(*ld.act_range, 8)
+    a_scale, a_zp = mq.mq_act_params(*ld.act_range, L.a_bits)
     out_scale, out_zp = mq.mq_act_params(*ld.out_range, L.out_bits)
-    a_q = mq.mq_quantize_act(x, a_scale, a_zp, 8)
+    a_q = mq.mq_quantize_act(x, a_scale, a_zp, L.a_bits)
     w_in = w_hat if w_hat is not None else w
     zw = rs = None
     if L.asym:
@@ -76,6 +76,10 @@ def gpu_layer(ld: LayerData, path: int = 0, keep_device=False, workspace=None):
         rs = mq.mq_act_rowsum(a_q)
         y_q = mq.mq_qlinear_asym(a_q, rs, wq, L.w_bits, ws, zw, cs, a_scale, a_zp, out_scale,
                                  out_zp, L.out_bits, bias=bias, path=path, workspace=workspace)
+    elif L.a_bits == 16:
+        wq, ws, cs = mq.mq_pack_weights(w_in, L.w_bits)
+        y_q = mq.mq_qlinear_a16(a_q, wq, L.w_bits, ws, cs, a_scale, a_zp, out_scale, out_zp,
+                                L.out_bits, bias=bias, path=path)
     else:
         wq, ws, cs = mq.mq_pack_weights(w_in, L.w_bits)
         y_q = mq.mq_qlinear(a_q, wq, L.w_bits, ws, cs, a_scale, a_zp, out_scale, out_zp,

@@ -129,6 +129,32 @@ def test_qlinear_asym_rejects_invalid_arguments(kw):
     assert qlin_asym(**kw) == 1
 
 
+def qlin_a16(**kw):
+    a = dict(a_q=NZ, M=4, K=64, N=8, w_q=NZ, w_bits=8, w_scale=NZ, w_colsum=NZ, a_scale=0.1,
+             a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None, y_q=NZ, path=0,
+             stream=None)
+    a.update(kw)
+    return mq.lib().mq_qlinear_a16(a["a_q"], a["M"], a["K"], a["N"], a["w_q"], a["w_bits"],
+                                   a["w_scale"], a["w_colsum"], a["a_scale"], a["a_zp"],
+                                   a["out_scale"], a["out_zp"], a["out_bits"], a["bias"],
+                                   a["y_q"], a["path"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(a_q=None), dict(K=0), dict(K=65537), dict(w_bits=4, K=63), dict(out_bits=12),
+    dict(a_zp=32768), dict(a_zp=-32769), dict(a_scale=0.0), dict(path=1, M=17), dict(path=9),
+])
+def test_qlinear_a16_rejects_invalid_arguments(kw):
+    assert qlin_a16(**kw) == 1
+
+
+def test_qlinear_a16_accepts_int16_zero_points():
+    # a zero-point outside int8 but inside int16 passes validation (M = 0:
+    # nothing is launched)
+    assert qlin_a16(M=0, a_zp=-30000) == 0
+    assert qlin(M=0, a_zp=-30000) == 1   # the 8-bit entry point still rejects it
+
+
 def test_qlinear_asym_empty_shapes_are_noops():
     assert qlin_asym(M=0, a_rowsum=None, a_q=None) == 0
     assert qlin_asym(N=0, w_zp=None) == 0
