@@ -12,6 +12,9 @@ Functions and the passages they follow (arXiv 2408.13933):
 * ``quantize_act``    -- Section 4.2, Eq.(4) (static per-tensor quantizer)
 * ``dequant``         -- inverse of Eq.(4)
 * ``fold_weights`` / ``fold_acts`` -- Section 3.2, Eq.(1) (S W and X S^-1)
+* ``smooth_scales``   -- Section 3.2: SmoothQuant's closed-form S
+* ``arl_forward`` / ``arl_backward`` -- Section 4.2, Eq.(2)-(4) in its
+  training form (learnable alpha, beta; straight-through rounding)
 * ``pack_weights``    -- Section 5.1 / appendix: symmetric per-channel W8, W4
 * ``pack_weights_asym`` -- Section 5.1: asymmetric W8, W4 (the quantizer of
   Eq.(2)-(4) over each output row's range, or the whole matrix's)
@@ -67,6 +70,17 @@ def _load():
     lib.oracle_fold_weights.restype = None
     lib.oracle_fold_acts.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int64, _f32p]
     lib.oracle_fold_acts.restype = None
+    lib.oracle_smooth_scales.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64, _f32p,
+                                         ctypes.c_int64, ctypes.c_float, _f32p, _f32p, _f32p]
+    lib.oracle_smooth_scales.restype = None
+    lib.oracle_arl_forward.argtypes = [_f32p, ctypes.c_int64, ctypes.c_float, ctypes.c_float,
+                                       ctypes.c_int, _f32p]
+    lib.oracle_arl_forward.restype = None
+    lib.oracle_arl_backward.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_float,
+                                        ctypes.c_float, ctypes.c_int, _f32p,
+                                        ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_double)]
+    lib.oracle_arl_backward.restype = None
     lib.oracle_pack_weights.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                         _vp, _f32p, _i32p]
     lib.oracle_pack_weights.restype = None
@@ -196,6 +210,41 @@ def pack_weights(w: np.ndarray, bits: int):
     colsum = np.empty(N, dtype=np.int32)
     _load().oracle_pack_weights(w, N, K, bits, _ptr(wq), scale, colsum)
     return wq, scale, colsum
+
+
+def smooth_scales(x: np.ndarray, w: np.ndarray, a: float):
+    """SmoothQuant's s_k = max|X_k|^a / max|W_k|^(1-a): (s, x_absmax, w_absmax)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    M, K = x.shape
+    N, K2 = w.shape
+    assert K == K2
+    s = np.empty(K, np.float32)
+    mx = np.empty(K, np.float32)
+    mw = np.empty(K, np.float32)
+    _load().oracle_smooth_scales(x, M, K, w, N, float(a), mx, mw, s)
+    return s, mx, mw
+
+
+def arl_forward(x: np.ndarray, alpha: float, beta: float, bits: int) -> np.ndarray:
+    """Fake-quantized X_hat = alpha (X_int + beta) of Eq.(2)-(4)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.empty_like(x)
+    _load().oracle_arl_forward(x.reshape(-1), x.size, float(alpha), float(beta), int(bits),
+                               y.reshape(-1))
+    return y
+
+
+def arl_backward(x: np.ndarray, g: np.ndarray, alpha: float, beta: float, bits: int):
+    """Straight-through gradients: (dL/dX, dL/dalpha, dL/dbeta)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    assert g.shape == x.shape
+    gx = np.empty_like(x)
+    ga, gb = ctypes.c_double(), ctypes.c_double()
+    _load().oracle_arl_backward(x.reshape(-1), g.reshape(-1), x.size, float(alpha), float(beta),
+                                int(bits), gx.reshape(-1), ctypes.byref(ga), ctypes.byref(gb))
+    return gx, float(ga.value), float(gb.value)
 
 
 def _packed_weight_buffer(N: int, K: int, bits: int) -> np.ndarray:

@@ -143,6 +143,86 @@ void oracle_fold_acts(const float* x, const float* s, int64_t M, int64_t K,
 }
 
 /* ------------------------------------------------------------------ */
+/* SmoothQuant's closed-form scaling vector, as the paper restates it in
+ * Section 3.2: s_k = max_m |X[m][k]|^a / max_n |W[n][k]|^(1-a) for each
+ * input channel k, a the migration strength in [0, 1].  Readings: the
+ * maxima run over finite entries; in fp64 with pow, rounded once to
+ * fp32; a channel whose activation or weight maximum is 0 gets s = 1.
+ * The column maxima are returned as well.                              */
+/* ------------------------------------------------------------------ */
+void oracle_smooth_scales(const float* x, int64_t M, int64_t K, const float* w,
+                          int64_t N, float a, float* x_absmax, float* w_absmax,
+                          float* s)
+{
+    for (int64_t k = 0; k < K; ++k) {
+        float mx = 0.0f, mw = 0.0f;
+        for (int64_t m = 0; m < M; ++m) {
+            const float v = fabsf(x[m * K + k]);
+            if (isfinite(v) && v > mx) mx = v;
+        }
+        for (int64_t n = 0; n < N; ++n) {
+            const float v = fabsf(w[n * K + k]);
+            if (isfinite(v) && v > mw) mw = v;
+        }
+        x_absmax[k] = mx;
+        w_absmax[k] = mw;
+        s[k] = (mx > 0.0f && mw > 0.0f)
+                   ? (float)(pow((double)mx, (double)a) / pow((double)mw, 1.0 - (double)a))
+                   : 1.0f;
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Activation range learning (Section 4.2, Eq.(2)-(4)), the training-time
+ * form with learnable scale alpha and offset beta (both real):
+ *   X_int = min(max(ste(X/alpha) - beta, 0), q_max),  q_max = 2^bw - 1
+ * Readings: ste rounds half to even in the forward pass and has
+ * derivative 1 in the backward pass; the simulated (fake-quantized)
+ * value is the inverse map X_hat = alpha * (X_int + beta); every forward
+ * step is one fp32 operation.  Backward, with mask = (0 <= u <= q_max),
+ * u = rint(X/alpha) - beta (the clamp passes the gradient at its ends):
+ *   dX_hat/dX     = mask
+ *   dX_hat/dalpha = (X_int + beta) - mask * X/alpha
+ *   dX_hat/dbeta  = alpha * (1 - mask)
+ * so outside the range X_hat is f_min = alpha beta or f_max = alpha q_max
+ * + alpha beta, the two ends the paper learns through alpha and beta.
+ * The parameter gradients are sums over the tensor, per-element terms in
+ * fp64 from the fp32 values, accumulated in fp64.                      */
+/* ------------------------------------------------------------------ */
+void oracle_arl_forward(const float* x, int64_t n, float alpha, float beta, int bits,
+                        float* y)
+{
+    const float q_max = (float)(((int64_t)1 << bits) - 1);      /* Eq.(2) */
+    for (int64_t i = 0; i < n; ++i) {
+        const float t = x[i] / alpha;
+        const float u = rintf(t) - beta;                         /* Eq.(4) */
+        const float c = fminf(fmaxf(u, 0.0f), q_max);
+        y[i] = alpha * (c + beta);
+    }
+}
+
+void oracle_arl_backward(const float* x, const float* g, int64_t n, float alpha,
+                         float beta, int bits, float* gx, double* g_alpha,
+                         double* g_beta)
+{
+    const float q_max = (float)(((int64_t)1 << bits) - 1);
+    double ga = 0.0, gb = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        const float t = x[i] / alpha;
+        const float u = rintf(t) - beta;
+        const float c = fminf(fmaxf(u, 0.0f), q_max);
+        const int in = u >= 0.0f && u <= q_max;
+        gx[i] = in ? g[i] : 0.0f;
+        const double da = (double)c + (double)beta - (in ? (double)t : 0.0);
+        const double db = in ? 0.0 : (double)alpha;
+        ga += (double)g[i] * da;
+        gb += (double)g[i] * db;
+    }
+    *g_alpha = ga;
+    *g_beta = gb;
+}
+
+/* ------------------------------------------------------------------ */
 /* Symmetric per-output-channel weight quantizer (Section 5.1 W8A8/W4A8
  * settings and the appendix's symmetric per-channel W4).
  * Readings: narrow range +-Q with Q = 2^(b-1)-1; scale = absmax/Q in fp32

@@ -799,3 +799,107 @@ def test_fold_invariance():
     # a wrong fold (S applied on the same side twice) would break invariance
     bad = xh.astype(np.float64) @ (w / s[None, :]).astype(np.float64).T
     assert np.linalg.norm(y64 - bad) / np.linalg.norm(y64) > 1e-2
+
+
+# ---------------------------------------------------------------------------
+# Section 3.2: SmoothQuant's closed-form scaling vector
+# ---------------------------------------------------------------------------
+def test_smooth_scales_closed_forms():
+    rng = np.random.default_rng(50)
+    M, N, K = 40, 24, 33
+    x = (rng.standard_normal((M, K)) * rng.uniform(0.1, 30, K)).astype(np.float32)
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    x[:, 3] = 0.0                        # a channel that never fires
+    w[:, 5] = 0.0                        # a channel with no weight
+    x[7, 9], x[8, 9], w[2, 11] = np.nan, np.inf, -np.inf   # ignored by the maxima
+    fin = lambda v: np.where(np.isfinite(v), np.abs(v), 0.0)
+    mx, mw = fin(x).max(axis=0), fin(w).max(axis=0)
+    live = (mx > 0) & (mw > 0)
+    s1, gx, gw = oracle.smooth_scales(x, w, 1.0)
+    assert np.array_equal(gx, mx) and np.array_equal(gw, mw)
+    assert np.array_equal(s1[live], mx[live])                      # a = 1: s = max|X|
+    assert np.all(s1[~live] == 1.0)
+    s0, _, _ = oracle.smooth_scales(x, w, 0.0)                     # a = 0: s = 1/max|W|
+    assert np.array_equal(s0[live], (1.0 / mw[live].astype(np.float64)).astype(np.float32))
+    for a in (0.25, 0.5, 0.8):
+        s, _, _ = oracle.smooth_scales(x, w, a)
+        with np.errstate(divide="ignore"):
+            ref = mx.astype(np.float64) ** a / mw.astype(np.float64) ** (1 - a)
+        assert np.all(np.abs(s[live] - ref[live]) <= ref[live] * 2.0 ** -23)
+    # a = 0.5 balances the folded operands: max|X_k / s_k| = max|W_k s_k|
+    s, _, _ = oracle.smooth_scales(x, w, 0.5)
+    xa = fin(x / s).max(axis=0)
+    wa = fin(w * s).max(axis=0)
+    assert np.allclose(xa[live], wa[live], rtol=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# Section 4.2, Eq.(2)-(4): the training form of activation range learning
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("bw", [8, 16])
+def test_arl_forward_equals_inference_quantizer_at_integer_offsets(bw):
+    # with an integer beta = -(zp + 2^(bw-1)) the simulated value is the
+    # dequantized code of the (separately pinned) inference quantizer
+    rng = np.random.default_rng(51)
+    for lo, hi in [(-3.0, 5.0), (-0.01, 40.0), (-7.0, 0.0)]:
+        alpha, zp = oracle.act_params(lo, hi, bw)
+        beta = float(-(zp + 2 ** (bw - 1)))
+        x = np.concatenate([rng.uniform(2 * lo - 1, 2 * hi + 1, 5000),
+                            [np.nan, np.inf, -np.inf, 0.0, lo, hi]]).astype(np.float32)
+        y = oracle.arl_forward(x, alpha, beta, bw)
+        q = oracle.quantize_act(x, alpha, zp, bw)
+        ref = oracle.dequant(q, alpha, zp)
+        assert np.array_equal(y.view(np.uint32), ref.view(np.uint32))
+
+
+def test_arl_forward_range_ends():
+    # outside the range the output is f_min = alpha beta or f_max = alpha
+    # q_max + alpha beta, the quantities the paper learns through alpha, beta
+    alpha, beta = np.float32(0.037), np.float32(-90.4)
+    x = np.array([-1e6, -50.0, 1e6, 50.0], np.float32)
+    y = oracle.arl_forward(x, float(alpha), float(beta), 8)
+    f_min = np.float32(alpha * beta)
+    f_max = np.float32(alpha * np.float32(np.float32(255.0) + beta))
+    assert y.tolist() == [f_min, f_min, f_max, f_max]
+
+
+@pytest.mark.parametrize("bw", [8, 4])
+def test_arl_backward_matches_autograd(bw):
+    # the straight-through gradients against torch's autograd on the same
+    # forward graph (round with an identity gradient, clamp, scale)
+    import torch
+    rng = np.random.default_rng(52 + bw)
+    x = (rng.standard_normal(3000) * 3).astype(np.float32)
+    x[:5] = [0.0, 1e4, -1e4, 2.5, -0.7]
+    g = rng.standard_normal(3000).astype(np.float32)
+    q_max = 2 ** bw - 1
+    for alpha, beta in ((0.02, -130.3), (0.5, -7.6), (0.01, -40.0)):
+        gx, ga, gb = oracle.arl_backward(x, g, alpha, beta, bw)
+        xt = torch.tensor(x, requires_grad=True)
+        at = torch.tensor(alpha, dtype=torch.float32, requires_grad=True)
+        bt = torch.tensor(beta, dtype=torch.float32, requires_grad=True)
+        t = xt / at
+        r = t + (torch.round(t) - t).detach()
+        c = torch.clamp(r - bt, 0.0, float(q_max))
+        y = at * (c + bt)
+        assert np.array_equal(y.detach().numpy(), oracle.arl_forward(x, alpha, beta, bw))
+        y.backward(torch.from_numpy(g))
+        assert np.allclose(xt.grad.numpy(), gx, rtol=1e-6, atol=0)
+        scale = float(np.abs(g).sum()) * (q_max + abs(beta) + 1)
+        assert abs(float(at.grad) - ga) <= 1e-5 * scale
+        assert abs(float(bt.grad) - gb) <= 1e-5 * scale * alpha
+        assert np.any(gx == 0) and np.any(gx != 0)   # both sides of the range occur
+
+
+def test_arl_backward_inside_the_range_is_the_rounding_residual():
+    # with every value inside the range: dL/dbeta = 0 and dL/dalpha =
+    # sum g (rint(x/alpha) - x/alpha)
+    rng = np.random.default_rng(53)
+    alpha, beta = 0.05, -128.0
+    x = rng.uniform(-6.0, 6.0, 2000).astype(np.float32)
+    g = rng.standard_normal(2000).astype(np.float32)
+    gx, ga, gb = oracle.arl_backward(x, g, alpha, beta, 8)
+    t = (x / np.float32(alpha)).astype(np.float64)
+    assert np.array_equal(gx, g) and gb == 0.0
+    assert abs(ga - float(np.sum(g.astype(np.float64) * (np.rint(t) - t)))) <= 1e-9
+
