@@ -306,6 +306,52 @@ mq_status mq_qlinear_a16(const int16_t* a_q, int64_t M, int64_t K, int64_t N,
                          const float* bias, void* y_q, int32_t path, void* stream);
 
 /*
+ * mq_smooth_scales -- SmoothQuant's closed-form scaling vector as the
+ * paper restates it (Section 3.2), for calibration:
+ *   x_absmax[k] = max_m |x[m][k]|,  w_absmax[k] = max_n |w[n][k]|
+ *   s[k] = x_absmax[k]^a / w_absmax[k]^(1-a)   (fp64 pow, rounded to fp32)
+ * over finite entries; s[k] = 1 where either maximum is 0.  Fold s with
+ * mq_fold_weights / mq_fold_acts (Eq.(1)).
+ *   x  device fp32 [M][K]   w  device fp32 [N][K]   a  in [0, 1]
+ *   x_absmax, w_absmax, s  device fp32 [K]
+ *   M, N >= 0 (0 rows give a maximum of 0), K >= 0 (0 -> nothing to do).
+ */
+mq_status mq_smooth_scales(const float* x, int64_t M, int64_t K, const float* w,
+                           int64_t N, float a, float* x_absmax, float* w_absmax,
+                           float* s, void* stream);
+
+/*
+ * mq_arl_forward -- activation range learning, the training form of
+ * Section 4.2, Eq.(2)-(4) with learnable scale alpha and offset beta:
+ *   y = alpha * (min(max(rint(x/alpha) - beta, 0), 2^bits - 1) + beta)
+ * each step one fp32 operation, rint half to even (the straight-through
+ * estimator only changes the backward pass).
+ *   x, y   device fp32 [numel] (may alias)
+ *   alpha  finite, > 0     beta  finite     bits in [2, 16]
+ */
+mq_status mq_arl_forward(const float* x, int64_t numel, float alpha, float beta,
+                         int32_t bits, float* y, void* stream);
+
+/* Partial sums mq_arl_backward keeps after its two results. */
+#define MQ_ARL_PARTIALS 1024
+
+/*
+ * mq_arl_backward -- straight-through gradients of mq_arl_forward.  With
+ * u = rint(x/alpha) - beta and mask = (0 <= u <= 2^bits - 1):
+ *   gx[i]    = g[i] * mask
+ *   grads[0] = sum_i g[i] * ((clamp(u) + beta) - mask * x[i]/alpha)   (dL/dalpha)
+ *   grads[1] = sum_i g[i] * alpha * (1 - mask)                        (dL/dbeta)
+ * per-element terms and sums in fp64; the sum runs over fixed per-block
+ * partials in block order, so a given numel always sums in the same order.
+ *   x, g, gx  device fp32 [numel]
+ *   grads     device fp64 [2 + 2 * MQ_ARL_PARTIALS]: the two results, then
+ *             scratch for the partial sums
+ */
+mq_status mq_arl_backward(const float* x, const float* g, int64_t numel, float alpha,
+                          float beta, int32_t bits, float* gx, double* grads,
+                          void* stream);
+
+/*
  * mq_dequant -- inverse of Eq.(4): y = alpha * (float)(q - zp), one exact
  * integer subtraction and one fp32 multiply.
  *   q      device int8 (bits 8) or int16 (bits 16) [numel]

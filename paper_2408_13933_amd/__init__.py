@@ -16,7 +16,7 @@ __all__ = [
     "MQError", "lib", "lib_path", "mq_version", "mq_act_params", "mq_fold_weights",
     "mq_fold_acts", "mq_quantize_act", "mq_pack_weights", "mq_qlinear", "mq_dequant",
     "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum", "mq_qlinear_asym",
-    "mq_qlinear_a16",
+    "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward", "mq_arl_backward", "ARL_PARTIALS",
     "mq_qlinear_workspace_bytes",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
 ]
@@ -27,6 +27,7 @@ lib_path = os.path.join(_HERE, "libmq.so")
 MQ_OK, MQ_ERR_INVALID_ARG, MQ_ERR_UNSUPPORTED, MQ_ERR_HIP = 0, 1, 2, 3
 PATH_AUTO, PATH_DECODE, PATH_PREFILL, PATH_GENERIC = 0, 1, 2, 3
 MAX_K = 65536
+ARL_PARTIALS = 1024
 
 _lib = None
 
@@ -76,6 +77,9 @@ def lib():
                                        c_p]
     L.mq_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_p, c_p]
     L.mq_quantize_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_p, c_p, c_p]
+    L.mq_smooth_scales.argtypes = [c_p, c_i64, c_i64, c_p, c_i64, c_f, c_p, c_p, c_p, c_p]
+    L.mq_arl_forward.argtypes = [c_p, c_i64, c_f, c_f, c_i32, c_p, c_p]
+    L.mq_arl_backward.argtypes = [c_p, c_p, c_i64, c_f, c_f, c_i32, c_p, c_p, c_p]
     L.mq_qlinear_a16.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32,
                                  c_f, c_i32, c_i32, c_p, c_p, c_i32, c_p]
     L.mq_qlinear_asym.argtypes = [c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_p,
@@ -84,7 +88,8 @@ def lib():
     for name in ("mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
-                 "mq_qlinear_asym", "mq_qlinear_a16"):
+                 "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
+                 "mq_arl_backward"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -292,6 +297,54 @@ def mq_qlinear_asym(a_q, a_rowsum, w_q, w_bits: int, w_scale, w_zp, w_colsum, a_
         _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), ws, ws_bytes, int(path),
         _stream_ptr(stream)), "mq_qlinear_asym")
     return out
+
+
+def mq_smooth_scales(x, w, a: float, s=None, x_absmax=None, w_absmax=None, stream=None):
+    """SmoothQuant's closed-form scales (Section 3.2): (s, x_absmax, w_absmax)."""
+    torch = _torch()
+    M, K = x.shape
+    N, K2 = w.shape
+    if K2 != K:
+        raise ValueError("x and w must have the same number of columns")
+    dev = x.device
+    s = torch.empty(K, dtype=torch.float32, device=dev) if s is None else s
+    x_absmax = torch.empty(K, dtype=torch.float32, device=dev) if x_absmax is None else x_absmax
+    w_absmax = torch.empty(K, dtype=torch.float32, device=dev) if w_absmax is None else w_absmax
+    _check(lib().mq_smooth_scales(_dev_ptr(x, torch.float32, "x"), M, K,
+                                  _dev_ptr(w, torch.float32, "w"), N, float(a),
+                                  _dev_ptr(x_absmax, torch.float32, "x_absmax", (K,)),
+                                  _dev_ptr(w_absmax, torch.float32, "w_absmax", (K,)),
+                                  _dev_ptr(s, torch.float32, "s", (K,)), _stream_ptr(stream)),
+           "mq_smooth_scales")
+    return s, x_absmax, w_absmax
+
+
+def mq_arl_forward(x, alpha: float, beta: float, bits: int, out=None, stream=None):
+    """Fake-quantized alpha * (X_int + beta) of Eq.(2)-(4) (training form)."""
+    torch = _torch()
+    out = torch.empty_like(x) if out is None else out
+    _check(lib().mq_arl_forward(_dev_ptr(x, torch.float32, "x"), x.numel(), float(alpha),
+                                float(beta), int(bits),
+                                _dev_ptr(out, torch.float32, "out", x.shape),
+                                _stream_ptr(stream)), "mq_arl_forward")
+    return out
+
+
+def mq_arl_backward(x, g, alpha: float, beta: float, bits: int, gx=None, grads=None,
+                    stream=None):
+    """Straight-through gradients: (gx, grads) with grads[0] = dL/dalpha and
+    grads[1] = dL/dbeta on the device (fp64; the rest is scratch)."""
+    torch = _torch()
+    gx = torch.empty_like(x) if gx is None else gx
+    grads = (torch.empty(2 + 2 * ARL_PARTIALS, dtype=torch.float64, device=x.device)
+             if grads is None else grads)
+    _check(lib().mq_arl_backward(_dev_ptr(x, torch.float32, "x"),
+                                 _dev_ptr(g, torch.float32, "g", x.shape), x.numel(),
+                                 float(alpha), float(beta), int(bits),
+                                 _dev_ptr(gx, torch.float32, "gx", x.shape),
+                                 _dev_ptr(grads, torch.float64, "grads", (2 + 2 * ARL_PARTIALS,)),
+                                 _stream_ptr(stream)), "mq_arl_backward")
+    return gx, grads
 
 
 def mq_qlinear_a16(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: int,

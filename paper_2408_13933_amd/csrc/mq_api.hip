@@ -136,6 +136,39 @@ mq_status mq_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bit
                                                  w_zp, w_colsum, as_stream(stream)));
 }
 
+mq_status mq_smooth_scales(const float* x, int64_t M, int64_t K, const float* w, int64_t N,
+                           float a, float* x_absmax, float* w_absmax, float* s, void* stream)
+{
+    if (M < 0 || N < 0 || K < 0 || M > kMaxElems || N > kMaxElems || K > 0x7FFFFFFF)
+        return MQ_ERR_INVALID_ARG;
+    if ((K > 0 && (M > kMaxElems / K || N > kMaxElems / K))) return MQ_ERR_INVALID_ARG;
+    if (!(a >= 0.0f && a <= 1.0f)) return MQ_ERR_INVALID_ARG;
+    if (K == 0) return MQ_OK;
+    if (!x_absmax || !w_absmax || !s || (M > 0 && !x) || (N > 0 && !w)) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_smooth_scales(x, M, K, w, N, a, x_absmax, w_absmax, s,
+                                             as_stream(stream)));
+}
+
+mq_status mq_arl_forward(const float* x, int64_t numel, float alpha, float beta, int32_t bits,
+                         float* y, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || bits < 2 || bits > 16) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(alpha) || !std::isfinite(beta)) return MQ_ERR_INVALID_ARG;
+    if (numel == 0) return MQ_OK;
+    if (!x || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_arl_forward(x, numel, alpha, beta, bits, y, as_stream(stream)));
+}
+
+mq_status mq_arl_backward(const float* x, const float* g, int64_t numel, float alpha, float beta,
+                          int32_t bits, float* gx, double* grads, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || bits < 2 || bits > 16) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(alpha) || !std::isfinite(beta)) return MQ_ERR_INVALID_ARG;
+    if (!grads || (numel > 0 && (!x || !g || !gx))) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_arl_backward(x, g, numel, alpha, beta, bits, gx, grads,
+                                            MQ_ARL_PARTIALS, as_stream(stream)));
+}
+
 mq_status mq_quantize_act_rowsum(const float* x, int64_t M, int64_t K, float alpha, int32_t zp,
                                  int8_t* x_q, int32_t* rowsum, void* stream)
 {

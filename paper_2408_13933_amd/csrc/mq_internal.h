@@ -49,6 +49,15 @@ hipError_t launch_quantize_act_rowsum(const float* x, int64_t M, int64_t K, floa
 hipError_t launch_act_rowsum(const int8_t* a, int64_t M, int64_t K, int32_t* rowsum,
                              hipStream_t s);
 
+hipError_t launch_arl_forward(const float* x, int64_t n, float alpha, float beta, int32_t bits,
+                              float* y, hipStream_t s);
+hipError_t launch_arl_backward(const float* x, const float* g, int64_t n, float alpha, float beta,
+                               int32_t bits, float* gx, double* grads, int32_t max_partials,
+                               hipStream_t s);
+hipError_t launch_smooth_scales(const float* x, int64_t M, int64_t K, const float* w, int64_t N,
+                                float a, float* x_absmax, float* w_absmax, float* s,
+                                hipStream_t st);
+
 hipError_t launch_qlinear_generic(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s);

@@ -234,3 +234,29 @@ def test_act_params_matches_oracle():
 def test_act_params_rejects(lo, hi, bits):
     with pytest.raises(mq.MQError):
         mq.mq_act_params(lo, hi, bits)
+
+
+@pytest.mark.parametrize("call", [
+    lambda L: L.mq_smooth_scales(NZ, 4, 8, NZ, 4, 1.5, NZ, NZ, NZ, None),
+    lambda L: L.mq_smooth_scales(NZ, 4, 8, NZ, 4, -0.1, NZ, NZ, NZ, None),
+    lambda L: L.mq_smooth_scales(NZ, 4, 8, NZ, 4, float("nan"), NZ, NZ, NZ, None),
+    lambda L: L.mq_smooth_scales(NZ, -1, 8, NZ, 4, 0.5, NZ, NZ, NZ, None),
+    lambda L: L.mq_smooth_scales(None, 4, 8, NZ, 4, 0.5, NZ, NZ, NZ, None),
+    lambda L: L.mq_smooth_scales(NZ, 4, 8, NZ, 4, 0.5, NZ, NZ, None, None),
+    lambda L: L.mq_arl_forward(NZ, 10, 0.0, 1.0, 8, NZ, None),
+    lambda L: L.mq_arl_forward(NZ, 10, 0.1, float("inf"), 8, NZ, None),
+    lambda L: L.mq_arl_forward(NZ, 10, 0.1, 1.0, 1, NZ, None),
+    lambda L: L.mq_arl_forward(NZ, 10, 0.1, 1.0, 17, NZ, None),
+    lambda L: L.mq_arl_forward(None, 10, 0.1, 1.0, 8, NZ, None),
+    lambda L: L.mq_arl_backward(NZ, NZ, 10, 0.1, 1.0, 8, NZ, None, None),
+    lambda L: L.mq_arl_backward(NZ, None, 10, 0.1, 1.0, 8, NZ, NZ, None),
+    lambda L: L.mq_arl_backward(NZ, NZ, 10, float("nan"), 1.0, 8, NZ, NZ, None),
+])
+def test_calibration_entry_points_reject_invalid_arguments(call):
+    assert call(mq.lib()) == 1
+
+
+def test_calibration_empty_calls():
+    L = mq.lib()
+    assert L.mq_smooth_scales(None, 0, 0, None, 0, 0.5, None, None, None, None) == 0
+    assert L.mq_arl_forward(None, 0, 0.1, 1.0, 8, None, None) == 0
