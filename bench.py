@@ -58,6 +58,9 @@ def parse():
                     help="after timing, stream this many MiB through a plain elementwise kernel "
                          "three times (one read and one write of that size: the calibration "
                          "kernel of the HBM byte counters)")
+    ap.add_argument("--calib-sweep", action="store_true",
+                    help="time the calibration-side kernels (range learning, SmoothQuant "
+                         "scales) instead of the step")
     ap.add_argument("--decode-sweep", action="store_true",
                     help="time the decode-shaped layers (M <= 16) cold: each launch reads a "
                          "different copy of the weights, >= 512 MB per sweep; prints one JSON "
@@ -398,8 +401,67 @@ def decode_sweep(launches_per_layer=400):
         torch.cuda.empty_cache()
 
 
+def calib_sweep(reps=5, per_graph=10):
+    """Calibration-side kernels on TinyLlama-sized tensors: activation range
+    learning forward/backward on a 2048x2048 fp32 activation and SmoothQuant
+    scales over X 2048x2048 and W 5632x2048.  Each op is captured
+    `per_graph` times into a HIP graph and replayed; algorithmic bytes per
+    launch / time against the 8 TB/s HBM peak."""
+    import torch
+
+    import paper_2408_13933_amd as mq
+
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    M, K, N = 2048, 2048, 5632
+    x = torch.randn((M, K), device=dev, generator=g) * 3
+    gr = torch.randn((M, K), device=dev, generator=g)
+    w = torch.randn((N, K), device=dev, generator=g) * 0.02
+    y = torch.empty_like(x)
+    gx = torch.empty_like(x)
+    grads = torch.empty(2 + 2 * mq.ARL_PARTIALS, dtype=torch.float64, device=dev)
+    s = torch.empty(K, device=dev)
+    mx = torch.empty(K, device=dev)
+    mw = torch.empty(K, device=dev)
+    ops = {
+        "arl_forward": (lambda: mq.mq_arl_forward(x, 0.05, -128.0, 8, out=y), 8 * M * K),
+        "arl_backward": (lambda: mq.mq_arl_backward(x, gr, 0.05, -128.0, 8, gx=gx, grads=grads),
+                         12 * M * K),
+        "smooth_scales": (lambda: mq.mq_smooth_scales(x, w, 0.5, s=s, x_absmax=mx, w_absmax=mw),
+                          4 * (M + N) * K + 12 * K),
+    }
+    for name, (fn, nbytes) in ops.items():
+        fn()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(graph, stream=cap):
+                for _ in range(per_graph):
+                    fn()
+        torch.cuda.current_stream().wait_stream(cap)
+        graph.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(reps):
+            graph.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        us = t0.elapsed_time(t1) * 1e3 / (reps * per_graph)
+        gbs = nbytes / us / 1e3
+        print(json.dumps({"op": name, "shape": [M, K] if name != "smooth_scales" else [M, N, K],
+                          "us_graph_replay": round(us, 2), "alg_bytes": nbytes,
+                          "GB/s": round(gbs, 1), "frac_hbm": round(gbs / 8000.0, 3)}), flush=True)
+
+
 def main():
     args = parse()
+    if args.calib_sweep:
+        calib_sweep()
+        return
     if args.decode_sweep:
         decode_sweep()
         return

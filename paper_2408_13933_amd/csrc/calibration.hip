@@ -35,17 +35,31 @@ __device__ inline float arl_u(float x, float alpha, float beta)
     return rintf(x / alpha) - beta;
 }
 
+__device__ inline float arl_y(float x, float alpha, float beta, float q_max)
+{
+#pragma clang fp contract(off)
+    const float c = fminf(fmaxf(arl_u(x, alpha, beta), 0.0f), q_max);
+    return alpha * (c + beta);
+}
+
+// 16-byte loads and stores for the aligned body (n4 float4s), elements
+// [begin, n) one by one
 __global__ __launch_bounds__(kThreads) void arl_forward_kernel(const float* __restrict__ x,
+                                                               int64_t n4, int64_t begin,
                                                                int64_t n, float alpha,
                                                                float beta, float q_max,
                                                                float* __restrict__ y)
 {
-#pragma clang fp contract(off)
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) {
-        const float c = fminf(fmaxf(arl_u(x[i], alpha, beta), 0.0f), q_max);
-        y[i] = alpha * (c + beta);
+    const int64_t t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    float4* y4 = reinterpret_cast<float4*>(y);
+    for (int64_t i = t0; i < n4; i += stride) {
+        const float4 v = x4[i];
+        y4[i] = make_float4(arl_y(v.x, alpha, beta, q_max), arl_y(v.y, alpha, beta, q_max),
+                            arl_y(v.z, alpha, beta, q_max), arl_y(v.w, alpha, beta, q_max));
     }
+    for (int64_t i = begin + t0; i < n; i += stride) y[i] = arl_y(x[i], alpha, beta, q_max);
 }
 
 __global__ __launch_bounds__(kThreads) void arl_backward_kernel(
@@ -90,18 +104,39 @@ __global__ __launch_bounds__(kThreads) void arl_backward_kernel(
     }
 }
 
-// The per-block partial sums in block order (deterministic for a given n).
-__global__ __launch_bounds__(64) void arl_reduce_kernel(const double* __restrict__ partials,
-                                                        int nblocks, double* __restrict__ out)
+// The per-block partial sums: thread t adds partials t, t + 256, ... in
+// order, then a fixed tree over the threads; the order depends on nblocks
+// only, so a given n always sums the same way.
+__global__ __launch_bounds__(kThreads) void arl_reduce_kernel(const double* __restrict__ partials,
+                                                              int nblocks,
+                                                              double* __restrict__ out)
 {
-    if (threadIdx.x != 0) return;
+    __shared__ double red[2][kThreads / 64];
     double a = 0.0, b = 0.0;
-    for (int i = 0; i < nblocks; ++i) {
+    for (int i = threadIdx.x; i < nblocks; i += kThreads) {
         a += partials[2 * i];
         b += partials[2 * i + 1];
     }
-    out[0] = a;
-    out[1] = b;
+    for (int o = 32; o > 0; o >>= 1) {
+        a += __shfl_xor(a, o);
+        b += __shfl_xor(b, o);
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        red[0][wave] = a;
+        red[1][wave] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double sa = 0.0, sb = 0.0;
+#pragma unroll
+        for (int w = 0; w < kThreads / 64; ++w) {
+            sa += red[0][w];
+            sb += red[1][w];
+        }
+        out[0] = sa;
+        out[1] = sb;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -116,21 +151,68 @@ __global__ __launch_bounds__(kThreads) void fill_u32_kernel(uint32_t* __restrict
     if (i < n) p[i] = v;
 }
 
+__device__ inline float absmax_finite(float m, float v)
+{
+    const float a = fabsf(v);
+    return __builtin_isfinite(a) && a > m ? a : m;
+}
+
+// A block covers 64 * COLS columns (COLS = 4: 16-byte loads, K % 4 == 0 and
+// an aligned base) and a chunk of rows; its four waves take every fourth
+// row, eight rows per trip in flight, meet in LDS, and wave 0 folds the
+// block's maxima into `out` with one atomic per column.
+template <int COLS>
 __global__ __launch_bounds__(kThreads) void col_absmax_kernel(const float* __restrict__ v,
                                                               int64_t rows, int64_t K,
                                                               int64_t rows_per_block,
                                                               uint32_t* __restrict__ out)
 {
-    const int64_t col = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (col >= K) return;
+    __shared__ float red[kThreads / 64][64 * COLS];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t col = ((int64_t)blockIdx.x * 64 + lane) * COLS;
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_block;
     const int64_t r1 = r0 + rows_per_block < rows ? r0 + rows_per_block : rows;
-    float m = 0.0f;
-    for (int64_t r = r0; r < r1; ++r) {
-        const float a = fabsf(v[r * K + col]);
-        if (__builtin_isfinite(a) && a > m) m = a;
+    constexpr int NW = kThreads / 64;
+    float m[COLS] = {};
+    if (col < K) {
+        int64_t r = r0 + wave;
+        for (; r + 7 * NW < r1; r += 8 * NW) {
+            if constexpr (COLS == 4) {
+                float4 t[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    t[u] = *reinterpret_cast<const float4*>(v + (r + u * NW) * K + col);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    m[0] = absmax_finite(m[0], t[u].x);
+                    m[1] = absmax_finite(m[1], t[u].y);
+                    m[2] = absmax_finite(m[2], t[u].z);
+                    m[3] = absmax_finite(m[3], t[u].w);
+                }
+            } else {
+                float t[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) t[u] = v[(r + u * NW) * K + col];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) m[0] = absmax_finite(m[0], t[u]);
+            }
+        }
+        for (; r < r1; r += NW)
+#pragma unroll
+            for (int c = 0; c < COLS; ++c) m[c] = absmax_finite(m[c], v[r * K + col + c]);
     }
-    if (m > 0.0f) atomicMax(out + col, __float_as_uint(m));
+#pragma unroll
+    for (int c = 0; c < COLS; ++c) red[wave][lane * COLS + c] = m[c];
+    __syncthreads();
+    if (wave == 0 && col < K) {
+#pragma unroll
+        for (int c = 0; c < COLS; ++c) {
+            float b = red[0][lane * COLS + c];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) b = fmaxf(b, red[w][lane * COLS + c]);
+            if (b > 0.0f) atomicMax(out + col + c, __float_as_uint(b));
+        }
+    }
 }
 
 // s_k = max|X_k|^a / max|W_k|^(1-a) in fp64, rounded once to fp32; 1 for a
@@ -154,8 +236,10 @@ hipError_t launch_arl_forward(const float* x, int64_t n, float alpha, float beta
                               float* y, hipStream_t st)
 {
     const float q_max = (float)((1 << bits) - 1);
-    arl_forward_kernel<<<grid_for(n, kThreads, 256 * 64), kThreads, 0, st>>>(x, n, alpha, beta,
-                                                                             q_max, y);
+    const bool vec = ((uintptr_t)x % 16) == 0 && ((uintptr_t)y % 16) == 0;
+    const int64_t n4 = vec ? n / 4 : 0;
+    arl_forward_kernel<<<grid_for(vec ? n4 : n, kThreads, 256 * 64), kThreads, 0, st>>>(
+        x, n4, n4 * 4, n, alpha, beta, q_max, y);
     return hipGetLastError();
 }
 
@@ -167,7 +251,7 @@ hipError_t launch_arl_backward(const float* x, const float* g, int64_t n, float 
     const int blocks = grid_for(n, kThreads * 4, max_partials);
     double* partials = grads + 2;
     arl_backward_kernel<<<blocks, kThreads, 0, st>>>(x, g, n, alpha, beta, q_max, gx, partials);
-    arl_reduce_kernel<<<1, 64, 0, st>>>(partials, blocks, grads);
+    arl_reduce_kernel<<<1, kThreads, 0, st>>>(partials, blocks, grads);
     return hipGetLastError();
 }
 
@@ -178,13 +262,17 @@ hipError_t launch_smooth_scales(const float* x, int64_t M, int64_t K, const floa
     const unsigned gk = (unsigned)((K + kThreads - 1) / kThreads);
     fill_u32_kernel<<<gk, kThreads, 0, st>>>(reinterpret_cast<uint32_t*>(x_absmax), K, 0u);
     fill_u32_kernel<<<gk, kThreads, 0, st>>>(reinterpret_cast<uint32_t*>(w_absmax), K, 0u);
-    // at least 64 rows per block, and at most 65535 row blocks (grid y limit)
+    // 64 rows per block (so each column takes rows / 64 atomics), more when
+    // the grid's y limit of 65535 row blocks needs it
     auto colmax = [&](const float* v, int64_t rows, float* out) {
+        const bool vec = K % 4 == 0 && ((uintptr_t)v % 16) == 0;
+        const int64_t gx = vec ? (K / 4 + 63) / 64 : (K + 63) / 64;
         int64_t rpb = 64;
         if ((rows + rpb - 1) / rpb > 65535) rpb = (rows + 65534) / 65535;
-        const unsigned gy = (unsigned)((rows + rpb - 1) / rpb);
-        col_absmax_kernel<<<dim3(gk, gy), kThreads, 0, st>>>(v, rows, K, rpb,
-                                                            reinterpret_cast<uint32_t*>(out));
+        const dim3 grid((unsigned)gx, (unsigned)((rows + rpb - 1) / rpb));
+        uint32_t* o = reinterpret_cast<uint32_t*>(out);
+        if (vec) col_absmax_kernel<4><<<grid, kThreads, 0, st>>>(v, rows, K, rpb, o);
+        else col_absmax_kernel<1><<<grid, kThreads, 0, st>>>(v, rows, K, rpb, o);
     };
     if (M > 0) colmax(x, M, x_absmax);
     if (N > 0) colmax(w, N, w_absmax);
