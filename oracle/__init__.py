@@ -13,6 +13,8 @@ Functions and the passages they follow (arXiv 2408.13933):
 * ``dequant``         -- inverse of Eq.(4)
 * ``fold_weights`` / ``fold_acts`` -- Section 3.2, Eq.(1) (S W and X S^-1)
 * ``smooth_scales``   -- Section 3.2: SmoothQuant's closed-form S
+* ``add_requant``, ``lut_build``, ``rmsnorm``, ``softmax`` -- decoder-block
+  glue on 16-bit integer activations (Section 4.1, Section 5.1)
 * ``arl_forward`` / ``arl_backward`` -- Section 4.2, Eq.(2)-(4) in its
   training form (learnable alpha, beta; straight-through rounding)
 * ``pack_weights``    -- Section 5.1 / appendix: symmetric per-channel W8, W4
@@ -70,6 +72,22 @@ def _load():
     lib.oracle_fold_weights.restype = None
     lib.oracle_fold_acts.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int64, _f32p]
     lib.oracle_fold_acts.restype = None
+    _i16p = np.ctypeslib.ndpointer(dtype=np.int16, flags="C_CONTIGUOUS")
+    lib.oracle_add_requant.argtypes = [_i16p, ctypes.c_float, ctypes.c_int32, _i16p,
+                                       ctypes.c_float, ctypes.c_int32, ctypes.c_int64,
+                                       ctypes.c_float, ctypes.c_int32, ctypes.c_int, _vp]
+    lib.oracle_add_requant.restype = None
+    lib.oracle_lut_build.argtypes = [ctypes.c_int, ctypes.c_float, ctypes.c_int32,
+                                     ctypes.c_float, ctypes.c_int32, ctypes.c_int, _vp]
+    lib.oracle_lut_build.restype = None
+    lib.oracle_rmsnorm.argtypes = [_i16p, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
+                                   ctypes.c_int32, _vp, ctypes.c_float, ctypes.c_float,
+                                   ctypes.c_int32, ctypes.c_int, _vp]
+    lib.oracle_rmsnorm.restype = None
+    lib.oracle_softmax.argtypes = [_i16p, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
+                                   ctypes.c_int32, ctypes.c_float, ctypes.c_int32, ctypes.c_int,
+                                   _vp]
+    lib.oracle_softmax.restype = None
     lib.oracle_smooth_scales.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64, _f32p,
                                          ctypes.c_int64, ctypes.c_float, _f32p, _f32p, _f32p]
     lib.oracle_smooth_scales.restype = None
@@ -210,6 +228,49 @@ def pack_weights(w: np.ndarray, bits: int):
     colsum = np.empty(N, dtype=np.int32)
     _load().oracle_pack_weights(w, N, K, bits, _ptr(wq), scale, colsum)
     return wq, scale, colsum
+
+
+LUT_SILU = 1
+
+
+def add_requant(x1, a1, z1, x2, a2, z2, ay, zy, bits_y):
+    """Residual add of two int16 code tensors, requantized."""
+    x1 = np.ascontiguousarray(x1, dtype=np.int16)
+    x2 = np.ascontiguousarray(x2, dtype=np.int16)
+    assert x1.shape == x2.shape
+    y = np.empty(x1.shape, dtype=_act_dtype(bits_y))
+    _load().oracle_add_requant(x1.reshape(-1), a1, z1, x2.reshape(-1), a2, z2, x1.size, ay, zy,
+                               bits_y, _ptr(y))
+    return y
+
+
+def lut_build(op, ax, zx, ay, zy, bits_y):
+    """65536-entry table of a non-linear op on int16 codes (entry i + 32768)."""
+    lut = np.empty(65536, dtype=_act_dtype(bits_y))
+    _load().oracle_lut_build(int(op), ax, zx, ay, zy, bits_y, _ptr(lut))
+    return lut
+
+
+def rmsnorm(x, ax, zx, gamma, eps, ay, zy, bits_y):
+    """RMSNorm over rows of int16 codes, requantized."""
+    x = np.ascontiguousarray(x, dtype=np.int16)
+    M, K = x.shape
+    g = None
+    if gamma is not None:
+        gamma = np.ascontiguousarray(gamma, dtype=np.float32)
+        g = _ptr(gamma)
+    y = np.empty((M, K), dtype=_act_dtype(bits_y))
+    _load().oracle_rmsnorm(x, M, K, ax, zx, g, eps, ay, zy, bits_y, _ptr(y))
+    return y
+
+
+def softmax(x, ax, zx, ay, zy, bits_y):
+    """Softmax over rows of int16 score codes, requantized."""
+    x = np.ascontiguousarray(x, dtype=np.int16)
+    M, K = x.shape
+    y = np.empty((M, K), dtype=_act_dtype(bits_y))
+    _load().oracle_softmax(x, M, K, ax, zx, ay, zy, bits_y, _ptr(y))
+    return y
 
 
 def smooth_scales(x: np.ndarray, w: np.ndarray, a: float):

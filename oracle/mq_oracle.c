@@ -223,6 +223,102 @@ void oracle_arl_backward(const float* x, const float* g, int64_t n, float alpha,
 }
 
 /* ------------------------------------------------------------------ */
+/* Decoder-block glue on integer activations (Section 4.1: the
+ * non-linear operators keep 16-bit integer activations; Section 5.1).
+ * The paper fixes the formats, not the arithmetic inside the operators.
+ * Readings: inputs are dequantized exactly (an fp32 scale times an
+ * integer of at most 17 bits is exact in fp64), each operator is
+ * evaluated in fp64 one IEEE operation at a time in the order written
+ * below, and the result is requantized with the Eq.(4) quantizer:
+ * code = clamp(rint(v / alpha_y) + zp_y) (rint half to even).          */
+/* ------------------------------------------------------------------ */
+static int64_t requant_f64(double v, float alpha_y, int32_t zp_y, int bits_y)
+{
+    double t = v / (double)alpha_y;
+    if (!(t == t)) t = -1e300;                         /* NaN -> low end */
+    if (t > 1e18) t = 1e18;
+    if (t < -1e18) t = -1e18;
+    return clamp_i64((int64_t)rint(t) + zp_y, qmin_of(bits_y), qmax_of(bits_y));
+}
+
+/* residual add: v = alpha_1 (x1 - zp_1) + alpha_2 (x2 - zp_2)          */
+void oracle_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                        float a2, int32_t z2, int64_t n, float ay, int32_t zy, int bits_y,
+                        void* y)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        const double v = (double)a1 * (double)((int64_t)x1[i] - z1) +
+                         (double)a2 * (double)((int64_t)x2[i] - z2);
+        store_q(y, bits_y, i, requant_f64(v, ay, zy, bits_y));
+    }
+}
+
+/* Elementwise non-linear operator on int16 codes as a 65536-entry table,
+ * entry i + 32768 for code i: f(alpha_x (i - zp_x)) requantized.
+ * op 1: SiLU, f(v) = v / (1 + exp(-v)).                                */
+static double glue_f(int op, double v)
+{
+    if (op == 1) return v / (1.0 + exp(-v));
+    return v;
+}
+
+void oracle_lut_build(int op, float ax, int32_t zx, float ay, int32_t zy, int bits_y,
+                      void* lut)
+{
+    for (int64_t i = -32768; i <= 32767; ++i) {
+        const double v = (double)ax * (double)(i - zx);
+        store_q(lut, bits_y, i + 32768, requant_f64(glue_f(op, v), ay, zy, bits_y));
+    }
+}
+
+/* RMSNorm over each row of K codes (gamma optional):
+ *   ss = sum_k (x - zp_x)^2 (exact, int64),  ms = alpha_x^2 ss / K + eps,
+ *   r = sqrt(ms),  v = alpha_x (x - zp_x) * gamma[k] / r                */
+void oracle_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                    const float* gamma, float eps, float ay, int32_t zy, int bits_y, void* y)
+{
+    for (int64_t m = 0; m < M; ++m) {
+        int64_t ss = 0;
+        for (int64_t k = 0; k < K; ++k) {
+            const int64_t d = (int64_t)x[m * K + k] - zx;
+            ss += d * d;
+        }
+        const double a = (double)ax;
+        const double ms = a * a * (double)ss / (double)K + (double)eps;
+        const double r = sqrt(ms);
+        for (int64_t k = 0; k < K; ++k) {
+            double v = a * (double)((int64_t)x[m * K + k] - zx);
+            if (gamma) v = v * (double)gamma[k];
+            v = v / r;
+            store_q(y, bits_y, m * K + k, requant_f64(v, ay, zy, bits_y));
+        }
+    }
+}
+
+/* Softmax over each row of K codes (scores):
+ *   e_k = exp(alpha_x (x_k - max_j x_j)),  p_k = e_k / sum_j e_j
+ * the sum in index order; the probabilities requantized.               */
+void oracle_softmax(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                    float ay, int32_t zy, int bits_y, void* y)
+{
+    (void)zx;  /* the zero-point cancels in x_k - max_j x_j */
+    double* e = (double*)malloc(sizeof(double) * (size_t)(K > 0 ? K : 1));
+    for (int64_t m = 0; m < M; ++m) {
+        int64_t mx = x[m * K];
+        for (int64_t k = 1; k < K; ++k)
+            if (x[m * K + k] > mx) mx = x[m * K + k];
+        double sum = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            e[k] = exp((double)ax * (double)((int64_t)x[m * K + k] - mx));
+            sum += e[k];
+        }
+        for (int64_t k = 0; k < K; ++k)
+            store_q(y, bits_y, m * K + k, requant_f64(e[k] / sum, ay, zy, bits_y));
+    }
+    free(e);
+}
+
+/* ------------------------------------------------------------------ */
 /* Symmetric per-output-channel weight quantizer (Section 5.1 W8A8/W4A8
  * settings and the appendix's symmetric per-channel W4).
  * Readings: narrow range +-Q with Q = 2^(b-1)-1; scale = absmax/Q in fp32

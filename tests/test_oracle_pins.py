@@ -903,3 +903,101 @@ def test_arl_backward_inside_the_range_is_the_rounding_residual():
     assert np.array_equal(gx, g) and gb == 0.0
     assert abs(ga - float(np.sum(g.astype(np.float64) * (np.rint(t) - t)))) <= 1e-9
 
+
+# ---------------------------------------------------------------------------
+# Decoder-block glue on 16-bit integer activations (Section 4.1, 5.1)
+# ---------------------------------------------------------------------------
+def _near_tie(v, band=1e-9):
+    """|frac(v) - 1/2| < band: a rounding decision fp64 may take either way."""
+    f = v - np.floor(v)
+    return np.abs(f - 0.5) < band
+
+
+def _check_codes(got, exact_pre, zp, lo, hi):
+    """got == clamp(rint(exact_pre) + zp), except one step either way where
+    exact_pre sits on a rounding tie."""
+    ref = np.clip(np.rint(exact_pre) + zp, lo, hi)
+    tie = _near_tie(exact_pre)
+    bad = (got != ref) & ~(tie & (np.abs(got.astype(np.int64) - ref) <= 1))
+    assert not np.any(bad), (got[bad][:5], ref[bad][:5])
+
+
+def test_add_requant_against_exact_rationals():
+    rng = np.random.default_rng(60)
+    n = 20000
+    x1 = rng.integers(-32768, 32768, n).astype(np.int16)
+    x2 = rng.integers(-32768, 32768, n).astype(np.int16)
+    a1, a2, ay = np.float32(3.1e-4), np.float32(7.7e-4), np.float32(1.3e-3)
+    z1, z2, zy = -12, 300, 5
+    y = oracle.add_requant(x1, float(a1), z1, x2, float(a2), z2, float(ay), zy, 16)
+    exact = np.array([float((Fraction(float(a1)) * (int(u) - z1) + Fraction(float(a2)) * (int(v) - z2))
+                            / Fraction(float(ay))) for u, v in zip(x1, x2)])
+    _check_codes(y.astype(np.int64), exact, zy, -32768, 32767)
+    # the same scale on both inputs and the output adds the integers
+    y = oracle.add_requant(x1, 0.5, 0, x2, 0.5, 0, 0.5, 0, 16)
+    assert np.array_equal(y, np.clip(x1.astype(np.int64) + x2, -32768, 32767))
+
+
+def test_silu_table():
+    ax, zx, ay, zy = 1e-3, -100, 0.05, 3
+    lut = oracle.lut_build(oracle.LUT_SILU, ax, zx, ay, zy, 8).astype(np.int64)
+    i = np.arange(-32768, 32768)
+    v = np.float64(np.float32(ax)) * (i - zx)
+    with np.errstate(over="ignore"):
+        exact = v / (1.0 + np.exp(-v)) / np.float64(np.float32(ay))
+    _check_codes(lut, exact, zy, -128, 127)
+    assert lut[zx + 32768] == zy                     # SiLU(0) = 0
+    # minimum of SiLU: -0.2785 at v = -1.2785
+    assert lut.min() == max(-128, int(np.rint(-0.27846454 / np.float32(ay))) + zy)
+
+
+def test_rmsnorm_against_torch():
+    import torch
+    rng = np.random.default_rng(61)
+    M, K = 7, 300
+    x = rng.integers(-20000, 20000, (M, K)).astype(np.int16)
+    x[3] = 0                                          # all zero row: eps keeps it finite
+    g = rng.uniform(0.5, 1.5, K).astype(np.float32)
+    ax, zx, ay, zy, eps = 4e-4, 17, 0.02, -3, 1e-5
+    y = oracle.rmsnorm(x, ax, zx, g, eps, ay, zy, 8).astype(np.int64)
+    xr = torch.tensor(np.float64(np.float32(ax)) * (x.astype(np.float64) - zx))
+    ref = torch.nn.functional.rms_norm(xr, (K,), torch.tensor(g, dtype=torch.float64),
+                                       eps=float(np.float32(eps))).numpy()
+    _check_codes(y, ref / np.float64(np.float32(ay)), zy, -128, 127)
+    # a constant row normalises to +-1; doubling (x - zp) changes nothing
+    c = np.full((2, K), 500, np.int16)
+    c[1] = -500 + 2 * zx
+    yc = oracle.rmsnorm(c, ax, zx, None, 0.0, 0.01, 0, 16)
+    assert yc[0].tolist() == [100] * K and yc[1].tolist() == [-100] * K
+    d = rng.integers(-8000, 8000, (M, 50))
+    x2 = (2 * d + zx).astype(np.int16)
+    x1 = (d + zx).astype(np.int16)
+    assert np.array_equal(oracle.rmsnorm(x1, ax, zx, None, 0.0, ay, zy, 16),
+                          oracle.rmsnorm(x2, ax, zx, None, 0.0, ay, zy, 16))
+
+
+def test_softmax_against_torch():
+    import torch
+    rng = np.random.default_rng(62)
+    M, K = 9, 257
+    x = rng.integers(-8000, 8000, (M, K)).astype(np.int16)
+    x[2] = 123                                        # uniform row
+    ax, zx, ay, zy = 1e-3, 40, 1.0 / 65535, -32768
+    y = oracle.softmax(x, ax, zx, ay, zy, 16).astype(np.int64)
+    xr = torch.tensor(np.float64(np.float32(ax)) * (x.astype(np.float64) - zx))
+    p = torch.softmax(xr, dim=1).numpy()
+    _check_codes(y, p / np.float64(np.float32(ay)), zy, -32768, 32767)
+    assert len(set(y[2].tolist())) == 1               # uniform row, uniform output
+    # scores whose exponentials overflow fp64 unless the row maximum comes
+    # off first (the largest score in the last column)
+    big = rng.integers(-32000, -15000, (3, 64)).astype(np.int16)
+    big[:, -1] = 32767
+    yb = oracle.softmax(big, 0.05, 0, ay, zy, 16).astype(np.int64)
+    pb = torch.softmax(torch.tensor(np.float64(np.float32(0.05)) * big.astype(np.float64)),
+                       dim=1).numpy()
+    _check_codes(yb, pb / np.float64(np.float32(ay)), zy, -32768, 32767)
+    # shifting every score of a row by a constant changes nothing
+    xs = (x[:, :100].astype(np.int64) - 500).astype(np.int16)
+    assert np.array_equal(oracle.softmax(x[:, :100], ax, zx, ay, zy, 16),
+                          oracle.softmax(xs, ax, zx, ay, zy, 16))
+
