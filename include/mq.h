@@ -306,6 +306,57 @@ mq_status mq_qlinear_a16(const int16_t* a_q, int64_t M, int64_t K, int64_t N,
                          const float* bias, void* y_q, int32_t path, void* stream);
 
 /*
+ * Decoder-block glue on 16-bit integer activations (Section 4.1 and 5.1:
+ * the operators between the quantized linears keep 16-bit integer
+ * activations).  The paper fixes the formats, not the arithmetic inside
+ * the operators; here every operator dequantizes exactly, evaluates in
+ * fp64 one IEEE operation at a time in the order written, and requantizes
+ * with Eq.(4): code = clamp(rint(v / ay) + zy) over out_bits (8 or 16).
+ * x codes are int16 with zero-points in the int16 range; all scales finite
+ * and > 0.
+ *
+ * mq_add_requant -- residual add:
+ *   v = a1 * (x1 - z1) + a2 * (x2 - z2)          x1, x2 device int16 [numel]
+ */
+mq_status mq_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                         float a2, int32_t z2, int64_t numel, float ay, int32_t zy,
+                         int32_t out_bits, void* y, void* stream);
+
+/* Table operators of mq_lut_build. */
+#define MQ_LUT_SILU 1
+
+/*
+ * mq_lut_build -- a 65536-entry table of an elementwise operator on int16
+ * codes: lut[i + 32768] = code of f(ax * (i - zx)); op MQ_LUT_SILU:
+ * f(v) = v / (1 + exp(-v)).  lut: device int8 or int16 [65536] (out_bits).
+ * mq_lut_apply -- y[i] = lut[x[i] + 32768].
+ */
+mq_status mq_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t zy,
+                       int32_t out_bits, void* lut, void* stream);
+mq_status mq_lut_apply(const int16_t* x, int64_t numel, const void* lut, int32_t out_bits,
+                       void* y, void* stream);
+
+/*
+ * mq_rmsnorm -- RMSNorm over each row of K codes:
+ *   ss = sum_k (x - zx)^2 (exact),  ms = ax^2 * ss / K + eps,  r = sqrt(ms),
+ *   v = ax * (x - zx) [* gamma[k]] / r
+ *   x device int16 [M][K]; gamma device fp32 [K] or NULL; eps >= 0;
+ *   1 <= K <= 2^20.
+ */
+mq_status mq_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                     const float* gamma, float eps, float ay, int32_t zy, int32_t out_bits,
+                     void* y, void* stream);
+
+/*
+ * mq_softmax -- softmax over each row of K score codes:
+ *   e_k = exp(ax * (x_k - max_j x_j)),  p_k = e_k / sum_j e_j
+ *   x device int16 [M][K]; 1 <= K <= 2^20.  For 16-bit probabilities over
+ *   the unsigned range take ay = 1/65535, zy = -32768.
+ */
+mq_status mq_softmax(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx, float ay,
+                     int32_t zy, int32_t out_bits, void* y, void* stream);
+
+/*
  * mq_smooth_scales -- SmoothQuant's closed-form scaling vector as the
  * paper restates it (Section 3.2), for calibration:
  *   x_absmax[k] = max_m |x[m][k]|,  w_absmax[k] = max_n |w[n][k]|

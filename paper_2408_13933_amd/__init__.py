@@ -17,6 +17,7 @@ __all__ = [
     "mq_fold_acts", "mq_quantize_act", "mq_pack_weights", "mq_qlinear", "mq_dequant",
     "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum", "mq_qlinear_asym",
     "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward", "mq_arl_backward", "ARL_PARTIALS",
+    "mq_add_requant", "mq_lut_build", "mq_lut_apply", "mq_rmsnorm", "mq_softmax", "LUT_SILU",
     "mq_qlinear_workspace_bytes",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
 ]
@@ -28,6 +29,7 @@ MQ_OK, MQ_ERR_INVALID_ARG, MQ_ERR_UNSUPPORTED, MQ_ERR_HIP = 0, 1, 2, 3
 PATH_AUTO, PATH_DECODE, PATH_PREFILL, PATH_GENERIC = 0, 1, 2, 3
 MAX_K = 65536
 ARL_PARTIALS = 1024
+LUT_SILU = 1
 
 _lib = None
 
@@ -77,6 +79,12 @@ def lib():
                                        c_p]
     L.mq_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_p, c_p]
     L.mq_quantize_act_rowsum.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_p, c_p, c_p]
+    L.mq_add_requant.argtypes = [c_p, c_f, c_i32, c_p, c_f, c_i32, c_i64, c_f, c_i32, c_i32, c_p,
+                                 c_p]
+    L.mq_lut_build.argtypes = [c_i32, c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p]
+    L.mq_lut_apply.argtypes = [c_p, c_i64, c_p, c_i32, c_p, c_p]
+    L.mq_rmsnorm.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_p, c_f, c_f, c_i32, c_i32, c_p, c_p]
+    L.mq_softmax.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p]
     L.mq_smooth_scales.argtypes = [c_p, c_i64, c_i64, c_p, c_i64, c_f, c_p, c_p, c_p, c_p]
     L.mq_arl_forward.argtypes = [c_p, c_i64, c_f, c_f, c_i32, c_p, c_p]
     L.mq_arl_backward.argtypes = [c_p, c_p, c_i64, c_f, c_f, c_i32, c_p, c_p, c_p]
@@ -89,7 +97,8 @@ def lib():
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
                  "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
-                 "mq_arl_backward"):
+                 "mq_arl_backward", "mq_add_requant", "mq_lut_build", "mq_lut_apply",
+                 "mq_rmsnorm", "mq_softmax"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -296,6 +305,69 @@ def mq_qlinear_asym(a_q, a_rowsum, w_q, w_bits: int, w_scale, w_zp, w_colsum, a_
         float(a_scale), int(a_zp), float(out_scale), int(out_zp), int(out_bits), bptr,
         _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), ws, ws_bytes, int(path),
         _stream_ptr(stream)), "mq_qlinear_asym")
+    return out
+
+
+def mq_add_requant(x1, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy: int,
+                   out_bits: int = 16, out=None, stream=None):
+    """Residual add of two int16 code tensors, requantized."""
+    torch = _torch()
+    out = torch.empty(x1.shape, dtype=_act_dtype(out_bits), device=x1.device) if out is None else out
+    _check(lib().mq_add_requant(_dev_ptr(x1, torch.int16, "x1"), float(a1), int(z1),
+                                _dev_ptr(x2, torch.int16, "x2", x1.shape), float(a2), int(z2),
+                                x1.numel(), float(ay), int(zy), int(out_bits),
+                                _dev_ptr(out, _act_dtype(out_bits), "out", x1.shape),
+                                _stream_ptr(stream)), "mq_add_requant")
+    return out
+
+
+def mq_lut_build(op: int, ax: float, zx: int, ay: float, zy: int, out_bits: int = 8, lut=None,
+                 stream=None):
+    """65536-entry table of an elementwise op on int16 codes."""
+    torch = _torch()
+    lut = torch.empty(65536, dtype=_act_dtype(out_bits), device="cuda") if lut is None else lut
+    _check(lib().mq_lut_build(int(op), float(ax), int(zx), float(ay), int(zy), int(out_bits),
+                              _dev_ptr(lut, _act_dtype(out_bits), "lut", (65536,)),
+                              _stream_ptr(stream)), "mq_lut_build")
+    return lut
+
+
+def mq_lut_apply(x, lut, out=None, stream=None):
+    """y = lut[x + 32768] elementwise."""
+    torch = _torch()
+    bits = _bits_of(lut)
+    out = torch.empty(x.shape, dtype=lut.dtype, device=x.device) if out is None else out
+    _check(lib().mq_lut_apply(_dev_ptr(x, torch.int16, "x"), x.numel(),
+                              _dev_ptr(lut, lut.dtype, "lut", (65536,)), int(bits),
+                              _dev_ptr(out, lut.dtype, "out", x.shape), _stream_ptr(stream)),
+           "mq_lut_apply")
+    return out
+
+
+def mq_rmsnorm(x, ax: float, zx: int, gamma, eps: float, ay: float, zy: int, out_bits: int = 8,
+               out=None, stream=None):
+    """RMSNorm over rows of int16 codes, requantized."""
+    torch = _torch()
+    M, K = x.shape
+    out = torch.empty((M, K), dtype=_act_dtype(out_bits), device=x.device) if out is None else out
+    gptr = None if gamma is None else _dev_ptr(gamma, torch.float32, "gamma", (K,))
+    _check(lib().mq_rmsnorm(_dev_ptr(x, torch.int16, "x"), M, K, float(ax), int(zx), gptr,
+                            float(eps), float(ay), int(zy), int(out_bits),
+                            _dev_ptr(out, _act_dtype(out_bits), "out", (M, K)),
+                            _stream_ptr(stream)), "mq_rmsnorm")
+    return out
+
+
+def mq_softmax(x, ax: float, zx: int, ay: float, zy: int, out_bits: int = 16, out=None,
+               stream=None):
+    """Softmax over rows of int16 score codes, requantized."""
+    torch = _torch()
+    M, K = x.shape
+    out = torch.empty((M, K), dtype=_act_dtype(out_bits), device=x.device) if out is None else out
+    _check(lib().mq_softmax(_dev_ptr(x, torch.int16, "x"), M, K, float(ax), int(zx), float(ay),
+                            int(zy), int(out_bits),
+                            _dev_ptr(out, _act_dtype(out_bits), "out", (M, K)),
+                            _stream_ptr(stream)), "mq_softmax")
     return out
 
 

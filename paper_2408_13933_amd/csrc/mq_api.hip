@@ -136,6 +136,64 @@ mq_status mq_pack_weights_asym(const float* w, int64_t N, int64_t K, int32_t bit
                                                  w_zp, w_colsum, as_stream(stream)));
 }
 
+mq_status mq_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2, float a2,
+                         int32_t z2, int64_t numel, float ay, int32_t zy, int32_t out_bits,
+                         void* y, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || !act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(a1) || !finite_pos(a2) || !finite_pos(ay)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(z1, 16) || !zp_ok(z2, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (numel == 0) return MQ_OK;
+    if (!x1 || !x2 || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_add_requant(x1, a1, z1, x2, a2, z2, numel, ay, zy, out_bits, y,
+                                           as_stream(stream)));
+}
+
+mq_status mq_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t zy, int32_t out_bits,
+                       void* lut, void* stream)
+{
+    if (op != MQ_LUT_SILU || !act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(ax) || !finite_pos(ay)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(zx, 16) || !zp_ok(zy, out_bits) || !lut) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_lut_build(op, ax, zx, ay, zy, out_bits, lut, as_stream(stream)));
+}
+
+mq_status mq_lut_apply(const int16_t* x, int64_t numel, const void* lut, int32_t out_bits,
+                       void* y, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || !act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (numel == 0) return MQ_OK;
+    if (!x || !lut || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_lut_apply(x, numel, lut, out_bits, y, as_stream(stream)));
+}
+
+mq_status mq_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                     const float* gamma, float eps, float ay, int32_t zy, int32_t out_bits,
+                     void* y, void* stream)
+{
+    if (M < 0 || M > 0x7FFFFFFF || K < 1 || K > (1 << 20) || !act_bits_ok(out_bits))
+        return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(ax) || !finite_pos(ay) || !std::isfinite(eps) || eps < 0.0f)
+        return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(zx, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (M == 0) return MQ_OK;
+    if (!x || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_rmsnorm(x, M, K, ax, zx, gamma, eps, ay, zy, out_bits, y,
+                                       as_stream(stream)));
+}
+
+mq_status mq_softmax(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx, float ay,
+                     int32_t zy, int32_t out_bits, void* y, void* stream)
+{
+    if (M < 0 || M > 0x7FFFFFFF || K < 1 || K > (1 << 20) || !act_bits_ok(out_bits))
+        return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(ax) || !finite_pos(ay)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(zx, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (M == 0) return MQ_OK;
+    if (!x || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_softmax(x, M, K, ax, ay, zy, out_bits, y, as_stream(stream)));
+}
+
 mq_status mq_smooth_scales(const float* x, int64_t M, int64_t K, const float* w, int64_t N,
                            float a, float* x_absmax, float* w_absmax, float* s, void* stream)
 {

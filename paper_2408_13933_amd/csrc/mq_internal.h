@@ -58,6 +58,19 @@ hipError_t launch_smooth_scales(const float* x, int64_t M, int64_t K, const floa
                                 float a, float* x_absmax, float* w_absmax, float* s,
                                 hipStream_t st);
 
+hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                              float a2, int32_t z2, int64_t n, float ay, int32_t zy,
+                              int32_t bits, void* y, hipStream_t st);
+hipError_t launch_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t zy, int32_t bits,
+                            void* lut, hipStream_t st);
+hipError_t launch_lut_apply(const int16_t* x, int64_t n, const void* lut, int32_t bits, void* y,
+                            hipStream_t st);
+hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                          const float* gamma, float eps, float ay, int32_t zy, int32_t bits,
+                          void* y, hipStream_t st);
+hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
+                          int32_t bits, void* y, hipStream_t st);
+
 hipError_t launch_qlinear_generic(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s);

@@ -260,3 +260,24 @@ def test_calibration_empty_calls():
     L = mq.lib()
     assert L.mq_smooth_scales(None, 0, 0, None, 0, 0.5, None, None, None, None) == 0
     assert L.mq_arl_forward(None, 0, 0.1, 1.0, 8, None, None) == 0
+
+
+@pytest.mark.parametrize("call", [
+    lambda L: L.mq_add_requant(NZ, 0.0, 0, NZ, 1.0, 0, 10, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_add_requant(NZ, 1.0, 40000, NZ, 1.0, 0, 10, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_add_requant(NZ, 1.0, 0, NZ, 1.0, 0, 10, 1.0, 200, 8, NZ, None),
+    lambda L: L.mq_add_requant(NZ, 1.0, 0, None, 1.0, 0, 10, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_lut_build(2, 1.0, 0, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_lut_build(1, 1.0, 0, 1.0, 0, 8, None, None),
+    lambda L: L.mq_lut_build(1, float("nan"), 0, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_lut_apply(NZ, 10, None, 8, NZ, None),
+    lambda L: L.mq_lut_apply(NZ, 10, NZ, 4, NZ, None),
+    lambda L: L.mq_rmsnorm(NZ, 4, 0, 1.0, 0, None, 0.0, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_rmsnorm(NZ, 4, 8, 1.0, 0, None, -1.0, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_rmsnorm(NZ, 4, 8, 1.0, 0, None, 0.0, 0.0, 0, 8, NZ, None),
+    lambda L: L.mq_softmax(NZ, 4, 0, 1.0, 0, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_softmax(NZ, 4, 8, 1.0, 0, 1.0, 0, 16, None, None),
+    lambda L: L.mq_softmax(NZ, -1, 8, 1.0, 0, 1.0, 0, 16, NZ, None),
+])
+def test_glue_entry_points_reject_invalid_arguments(call):
+    assert call(mq.lib()) == 1
