@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--calib-sweep", action="store_true",
                     help="time the calibration-side kernels (range learning, SmoothQuant "
                          "scales) instead of the step")
+    ap.add_argument("--glue-sweep", action="store_true",
+                    help="time the decoder-block glue kernels (residual add, SiLU lookup, "
+                         "RMSNorm, softmax) instead of the step")
     ap.add_argument("--decode-sweep", action="store_true",
                     help="time the decode-shaped layers (M <= 16) cold: each launch reads a "
                          "different copy of the weights, >= 512 MB per sweep; prints one JSON "
@@ -457,10 +460,83 @@ def calib_sweep(reps=5, per_graph=10):
                           "GB/s": round(gbs, 1), "frac_hbm": round(gbs / 8000.0, 3)}), flush=True)
 
 
+def _time_graph(fn, reps=5, per_graph=10):
+    """Per-launch time of fn from a HIP graph of `per_graph` launches."""
+    import torch
+
+    fn()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(graph, stream=cap):
+            for _ in range(per_graph):
+                fn()
+    torch.cuda.current_stream().wait_stream(cap)
+    graph.replay()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        graph.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) * 1e3 / (reps * per_graph)
+
+
+def glue_sweep():
+    """The decoder-block glue at TinyLlama shapes, seq 1024: residual add on
+    the 1024x2048 hidden state (int16 + int16 -> int16), SiLU lookup on the
+    1024x5632 gate output (int16 -> int8), RMSNorm 1024x2048 (int16 -> int8),
+    softmax over 32 heads x 1024 x 1024 scores (int16 -> int16).  Codes are
+    uniform random int16 from torch's seeded generator."""
+    import torch
+
+    import paper_2408_13933_amd as mq
+
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+
+    def codes(*shape):
+        return torch.randint(-32768, 32768, shape, dtype=torch.int32, device=dev,
+                             generator=g).to(torch.int16)
+
+    h1, h2 = codes(1024, 2048), codes(1024, 2048)
+    gate = codes(1024, 5632)
+    scores = codes(32 * 1024, 1024)
+    lut = mq.mq_lut_build(mq.LUT_SILU, 1e-3, 0, 0.05, 0, 8)
+    gamma = torch.ones(2048, device=dev)
+    out16 = torch.empty_like(h1)
+    out8 = torch.empty((1024, 2048), dtype=torch.int8, device=dev)
+    g8 = torch.empty((1024, 5632), dtype=torch.int8, device=dev)
+    p16 = torch.empty_like(scores)
+    ops = {
+        "add_requant": (lambda: mq.mq_add_requant(h1, 3e-4, 0, h2, 5e-4, 0, 6e-4, 0, 16,
+                                                  out=out16), 6 * h1.numel(), [1024, 2048]),
+        "silu_lookup": (lambda: mq.mq_lut_apply(gate, lut, out=g8), 3 * gate.numel(),
+                        [1024, 5632]),
+        "rmsnorm": (lambda: mq.mq_rmsnorm(h1, 3e-4, 0, gamma, 1e-5, 0.02, 0, 8, out=out8),
+                    3 * h1.numel() + 4 * 2048, [1024, 2048]),
+        "softmax": (lambda: mq.mq_softmax(scores, 1e-3, 0, 1.0 / 65535, -32768, 16, out=p16),
+                    4 * scores.numel(), [32 * 1024, 1024]),
+    }
+    for name, (fn, nbytes, shape) in ops.items():
+        us = _time_graph(fn)
+        gbs = nbytes / us / 1e3
+        print(json.dumps({"op": name, "shape": shape, "us_graph_replay": round(us, 2),
+                          "alg_bytes": nbytes, "GB/s": round(gbs, 1),
+                          "frac_hbm": round(gbs / 8000.0, 3)}), flush=True)
+
+
 def main():
     args = parse()
     if args.calib_sweep:
         calib_sweep()
+        return
+    if args.glue_sweep:
+        glue_sweep()
         return
     if args.decode_sweep:
         decode_sweep()

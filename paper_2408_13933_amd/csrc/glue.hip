@@ -47,17 +47,39 @@ __device__ inline void store_code(void* y, int64_t i, int32_t v)
 // ---------------------------------------------------------------------------
 // Residual add: v = alpha_1 (x1 - zp_1) + alpha_2 (x2 - zp_2), requantized.
 template <int BITS>
-__global__ __launch_bounds__(kThreads) void add_requant_kernel(
-    const int16_t* __restrict__ x1, float a1, int32_t z1, const int16_t* __restrict__ x2,
-    float a2, int32_t z2, int64_t n, float ay, int32_t zy, void* __restrict__ y)
+__device__ inline int32_t add_one(int32_t u, int32_t v, float a1, int32_t z1, float a2,
+                                  int32_t z2, float ay, int32_t zy)
 {
 #pragma clang fp contract(off)
+    const double s = (double)a1 * (double)(u - z1) + (double)a2 * (double)(v - z2);
+    return requant_f64<BITS>(s, (double)ay, zy);
+}
+
+// n4 groups of four codes through 8-byte loads (aligned buffers), the
+// codes [begin, n) one by one
+template <int BITS>
+__global__ __launch_bounds__(kThreads) void add_requant_kernel(
+    const int16_t* __restrict__ x1, float a1, int32_t z1, const int16_t* __restrict__ x2,
+    float a2, int32_t z2, int64_t n4, int64_t begin, int64_t n, float ay, int32_t zy,
+    void* __restrict__ y)
+{
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) {
-        const double v = (double)a1 * (double)((int32_t)x1[i] - z1) +
-                         (double)a2 * (double)((int32_t)x2[i] - z2);
-        store_code<BITS>(y, i, requant_f64<BITS>(v, (double)ay, zy));
+    const int64_t t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    for (int64_t i = t0; i < n4; i += stride) {
+        const short4 u = reinterpret_cast<const short4*>(x1)[i];
+        const short4 v = reinterpret_cast<const short4*>(x2)[i];
+        const int32_t r0 = add_one<BITS>(u.x, v.x, a1, z1, a2, z2, ay, zy);
+        const int32_t r1 = add_one<BITS>(u.y, v.y, a1, z1, a2, z2, ay, zy);
+        const int32_t r2 = add_one<BITS>(u.z, v.z, a1, z1, a2, z2, ay, zy);
+        const int32_t r3 = add_one<BITS>(u.w, v.w, a1, z1, a2, z2, ay, zy);
+        if constexpr (BITS == 8)
+            reinterpret_cast<char4*>(y)[i] = make_char4((char)r0, (char)r1, (char)r2, (char)r3);
+        else
+            reinterpret_cast<short4*>(y)[i] =
+                make_short4((short)r0, (short)r1, (short)r2, (short)r3);
     }
+    for (int64_t i = begin + t0; i < n; i += stride)
+        store_code<BITS>(y, i, add_one<BITS>(x1[i], x2[i], a1, z1, a2, z2, ay, zy));
 }
 
 // ---------------------------------------------------------------------------
@@ -75,19 +97,54 @@ __global__ __launch_bounds__(kThreads) void lut_build_kernel(int32_t op, float a
     store_code<BITS>(lut, idx, requant_f64<BITS>(f, (double)ay, zy));
 }
 
-// y[i] = lut[x[i] + 32768]; the table stays in the L1/L2 caches.
+// y[i] = lut[x[i] + 32768].  The table (64 or 128 KiB) is copied into LDS
+// once per block, and each block then streams many codes: 8 per thread
+// per trip through 16-byte loads when the buffers are aligned.
+constexpr int kLutThreads = 1024;
+
 template <int BITS>
-__global__ __launch_bounds__(kThreads) void lut_apply_kernel(const int16_t* __restrict__ x,
-                                                             int64_t n,
-                                                             const void* __restrict__ lut,
-                                                             void* __restrict__ y)
+__global__ __launch_bounds__(kLutThreads) void lut_apply_kernel(const int16_t* __restrict__ x,
+                                                                int64_t n8, int64_t begin,
+                                                                int64_t n,
+                                                                const void* __restrict__ lut,
+                                                                void* __restrict__ y)
 {
     using T = typename std::conditional<BITS == 8, int8_t, int16_t>::type;
-    const T* t = static_cast<const T*>(lut);
+    extern __shared__ __align__(16) int8_t lds_table[];
+    T* tab = reinterpret_cast<T*>(lds_table);
+    {
+        const int4* src = static_cast<const int4*>(lut);
+        int4* dst = reinterpret_cast<int4*>(lds_table);
+        constexpr int chunks = 65536 * sizeof(T) / 16;
+        for (int i = threadIdx.x; i < chunks; i += kLutThreads) dst[i] = src[i];
+    }
+    __syncthreads();
     T* out = static_cast<T*>(y);
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride)
-        out[i] = t[(int32_t)x[i] + 32768];
+    const int64_t stride = (int64_t)gridDim.x * kLutThreads;
+    const int64_t t0 = (int64_t)blockIdx.x * kLutThreads + threadIdx.x;
+    for (int64_t i = t0; i < n8; i += stride) {
+        const int4 v = reinterpret_cast<const int4*>(x)[i];
+        const int16_t* c = reinterpret_cast<const int16_t*>(&v);
+        T r[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) r[u] = tab[(int32_t)c[u] + 32768];
+        if constexpr (BITS == 8) {
+            uint2 o;
+            o.x = ((uint32_t)(uint8_t)r[0]) | ((uint32_t)(uint8_t)r[1] << 8) |
+                  ((uint32_t)(uint8_t)r[2] << 16) | ((uint32_t)(uint8_t)r[3] << 24);
+            o.y = ((uint32_t)(uint8_t)r[4]) | ((uint32_t)(uint8_t)r[5] << 8) |
+                  ((uint32_t)(uint8_t)r[6] << 16) | ((uint32_t)(uint8_t)r[7] << 24);
+            reinterpret_cast<uint2*>(out)[i] = o;
+        } else {
+            int4 o;
+            o.x = (int)(((uint32_t)(uint16_t)r[0]) | ((uint32_t)(uint16_t)r[1] << 16));
+            o.y = (int)(((uint32_t)(uint16_t)r[2]) | ((uint32_t)(uint16_t)r[3] << 16));
+            o.z = (int)(((uint32_t)(uint16_t)r[4]) | ((uint32_t)(uint16_t)r[5] << 16));
+            o.w = (int)(((uint32_t)(uint16_t)r[6]) | ((uint32_t)(uint16_t)r[7] << 16));
+            reinterpret_cast<int4*>(out)[i] = o;
+        }
+    }
+    for (int64_t i = begin + t0; i < n; i += stride) out[i] = tab[(int32_t)x[i] + 32768];
 }
 
 // ---------------------------------------------------------------------------
@@ -102,6 +159,140 @@ __device__ inline int64_t block_sum_i64(int64_t v, int64_t* red)
     for (int w = 0; w < kThreads / 64; ++w) t += red[w];
     __syncthreads();
     return t;
+}
+
+// Rows of at most 8 * 256 * NCH codes with K % 8 == 0 and 16-byte aligned
+// rows stay in registers: chunk c of thread t holds codes
+// 8 (t + 256 c) .. +7, read once with a 16-byte load.
+// Eight codes to y[i .. i+7] with one 8-byte (int8) or 16-byte (int16)
+// store; i is a multiple of 8 and y is 16-byte aligned.
+template <int BITS>
+__device__ inline void store8(void* y, int64_t i, const int32_t* q)
+{
+    if constexpr (BITS == 8) {
+        uint2 o;
+        o.x = ((uint32_t)(uint8_t)q[0]) | ((uint32_t)(uint8_t)q[1] << 8) |
+              ((uint32_t)(uint8_t)q[2] << 16) | ((uint32_t)(uint8_t)q[3] << 24);
+        o.y = ((uint32_t)(uint8_t)q[4]) | ((uint32_t)(uint8_t)q[5] << 8) |
+              ((uint32_t)(uint8_t)q[6] << 16) | ((uint32_t)(uint8_t)q[7] << 24);
+        *reinterpret_cast<uint2*>(static_cast<int8_t*>(y) + i) = o;
+    } else {
+        int4 o;
+        o.x = (int)(((uint32_t)(uint16_t)q[0]) | ((uint32_t)(uint16_t)q[1] << 16));
+        o.y = (int)(((uint32_t)(uint16_t)q[2]) | ((uint32_t)(uint16_t)q[3] << 16));
+        o.z = (int)(((uint32_t)(uint16_t)q[4]) | ((uint32_t)(uint16_t)q[5] << 16));
+        o.w = (int)(((uint32_t)(uint16_t)q[6]) | ((uint32_t)(uint16_t)q[7] << 16));
+        *reinterpret_cast<int4*>(static_cast<int16_t*>(y) + i) = o;
+    }
+}
+
+template <int NCH>
+struct RowRegs {
+    int16_t v[NCH][8];
+    bool live[NCH];
+    __device__ void load(const int16_t* row, int64_t K)
+    {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int64_t k0 = 8 * ((int64_t)threadIdx.x + kThreads * c);
+            live[c] = k0 < K;
+            int4 q = {0, 0, 0, 0};
+            if (live[c]) q = *reinterpret_cast<const int4*>(row + k0);
+            const int16_t* e = reinterpret_cast<const int16_t*>(&q);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[c][u] = e[u];
+        }
+    }
+};
+
+template <int BITS, int NCH>
+__global__ __launch_bounds__(kThreads) void rmsnorm_regs_kernel(const int16_t* __restrict__ x,
+                                                                int64_t K, float ax, int32_t zx,
+                                                                const float* __restrict__ gamma,
+                                                                float eps, float ay, int32_t zy,
+                                                                void* __restrict__ y)
+{
+#pragma clang fp contract(off)
+    __shared__ int64_t red[kThreads / 64];
+    const int64_t m = blockIdx.x;
+    RowRegs<NCH> r;
+    r.load(x + m * K, K);
+    int64_t ss = 0;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+        if (r.live[c])
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int64_t d = (int64_t)r.v[c][u] - zx;
+                ss += d * d;
+            }
+    ss = block_sum_i64(ss, red);
+    const double a = (double)ax;
+    const double ms = a * a * (double)ss / (double)K + (double)eps;
+    const double rt = sqrt(ms);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (!r.live[c]) continue;
+        const int64_t k0 = 8 * ((int64_t)threadIdx.x + kThreads * c);
+        int32_t q[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            double v = a * (double)((int64_t)r.v[c][u] - zx);
+            if (gamma) v = v * (double)gamma[k0 + u];
+            v = v / rt;
+            q[u] = requant_f64<BITS>(v, (double)ay, zy);
+        }
+        store8<BITS>(y, m * K + k0, q);
+    }
+}
+
+template <int BITS, int NCH>
+__global__ __launch_bounds__(kThreads) void softmax_regs_kernel(const int16_t* __restrict__ x,
+                                                                int64_t K, float ax, float ay,
+                                                                int32_t zy, void* __restrict__ y)
+{
+#pragma clang fp contract(off)
+    __shared__ int32_t red_i[kThreads / 64];
+    __shared__ double red_d[kThreads / 64];
+    const int64_t m = blockIdx.x;
+    RowRegs<NCH> r;
+    r.load(x + m * K, K);
+    int32_t mx = -32768;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+        if (r.live[c])
+#pragma unroll
+            for (int u = 0; u < 8; ++u) mx = max(mx, (int32_t)r.v[c][u]);
+    for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o));
+    if ((threadIdx.x & 63) == 0) red_i[threadIdx.x >> 6] = mx;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) mx = max(mx, red_i[w]);
+    const double a = (double)ax;
+    double e[NCH][8];
+    double sum = 0.0;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            e[c][u] = r.live[c] ? exp(a * (double)((int32_t)r.v[c][u] - mx)) : 0.0;
+            sum += e[c][u];
+        }
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    if ((threadIdx.x & 63) == 0) red_d[threadIdx.x >> 6] = sum;
+    __syncthreads();
+    sum = 0.0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) sum += red_d[w];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (!r.live[c]) continue;
+        const int64_t k0 = 8 * ((int64_t)threadIdx.x + kThreads * c);
+        int32_t q[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) q[u] = requant_f64<BITS>(e[c][u] / sum, (double)ay, zy);
+        store8<BITS>(y, m * K + k0, q);
+    }
 }
 
 // RMSNorm: ss = sum (x - zp_x)^2 (exact, int64); ms = alpha^2 ss / K + eps;
@@ -174,11 +365,17 @@ hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int
                               float a2, int32_t z2, int64_t n, float ay, int32_t zy,
                               int32_t bits, void* y, hipStream_t st)
 {
-    const int g = grid_for(n, kThreads * 4, 256 * 64);
+    const uintptr_t ya = bits == 8 ? 4 : 8;
+    const bool vec = ((uintptr_t)x1 % 8) == 0 && ((uintptr_t)x2 % 8) == 0 &&
+                     ((uintptr_t)y % ya) == 0;
+    const int64_t n4 = vec ? n / 4 : 0;
+    const int g = grid_for(vec ? n4 : n, kThreads * 2, 256 * 64);
     if (bits == 8)
-        add_requant_kernel<8><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n, ay, zy, y);
+        add_requant_kernel<8><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n4, n4 * 4, n, ay,
+                                                      zy, y);
     else
-        add_requant_kernel<16><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n, ay, zy, y);
+        add_requant_kernel<16><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n4, n4 * 4, n, ay,
+                                                       zy, y);
     return hipGetLastError();
 }
 
@@ -193,16 +390,72 @@ hipError_t launch_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t 
 hipError_t launch_lut_apply(const int16_t* x, int64_t n, const void* lut, int32_t bits, void* y,
                             hipStream_t st)
 {
-    const int g = grid_for(n, kThreads * 4, 256 * 64);
-    if (bits == 8) lut_apply_kernel<8><<<g, kThreads, 0, st>>>(x, n, lut, y);
-    else lut_apply_kernel<16><<<g, kThreads, 0, st>>>(x, n, lut, y);
+    // one or two blocks per CU (the table fills 64 or 128 KiB of LDS), each
+    // streaming at least 32 codes per thread
+    const uintptr_t ya = bits == 8 ? 8 : 16;
+    const bool vec = ((uintptr_t)x % 16) == 0 && ((uintptr_t)y % ya) == 0 &&
+                     ((uintptr_t)lut % 16) == 0;
+    const int64_t n8 = vec ? n / 8 : 0;
+    const int cap = bits == 8 ? 512 : 256;
+    const int g = grid_for(n, kLutThreads * 32, cap);
+    const size_t lds = 65536 * (bits / 8);
+    if (bits == 8) {
+        static const hipError_t a8 = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&lut_apply_kernel<8>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (a8 != hipSuccess) return a8;
+        lut_apply_kernel<8><<<g, kLutThreads, lds, st>>>(x, n8, n8 * 8, n, lut, y);
+    } else {
+        static const hipError_t a16 = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&lut_apply_kernel<16>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (a16 != hipSuccess) return a16;
+        lut_apply_kernel<16><<<g, kLutThreads, lds, st>>>(x, n8, n8 * 8, n, lut, y);
+    }
     return hipGetLastError();
+}
+
+template <int BITS, int NCH>
+void rmsnorm_regs(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                  const float* gamma, float eps, float ay, int32_t zy, void* y, hipStream_t st)
+{
+    rmsnorm_regs_kernel<BITS, NCH><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, zx, gamma, eps, ay,
+                                                                    zy, y);
+}
+
+template <int BITS, int NCH>
+void softmax_regs(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy, void* y,
+                  hipStream_t st)
+{
+    softmax_regs_kernel<BITS, NCH><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, y);
+}
+
+// register-resident rows: K % 8 == 0, 16-byte aligned x and y, chunks per
+// thread (0: the strided kernel)
+static int row_chunks(const int16_t* x, const void* y, int64_t K)
+{
+    if (K % 8 != 0 || ((uintptr_t)x % 16) != 0 || ((uintptr_t)y % 16) != 0) return 0;
+    const int64_t ch = (K / 8 + kThreads - 1) / kThreads;
+    return ch <= 1 ? 1 : ch <= 2 ? 2 : ch <= 4 ? 4 : 0;
 }
 
 hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
                           const float* gamma, float eps, float ay, int32_t zy, int32_t bits,
                           void* y, hipStream_t st)
 {
+    const int ch = row_chunks(x, y, K);
+    if (ch > 0) {
+        if (bits == 8) {
+            if (ch == 1) rmsnorm_regs<8, 1>(x, M, K, ax, zx, gamma, eps, ay, zy, y, st);
+            else if (ch == 2) rmsnorm_regs<8, 2>(x, M, K, ax, zx, gamma, eps, ay, zy, y, st);
+            else rmsnorm_regs<8, 4>(x, M, K, ax, zx, gamma, eps, ay, zy, y, st);
+        } else {
+            if (ch == 1) rmsnorm_regs<16, 1>(x, M, K, ax, zx, gamma, eps, ay, zy, y, st);
+            else if (ch == 2) rmsnorm_regs<16, 2>(x, M, K, ax, zx, gamma, eps, ay, zy, y, st);
+            else rmsnorm_regs<16, 4>(x, M, K, ax, zx, gamma, eps, ay, zy, y, st);
+        }
+        return hipGetLastError();
+    }
     if (bits == 8)
         rmsnorm_kernel<8><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, zx, gamma, eps, ay, zy, y);
     else
@@ -213,6 +466,19 @@ hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int3
 hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
                           int32_t bits, void* y, hipStream_t st)
 {
+    const int ch = row_chunks(x, y, K);
+    if (ch > 0) {
+        if (bits == 8) {
+            if (ch == 1) softmax_regs<8, 1>(x, M, K, ax, ay, zy, y, st);
+            else if (ch == 2) softmax_regs<8, 2>(x, M, K, ax, ay, zy, y, st);
+            else softmax_regs<8, 4>(x, M, K, ax, ay, zy, y, st);
+        } else {
+            if (ch == 1) softmax_regs<16, 1>(x, M, K, ax, ay, zy, y, st);
+            else if (ch == 2) softmax_regs<16, 2>(x, M, K, ax, ay, zy, y, st);
+            else softmax_regs<16, 4>(x, M, K, ax, ay, zy, y, st);
+        }
+        return hipGetLastError();
+    }
     if (bits == 8) softmax_kernel<8><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, y);
     else softmax_kernel<16><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, y);
     return hipGetLastError();
