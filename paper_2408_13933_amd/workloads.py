@@ -97,6 +97,19 @@ def _tinyllama_block(M: int, asym: bool = False, a_bits: int = 8):
     )
 
 
+def _tinyllama_block_fused(M: int):
+    # q/k/v as one 2560-channel GEMM and gate/up as one 11264-channel GEMM,
+    # each with one joint output range (the fused layers share a per-tensor
+    # output format)
+    L = dict(out_bits=16, bias=False)
+    return (
+        Layer("qkv_proj", M, 2048, 2560, smooth="attn_norm", smooth_len=2048, **L),
+        Layer("o_proj", M, 2048, 2048, smooth="v_to_o", smooth_len=256, **L),
+        Layer("gate_up_proj", M, 2048, 11264, smooth="mlp_norm", smooth_len=2048, **L),
+        Layer("down_proj", M, 5632, 2048, smooth="up_to_down", smooth_len=5632, **L),
+    )
+
+
 WORKLOADS = {
     "decode_w8a8_m16": Workload(
         "decode_w8a8_m16",
@@ -121,6 +134,11 @@ WORKLOADS = {
         "intermediate-5632 decoder block at batch 1, seq 1024, W8A8 with "
         "folded smoothing vectors, int8 in, int16 out",
         _tinyllama_block(1024)),
+    "block_w8a8_fused_tinyllama_s1024": Workload(
+        "block_w8a8_fused_tinyllama_s1024",
+        "the same decoder block with q/k/v fused into one N=2560 GEMM and gate/up "
+        "into one N=11264 GEMM (one output range each)",
+        _tinyllama_block_fused(1024)),
     "block_w8a8_asym_tinyllama_s1024": Workload(
         "block_w8a8_asym_tinyllama_s1024",
         "the same decoder block in the paper's main W8A8 setting: asymmetric "
@@ -273,9 +291,9 @@ def _w_name(layer: Layer) -> str:
 
 def _x_key(workload: str, layer: Layer):
     name = _w_name(layer)
-    if name in ("q_proj", "k_proj", "v_proj"):
+    if name in ("q_proj", "k_proj", "v_proj", "qkv_proj"):
         name = "qkv_in"
-    if name in ("gate_proj", "up_proj"):
+    if name in ("gate_proj", "up_proj", "gate_up_proj"):
         name = "mlp_in"
     return (workload, name)
 
