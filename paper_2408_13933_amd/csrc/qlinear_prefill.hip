@@ -876,6 +876,17 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
 template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2, 1>;
 template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2, 4>;
 template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
+// 192 tokens x 256 channels: 3/4 of the 256x256 tile's work per block, so a
+// layer whose 256x256 tiles leave CUs idle (2048 x 5632: 176 tiles on 256
+// CUs) fills more of the chip (242 tiles).  Eight waves, two per SIMD, each
+// 96 tokens x 64 channels: while one wave of a SIMD waits (stage barrier,
+// LDS reads, DMA issue) the other keeps the matrix core busy, and the two
+// interleave their epilogues (measured on MI355X: ~9% faster than four
+// waves of 96 x 128).  int4 weights keep four waves: their smaller stages
+// leave no room for eight waves' staged stores.
+template <int WB, int OB>
+using T192x256 = std::conditional_t<WB == 8, Cfg<WB, OB, 192, 256, 2, 4, 64, 4, 2, 1>,
+                                    Cfg<WB, OB, 192, 256, 2, 2, 64, 4, 2, 1>>;
 // 16-bit activation codes: 128x128 tokens x channels, 64 k per stage (128
 // bytes of each activation row), DMA spread over both steps of a stage
 template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16>;
@@ -890,7 +901,11 @@ constexpr TileModel kTiles[] = {
     {256, 256, 64, 6500, 1450, 9800},
     {256, 128, 128, 6000, 1500, 6000},
     {128, 128, 128, 5300, 980, 3300},
+    {192, 256, 64, 5600, 990, 4600},  // eight waves (int8 weights)
 };
+// the 192x256 tile with int4 weights runs four waves
+constexpr TileModel kTile192x256W4 = {192, 256, 64, 7000, 1175, 8300};
+constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 // A split adds round trips to memory (partial stores, the counter, the
 // partial loads) and moves every slice's int32 tile through memory and back
 // (write-through, read around the caches): ~4 TB/s, about 2 KB per cycle
@@ -913,11 +928,11 @@ Choice choose(const QLinearArgs& p, bool can_split)
     int only = -1;
     if (const char* e = std::getenv("MQ_PREFILL_TILE")) {
         const int v = std::atoi(e);
-        if (v >= 0 && v <= 2) only = v;
+        if (v >= 0 && v < kNumTiles) only = v;
     }
-    for (int c = 0; c < 3; ++c) {
+    for (int c = 0; c < kNumTiles; ++c) {
         if (only >= 0 && c != only) continue;
-        const TileModel& t = kTiles[c];
+        const TileModel& t = c == 3 && p.w_bits == 4 ? kTile192x256W4 : kTiles[c];
         const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn);
         const int64_t kt = (p.K + t.bk - 1) / t.bk;
         const bool tile_splits = t.tm * t.tn < 256 * 256;  // Cfg::SPLITK
@@ -957,6 +972,7 @@ hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
     switch (ch.tile) {
     case 0: return launch_cfg<T256x256<WB, OB>, ASYM>(p, ch.splits, s);
     case 1: return launch_cfg<T256x128<WB, OB>, ASYM>(p, ch.splits, s);
+    case 3: return launch_cfg<T192x256<WB, OB>, ASYM>(p, ch.splits, s);
     default: return launch_cfg<T128x128<WB, OB>, ASYM>(p, ch.splits, s);
     }
 }

@@ -268,7 +268,7 @@ def test_extreme_accumulators_at_max_k(w_bits):
             assert np.array_equal(y.cpu().numpy(), ref), (M, path, a_zp)
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "2"])
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3"])
 @pytest.mark.parametrize("asym", [False, True])
 def test_prefill_epilogue_forms(tile, asym, monkeypatch):
     """Every epilogue form of every prefill tile: per-column rescale factors
