@@ -403,6 +403,55 @@ mq_status mq_arl_backward(const float* x, const float* g, int64_t numel, float a
                           void* stream);
 
 /*
+ * mq_attn_matmul -- the batched integer matmuls of self-attention.  In the
+ * W8A16 setting (Section 5.6) the attention products multiply 16-bit by
+ * 8-bit activation codes; both operands are per-tensor quantized
+ * activations (Eq.(2)-(4)) with their own zero-points.  For every head h
+ * in [0, H), with group g = h / (H / G) (grouped-query attention: G heads
+ * of keys and values):
+ *   c[h][m][n] = sat_int32( sum_k (A[h][m][k] - a_zp) * (B[g][n][k] - b_zp) )
+ * (the sum exact), then the requant of mq_qlinear with
+ * M = a_scale * b_scale / out_scale and no bias.
+ *   Q K^T: A = query codes (m = query token, k = head dimension), B = key
+ *          codes (n = key token).
+ *   P V:   A = probability codes (k = key token), B = value codes in the
+ *          [group][head dimension][token] layout (mq_transpose_i8 of the
+ *          [token][G * head dimension] value matrix).
+ *   a         device int16; element (h, m, k) at a[h * a_hs + m * lda + k]
+ *   b         device int8;  element (g, n, k) at b[g * b_hs + n * ldb + k]
+ *   y         device int8 (out_bits 8) or int16 (16); element (h, m, n) at
+ *             y[h * y_hs + m * ldy + n]
+ *   H >= 1, G >= 1, H % G == 0; M, N >= 0 (0 -> nothing to do);
+ *   1 <= K <= MQ_MAX_K; lda, ldb >= K; ldy >= N; strides >= 0, in elements
+ *   a_zp in [-32768, 32767], b_zp in [-128, 127], out_zp in the range of
+ *   out_bits; scales finite and > 0
+ *   workspace  device, 256-byte aligned, >= mq_attn_matmul_workspace_bytes
+ *              bytes; overwritten with the per-row zero-point terms, the
+ *              per-row sums of B and b_scale (calls that may run
+ *              concurrently must not share it)
+ *   path       MQ_PATH_AUTO (tiled MFMA kernel for M > 16 when the strides
+ *              keep 16-byte aligned rows, else the generic kernel),
+ *              MQ_PATH_PREFILL or MQ_PATH_GENERIC
+ * Errors: MQ_ERR_INVALID_ARG for any violation above.
+ */
+int64_t mq_attn_matmul_workspace_bytes(int32_t H, int32_t G, int64_t M, int64_t N);
+mq_status mq_attn_matmul(const int16_t* a, int64_t lda, int64_t a_hs, int32_t H,
+                         const int8_t* b, int64_t ldb, int64_t b_hs, int32_t G, int64_t M,
+                         int64_t N, int64_t K, float a_scale, int32_t a_zp, float b_scale,
+                         int32_t b_zp, float out_scale, int32_t out_zp, int32_t out_bits,
+                         void* y, int64_t ldy, int64_t y_hs, void* workspace,
+                         int64_t workspace_bytes, int32_t path, void* stream);
+
+/*
+ * mq_transpose_i8 -- y[c][r] = x[r][c] for an int8 [rows][cols] matrix with
+ * row stride ldx (elements); y is dense [cols][rows].  Lays the value codes
+ * out as the B operand of the P V product in mq_attn_matmul.
+ *   0 <= rows <= 65535 * 64, cols >= 0, ldx >= cols; x, y device.
+ */
+mq_status mq_transpose_i8(const int8_t* x, int64_t rows, int64_t cols, int64_t ldx,
+                          int8_t* y, void* stream);
+
+/*
  * mq_dequant -- inverse of Eq.(4): y = alpha * (float)(q - zp), one exact
  * integer subtraction and one fp32 multiply.
  *   q      device int8 (bits 8) or int16 (bits 16) [numel]

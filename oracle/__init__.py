@@ -410,6 +410,33 @@ def qlinear(a_q: np.ndarray, w_q: np.ndarray, bits: int, w_scale: np.ndarray,
     return y
 
 
+def attn_matmul(a: np.ndarray, b: np.ndarray, a_scale: float, a_zp: int, b_scale: float,
+                b_zp: int, out_scale: float, out_zp: int, bits_y: int,
+                nthreads: int | None = None) -> np.ndarray:
+    """Batched matmul of self-attention between 16-bit and 8-bit activation
+    codes (Section 5.6: the W8A16 setting multiplies 8-bit by 16-bit
+    activations in the attention products), both per-tensor quantized
+    (Eq.(2)-(4)) with their own zero-points.  For head h, with the G groups
+    of b shared by H / G consecutive heads:
+        Y[h] = requant( (A[h] - a_zp) (B[h // (H / G)] - b_zp)^T )
+    with the rescale a_scale * b_scale / out_scale and no bias: the integer
+    linear layer of `qlinear`, with b as per-tensor asymmetric "weights".
+    a: int16 [H][M][K], b: int8 [G][N][K] -> [H][M][N]."""
+    a = np.asarray(a)
+    b = np.asarray(b)
+    assert a.dtype == np.int16 and b.dtype == np.int8 and a.ndim == 3 and b.ndim == 3
+    H, M, K = a.shape
+    G, N, Kb = b.shape
+    assert Kb == K and G >= 1 and H % G == 0
+    y = np.empty((H, M, N), dtype=_act_dtype(bits_y))
+    w_scale = np.full(N, b_scale, dtype=np.float32)
+    w_zp = np.full(N, b_zp, dtype=np.int32)
+    for h in range(H):
+        y[h] = qlinear(a[h], b[h // (H // G)], 8, w_scale, a_scale, a_zp, out_scale, out_zp,
+                       bits_y, nthreads=nthreads, w_zp=w_zp)
+    return y
+
+
 def int_matmul(a_q: np.ndarray, w_q: np.ndarray, bits: int) -> np.ndarray:
     """sum_k A_q[m][k] * W_q[n][k], exact, int64 [M][N]."""
     a_q = np.ascontiguousarray(a_q, dtype=np.int8)

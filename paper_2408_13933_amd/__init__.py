@@ -93,7 +93,13 @@ def lib():
     L.mq_qlinear_asym.argtypes = [c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_p,
                                   c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p, c_p, c_i64, c_i32,
                                   c_p]
-    for name in ("mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
+    L.mq_attn_matmul_workspace_bytes.argtypes = [c_i32, c_i32, c_i64, c_i64]
+    L.mq_attn_matmul_workspace_bytes.restype = ctypes.c_int64
+    L.mq_attn_matmul.argtypes = [c_p, c_i64, c_i64, c_i32, c_p, c_i64, c_i64, c_i32, c_i64, c_i64,
+                                 c_i64, c_f, c_i32, c_f, c_i32, c_f, c_i32, c_i32, c_p, c_i64,
+                                 c_i64, c_p, c_i64, c_i32, c_p]
+    L.mq_transpose_i8.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_p]
+    for name in ("mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
                  "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
@@ -437,6 +443,74 @@ def mq_qlinear_a16(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_z
         float(out_scale), int(out_zp), int(out_bits), bptr,
         _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), int(path), _stream_ptr(stream)),
         "mq_qlinear_a16")
+    return out
+
+
+def _strided3(t, dtype, name, shape=None):
+    """Pointer and (batch, row) element strides of a [batch][rows][cols] view
+    whose last dimension is contiguous."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != 3 or (t.shape[2] > 1 and t.stride(2) != 1):
+        raise ValueError(f"{name} must be a 3-d view with a contiguous last dimension")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    bs, rs = t.stride(0), t.stride(1)
+    if t.shape[1] <= 1:
+        rs = max(rs, t.shape[2])
+    return ctypes.c_void_p(t.data_ptr()), int(bs), int(rs)
+
+
+def mq_attn_matmul_workspace_bytes(H: int, G: int, M: int, N: int) -> int:
+    n = lib().mq_attn_matmul_workspace_bytes(int(H), int(G), int(M), int(N))
+    if n < 0:
+        raise ValueError(f"mq_attn_matmul_workspace_bytes: invalid shape {(H, G, M, N)}")
+    return n
+
+
+def mq_attn_matmul(a, b, a_scale: float, a_zp: int, b_scale: float, b_zp: int,
+                   out_scale: float, out_zp: int, out_bits: int = 16, out=None, workspace=None,
+                   path: int = PATH_AUTO, stream=None):
+    """Batched attention matmul between 16-bit codes a [H][M][K] and 8-bit
+    codes b [G][N][K] (views with a contiguous last dimension; head h uses
+    b[h // (H // G)]) -> y [H][M][N]."""
+    torch = _torch()
+    H, M, K = a.shape
+    G, N, Kb = b.shape
+    if Kb != K:
+        raise ValueError("a and b must share K")
+    pa, a_hs, lda = _strided3(a, torch.int16, "a")
+    pb, b_hs, ldb = _strided3(b, torch.int8, "b")
+    if out is None:
+        out = torch.empty((H, M, N), dtype=_act_dtype(out_bits), device=a.device)
+    py, y_hs, ldy = _strided3(out, _act_dtype(out_bits), "out", (H, M, N))
+    if workspace is None:
+        workspace = torch.empty(mq_attn_matmul_workspace_bytes(H, G, M, N), dtype=torch.uint8,
+                                device=a.device)
+    _check(lib().mq_attn_matmul(
+        pa, lda, a_hs, int(H), pb, ldb, b_hs, int(G), int(M), int(N), int(K), float(a_scale),
+        int(a_zp), float(b_scale), int(b_zp), float(out_scale), int(out_zp), int(out_bits), py,
+        ldy, y_hs, _dev_ptr(workspace, torch.uint8, "workspace"), int(workspace.numel()),
+        int(path), _stream_ptr(stream)), "mq_attn_matmul")
+    return out
+
+
+def mq_transpose_i8(x, out=None, stream=None):
+    """y[c][r] = x[r][c] for an int8 [rows][cols] view with contiguous rows."""
+    torch = _torch()
+    rows, cols = x.shape
+    if not isinstance(x, torch.Tensor) or not x.is_cuda or x.dtype != torch.int8:
+        raise ValueError("x must be an int8 GPU tensor")
+    if cols > 1 and x.stride(1) != 1:
+        raise ValueError("x must have contiguous rows")
+    ldx = max(int(x.stride(0)), cols)
+    out = torch.empty((cols, rows), dtype=torch.int8, device=x.device) if out is None else out
+    _check(lib().mq_transpose_i8(ctypes.c_void_p(x.data_ptr()), rows, cols, ldx,
+                                 _dev_ptr(out, torch.int8, "out", (cols, rows)),
+                                 _stream_ptr(stream)), "mq_transpose_i8")
     return out
 
 

@@ -380,4 +380,106 @@ mq_status mq_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const v
                          out_zp, out_bits, bias, y_q, MQ_PATH_AUTO, stream);
 }
 
+// Batched attention matmuls: workspace = [row terms: H*M int64][colsum:
+// G*N int32][b_scale: float], each part 256-byte aligned.
+static int64_t attn_ws_parts(int32_t H, int32_t G, int64_t M, int64_t N, int64_t* off_cs,
+                             int64_t* off_sc)
+{
+    auto up = [](int64_t v) { return (v + 255) / 256 * 256; };
+    const int64_t ro = up((int64_t)H * M * 8);
+    const int64_t cs = up((int64_t)G * N * 4);
+    *off_cs = ro;
+    *off_sc = ro + cs;
+    return ro + cs + 256;
+}
+
+int64_t mq_attn_matmul_workspace_bytes(int32_t H, int32_t G, int64_t M, int64_t N)
+{
+    if (H < 1 || G < 1 || H % G != 0 || M < 0 || N < 0) return -1;
+    if (M > kMaxElems / H || N > kMaxElems / G) return -1;
+    int64_t a, b;
+    return attn_ws_parts(H, G, M, N, &a, &b);
+}
+
+mq_status mq_attn_matmul(const int16_t* a, int64_t lda, int64_t a_hs, int32_t H, const int8_t* b,
+                         int64_t ldb, int64_t b_hs, int32_t G, int64_t M, int64_t N, int64_t K,
+                         float a_scale, int32_t a_zp, float b_scale, int32_t b_zp,
+                         float out_scale, int32_t out_zp, int32_t out_bits, void* y, int64_t ldy,
+                         int64_t y_hs, void* workspace, int64_t workspace_bytes, int32_t path,
+                         void* stream)
+{
+    if (H < 1 || G < 1 || H % G != 0) return MQ_ERR_INVALID_ARG;
+    if (M < 0 || N < 0 || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
+    if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || (M > 0 && N > kMaxElems / M)) return MQ_ERR_INVALID_ARG;
+    if (lda < K || ldb < K || ldy < N || a_hs < 0 || b_hs < 0 || y_hs < 0)
+        return MQ_ERR_INVALID_ARG;
+    if (!act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(a_scale) || !finite_pos(b_scale) || !finite_pos(out_scale))
+        return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(a_zp, 16) || !zp_ok(b_zp, 8) || !zp_ok(out_zp, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (path != MQ_PATH_AUTO && path != MQ_PATH_PREFILL && path != MQ_PATH_GENERIC)
+        return MQ_ERR_INVALID_ARG;
+    int64_t off_cs, off_sc;
+    const int64_t need = mq_attn_matmul_workspace_bytes(H, G, M, N);
+    if (need < 0) return MQ_ERR_INVALID_ARG;
+    attn_ws_parts(H, G, M, N, &off_cs, &off_sc);
+    if (M == 0 || N == 0) return MQ_OK;
+    if (!a || !b || !y || !workspace) return MQ_ERR_INVALID_ARG;
+    if (workspace_bytes < need || ((uintptr_t)workspace % 256) != 0) return MQ_ERR_INVALID_ARG;
+
+    hipStream_t s = as_stream(stream);
+    int8_t* ws = static_cast<int8_t*>(workspace);
+    int64_t* row_off = reinterpret_cast<int64_t*>(ws);
+    int32_t* colsum = reinterpret_cast<int32_t*>(ws + off_cs);
+    float* scale = reinterpret_cast<float*>(ws + off_sc);
+    hipError_t e = mq::launch_attn_sums(a, lda, a_hs, H, M, b, ldb, b_hs, G, N, K, a_zp, b_zp,
+                                        b_scale, row_off, colsum, scale, s);
+    if (e != hipSuccess) return MQ_ERR_HIP;
+
+    mq::QLinearArgs p;
+    p.a = reinterpret_cast<const int8_t*>(a);
+    p.a_bits = 16;
+    p.w = b;
+    p.w_scale = scale;
+    p.ws_stride = 0;
+    p.colsum = colsum;
+    p.bias = nullptr;
+    p.y = y;
+    p.M = M;
+    p.K = K;
+    p.N = N;
+    p.a_scale = a_scale;
+    p.out_scale = out_scale;
+    p.a_zp = a_zp;
+    p.out_zp = out_zp;
+    p.w_bits = 8;
+    p.out_bits = out_bits;
+    p.lda = lda;
+    p.ldw = ldb;
+    p.ldy = ldy;
+    p.batch = H;
+    p.group = H / G;
+    p.a_bs = a_hs;
+    p.w_bs = b_hs;
+    p.y_bs = y_hs;
+    p.cs_bs = N;
+    p.ro_bs = M;
+    p.row_off = row_off;
+    if (path == MQ_PATH_AUTO) path = M <= 16 ? MQ_PATH_GENERIC : MQ_PATH_PREFILL;
+    if (path == MQ_PATH_PREFILL && mq::prefill_supported(p))
+        return from_hip(mq::launch_qlinear_prefill(p, s));
+    return from_hip(mq::launch_qlinear_generic(p, s));
+}
+
+mq_status mq_transpose_i8(const int8_t* x, int64_t rows, int64_t cols, int64_t ldx, int8_t* y,
+                          void* stream)
+{
+    if (rows < 0 || cols < 0 || ldx < cols) return MQ_ERR_INVALID_ARG;
+    if (rows > (int64_t)65535 * 64 || cols > kMaxElems || (rows > 0 && cols > kMaxElems / rows))
+        return MQ_ERR_INVALID_ARG;
+    if (rows == 0 || cols == 0) return MQ_OK;
+    if (!x || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_transpose_i8(x, rows, cols, ldx, y, as_stream(stream)));
+}
+
 }  // extern "C"

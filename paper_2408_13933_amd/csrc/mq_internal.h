@@ -29,7 +29,23 @@ struct QLinearArgs {
     const int32_t* w_zp = nullptr;
     const int32_t* a_rowsum = nullptr;
     int32_t a_bits = 8;     // 8, or 16 (W8A16: 16-bit activation codes)
+    // Row strides in elements (0: dense, K for a and w, N for y).
+    int64_t lda = 0, ldw = 0, ldy = 0;
+    // Batched products (the attention matmuls): batch b reads a, y, row_off
+    // at b times their batch strides and w, colsum at (b / group) times
+    // theirs; w_scale[n * ws_stride] (0: one scale for every n).
+    int32_t batch = 1, group = 1;
+    int64_t a_bs = 0, w_bs = 0, y_bs = 0, cs_bs = 0, ro_bs = 0;
+    int32_t ws_stride = 1;
+    // per-row int64 term added to the exact sum before the saturation (the
+    // zero-point term of a per-tensor asymmetric "weight" operand), or nullptr
+    const int64_t* row_off = nullptr;
 };
+
+// Dense defaults of the stride fields.
+__host__ __device__ inline int64_t eff_lda(const QLinearArgs& p) { return p.lda ? p.lda : p.K; }
+__host__ __device__ inline int64_t eff_ldw(const QLinearArgs& p) { return p.ldw ? p.ldw : p.K; }
+__host__ __device__ inline int64_t eff_ldy(const QLinearArgs& p) { return p.ldy ? p.ldy : p.N; }
 
 hipError_t launch_quantize_act(const float* x, int64_t n, float alpha, int32_t zp,
                                int32_t bits, void* q, hipStream_t s);
@@ -70,6 +86,13 @@ hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int3
                           void* y, hipStream_t st);
 hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
                           int32_t bits, void* y, hipStream_t st);
+
+hipError_t launch_attn_sums(const int16_t* a, int64_t lda, int64_t a_bs, int32_t H, int64_t M,
+                            const int8_t* b, int64_t ldb, int64_t b_bs, int32_t G, int64_t N,
+                            int64_t K, int32_t a_zp, int32_t b_zp, float b_scale,
+                            int64_t* row_off, int32_t* colsum, float* scale_out, hipStream_t s);
+hipError_t launch_transpose_i8(const int8_t* x, int64_t rows, int64_t cols, int64_t ldx,
+                               int8_t* y, hipStream_t s);
 
 hipError_t launch_qlinear_generic(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);

@@ -276,7 +276,11 @@ hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 bool decode_supported(const QLinearArgs& p)
 {
     const uintptr_t wa = p.w_bits == 8 ? 16 : 8;
-    return p.M <= 16 && p.K % 16 == 0 && ((uintptr_t)p.a % 16) == 0 &&
+    // dense, single products only (no strides, batches, row terms or
+    // broadcast scales)
+    const bool dense = p.lda == 0 && p.ldw == 0 && p.ldy == 0 && p.batch == 1 &&
+                       p.row_off == nullptr && p.ws_stride == 1;
+    return dense && p.M <= 16 && p.K % 16 == 0 && ((uintptr_t)p.a % 16) == 0 &&
            ((uintptr_t)p.w % wa) == 0 && ((uintptr_t)p.y % 8) == 0 &&
            (p.N + 15) / 16 <= 0x7FFFFFFF;
 }

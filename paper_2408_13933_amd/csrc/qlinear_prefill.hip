@@ -118,8 +118,9 @@ struct Cfg {
     // + per-column epilogue constants + one flag word per wave
     static constexpr int LDS = STAGES * STAGE + TN * 16 + NWAVES * 4;
     // asymmetric weights add per channel -w_zp and per token row sum; 16-bit
-    // activations use the channel array for the low part of the offset
-    static constexpr int LDS_ASYM = LDS + (TN + TM) * 4;
+    // activations use the channel array for the low part of the offset and
+    // two words per token row for an int64 row term
+    static constexpr int LDS_ASYM = LDS + (TN + 2 * TM) * 4;
     static_assert(!A16 || (WBITS == 8 && !SPLITK), "16-bit activations: int8 weights, no split");
     static_assert(TM % (WM * 32) == 0 && TN % (WN * 32) == 0, "wave grid");
     static_assert((TM * CA) % 64 == 0 && (TN * CW) % 64 == 0, "whole wave loads");
@@ -147,7 +148,9 @@ __device__ inline int swz(int row, int nchunks)
 
 struct EpiCtx {
     const int32_t* e_nzw;  // asymmetric weights: -w_zp per tile channel
-    const int32_t* e_rs;   // asymmetric weights: sum_k (a - a_zp) per tile token row
+    const int32_t* e_rs;   // asymmetric weights: sum_k (a - a_zp) per tile token row;
+                           // 16-bit codes: low words of the int64 row terms
+    const int32_t* e_rhi;  // 16-bit codes: high words of the int64 row terms
     const int32_t* e_off;
     const int32_t* e_m0;
     const int32_t* e_rnd;
@@ -202,7 +205,9 @@ struct Staging {
 // the tile needs them.
 // ASYM (asymmetric weights) adds -w_zp[n] * rs[m]: the fast form has it in
 // the accumulator's start value already, the other adds it exactly in
-// int64 before the saturation.
+// int64 before the saturation.  With 16-bit codes ASYM instead adds an
+// int64 term per token row (a per-tensor zero-point of the other operand),
+// also before the saturation.
 template <class C, bool ASYM, bool FAST, bool PRE, bool STAGED, class Acc, class Acc2>
 __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const EpiCtx& x)
 {
@@ -213,10 +218,18 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
     static_assert(!STAGED || FAST, "staged stores assume whole 4-channel groups");
     constexpr int PASSES = STAGED ? S::PASSES : 1;
     constexpr int FNP = C::FN / PASSES;
+    constexpr bool CASYM = ASYM && !C::A16;  // per-channel weight zero-points
+    constexpr bool ROFF = ASYM && C::A16;    // int64 row terms
     int32_t rs[C::FM];  // this lane's token rows
+    int64_t roff[C::FM];
 #pragma unroll
-    for (int j = 0; j < C::FM; ++j)
-        rs[j] = ASYM && !FAST ? x.e_rs[x.wave_row0 + j * 32 + x.r32] : 0;
+    for (int j = 0; j < C::FM; ++j) {
+        const int row = x.wave_row0 + j * 32 + x.r32;
+        rs[j] = CASYM && !FAST ? x.e_rs[row] : 0;
+        roff[j] = ROFF ? (int64_t)(((uint64_t)(uint32_t)x.e_rhi[row] << 32) |
+                                   (uint64_t)(uint32_t)x.e_rs[row])
+                       : 0;
+    }
 #pragma unroll
     for (int pass = 0; pass < PASSES; ++pass) {
 #pragma unroll
@@ -226,7 +239,7 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
             const int nl = x.col0 + i * 32 + 8 * g;  // tile-local channel
             v4i off = {0, 0, 0, 0}, nzw = {0, 0, 0, 0};
             if constexpr (!FAST) off = *reinterpret_cast<const v4i*>(x.e_off + nl);
-            if constexpr ((ASYM || C::A16) && !FAST)
+            if constexpr ((CASYM || C::A16) && !FAST)
                 nzw = *reinterpret_cast<const v4i*>(x.e_nzw + nl);  // A16: offset low part
             const v4i m0 = *reinterpret_cast<const v4i*>(x.e_m0 + nl);
             const v4i rnd = *reinterpret_cast<const v4i*>(x.e_rnd + nl);
@@ -253,9 +266,10 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                         // the same way, when it is not in the start values)
                         int64_t c64 = ((int64_t)a32 << 8) + acc2[i][j][4 * g + r];
                         if constexpr (!FAST) c64 += ((int64_t)off[r] << 8) + nzw[r];
+                        if constexpr (ROFF) c64 += roff[j];
                         c = sat32(c64);
                     } else if constexpr (!FAST) {
-                        if constexpr (ASYM)
+                        if constexpr (CASYM)
                             c = corrected_acc_asym(a32, off[r], nzw[r], rs[j]);
                         else
                             c = __builtin_elementwise_add_sat(a32, off[r]);
@@ -354,6 +368,9 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     int32_t* e_flag = e_sp + C::TN;  // per wave: bit 0 all pre == 0, bit 1 zp foldable
     int32_t* e_nzw = e_flag + C::NWAVES;  // asymmetric weights only
     int32_t* e_rs = e_nzw + C::TN;
+    int32_t* e_rhi = e_rs + C::TM;        // 16-bit codes with row terms
+    constexpr bool CASYM = ASYM && !C::A16;  // per-channel weight zero-points
+    constexpr bool ROFF = ASYM && C::A16;    // int64 row terms
 
     // ---- tile and K slice: the blocks of one XCD (block id mod 8) take a
     // contiguous run of work items, so they share operand tiles in that
@@ -372,6 +389,10 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     const int tm = tile % tiles_m;
     const int64_t n_tile = (int64_t)tn * C::TN;
     const int64_t m_tile = (int64_t)tm * C::TM;
+    // batched, strided products (the attention matmuls) run on the 16-bit
+    // tile only: this block's batch and the group whose weights it reads
+    constexpr bool STR = C::A16;
+    const int64_t bt = STR ? (int64_t)blockIdx.y : 0, bg = STR ? bt / p.group : 0;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -384,7 +405,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     // ---- buffer descriptors covering only this tile's valid rows, from the
     // first K byte of this block's slice; KL = the slice's length in K
     const int64_t K = p.K;
-    const int64_t wrow = C::WBITS == 8 ? K : K / 2;
+    const int64_t lda = STR ? eff_lda(p) : K;  // activation row stride, elements
+    const int64_t wrow = C::WBITS == 8 ? (STR ? eff_ldw(p) : K) : K / 2;  // bytes
     const int64_t k_begin = C::SPLITK ? (int64_t)split * kt_per_split * C::BK : 0;
     const int64_t KL = !C::SPLITK ? K
                        : (K - k_begin) < (int64_t)kt_per_split * C::BK
@@ -394,11 +416,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     const int rows_a = (int)((p.M - m_tile) < C::TM ? (p.M - m_tile) : C::TM);
     const int rows_w = (int)((p.N - n_tile) < C::TN ? (p.N - n_tile) : C::TN);
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.a + (m_tile * K + k_begin) * C::AB), (short)0,
-        (int)((rows_a * K - k_begin) * C::AB), 0x00020000);
+        (void*)(p.a + (bt * p.a_bs + m_tile * lda + k_begin) * C::AB), (short)0,
+        (int)(((rows_a - 1) * lda + K - k_begin) * C::AB), 0x00020000);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(static_cast<const int8_t*>(p.w) + n_tile * wrow + k_begin_w), (short)0,
-        (int)(rows_w * wrow - k_begin_w), 0x00020000);
+        (void*)(static_cast<const int8_t*>(p.w) + bg * p.w_bs + n_tile * wrow + k_begin_w),
+        (short)0, (int)((rows_w - 1) * wrow + (C::WBITS == 8 ? K : K / 2) - k_begin_w),
+        0x00020000);
 
     // Source offsets of this lane's chunks at k = 0; a stage adds kt*BK.  A
     // chunk past the end of its row (K tail) is pushed out of range.
@@ -417,7 +440,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     for (int i = 0; i < C::A_PER_WAVE; ++i) {
         const int row = ((wave + i * C::NWAVES) * 64 + lane) / C::CA;
         a_off[i] = wave + i * C::NWAVES < C::A_WLOADS
-                       ? (uint32_t)(row * (int)K * C::AB + a_kb(i)) : kOOB;
+                       ? (uint32_t)(row * (int)lda * C::AB + a_kb(i)) : kOOB;
     }
 #pragma unroll
     for (int i = 0; i < C::W_PER_WAVE; ++i) {
@@ -460,18 +483,30 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     if (tid < C::TN) {
         int64_t n = n_tile + tid;
         if (n >= p.N) n = p.N - 1;
-        col_ws = p.w_scale[n];
-        col_cs = p.colsum[n];
-        col_bias = (p.bias ? p.bias : p.w_scale)[n];  // branch-free; unused without bias
-        if constexpr (ASYM) col_zw = p.w_zp[n];
+        col_ws = p.w_scale[STR ? n * p.ws_stride : n];
+        col_cs = p.colsum[STR ? bg * p.cs_bs + n : n];
+        // branch-free; without bias the (unused) load reads w_scale[0]
+        col_bias = (p.bias ? p.bias : p.w_scale)[p.bias ? n : 0];
+        if constexpr (CASYM) col_zw = p.w_zp[n];
     }
-    if (ASYM && tid < C::TM) row_sum = p.a_rowsum[tid < rows_a ? m_tile + tid : m_tile];
+    int32_t row_hi = 0;
+    if (CASYM && tid < C::TM) row_sum = p.a_rowsum[tid < rows_a ? m_tile + tid : m_tile];
+    if (ROFF && tid < C::TM) {
+        const int64_t v = p.row_off[bt * p.ro_bs + (tid < rows_a ? m_tile + tid : m_tile)];
+        row_sum = (int32_t)(uint32_t)(uint64_t)v;
+        row_hi = (int32_t)(v >> 32);
+    }
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s) issue(s, s);
     // keep every use of the loaded values behind the DMA issue
     asm volatile("" : "+v"(col_ws), "+v"(col_cs), "+v"(col_bias));
-    if constexpr (ASYM) asm volatile("" : "+v"(col_zw), "+v"(row_sum));
-    if (ASYM && tid < C::TM) e_rs[tid] = row_sum - (int32_t)K * p.a_zp;
+    if constexpr (CASYM) asm volatile("" : "+v"(col_zw), "+v"(row_sum));
+    if constexpr (ROFF) asm volatile("" : "+v"(row_sum), "+v"(row_hi));
+    if (CASYM && tid < C::TM) e_rs[tid] = row_sum - (int32_t)K * p.a_zp;
+    if (ROFF && tid < C::TM) {
+        e_rs[tid] = row_sum;
+        e_rhi[tid] = row_hi;
+    }
 
     int col_pre0 = 1, col_fold = 1, col_offin = 1;
     if (tid < C::TN) {
@@ -494,13 +529,13 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         // term -w_zp * rs, |rs| <= 255 K, formed by a 24-bit multiply
         // (|rs| < 2^23).
         int64_t offa = cp.off < 0 ? -(int64_t)cp.off : (int64_t)cp.off;
-        if constexpr (ASYM) {
+        if constexpr (CASYM) {
             e_nzw[tid] = -col_zw;
             offa += (col_zw < 0 ? -(int64_t)col_zw : (int64_t)col_zw) * 255 * K;
         }
         offa *= C::WBITS == 4 ? 16 : 1;
         col_offin = offa + (K << 14) < ((int64_t)1 << 31) &&
-                    (!ASYM || 255 * K < ((int64_t)1 << 23));
+                    (!CASYM || 255 * K < ((int64_t)1 << 23));
         if constexpr (C::A16) {
             // the offset bias_q + (128 - a_zp) colsum (int64) split as
             // 256 hi + lo, lo in [0, 255]; hi starts the high-plane sums
@@ -575,21 +610,21 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
         int32_t rs[C::FM];
 #pragma unroll
         for (int j = 0; j < C::FM; ++j)
-            rs[j] = ASYM ? e_rs[wm * (C::TM / C::WM) + j * 32 + r32] : 0;
+            rs[j] = CASYM ? e_rs[wm * (C::TM / C::WM) + j * 32 + r32] : 0;
 #pragma unroll
         for (int i = 0; i < C::FN; ++i)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const v4i o = *reinterpret_cast<const v4i*>(e_off + col0 + i * 32 + 8 * g);
                 v4i z = {0, 0, 0, 0};
-                if constexpr (ASYM || C::A16)
+                if constexpr (CASYM || C::A16)
                     z = *reinterpret_cast<const v4i*>(e_nzw + col0 + i * 32 + 8 * g);
 #pragma unroll
                 for (int j = 0; j < C::FM; ++j)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         int32_t v = o[r];
-                        if constexpr (ASYM) v += __mul24(z[r], rs[j]);
+                        if constexpr (CASYM) v += __mul24(z[r], rs[j]);
                         if constexpr (C::WBITS == 4) v *= 16;
                         acc[i][j][4 * g + r] = v;
                         if constexpr (C::A16) acc2[i][j][4 * g + r] = z[r];
@@ -816,11 +851,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     EpiCtx ctx;
     ctx.e_nzw = e_nzw;
     ctx.e_rs = e_rs;
+    ctx.e_rhi = e_rhi;
     ctx.e_off = e_off;
     ctx.e_m0 = e_m0;
     ctx.e_rnd = e_rnd;
     ctx.e_sp = e_sp;
-    ctx.row_bytes = (int32_t)(p.N * (C::OBITS / 8));
+    ctx.row_bytes = (int32_t)((STR ? eff_ldy(p) : p.N) * (C::OBITS / 8));
     ctx.lane_row_off = (wm * (C::TM / C::WM) + r32) * ctx.row_bytes;
     ctx.col0 = wn * (C::TN / C::WN) + 4 * hk;
     ctx.n_left = (int32_t)(p.N - n_tile);
@@ -830,12 +866,14 @@ __global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearA
     ctx.wave_row0 = wm * (C::TM / C::WM);
     ctx.wave_col0 = wn * (C::TN / C::WN);
     ctx.stage = (MQ_LDS int8_t*)smem + wave * Staging<C>::BYTES;
+    int8_t* const y_batch =
+        static_cast<int8_t*>(p.y) + (STR ? bt * p.y_bs * (C::OBITS / 8) : 0);
     ctx.ry = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(static_cast<int8_t*>(p.y) + m_tile * (int64_t)ctx.row_bytes), (short)0,
+        (void*)(y_batch + m_tile * (int64_t)ctx.row_bytes), (short)0,
         (int)(rows_a * ctx.row_bytes), 0x00020000);
     // staged stores need the tile's channels inside N and 16-byte row chunks
     const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
-                        ((uintptr_t)p.y % 16) == 0;
+                        ((uintptr_t)y_batch % 16) == 0;
     if constexpr (kPreForms) {
         if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true>(acc, acc2, ctx);
         else if (staged) prefill_epilogue<C, ASYM, true, true, true>(acc, acc2, ctx);
@@ -857,14 +895,15 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
     const int64_t kt = (p.K + C::BK - 1) / C::BK;
     const int64_t kt_per_split = (kt + splits - 1) / splits;
     splits = (int)((kt + kt_per_split - 1) / kt_per_split);  // every slice non-empty
-    if (total * splits > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (total * splits > 0x7FFFFFFF || p.batch > 65535) return hipErrorInvalidValue;
     // more than 64 KiB of dynamic LDS must be opted into once per kernel
     constexpr int lds = ASYM || C::A16 ? C::LDS_ASYM : C::LDS;
     static const hipError_t attr = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&qlinear_prefill_kernel<C, ASYM>),
         hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (attr != hipSuccess) return attr;
-    qlinear_prefill_kernel<C, ASYM><<<dim3((unsigned)(total * splits)), dim3(C::THREADS), lds, s>>>(
+    qlinear_prefill_kernel<C, ASYM><<<dim3((unsigned)(total * splits), (unsigned)p.batch),
+                                      dim3(C::THREADS), lds, s>>>(
         p, (int)tiles_n, (int)tiles_m, splits, (int)kt_per_split);
     return hipGetLastError();
 }
@@ -987,15 +1026,26 @@ hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 
 bool prefill_supported(const QLinearArgs& p)
 {
+    const int64_t ab = p.a_bits / 8, ob = p.out_bits / 8;
+    const int64_t lda = eff_lda(p) * ab, ldy = eff_ldy(p) * ob;
+    const int64_t ldw = p.w_bits == 8 ? eff_ldw(p) : (p.ldw ? p.ldw : p.K / 2);
     // whole 16-byte chunks per row (packed int4 rows too), 16-byte aligned
-    // bases, and per-tile buffer ranges below 2^31 bytes
+    // rows and batches, 8-byte aligned output rows and batches
     const bool kok = p.w_bits == 8 ? (p.K % 16 == 0) : (p.K % 32 == 0);
+    const bool align = ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
+                       ((uintptr_t)p.y % 8) == 0 && lda % 16 == 0 && ldw % 16 == 0 &&
+                       ldy % 8 == 0 && (p.a_bs * ab) % 16 == 0 && p.w_bs % 16 == 0 &&
+                       (p.y_bs * ob) % 8 == 0;
     // byte offsets inside one 256-row tile must fit the 32-bit buffer offset
-    const bool nok = 256 * p.N * (p.out_bits / 8) < ((int64_t)1 << 31);
-    // 16-bit activation codes: int8 weights only (the W8A16 tile)
-    const bool aok = p.a_bits == 8 || (p.w_bits == 8 && p.w_zp == nullptr);
-    return kok && nok && aok && ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
-           ((uintptr_t)p.y % 8) == 0;
+    const int64_t lim = (int64_t)1 << 31;
+    const bool nok = 256 * ldy < lim && 256 * lda < lim && 256 * ldw < lim;
+    // 16-bit activation codes: int8 weights only (the W8A16 tile), which
+    // also takes strides, batches and int64 row terms; the 8-bit tiles take
+    // dense single products
+    const bool dense = p.lda == 0 && p.ldw == 0 && p.ldy == 0 && p.batch == 1 &&
+                       p.row_off == nullptr && p.ws_stride == 1;
+    const bool aok = p.a_bits == 8 ? dense : (p.w_bits == 8 && p.w_zp == nullptr);
+    return kok && align && nok && aok && p.batch >= 1 && p.batch <= 65535;
 }
 
 int64_t prefill_workspace_bytes(const QLinearArgs& p)
@@ -1005,7 +1055,11 @@ int64_t prefill_workspace_bytes(const QLinearArgs& p)
 
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s)
 {
-    if (p.a_bits == 16) {  // one tile shape, no K split
+    if (p.a_bits == 16) {  // one tile shape, no K split; ASYM: int64 row terms
+        if (p.row_off) {
+            if (p.out_bits == 8) return launch_cfg<T128x128A16<8>, true>(p, 1, s);
+            return launch_cfg<T128x128A16<16>, true>(p, 1, s);
+        }
         if (p.out_bits == 8) return launch_cfg<T128x128A16<8>, false>(p, 1, s);
         return launch_cfg<T128x128A16<16>, false>(p, 1, s);
     }

@@ -281,3 +281,41 @@ def test_calibration_empty_calls():
 ])
 def test_glue_entry_points_reject_invalid_arguments(call):
     assert call(mq.lib()) == 1
+
+
+def attn(**kw):
+    a = dict(a=NZ, lda=64, a_hs=64 * 16, H=4, b=NZ, ldb=64, b_hs=64 * 16, G=2, M=16, N=16, K=64,
+             a_scale=0.1, a_zp=0, b_scale=0.1, b_zp=0, out_scale=0.1, out_zp=0, out_bits=16,
+             y=NZ, ldy=16, y_hs=256, ws=P(256), ws_bytes=1 << 20, path=0, stream=None)
+    a.update(kw)
+    return mq.lib().mq_attn_matmul(a["a"], a["lda"], a["a_hs"], a["H"], a["b"], a["ldb"],
+                                   a["b_hs"], a["G"], a["M"], a["N"], a["K"], a["a_scale"],
+                                   a["a_zp"], a["b_scale"], a["b_zp"], a["out_scale"],
+                                   a["out_zp"], a["out_bits"], a["y"], a["ldy"], a["y_hs"],
+                                   a["ws"], a["ws_bytes"], a["path"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(H=0), dict(G=0), dict(H=4, G=3), dict(M=-1), dict(K=0), dict(K=65537),
+    dict(lda=63), dict(ldb=32), dict(ldy=15), dict(a_hs=-1), dict(out_bits=4),
+    dict(a_scale=0.0), dict(b_scale=float("inf")), dict(out_scale=-1.0),
+    dict(a_zp=40000), dict(b_zp=128), dict(out_zp=200, out_bits=8), dict(path=1),
+    dict(a=None), dict(b=None), dict(y=None), dict(ws=None), dict(ws_bytes=16),
+    dict(ws=P(264)),
+])
+def test_attn_matmul_rejects_invalid_arguments(kw):
+    assert attn(**kw) == 1
+
+
+def test_attn_matmul_sizes_and_empty_calls():
+    L = mq.lib()
+    n = L.mq_attn_matmul_workspace_bytes(32, 4, 1024, 1024)
+    assert n >= 32 * 1024 * 8 + 4 * 1024 * 4 and n % 256 == 0
+    assert L.mq_attn_matmul_workspace_bytes(4, 3, 8, 8) == -1
+    assert L.mq_attn_matmul_workspace_bytes(0, 1, 8, 8) == -1
+    assert attn(M=0, a=None, b=None, y=None, ws=None) == 0
+    assert attn(N=0, a=None, b=None, y=None, ws=None, ldy=0) == 0
+    assert L.mq_transpose_i8(None, 0, 5, 5, None, None) == 0
+    assert L.mq_transpose_i8(NZ, 4, 5, 4, NZ, None) == 1
+    assert L.mq_transpose_i8(None, 4, 5, 5, NZ, None) == 1
+    assert L.mq_transpose_i8(NZ, -1, 5, 5, NZ, None) == 1

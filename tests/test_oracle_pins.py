@@ -1001,3 +1001,55 @@ def test_softmax_against_torch():
     assert np.array_equal(oracle.softmax(x[:, :100], ax, zx, ay, zy, 16),
                           oracle.softmax(xs, ax, zx, ay, zy, 16))
 
+
+
+# ---------------------------------------------------------------------------
+# attention matmuls between 16-bit and 8-bit activation codes (Section 5.6)
+
+@pytest.mark.parametrize("out_bits", [8, 16])
+def test_attn_matmul_bruteforce_tiny(out_bits):
+    # every head against the exact rational reference with both zero-points,
+    # heads 2h and 2h+1 sharing group h of b
+    rng = np.random.default_rng(70 + out_bits)
+    for (H, G, M, N, K) in [(1, 1, 1, 1, 1), (2, 1, 3, 2, 5), (4, 2, 2, 3, 4), (6, 3, 1, 4, 3)]:
+        a = rng.integers(-32768, 32768, (H, M, K)).astype(np.int16)
+        b = rng.integers(-128, 128, (G, N, K)).astype(np.int8)
+        a[0, 0, 0], b[0, 0, 0] = -32768, 127
+        a_scale = float(np.float32(rng.uniform(1e-5, 2e-4)))
+        b_scale = float(np.float32(rng.uniform(0.01, 0.05)))
+        out_scale = float(np.float32(rng.uniform(1e-3, 1e-2) * (1e-2 if out_bits == 16 else 1)))
+        a_zp = int(rng.choice([-32768, -7, 0, 32767]))
+        b_zp = int(rng.choice([-128, -3, 0, 127]))
+        out_zp = int(rng.integers(-50, 50))
+        y = oracle.attn_matmul(a, b, a_scale, a_zp, b_scale, b_zp, out_scale, out_zp, out_bits,
+                               nthreads=2)
+        M0, sh, _ = _exact_params(a_scale, np.full(N, b_scale, np.float32), out_scale, None)
+        for h in range(H):
+            g = h // (H // G)
+            ref = bf.qlinear_exact(a[h].astype(int).tolist(), b[g].astype(int).tolist(), a_zp,
+                                   [0] * N, M0, sh, out_zp, out_bits, zp_w=[b_zp] * N)
+            assert y[h].astype(int).tolist() == ref, (H, G, M, N, K, h)
+
+
+def test_attn_matmul_invariances():
+    rng = np.random.default_rng(77)
+    H, G, M, N, K = 4, 2, 5, 6, 16
+    a = rng.integers(-2000, 2000, (H, M, K)).astype(np.int16)
+    b = rng.integers(-100, 100, (G, N, K)).astype(np.int8)
+    args = (3e-4, 11, 0.02, -5, 2e-3, 3, 16)
+    y = oracle.attn_matmul(a, b, *args[:3], args[3], *args[4:])
+    # shifting b's codes and zero-point together changes nothing (the
+    # zero-point is subtracted from every code)
+    y2 = oracle.attn_matmul(a, (b.astype(np.int16) + 20).astype(np.int8), args[0], args[1],
+                            args[2], args[3] + 20, *args[4:])
+    assert np.array_equal(y, y2)
+    # and the same for a
+    y3 = oracle.attn_matmul((a + 1000).astype(np.int16), b, args[0], args[1] + 1000, *args[2:])
+    assert np.array_equal(y, y3)
+    # codes at the zero-points give the output zero-point everywhere
+    z = oracle.attn_matmul(np.full((H, M, K), args[1], np.int16), b, *args)
+    assert np.all(z == args[5])
+    # heads of one group see the same b: equal a rows give equal outputs
+    a[1] = a[0]
+    y4 = oracle.attn_matmul(a, b, *args)
+    assert np.array_equal(y4[0], y4[1]) and not np.array_equal(y4[0], y4[2])
