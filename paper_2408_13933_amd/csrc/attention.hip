@@ -7,29 +7,53 @@
 namespace mq {
 namespace {
 
-// One wave per row: rows [0, H*M) are rows of A (int16), rows [H*M,
-// H*M + G*N) rows of B (int8).  A rows give the term of B's zero-point,
-// -b_zp * sum_k (A[k] - a_zp) (int64, exact); B rows give sum_k B[k].
+// Sum of K codes starting at x: 16-byte loads when `vec` (x 16-byte
+// aligned), else element loads; the wave's partial sums are reduced by the
+// caller.
+template <class T>
+__device__ inline int64_t row_sum_part(const T* x, int64_t K, int lane, bool vec)
+{
+    constexpr int PER = 16 / sizeof(T);  // codes per 16-byte load
+    int64_t s = 0;
+    int64_t k0 = 0;
+    if (vec) {
+        const int64_t full = K / (64 * PER) * (64 * PER);
+        for (int64_t k = (int64_t)lane * PER; k < full; k += 64 * PER) {
+            const int4 v = *reinterpret_cast<const int4*>(x + k);
+            const T* e = reinterpret_cast<const T*>(&v);
+            int32_t t = 0;
+#pragma unroll
+            for (int i = 0; i < PER; ++i) t += e[i];
+            s += t;
+        }
+        k0 = full;
+    }
+    for (int64_t k = k0 + lane; k < K; k += 64) s += x[k];
+    return s;
+}
+
+// One wave per row: rows [0, rows_a) are rows of A (int16; none when B's
+// zero-point is 0), rows [rows_a, rows_a + rows_b) rows of B (int8).  A rows
+// give the term of B's zero-point, -b_zp * sum_k (A[k] - a_zp) (int64,
+// exact); B rows give sum_k B[k].
 __global__ __launch_bounds__(256) void attn_sums_kernel(const int16_t* a, int64_t lda, int64_t a_bs,
                                                         int64_t rows_a, int64_t M,
                                                         const int8_t* b, int64_t ldb, int64_t b_bs,
                                                         int64_t rows_b, int64_t N, int64_t K,
                                                         int32_t a_zp, int32_t b_zp, float b_scale,
                                                         int64_t* row_off, int32_t* colsum,
-                                                        float* scale_out)
+                                                        float* scale_out, bool vec_a, bool vec_b)
 {
     const int lane = threadIdx.x & 63;
     if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = b_scale;
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= rows_a + rows_b) return;
-    int64_t s = 0;
-    if (row < rows_a) {
-        const int16_t* x = a + (row / M) * a_bs + (row % M) * lda;
-        for (int64_t k = lane; k < K; k += 64) s += x[k];
-    } else {
+    int64_t s;
+    if (row < rows_a)
+        s = row_sum_part(a + (row / M) * a_bs + (row % M) * lda, K, lane, vec_a);
+    else {
         const int64_t r = row - rows_a;
-        const int8_t* x = b + (r / N) * b_bs + (r % N) * ldb;
-        for (int64_t k = lane; k < K; k += 64) s += x[k];
+        s = row_sum_part(b + (r / N) * b_bs + (r % N) * ldb, K, lane, vec_b);
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
@@ -66,13 +90,16 @@ hipError_t launch_attn_sums(const int16_t* a, int64_t lda, int64_t a_bs, int32_t
                             int64_t K, int32_t a_zp, int32_t b_zp, float b_scale,
                             int64_t* row_off, int32_t* colsum, float* scale_out, hipStream_t s)
 {
-    const int64_t rows_a = (int64_t)H * M, rows_b = (int64_t)G * N;
+    // B's zero-point 0: the row terms vanish and A is not read
+    const int64_t rows_a = b_zp != 0 ? (int64_t)H * M : 0, rows_b = (int64_t)G * N;
     const int64_t blocks = (rows_a + rows_b + 3) / 4;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const bool vec_a = (uintptr_t)a % 16 == 0 && (lda * 2) % 16 == 0 && (a_bs * 2) % 16 == 0;
+    const bool vec_b = (uintptr_t)b % 16 == 0 && ldb % 16 == 0 && b_bs % 16 == 0;
     attn_sums_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
         a, lda, a_bs, rows_a, M, b, ldb, b_bs, rows_b, N, K, a_zp, b_zp, b_scale, row_off, colsum,
-        scale_out);
+        scale_out, vec_a, vec_b);
     return hipGetLastError();
 }
 

@@ -464,7 +464,7 @@ mq_status mq_attn_matmul(const int16_t* a, int64_t lda, int64_t a_hs, int32_t H,
     p.y_bs = y_hs;
     p.cs_bs = N;
     p.ro_bs = M;
-    p.row_off = row_off;
+    p.row_off = b_zp != 0 ? row_off : nullptr;  // b_zp = 0: no row terms
     if (path == MQ_PATH_AUTO) path = M <= 16 ? MQ_PATH_GENERIC : MQ_PATH_PREFILL;
     if (path == MQ_PATH_PREFILL && mq::prefill_supported(p))
         return from_hip(mq::launch_qlinear_prefill(p, s));

@@ -83,6 +83,9 @@ struct Cfg {
     static constexpr int TM = TM_, TN = TN_, WM = WM_, WN = WN_, BK = BK_;
     static constexpr int STAGES = STAGES_, SWZ = SWZ_;
     static constexpr int NWAVES = WM * WN;
+    // work-groups per CU the register budget is sized for: the short-K
+    // 16-bit tile (two stages) shares a CU between two
+    static constexpr int OCC = (ABITS_ == 16 && STAGES_ == 2) ? 2 : 1;
     static constexpr int THREADS = 64 * NWAVES;
     static constexpr int FM = TM / (WM * 32);   // 32-token fragments per wave
     static constexpr int FN = TN / (WN * 32);   // 32-channel fragments per wave
@@ -351,7 +354,7 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
 }
 
 template <class C, bool ASYM>
-__global__ __launch_bounds__(C::THREADS, 1) void qlinear_prefill_kernel(QLinearArgs p,
+__global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLinearArgs p,
                                                                        int tiles_n, int tiles_m,
                                                                        int splits,
                                                                        int kt_per_split)
@@ -929,6 +932,11 @@ using T192x256 = std::conditional_t<WB == 8, Cfg<WB, OB, 192, 256, 2, 4, 64, 4, 
 // 16-bit activation codes: 128x128 tokens x channels, 64 k per stage (128
 // bytes of each activation row), DMA spread over both steps of a stage
 template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16>;
+// short K (<= 128 codes, e.g. the attention scores over a 64-dimensional
+// head): two stages are all the pipeline needs, and half the LDS lets two
+// work-groups share a CU, so one's prologue and epilogue overlap the
+// other's products
+template <int OB> using T128x128A16S2 = Cfg<8, OB, 128, 128, 2, 2, 64, 2, 2, 1, 16>;
 
 // Per-block cycle model of each tile shape on MI355X (phase timings of the
 // kernel): fixed prologue + K-loop cycles per stage + epilogue.
@@ -1053,16 +1061,26 @@ int64_t prefill_workspace_bytes(const QLinearArgs& p)
     return workspace_for(p, choose(p, true));
 }
 
+// 16-bit activation codes: no K split; ASYM: int64 row terms
+template <int>
+hipError_t launch_a16(const QLinearArgs& p, hipStream_t s)
+{
+    const bool ro = p.row_off != nullptr, o8 = p.out_bits == 8;
+    if (p.K <= 128) {
+        if (ro) return o8 ? launch_cfg<T128x128A16S2<8>, true>(p, 1, s)
+                          : launch_cfg<T128x128A16S2<16>, true>(p, 1, s);
+        return o8 ? launch_cfg<T128x128A16S2<8>, false>(p, 1, s)
+                  : launch_cfg<T128x128A16S2<16>, false>(p, 1, s);
+    }
+    if (ro) return o8 ? launch_cfg<T128x128A16<8>, true>(p, 1, s)
+                      : launch_cfg<T128x128A16<16>, true>(p, 1, s);
+    return o8 ? launch_cfg<T128x128A16<8>, false>(p, 1, s)
+              : launch_cfg<T128x128A16<16>, false>(p, 1, s);
+}
+
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s)
 {
-    if (p.a_bits == 16) {  // one tile shape, no K split; ASYM: int64 row terms
-        if (p.row_off) {
-            if (p.out_bits == 8) return launch_cfg<T128x128A16<8>, true>(p, 1, s);
-            return launch_cfg<T128x128A16<16>, true>(p, 1, s);
-        }
-        if (p.out_bits == 8) return launch_cfg<T128x128A16<8>, false>(p, 1, s);
-        return launch_cfg<T128x128A16<16>, false>(p, 1, s);
-    }
+    if (p.a_bits == 16) return launch_a16<8>(p, s);
     if (p.w_bits == 8 && p.out_bits == 8) return launch_t<8, 8>(p, s);
     if (p.w_bits == 8) return launch_t<8, 16>(p, s);
     if (p.out_bits == 8) return launch_t<4, 8>(p, s);

@@ -31,6 +31,8 @@ A16_CASES = [
     (129, 640, 257, 8, 16, False),
     (261, 1088, 384, 8, 16, True),
     (200, 1024, 300, 4, 16, False),    # int4 weights above 16 tokens: generic kernel
+    (300, 64, 257, 8, 16, True),       # short K: the two-stage tile
+    (129, 128, 200, 8, 8, False),
 ]
 
 
