@@ -322,6 +322,32 @@ mq_status mq_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t*
                          float a2, int32_t z2, int64_t numel, float ay, int32_t zy,
                          int32_t out_bits, void* y, void* stream);
 
+/*
+ * mq_mul_requant -- product of two code tensors (the gated unit of the
+ * feed-forward block, SiLU(gate) * up):
+ *   v = (a1 * (x1 - z1)) * (a2 * (x2 - z2))      x1, x2 device int16 [numel]
+ * each factor exact in fp64, the product one rounding.
+ */
+mq_status mq_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                         float a2, int32_t z2, int64_t numel, float ay, int32_t zy,
+                         int32_t out_bits, void* y, void* stream);
+
+/*
+ * mq_rope -- rotary position embedding on the query or key codes of a
+ * Llama-family block (the paper's models; a non-linear operator kept at 16
+ * bits): for token t, head h and pair i < D/2 (dimensions i and i + D/2 of
+ * the head), with the angle (t + pos0) * base^(-2i/D):
+ *   u = ax * (x[t][h*D + i] - zx),  w = ax * (x[t][h*D + i + D/2] - zx)
+ *   y[t][h*D + i] = u cos - w sin,  y[t][h*D + i + D/2] = w cos + u sin
+ * (fp64: inverse frequency by pow, the angle one product, cos and sin).
+ *   x      device int16 [T][H * D]; y device int8 or int16 [T][H * D]
+ *   table  device fp64 scratch of T * D values (the cos/sin table)
+ *   T >= 0, H >= 1, D >= 2 even, base finite and > 1, 0 <= pos0 <= 2^40.
+ */
+mq_status mq_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                  double base, int64_t pos0, float ay, int32_t zy, int32_t out_bits,
+                  double* table, void* y, void* stream);
+
 /* Table operators of mq_lut_build. */
 #define MQ_LUT_SILU 1
 
@@ -355,6 +381,18 @@ mq_status mq_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int32_t z
  */
 mq_status mq_softmax(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx, float ay,
                      int32_t zy, int32_t out_bits, void* y, void* stream);
+
+/*
+ * mq_softmax_causal -- mq_softmax over the keys a decoder's causal
+ * self-attention lets each query see: row m covers the keys
+ * k <= (m mod period) + offset (the rows of one head are `period`
+ * consecutive queries, `offset` the keys before the first of them); the
+ * softmax runs over those keys and the others get probability 0 (code zy).
+ *   period >= 1, offset >= 0; everything else as in mq_softmax.
+ */
+mq_status mq_softmax_causal(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                            float ay, int32_t zy, int32_t out_bits, int64_t period,
+                            int64_t offset, void* y, void* stream);
 
 /*
  * mq_smooth_scales -- SmoothQuant's closed-form scaling vector as the

@@ -88,6 +88,19 @@ def _load():
                                    ctypes.c_int32, ctypes.c_float, ctypes.c_int32, ctypes.c_int,
                                    _vp]
     lib.oracle_softmax.restype = None
+    lib.oracle_softmax_causal.argtypes = [_i16p, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
+                                          ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
+                                          ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_void_p]
+    lib.oracle_softmax_causal.restype = None
+    lib.oracle_mul_requant.argtypes = [_i16p, ctypes.c_float, ctypes.c_int32, _i16p, ctypes.c_float,
+                                       ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                       ctypes.c_int32, ctypes.c_int, ctypes.c_void_p]
+    lib.oracle_mul_requant.restype = None
+    lib.oracle_rope.argtypes = [_i16p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                ctypes.c_float, ctypes.c_int32, ctypes.c_double, ctypes.c_int64,
+                                ctypes.c_float, ctypes.c_int32, ctypes.c_int, ctypes.c_void_p]
+    lib.oracle_rope.restype = None
     lib.oracle_smooth_scales.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int64, _f32p,
                                          ctypes.c_int64, ctypes.c_float, _f32p, _f32p, _f32p]
     lib.oracle_smooth_scales.restype = None
@@ -244,6 +257,28 @@ def add_requant(x1, a1, z1, x2, a2, z2, ay, zy, bits_y):
     return y
 
 
+def mul_requant(x1, a1, z1, x2, a2, z2, ay, zy, bits_y):
+    """Elementwise product of two int16 code tensors, requantized."""
+    x1 = np.ascontiguousarray(x1, dtype=np.int16)
+    x2 = np.ascontiguousarray(x2, dtype=np.int16)
+    assert x1.shape == x2.shape
+    y = np.empty(x1.shape, dtype=_act_dtype(bits_y))
+    _load().oracle_mul_requant(x1, a1, z1, x2, a2, z2, x1.size, ay, zy, bits_y, _ptr(y))
+    return y
+
+
+def rope(x, heads, ax, zx, ay, zy, bits_y, base=10000.0, pos0=0):
+    """Rotary position embedding on int16 codes [T][heads * D], pairs
+    (i, i + D/2) of every head, requantized."""
+    x = np.ascontiguousarray(x, dtype=np.int16)
+    T, HD = x.shape
+    D = HD // heads
+    assert D * heads == HD and D % 2 == 0
+    y = np.empty(x.shape, dtype=_act_dtype(bits_y))
+    _load().oracle_rope(x, T, heads, D, ax, zx, float(base), int(pos0), ay, zy, bits_y, _ptr(y))
+    return y
+
+
 def lut_build(op, ax, zx, ay, zy, bits_y):
     """65536-entry table of a non-linear op on int16 codes (entry i + 32768)."""
     lut = np.empty(65536, dtype=_act_dtype(bits_y))
@@ -264,12 +299,15 @@ def rmsnorm(x, ax, zx, gamma, eps, ay, zy, bits_y):
     return y
 
 
-def softmax(x, ax, zx, ay, zy, bits_y):
-    """Softmax over rows of int16 score codes, requantized."""
+def softmax(x, ax, zx, ay, zy, bits_y, causal_period: int = 0, causal_offset: int = 0):
+    """Softmax over rows of int16 score codes, requantized.  causal_period
+    > 0: row m sees only keys k <= (m mod causal_period) + causal_offset
+    (the others get probability 0)."""
     x = np.ascontiguousarray(x, dtype=np.int16)
     M, K = x.shape
     y = np.empty((M, K), dtype=_act_dtype(bits_y))
-    _load().oracle_softmax(x, M, K, ax, zx, ay, zy, bits_y, _ptr(y))
+    _load().oracle_softmax_causal(x, M, K, ax, zx, ay, zy, bits_y, int(causal_period),
+                                  int(causal_offset), _ptr(y))
     return y
 
 

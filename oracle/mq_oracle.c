@@ -253,6 +253,48 @@ void oracle_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* 
     }
 }
 
+/* Elementwise product of two int16 code tensors (the gated unit of the
+ * feed-forward block, SiLU(gate) * up), requantized:
+ *   v = (a1 (x1 - z1)) * (a2 (x2 - z2)), each factor exact in fp64, the
+ * product one rounding.                                                */
+void oracle_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                        float a2, int32_t z2, int64_t n, float ay, int32_t zy, int bits_y,
+                        void* y)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        const double f1 = (double)a1 * (double)((int64_t)x1[i] - z1);
+        const double f2 = (double)a2 * (double)((int64_t)x2[i] - z2);
+        store_q(y, bits_y, i, requant_f64(f1 * f2, ay, zy, bits_y));
+    }
+}
+
+/* Rotary position embedding on int16 codes [T][H * D] (the query and key
+ * projections of a Llama-family block; the paper's models use it, the
+ * paper leaves it in higher precision like the other non-linear operators,
+ * Section 4.1).  Pairs (i, i + D/2) of every head rotate by the angle
+ * (t + pos0) * base^(-2i/D) of token t:
+ *   u = ax (x_i - zx), w = ax (x_{i+D/2} - zx)
+ *   y_i = u cos - w sin,   y_{i+D/2} = w cos + u sin
+ * in fp64 (inverse frequency by pow, angle one product, then cos and sin),
+ * requantized.                                                         */
+void oracle_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                 double base, int64_t pos0, float ay, int32_t zy, int bits_y, void* y)
+{
+    const int64_t half = D / 2;
+    for (int64_t t = 0; t < T; ++t)
+        for (int64_t h = 0; h < H; ++h)
+            for (int64_t i = 0; i < half; ++i) {
+                const double inv = pow(base, -(double)(2 * i) / (double)D);
+                const double ang = (double)(t + pos0) * inv;
+                const double c = cos(ang), sn = sin(ang);
+                const int64_t j0 = t * H * D + h * D + i, j1 = j0 + half;
+                const double u = (double)ax * (double)((int64_t)x[j0] - zx);
+                const double w = (double)ax * (double)((int64_t)x[j1] - zx);
+                store_q(y, bits_y, j0, requant_f64(u * c - w * sn, ay, zy, bits_y));
+                store_q(y, bits_y, j1, requant_f64(w * c + u * sn, ay, zy, bits_y));
+            }
+}
+
 /* Elementwise non-linear operator on int16 codes as a 65536-entry table,
  * entry i + 32768 for code i: f(alpha_x (i - zp_x)) requantized.
  * op 1: SiLU, f(v) = v / (1 + exp(-v)).                                */
@@ -298,24 +340,38 @@ void oracle_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx
 /* Softmax over each row of K codes (scores):
  *   e_k = exp(alpha_x (x_k - max_j x_j)),  p_k = e_k / sum_j e_j
  * the sum in index order; the probabilities requantized.               */
-void oracle_softmax(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
-                    float ay, int32_t zy, int bits_y, void* y)
+/* Causal form (self-attention scores of a decoder): row m sees the keys
+ * k <= (m mod period) + offset, the rows of one head being the period
+ * consecutive queries and offset the keys before the first query; the
+ * softmax runs over those keys and the others get probability 0 (code
+ * zp_y).  period = 0: every key. */
+void oracle_softmax_causal(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                           float ay, int32_t zy, int bits_y, int64_t period, int64_t offset,
+                           void* y)
 {
     (void)zx;  /* the zero-point cancels in x_k - max_j x_j */
     double* e = (double*)malloc(sizeof(double) * (size_t)(K > 0 ? K : 1));
     for (int64_t m = 0; m < M; ++m) {
+        int64_t n = K;  /* keys seen by this row */
+        if (period > 0 && (m % period) + offset + 1 < K) n = (m % period) + offset + 1;
         int64_t mx = x[m * K];
-        for (int64_t k = 1; k < K; ++k)
+        for (int64_t k = 1; k < n; ++k)
             if (x[m * K + k] > mx) mx = x[m * K + k];
         double sum = 0.0;
-        for (int64_t k = 0; k < K; ++k) {
+        for (int64_t k = 0; k < n; ++k) {
             e[k] = exp((double)ax * (double)((int64_t)x[m * K + k] - mx));
             sum += e[k];
         }
         for (int64_t k = 0; k < K; ++k)
-            store_q(y, bits_y, m * K + k, requant_f64(e[k] / sum, ay, zy, bits_y));
+            store_q(y, bits_y, m * K + k, requant_f64(k < n ? e[k] / sum : 0.0, ay, zy, bits_y));
     }
     free(e);
+}
+
+void oracle_softmax(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                    float ay, int32_t zy, int bits_y, void* y)
+{
+    oracle_softmax_causal(x, M, K, ax, zx, ay, zy, bits_y, 0, 0, y);
 }
 
 /* ------------------------------------------------------------------ */

@@ -85,6 +85,12 @@ def lib():
     L.mq_lut_apply.argtypes = [c_p, c_i64, c_p, c_i32, c_p, c_p]
     L.mq_rmsnorm.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_p, c_f, c_f, c_i32, c_i32, c_p, c_p]
     L.mq_softmax.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p]
+    L.mq_mul_requant.argtypes = [c_p, c_f, c_i32, c_p, c_f, c_i32, c_i64, c_f, c_i32, c_i32, c_p,
+                                 c_p]
+    L.mq_rope.argtypes = [c_p, c_i64, c_i64, c_i64, c_f, c_i32, ctypes.c_double, c_i64, c_f, c_i32,
+                          c_i32, c_p, c_p, c_p]
+    L.mq_softmax_causal.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_f, c_i32, c_i32, c_i64,
+                                    c_i64, c_p, c_p]
     L.mq_smooth_scales.argtypes = [c_p, c_i64, c_i64, c_p, c_i64, c_f, c_p, c_p, c_p, c_p]
     L.mq_arl_forward.argtypes = [c_p, c_i64, c_f, c_f, c_i32, c_p, c_p]
     L.mq_arl_backward.argtypes = [c_p, c_p, c_i64, c_f, c_f, c_i32, c_p, c_p, c_p]
@@ -104,7 +110,8 @@ def lib():
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
                  "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
                  "mq_arl_backward", "mq_add_requant", "mq_lut_build", "mq_lut_apply",
-                 "mq_rmsnorm", "mq_softmax"):
+                 "mq_rmsnorm", "mq_softmax", "mq_softmax_causal", "mq_mul_requant",
+                 "mq_rope"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -374,6 +381,55 @@ def mq_softmax(x, ax: float, zx: int, ay: float, zy: int, out_bits: int = 16, ou
                             int(zy), int(out_bits),
                             _dev_ptr(out, _act_dtype(out_bits), "out", (M, K)),
                             _stream_ptr(stream)), "mq_softmax")
+    return out
+
+
+def mq_mul_requant(x1, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy: int,
+                   out_bits: int = 8, out=None, stream=None):
+    """Product of two int16 code tensors, requantized."""
+    torch = _torch()
+    if tuple(x1.shape) != tuple(x2.shape):
+        raise ValueError("x1 and x2 must have the same shape")
+    out = torch.empty(x1.shape, dtype=_act_dtype(out_bits), device=x1.device) if out is None else out
+    _check(lib().mq_mul_requant(_dev_ptr(x1, torch.int16, "x1"), float(a1), int(z1),
+                                _dev_ptr(x2, torch.int16, "x2"), float(a2), int(z2), x1.numel(),
+                                float(ay), int(zy), int(out_bits),
+                                _dev_ptr(out, _act_dtype(out_bits), "out", tuple(x1.shape)),
+                                _stream_ptr(stream)), "mq_mul_requant")
+    return out
+
+
+def mq_rope(x, heads: int, ax: float, zx: int, ay: float, zy: int, out_bits: int = 16,
+            base: float = 10000.0, pos0: int = 0, out=None, table=None, stream=None):
+    """Rotary position embedding on int16 codes [T][heads * D]."""
+    torch = _torch()
+    T, HD = x.shape
+    D = HD // int(heads)
+    if D * int(heads) != HD:
+        raise ValueError("x's row length must be heads * D")
+    out = torch.empty((T, HD), dtype=_act_dtype(out_bits), device=x.device) if out is None else out
+    if table is None:
+        table = torch.empty(max(T * D, 1), dtype=torch.float64, device=x.device)
+    if table.numel() < T * D:
+        raise ValueError("table needs T * D fp64 values")
+    _check(lib().mq_rope(_dev_ptr(x, torch.int16, "x"), T, int(heads), D, float(ax), int(zx),
+                         float(base), int(pos0), float(ay), int(zy), int(out_bits),
+                         _dev_ptr(table, torch.float64, "table"),
+                         _dev_ptr(out, _act_dtype(out_bits), "out", (T, HD)),
+                         _stream_ptr(stream)), "mq_rope")
+    return out
+
+
+def mq_softmax_causal(x, ax: float, zx: int, ay: float, zy: int, period: int, offset: int = 0,
+                      out_bits: int = 16, out=None, stream=None):
+    """Causal softmax: row m covers keys k <= (m % period) + offset."""
+    torch = _torch()
+    M, K = x.shape
+    out = torch.empty((M, K), dtype=_act_dtype(out_bits), device=x.device) if out is None else out
+    _check(lib().mq_softmax_causal(_dev_ptr(x, torch.int16, "x"), M, K, float(ax), int(zx),
+                                   float(ay), int(zy), int(out_bits), int(period), int(offset),
+                                   _dev_ptr(out, _act_dtype(out_bits), "out", (M, K)),
+                                   _stream_ptr(stream)), "mq_softmax_causal")
     return out
 
 

@@ -55,9 +55,30 @@ __device__ inline int32_t add_one(int32_t u, int32_t v, float a1, int32_t z1, fl
     return requant_f64<BITS>(s, (double)ay, zy);
 }
 
+// Product of the two dequantized codes (each factor exact in fp64, the
+// product one rounding): the gated unit SiLU(gate) * up.
+template <int BITS>
+__device__ inline int32_t mul_one(int32_t u, int32_t v, float a1, int32_t z1, float a2,
+                                  int32_t z2, float ay, int32_t zy)
+{
+#pragma clang fp contract(off)
+    const double f1 = (double)a1 * (double)(u - z1);
+    const double f2 = (double)a2 * (double)(v - z2);
+    return requant_f64<BITS>(f1 * f2, (double)ay, zy);
+}
+
+template <int BITS, int OP>
+__device__ inline int32_t binary_one(int32_t u, int32_t v, float a1, int32_t z1, float a2,
+                                     int32_t z2, float ay, int32_t zy)
+{
+    if constexpr (OP == 0) return add_one<BITS>(u, v, a1, z1, a2, z2, ay, zy);
+    else return mul_one<BITS>(u, v, a1, z1, a2, z2, ay, zy);
+}
+
 // n4 groups of four codes through 8-byte loads (aligned buffers), the
 // codes [begin, n) one by one
-template <int BITS>
+// OP 0: sum, OP 1: product of the dequantized codes.
+template <int BITS, int OP>
 __global__ __launch_bounds__(kThreads) void add_requant_kernel(
     const int16_t* __restrict__ x1, float a1, int32_t z1, const int16_t* __restrict__ x2,
     float a2, int32_t z2, int64_t n4, int64_t begin, int64_t n, float ay, int32_t zy,
@@ -68,10 +89,10 @@ __global__ __launch_bounds__(kThreads) void add_requant_kernel(
     for (int64_t i = t0; i < n4; i += stride) {
         const short4 u = reinterpret_cast<const short4*>(x1)[i];
         const short4 v = reinterpret_cast<const short4*>(x2)[i];
-        const int32_t r0 = add_one<BITS>(u.x, v.x, a1, z1, a2, z2, ay, zy);
-        const int32_t r1 = add_one<BITS>(u.y, v.y, a1, z1, a2, z2, ay, zy);
-        const int32_t r2 = add_one<BITS>(u.z, v.z, a1, z1, a2, z2, ay, zy);
-        const int32_t r3 = add_one<BITS>(u.w, v.w, a1, z1, a2, z2, ay, zy);
+        const int32_t r0 = binary_one<BITS, OP>(u.x, v.x, a1, z1, a2, z2, ay, zy);
+        const int32_t r1 = binary_one<BITS, OP>(u.y, v.y, a1, z1, a2, z2, ay, zy);
+        const int32_t r2 = binary_one<BITS, OP>(u.z, v.z, a1, z1, a2, z2, ay, zy);
+        const int32_t r3 = binary_one<BITS, OP>(u.w, v.w, a1, z1, a2, z2, ay, zy);
         if constexpr (BITS == 8)
             reinterpret_cast<char4*>(y)[i] = make_char4((char)r0, (char)r1, (char)r2, (char)r3);
         else
@@ -79,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void add_requant_kernel(
                 make_short4((short)r0, (short)r1, (short)r2, (short)r3);
     }
     for (int64_t i = begin + t0; i < n; i += stride)
-        store_code<BITS>(y, i, add_one<BITS>(x1[i], x2[i], a1, z1, a2, z2, ay, zy));
+        store_code<BITS>(y, i, binary_one<BITS, OP>(x1[i], x2[i], a1, z1, a2, z2, ay, zy));
 }
 
 // ---------------------------------------------------------------------------
@@ -246,15 +267,27 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_regs_kernel(const int16_t* _
     }
 }
 
+// Keys row m of a causal softmax sees: (m mod period) + offset + 1, at most
+// K (period 0: all K).
+__device__ inline int64_t causal_keys(int64_t m, int64_t K, int64_t period, int64_t offset)
+{
+    if (period <= 0) return K;
+    const int64_t n = m % period + offset + 1;
+    return n < K ? n : K;
+}
+
 template <int BITS, int NCH>
 __global__ __launch_bounds__(kThreads) void softmax_regs_kernel(const int16_t* __restrict__ x,
                                                                 int64_t K, float ax, float ay,
-                                                                int32_t zy, void* __restrict__ y)
+                                                                int32_t zy, int64_t period,
+                                                                int64_t offset,
+                                                                void* __restrict__ y)
 {
 #pragma clang fp contract(off)
     __shared__ int32_t red_i[kThreads / 64];
     __shared__ double red_d[kThreads / 64];
     const int64_t m = blockIdx.x;
+    const int64_t n = causal_keys(m, K, period, offset);  // keys this row sees
     RowRegs<NCH> r;
     r.load(x + m * K, K);
     int32_t mx = -32768;
@@ -262,7 +295,9 @@ __global__ __launch_bounds__(kThreads) void softmax_regs_kernel(const int16_t* _
     for (int c = 0; c < NCH; ++c)
         if (r.live[c])
 #pragma unroll
-            for (int u = 0; u < 8; ++u) mx = max(mx, (int32_t)r.v[c][u]);
+            for (int u = 0; u < 8; ++u)
+                if (8 * ((int64_t)threadIdx.x + kThreads * c) + u < n)
+                    mx = max(mx, (int32_t)r.v[c][u]);
     for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o));
     if ((threadIdx.x & 63) == 0) red_i[threadIdx.x >> 6] = mx;
     __syncthreads();
@@ -275,7 +310,8 @@ __global__ __launch_bounds__(kThreads) void softmax_regs_kernel(const int16_t* _
     for (int c = 0; c < NCH; ++c)
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-            e[c][u] = r.live[c] ? exp(a * (double)((int32_t)r.v[c][u] - mx)) : 0.0;
+            const bool seen = r.live[c] && 8 * ((int64_t)threadIdx.x + kThreads * c) + u < n;
+            e[c][u] = seen ? exp(a * (double)((int32_t)r.v[c][u] - mx)) : 0.0;
             sum += e[c][u];
         }
     for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
@@ -329,15 +365,17 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const int16_t* __rest
 template <int BITS>
 __global__ __launch_bounds__(kThreads) void softmax_kernel(const int16_t* __restrict__ x,
                                                            int64_t K, float ax, float ay,
-                                                           int32_t zy, void* __restrict__ y)
+                                                           int32_t zy, int64_t period,
+                                                           int64_t offset, void* __restrict__ y)
 {
 #pragma clang fp contract(off)
     __shared__ int32_t red_i[kThreads / 64];
     __shared__ double red_d[kThreads / 64];
     const int64_t m = blockIdx.x;
+    const int64_t n = causal_keys(m, K, period, offset);  // keys this row sees
     const int16_t* row = x + m * K;
     int32_t mx = -32768;
-    for (int64_t k = threadIdx.x; k < K; k += kThreads) mx = max(mx, (int32_t)row[k]);
+    for (int64_t k = threadIdx.x; k < n; k += kThreads) mx = max(mx, (int32_t)row[k]);
     for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o));
     if ((threadIdx.x & 63) == 0) red_i[threadIdx.x >> 6] = mx;
     __syncthreads();
@@ -345,7 +383,7 @@ __global__ __launch_bounds__(kThreads) void softmax_kernel(const int16_t* __rest
     for (int w = 0; w < kThreads / 64; ++w) mx = max(mx, red_i[w]);
     const double a = (double)ax;
     double sum = 0.0;
-    for (int64_t k = threadIdx.x; k < K; k += kThreads)
+    for (int64_t k = threadIdx.x; k < n; k += kThreads)
         sum += exp(a * (double)((int32_t)row[k] - mx));
     for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
     if ((threadIdx.x & 63) == 0) red_d[threadIdx.x >> 6] = sum;
@@ -354,16 +392,17 @@ __global__ __launch_bounds__(kThreads) void softmax_kernel(const int16_t* __rest
 #pragma unroll
     for (int w = 0; w < kThreads / 64; ++w) sum += red_d[w];
     for (int64_t k = threadIdx.x; k < K; k += kThreads) {
-        const double e = exp(a * (double)((int32_t)row[k] - mx));
+        const double e = k < n ? exp(a * (double)((int32_t)row[k] - mx)) : 0.0;
         store_code<BITS>(y, m * K + k, requant_f64<BITS>(e / sum, (double)ay, zy));
     }
 }
 
 }  // namespace
 
-hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
-                              float a2, int32_t z2, int64_t n, float ay, int32_t zy,
-                              int32_t bits, void* y, hipStream_t st)
+template <int OP>
+static hipError_t launch_binary(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                                float a2, int32_t z2, int64_t n, float ay, int32_t zy,
+                                int32_t bits, void* y, hipStream_t st)
 {
     const uintptr_t ya = bits == 8 ? 4 : 8;
     const bool vec = ((uintptr_t)x1 % 8) == 0 && ((uintptr_t)x2 % 8) == 0 &&
@@ -371,12 +410,26 @@ hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int
     const int64_t n4 = vec ? n / 4 : 0;
     const int g = grid_for(vec ? n4 : n, kThreads * 2, 256 * 64);
     if (bits == 8)
-        add_requant_kernel<8><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n4, n4 * 4, n, ay,
-                                                      zy, y);
+        add_requant_kernel<8, OP><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n4, n4 * 4, n,
+                                                          ay, zy, y);
     else
-        add_requant_kernel<16><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n4, n4 * 4, n, ay,
-                                                       zy, y);
+        add_requant_kernel<16, OP><<<g, kThreads, 0, st>>>(x1, a1, z1, x2, a2, z2, n4, n4 * 4, n,
+                                                           ay, zy, y);
     return hipGetLastError();
+}
+
+hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                              float a2, int32_t z2, int64_t n, float ay, int32_t zy,
+                              int32_t bits, void* y, hipStream_t st)
+{
+    return launch_binary<0>(x1, a1, z1, x2, a2, z2, n, ay, zy, bits, y, st);
+}
+
+hipError_t launch_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                              float a2, int32_t z2, int64_t n, float ay, int32_t zy,
+                              int32_t bits, void* y, hipStream_t st)
+{
+    return launch_binary<1>(x1, a1, z1, x2, a2, z2, n, ay, zy, bits, y, st);
 }
 
 hipError_t launch_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t zy, int32_t bits,
@@ -424,10 +477,11 @@ void rmsnorm_regs(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
 }
 
 template <int BITS, int NCH>
-void softmax_regs(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy, void* y,
-                  hipStream_t st)
+void softmax_regs(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
+                  int64_t period, int64_t offset, void* y, hipStream_t st)
 {
-    softmax_regs_kernel<BITS, NCH><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, y);
+    softmax_regs_kernel<BITS, NCH><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, period,
+                                                                    offset, y);
 }
 
 // register-resident rows: K % 8 == 0, 16-byte aligned x and y, chunks per
@@ -464,23 +518,90 @@ hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int3
 }
 
 hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
-                          int32_t bits, void* y, hipStream_t st)
+                          int32_t bits, int64_t period, int64_t offset, void* y, hipStream_t st)
 {
     const int ch = row_chunks(x, y, K);
+    const int64_t P = period, O = offset;
     if (ch > 0) {
         if (bits == 8) {
-            if (ch == 1) softmax_regs<8, 1>(x, M, K, ax, ay, zy, y, st);
-            else if (ch == 2) softmax_regs<8, 2>(x, M, K, ax, ay, zy, y, st);
-            else softmax_regs<8, 4>(x, M, K, ax, ay, zy, y, st);
+            if (ch == 1) softmax_regs<8, 1>(x, M, K, ax, ay, zy, P, O, y, st);
+            else if (ch == 2) softmax_regs<8, 2>(x, M, K, ax, ay, zy, P, O, y, st);
+            else softmax_regs<8, 4>(x, M, K, ax, ay, zy, P, O, y, st);
         } else {
-            if (ch == 1) softmax_regs<16, 1>(x, M, K, ax, ay, zy, y, st);
-            else if (ch == 2) softmax_regs<16, 2>(x, M, K, ax, ay, zy, y, st);
-            else softmax_regs<16, 4>(x, M, K, ax, ay, zy, y, st);
+            if (ch == 1) softmax_regs<16, 1>(x, M, K, ax, ay, zy, P, O, y, st);
+            else if (ch == 2) softmax_regs<16, 2>(x, M, K, ax, ay, zy, P, O, y, st);
+            else softmax_regs<16, 4>(x, M, K, ax, ay, zy, P, O, y, st);
         }
         return hipGetLastError();
     }
-    if (bits == 8) softmax_kernel<8><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, y);
-    else softmax_kernel<16><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, y);
+    if (bits == 8) softmax_kernel<8><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, P, O, y);
+    else softmax_kernel<16><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, ay, zy, P, O, y);
+    return hipGetLastError();
+}
+
+}  // namespace mq
+
+namespace mq {
+namespace {
+
+// Rotary position embedding.  The angle table holds cos and sin of
+// (t + pos0) * base^(-2i/D) for every token t and pair i (fp64: inverse
+// frequency by pow, one product, cos, sin); the main kernel rotates each
+// pair (i, i + D/2) of every head of x [T][H * D] and requantizes.
+__global__ __launch_bounds__(256) void rope_table_kernel(int64_t T, int64_t half, int64_t D,
+                                                         double base, int64_t pos0,
+                                                         double* __restrict__ cs)
+{
+#pragma clang fp contract(off)
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= T * half) return;
+    const int64_t t = idx / half, i = idx - t * half;
+    const double inv = pow(base, -(double)(2 * i) / (double)D);
+    const double ang = (double)(t + pos0) * inv;
+    cs[2 * idx] = cos(ang);
+    cs[2 * idx + 1] = sin(ang);
+}
+
+template <int BITS>
+__global__ __launch_bounds__(256) void rope_kernel(const int16_t* __restrict__ x, int64_t T,
+                                                   int64_t H, int64_t D, float ax, int32_t zx,
+                                                   const double* __restrict__ cs, float ay,
+                                                   int32_t zy, void* __restrict__ y)
+{
+#pragma clang fp contract(off)
+    const int64_t half = D / 2;
+    const int64_t pairs = T * H * half;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < pairs; p += stride) {
+        const int64_t i = p % half, th = p / half;  // th = t * H + h
+        const int64_t t = th / H;
+        const int64_t j0 = th * D + i, j1 = j0 + half;
+        const double c = cs[2 * (t * half + i)], sn = cs[2 * (t * half + i) + 1];
+        const double u = (double)ax * (double)((int32_t)x[j0] - zx);
+        const double w = (double)ax * (double)((int32_t)x[j1] - zx);
+        store_code<BITS>(y, j0, requant_f64<BITS>(u * c - w * sn, (double)ay, zy));
+        store_code<BITS>(y, j1, requant_f64<BITS>(w * c + u * sn, (double)ay, zy));
+    }
+}
+
+}  // namespace
+
+hipError_t launch_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                       double base, int64_t pos0, float ay, int32_t zy, int32_t bits,
+                       double* table, void* y, hipStream_t st)
+{
+    const int64_t half = D / 2;
+    const int64_t entries = T * half;
+    if (entries == 0) return hipSuccess;
+    rope_table_kernel<<<(unsigned)((entries + 255) / 256), 256, 0, st>>>(T, half, D, base, pos0,
+                                                                         table);
+    const int64_t pairs = T * H * half;
+    int64_t g = (pairs + 255) / 256;
+    if (g > 256 * 64) g = 256 * 64;
+    if (bits == 8)
+        rope_kernel<8><<<(unsigned)g, 256, 0, st>>>(x, T, H, D, ax, zx, table, ay, zy, y);
+    else
+        rope_kernel<16><<<(unsigned)g, 256, 0, st>>>(x, T, H, D, ax, zx, table, ay, zy, y);
     return hipGetLastError();
 }
 

@@ -149,6 +149,35 @@ mq_status mq_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t*
                                            as_stream(stream)));
 }
 
+mq_status mq_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2, float a2,
+                         int32_t z2, int64_t numel, float ay, int32_t zy, int32_t out_bits,
+                         void* y, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || !act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(a1) || !finite_pos(a2) || !finite_pos(ay)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(z1, 16) || !zp_ok(z2, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (numel == 0) return MQ_OK;
+    if (!x1 || !x2 || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_mul_requant(x1, a1, z1, x2, a2, z2, numel, ay, zy, out_bits, y,
+                                           as_stream(stream)));
+}
+
+mq_status mq_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                  double base, int64_t pos0, float ay, int32_t zy, int32_t out_bits,
+                  double* table, void* y, void* stream)
+{
+    if (T < 0 || H < 1 || D < 2 || D % 2 != 0 || !act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (H > kMaxElems / D || (T > 0 && T > kMaxElems / (H * D))) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(ax) || !finite_pos(ay) || !std::isfinite(base) || !(base > 1.0))
+        return MQ_ERR_INVALID_ARG;
+    if (pos0 < 0 || pos0 > ((int64_t)1 << 40)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(zx, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (T == 0) return MQ_OK;
+    if (!x || !y || !table) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_rope(x, T, H, D, ax, zx, base, pos0, ay, zy, out_bits, table, y,
+                                    as_stream(stream)));
+}
+
 mq_status mq_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t zy, int32_t out_bits,
                        void* lut, void* stream)
 {
@@ -191,7 +220,22 @@ mq_status mq_softmax(const int16_t* x, int64_t M, int64_t K, float ax, int32_t z
     if (!zp_ok(zx, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
     if (M == 0) return MQ_OK;
     if (!x || !y) return MQ_ERR_INVALID_ARG;
-    return from_hip(mq::launch_softmax(x, M, K, ax, ay, zy, out_bits, y, as_stream(stream)));
+    return from_hip(mq::launch_softmax(x, M, K, ax, ay, zy, out_bits, 0, 0, y, as_stream(stream)));
+}
+
+mq_status mq_softmax_causal(const int16_t* x, int64_t M, int64_t K, float ax, int32_t zx,
+                            float ay, int32_t zy, int32_t out_bits, int64_t period,
+                            int64_t offset, void* y, void* stream)
+{
+    if (M < 0 || M > 0x7FFFFFFF || K < 1 || K > (1 << 20) || !act_bits_ok(out_bits))
+        return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(ax) || !finite_pos(ay)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(zx, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (period < 1 || offset < 0 || offset > ((int64_t)1 << 40)) return MQ_ERR_INVALID_ARG;
+    if (M == 0) return MQ_OK;
+    if (!x || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_softmax(x, M, K, ax, ay, zy, out_bits, period, offset, y,
+                                       as_stream(stream)));
 }
 
 mq_status mq_smooth_scales(const float* x, int64_t M, int64_t K, const float* w, int64_t N,

@@ -77,6 +77,12 @@ hipError_t launch_smooth_scales(const float* x, int64_t M, int64_t K, const floa
 hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
                               float a2, int32_t z2, int64_t n, float ay, int32_t zy,
                               int32_t bits, void* y, hipStream_t st);
+hipError_t launch_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                              float a2, int32_t z2, int64_t n, float ay, int32_t zy,
+                              int32_t bits, void* y, hipStream_t st);
+hipError_t launch_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                       double base, int64_t pos0, float ay, int32_t zy, int32_t bits,
+                       double* table, void* y, hipStream_t st);
 hipError_t launch_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t zy, int32_t bits,
                             void* lut, hipStream_t st);
 hipError_t launch_lut_apply(const int16_t* x, int64_t n, const void* lut, int32_t bits, void* y,
@@ -85,7 +91,7 @@ hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int3
                           const float* gamma, float eps, float ay, int32_t zy, int32_t bits,
                           void* y, hipStream_t st);
 hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
-                          int32_t bits, void* y, hipStream_t st);
+                          int32_t bits, int64_t period, int64_t offset, void* y, hipStream_t st);
 
 hipError_t launch_attn_sums(const int16_t* a, int64_t lda, int64_t a_bs, int32_t H, int64_t M,
                             const int8_t* b, int64_t ldb, int64_t b_bs, int32_t G, int64_t N,

@@ -319,3 +319,29 @@ def test_attn_matmul_sizes_and_empty_calls():
     assert L.mq_transpose_i8(NZ, 4, 5, 4, NZ, None) == 1
     assert L.mq_transpose_i8(None, 4, 5, 5, NZ, None) == 1
     assert L.mq_transpose_i8(NZ, -1, 5, 5, NZ, None) == 1
+
+
+@pytest.mark.parametrize("call", [
+    lambda L: L.mq_softmax_causal(NZ, 4, 8, 1.0, 0, 1.0, 0, 16, 0, 0, NZ, None),
+    lambda L: L.mq_softmax_causal(NZ, 4, 8, 1.0, 0, 1.0, 0, 16, 4, -1, NZ, None),
+    lambda L: L.mq_softmax_causal(NZ, 4, 0, 1.0, 0, 1.0, 0, 16, 4, 0, NZ, None),
+    lambda L: L.mq_softmax_causal(None, 4, 8, 1.0, 0, 1.0, 0, 16, 4, 0, NZ, None),
+    lambda L: L.mq_softmax_causal(NZ, 4, 8, 0.0, 0, 1.0, 0, 16, 4, 0, NZ, None),
+])
+def test_softmax_causal_rejects_invalid_arguments(call):
+    assert call(mq.lib()) == 1
+
+
+@pytest.mark.parametrize("call", [
+    lambda L: L.mq_mul_requant(NZ, 0.0, 0, NZ, 1.0, 0, 10, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_mul_requant(NZ, 1.0, 0, NZ, 1.0, 0, 10, 1.0, 200, 8, NZ, None),
+    lambda L: L.mq_mul_requant(NZ, 1.0, 0, None, 1.0, 0, 10, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_rope(NZ, 4, 2, 3, 1.0, 0, 10000.0, 0, 1.0, 0, 16, NZ, NZ, None),
+    lambda L: L.mq_rope(NZ, 4, 0, 8, 1.0, 0, 10000.0, 0, 1.0, 0, 16, NZ, NZ, None),
+    lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, 1.0, 0, 1.0, 0, 16, NZ, NZ, None),
+    lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, 10000.0, -1, 1.0, 0, 16, NZ, NZ, None),
+    lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, 10000.0, 0, 1.0, 0, 16, None, NZ, None),
+    lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, float("nan"), 0, 1.0, 0, 16, NZ, NZ, None),
+])
+def test_mul_and_rope_reject_invalid_arguments(call):
+    assert call(mq.lib()) == 1

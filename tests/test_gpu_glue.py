@@ -97,3 +97,57 @@ def test_softmax_parity(M, K):
     xr = torch.tensor(np.float64(np.float32(ax)) * (x.astype(np.float64) - zx))
     pre = torch.softmax(xr, dim=1).numpy() / np.float64(np.float32(ay))
     _equal_but_ties(y, ref, pre)
+
+
+@pytest.mark.parametrize("M,K,period,offset", [(4 * 256, 256, 256, 0), (3 * 100, 100, 100, 0),
+                                               (2 * 64, 1024, 64, 960), (5, 4099, 5, 2)])
+def test_softmax_causal_parity(M, K, period, offset):
+    import torch
+    mq = _mq()
+    rng = np.random.default_rng(M + K + offset)
+    x = rng.integers(-9000, 9000, (M, K)).astype(np.int16)
+    ax, zx, ay, zy = 1e-3, 12, 1.0 / 65535, -32768
+    y = mq.mq_softmax_causal(_dev(x), ax, zx, ay, zy, period, offset, 16).cpu().numpy()
+    ref = oracle.softmax(x, ax, zx, ay, zy, 16, causal_period=period, causal_offset=offset)
+    n = np.minimum(np.arange(M) % period + offset + 1, K)
+    mask = np.arange(K)[None, :] < n[:, None]
+    xr = np.float64(np.float32(ax)) * (x.astype(np.float64) - zx)
+    xr = np.where(mask, xr, -np.inf)
+    pre = torch.softmax(torch.tensor(xr), dim=1).numpy() / np.float64(np.float32(ay))
+    _equal_but_ties(y, ref, pre)
+    assert np.all(y[~mask] == zy)
+
+
+@pytest.mark.parametrize("n", [1, 777, 1024 * 5632])
+@pytest.mark.parametrize("out_bits", [8, 16])
+def test_mul_requant_parity(n, out_bits):
+    mq = _mq()
+    rng = np.random.default_rng(n + out_bits + 5)
+    x1 = rng.integers(-32768, 32768, n).astype(np.int16)
+    x2 = rng.integers(-32768, 32768, n).astype(np.int16)
+    args = (3.1e-4, -12, 7.7e-4, 300, 0.05 if out_bits == 8 else 1e-3, 5)
+    y = mq.mq_mul_requant(_dev(x1), args[0], args[1], _dev(x2), args[2], args[3], args[4],
+                          args[5], out_bits)
+    ref = oracle.mul_requant(x1, args[0], args[1], x2, args[2], args[3], args[4], args[5], out_bits)
+    assert np.array_equal(y.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("T,H,D,pos0,out_bits", [(1024, 32, 64, 0, 16), (1024, 4, 64, 0, 8),
+                                                 (7, 3, 128, 1000, 16), (1, 2, 2, 5, 8)])
+def test_rope_parity(T, H, D, pos0, out_bits):
+    mq = _mq()
+    rng = np.random.default_rng(T + H + D + pos0)
+    x = rng.integers(-30000, 30000, (T, H * D)).astype(np.int16)
+    ax, zx = 2e-4, -7
+    ay, zy = (3e-4, 4) if out_bits == 16 else (0.05, -2)
+    y = mq.mq_rope(_dev(x), H, ax, zx, ay, zy, out_bits, pos0=pos0).cpu().numpy()
+    ref = oracle.rope(x, H, ax, zx, ay, zy, out_bits, pos0=pos0)
+    # fp64 reference for the tie check
+    xf = np.float64(np.float32(ax)) * (x.astype(np.float64) - zx)
+    xh = xf.reshape(T, H, D)
+    inv = 10000.0 ** (-np.arange(0, D, 2, dtype=np.float64) / D)
+    ang = (np.arange(T, dtype=np.float64) + pos0)[:, None] * inv[None, :]
+    c, s = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+    u, w = xh[..., :D // 2], xh[..., D // 2:]
+    pre = np.concatenate([u * c - w * s, w * c + u * s], axis=-1).reshape(T, H * D)
+    _equal_but_ties(y, ref, pre / np.float64(np.float32(ay)))

@@ -1053,3 +1053,93 @@ def test_attn_matmul_invariances():
     a[1] = a[0]
     y4 = oracle.attn_matmul(a, b, *args)
     assert np.array_equal(y4[0], y4[1]) and not np.array_equal(y4[0], y4[2])
+
+
+def test_softmax_causal_pins():
+    # causal rows equal the plain softmax over each row's visible keys, the
+    # hidden keys get the probability-0 code; heads repeat every `period`
+    # rows; an offset past the row length is the plain softmax
+    rng = np.random.default_rng(91)
+    T, heads = 9, 3
+    x = rng.integers(-9000, 9000, (heads * T, T)).astype(np.int16)
+    args = (1e-3, 5, 1.0 / 65535, -32768, 16)
+    y = oracle.softmax(x, *args, causal_period=T)
+    for m in range(heads * T):
+        n = m % T + 1
+        ref = oracle.softmax(x[m:m + 1, :n], *args)[0]
+        assert np.array_equal(y[m, :n], ref), m
+        assert np.all(y[m, n:] == -32768), m
+    y2 = oracle.softmax(x, *args, causal_period=T, causal_offset=3)
+    for m in range(heads * T):
+        n = min(T, m % T + 4)
+        assert np.array_equal(y2[m, :n], oracle.softmax(x[m:m + 1, :n], *args)[0])
+        assert np.all(y2[m, n:] == -32768)
+    assert np.array_equal(oracle.softmax(x, *args, causal_period=T, causal_offset=T),
+                          oracle.softmax(x, *args))
+
+
+def _np_requant(v, ay, zy, bits):
+    lo, hi = -(1 << (bits - 1)), (1 << (bits - 1)) - 1
+    return np.clip(np.rint(v / np.float64(np.float32(ay))) + zy, lo, hi).astype(np.int64)
+
+
+def test_mul_requant_pins():
+    # the product of the two dequantized factors (each exact in fp64, one
+    # IEEE rounding for the product) gives the same bits as numpy's fp64
+    # arithmetic; equal to the exact rational product except at rounding
+    # ties of v / ay
+    from fractions import Fraction
+    rng = np.random.default_rng(93)
+    x1 = rng.integers(-32768, 32768, 5000).astype(np.int16)
+    x2 = rng.integers(-32768, 32768, 5000).astype(np.int16)
+    a1, z1, a2, z2, ay, zy = 3e-4, -17, 7e-4, 250, 0.004, -3
+    for bits in (8, 16):
+        y = oracle.mul_requant(x1, a1, z1, x2, a2, z2, ay, zy, bits)
+        f1 = np.float64(np.float32(a1)) * (x1.astype(np.float64) - z1)
+        f2 = np.float64(np.float32(a2)) * (x2.astype(np.float64) - z2)
+        assert np.array_equal(y.astype(np.int64), _np_requant(f1 * f2, ay, zy, bits))
+    y = oracle.mul_requant(x1, a1, z1, x2, a2, z2, ay, zy, 16).astype(int)
+    fa1, fa2, fay = (Fraction(float(np.float32(v))) for v in (a1, a2, ay))
+    for i in range(0, 5000, 7):
+        q = fa1 * (int(x1[i]) - z1) * fa2 * (int(x2[i]) - z2) / fay
+        exact = max(-32768, min(32767, round(q) + zy))  # round: half to even, like rint
+        near_tie = abs(q - math.floor(q) - Fraction(1, 2)) < Fraction(1, 10 ** 9)
+        assert y[i] == exact or (near_tie and abs(y[i] - exact) == 1), i
+    # a factor at its zero-point gives the output zero-point
+    assert np.all(oracle.mul_requant(np.full(9, z1, np.int16), a1, z1, x2[:9], a2, z2, ay, zy, 8) == zy)
+
+
+def test_rope_pins():
+    rng = np.random.default_rng(94)
+    T, H, D = 6, 3, 8
+    x = rng.integers(-20000, 20000, (T, H * D)).astype(np.int16)
+    ax, zx = 2e-4, 11
+    # position 0: the identity (cos 0 = 1, sin 0 = 0 exactly)
+    y0 = oracle.rope(x[:1], H, ax, zx, ax, zx, 16)
+    assert np.array_equal(y0, x[:1])
+    # an independent numpy formulation with the rotate-half layout
+    ay, zy = 3e-4, -5
+    y = oracle.rope(x, H, ax, zx, ay, zy, 16, pos0=3)
+    xf = np.float64(np.float32(ax)) * (x.astype(np.float64) - zx)
+    xh = xf.reshape(T, H, D)
+    inv = 10000.0 ** (-np.arange(0, D, 2, dtype=np.float64) / D)
+    ang = (np.arange(T, dtype=np.float64) + 3)[:, None] * inv[None, :]
+    cos, sin = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+    u, w = xh[..., :D // 2], xh[..., D // 2:]
+    ref = np.concatenate([u * cos - w * sin, w * cos + u * sin], axis=-1).reshape(T, H * D)
+    pre = ref / np.float64(np.float32(ay))
+    got, exp = y.astype(np.int64), _np_requant(ref, ay, zy, 16)
+    tie = np.abs(pre - np.floor(pre) - 0.5) < 1e-9
+    assert np.all((got == exp) | (tie & (np.abs(got - exp) <= 1)))
+    # a hand-worked pair: D = 4, head 0, the unit vector on dimension 0 at
+    # position 1 goes to (cos 1, 0, sin 1, 0)
+    e = np.zeros((2, 4), np.int16)
+    e[1, 0] = 10000
+    r = oracle.rope(e, 1, 1e-4, 0, 1e-4, 0, 16)
+    assert r[1].tolist() == [round(10000 * np.cos(1.0)), 0, round(10000 * np.sin(1.0)), 0]
+    # norms of every rotated pair are kept within the requant rounding
+    ya = oracle.rope(x, H, ax, zx, ax, zx, 16, pos0=7).astype(np.float64) - zx
+    xa = x.astype(np.float64) - zx
+    n0 = xa.reshape(T, H, 2, D // 2) ** 2
+    n1 = ya.reshape(T, H, 2, D // 2) ** 2
+    assert np.allclose(np.sqrt(n0.sum(axis=2)), np.sqrt(n1.sum(axis=2)), atol=1.0)
