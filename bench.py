@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--calib-sweep", action="store_true",
                     help="time the calibration-side kernels (range learning, SmoothQuant "
                          "scales) instead of the step")
+    ap.add_argument("--block-sweep", action="store_true",
+                    help="time one whole TinyLlama decoder block on integer codes (1024 tokens) "
+                         "and each of its steps, and exit")
     ap.add_argument("--attn-sweep", action="store_true",
                     help="time the attention matmuls (Q K^T, P V) and the value transpose "
                          "at the TinyLlama shape, seq 1024, and exit")
@@ -594,8 +597,38 @@ def attn_sweep():
         print(json.dumps(rec), flush=True)
 
 
+def block_sweep(T=1024):
+    """One TinyLlama decoder block on integer codes, every step on the GPU
+    (paper_2408_13933_amd.block): RMSNorm, q/k/v projections, RoPE, Q K^T,
+    causal softmax, P V, o projection, residual add, RMSNorm, gate/up, SiLU
+    table, gated product, down projection, residual add.  Inputs: seeded
+    synthetic residual stream and weights (workloads.make_block), static
+    formats from the float pass.  Prints the graph-replayed time of each
+    step and of the whole block."""
+    import torch
+
+    from paper_2408_13933_amd import block as blk
+    from paper_2408_13933_amd import workloads as wl
+
+    g = blk.BlockGPU(wl.make_block(T))
+    g.run()
+    torch.cuda.synchronize()
+    total = 0.0
+    for name, fn in g.stages():
+        us = _time_graph(fn)
+        total += us
+        print(json.dumps({"step": name, "tokens": T, "us_graph_replay": round(us, 2)}), flush=True)
+    us = _time_graph(g.run, reps=5, per_graph=2)
+    print(json.dumps({"block": "tinyllama_w8a8_attn_a16", "tokens": T,
+                      "us_graph_replay": round(us, 2), "sum_of_steps_us": round(total, 2),
+                      "ops": g.ops(), "TOPS": round(g.ops() / us / 1e6, 1)}), flush=True)
+
+
 def main():
     args = parse()
+    if args.block_sweep:
+        block_sweep()
+        return
     if args.attn_sweep:
         attn_sweep()
         return

@@ -314,3 +314,119 @@ def scaled_layer(layer: Layer, M=None, K=None, N=None, name=None) -> Layer:
                                N=layer.N if N is None else N,
                                name=layer.name if name is None else name,
                                smooth_len=K2 if layer.smooth else 0)
+
+
+# ---------------------------------------------------------------------------
+# One whole decoder block (TinyLlama-shaped: hidden 2048, 32 query heads, 4
+# key/value heads of 64, feed-forward 5632) on integer codes.  The inputs
+# are the block's residual stream, the seven projection matrices and the two
+# RMSNorm gains, drawn as above; the static float range of every
+# intermediate comes from an fp64 float forward pass of the same block (the
+# paper calibrates its static activation ranges on a float model, Section
+# 4.2).  The float pass (fp32 products, fp64 elsewhere) is a statistic of
+# the synthetic data, like the layer output ranges above: no quantization
+# arithmetic happens here.
+
+BLOCK_DIMS = dict(hidden=2048, heads=32, kv_heads=4, head_dim=64, ffn=5632, eps=1e-5,
+                  rope_base=10000.0)
+BLOCK_LINEARS = (("q_proj", "hidden", "hidden"), ("k_proj", "kv", "hidden"),
+                 ("v_proj", "kv", "hidden"), ("o_proj", "hidden", "hidden"),
+                 ("gate_proj", "ffn", "hidden"), ("up_proj", "ffn", "hidden"),
+                 ("down_proj", "hidden", "ffn"))
+
+
+@dataclasses.dataclass
+class BlockData:
+    T: int
+    h0: np.ndarray                 # fp32 [T][hidden], residual stream entering the block
+    w: dict                        # name -> fp32 [N][K]
+    gamma1: np.ndarray             # fp32 [hidden]
+    gamma2: np.ndarray
+    ranges: dict                   # stage -> (f_min, f_max), static ranges
+    floats: Optional[dict] = None  # stage -> float values of the float pass (keep_floats)
+
+
+def _block_dim(name: str) -> int:
+    d = BLOCK_DIMS
+    return {"hidden": d["hidden"], "kv": d["kv_heads"] * d["head_dim"], "ffn": d["ffn"]}[name]
+
+
+def _rope_f64(x: np.ndarray, heads: int, base: float) -> np.ndarray:
+    T, HD = x.shape
+    D = HD // heads
+    xh = x.reshape(T, heads, D)
+    inv = base ** (-np.arange(0, D, 2, dtype=np.float64) / D)
+    ang = np.arange(T, dtype=np.float64)[:, None] * inv[None, :]
+    c, s = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+    u, w = xh[..., :D // 2], xh[..., D // 2:]
+    return np.concatenate([u * c - w * s, w * c + u * s], axis=-1).reshape(T, HD)
+
+
+def _rmsnorm_f64(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    return x / np.sqrt(np.mean(x * x, axis=1, keepdims=True) + eps) * g[None, :]
+
+
+def _range(v: np.ndarray, pad: float = 1.05) -> tuple:
+    lo, hi = float(v.min()), float(v.max())
+    return (float(np.float32(min(lo, 0.0) * pad)), float(np.float32(max(hi, 0.0) * pad)))
+
+
+def make_block(T: int, seed: str = "block_tinyllama", keep_floats: bool = False) -> BlockData:
+    d = BLOCK_DIMS
+    H, G, D, F = d["heads"], d["kv_heads"], d["head_dim"], d["ffn"]
+    hid = d["hidden"]
+    h0 = gen_activations(T, hid, "outlier", (seed, "h0"))
+    w = {n: gen_weights(_block_dim(a), _block_dim(b), (seed, n)) for n, a, b in BLOCK_LINEARS}
+    rng = _rng("gamma", seed)
+    g1 = rng.uniform(0.5, 1.5, hid).astype(np.float32)
+    g2 = rng.uniform(0.5, 1.5, hid).astype(np.float32)
+    # float pass: fp32 products (ranges need no more), the rest in fp64
+    def mm(x, name):
+        return (x.astype(np.float32) @ w[name].T).astype(np.float64)
+
+    r = {}
+    h = h0.astype(np.float64)
+    r["h0"] = _range(h)
+    x1 = _rmsnorm_f64(h, g1.astype(np.float64), d["eps"])
+    r["x1"] = _range(x1)
+    q, k, v = mm(x1, "q_proj"), mm(x1, "k_proj"), mm(x1, "v_proj")
+    r["q"], r["k"], r["v"] = _range(q), _range(k), _range(v)
+    qr, kr = _rope_f64(q, H, d["rope_base"]), _rope_f64(k, G, d["rope_base"])
+    r["qr"], r["kr"] = _range(qr), _range(kr)
+    qh = qr.reshape(T, H, D).transpose(1, 0, 2)
+    kh = kr.reshape(T, G, D).transpose(1, 0, 2)
+    vh = v.reshape(T, G, D).transpose(1, 0, 2)
+    scores = np.stack([qh[h_] @ kh[h_ // (H // G)].T for h_ in range(H)])
+    r["scores"] = _range(scores)
+    z = scores / np.sqrt(D)
+    mask = np.triu(np.ones((T, T), dtype=bool), 1)
+    z = np.where(mask[None], -np.inf, z)
+    z = z - z.max(axis=2, keepdims=True)
+    p = np.exp(z)
+    p /= p.sum(axis=2, keepdims=True)
+    r["probs"] = (0.0, 1.0)
+    ctx = np.stack([p[h_] @ vh[h_ // (H // G)] for h_ in range(H)])  # [H][T][D]
+    ctx = ctx.transpose(1, 0, 2).reshape(T, H * D)
+    r["ctx"] = _range(ctx)
+    o = mm(ctx, "o_proj")
+    r["o"] = _range(o)
+    h1 = h + o
+    r["h1"] = _range(h1)
+    x2 = _rmsnorm_f64(h1, g2.astype(np.float64), d["eps"])
+    r["x2"] = _range(x2)
+    gt, up = mm(x2, "gate_proj"), mm(x2, "up_proj")
+    r["gate"], r["up"] = _range(gt), _range(up)
+    sg = gt / (1.0 + np.exp(-gt))
+    r["silu"] = _range(sg)
+    m = sg * up
+    r["mul"] = _range(m)
+    dn = mm(m, "down_proj")
+    r["down"] = _range(dn)
+    h2 = h1 + dn
+    r["h2"] = _range(h2)
+    del F
+    floats = None
+    if keep_floats:
+        floats = dict(h0=h, x1=x1, q=q, k=k, v=v, qr=qr, kr=kr, scores=scores, probs=p, ctx=ctx,
+                      o=o, h1=h1, x2=x2, gate=gt, up=up, silu=sg, mul=m, down=dn, h2=h2)
+    return BlockData(T, h0, w, g1, g2, r, floats)

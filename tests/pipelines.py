@@ -123,3 +123,53 @@ def assert_same(g: LayerResult, o: LayerResult, rows=None, check_weights=True):
     gf = g.y if rows is None else g.y[rows]
     denom = np.maximum(np.abs(o.y), np.float32(1e-30))
     assert np.all(np.abs(gf - o.y) <= 1e-6 * denom), "dequantized outputs differ"
+
+
+# ---------------------------------------------------------------------------
+# the decoder block through the oracle (the same stages as
+# paper_2408_13933_amd.block, each computed by the oracle's own functions
+# from the same float inputs and static ranges)
+
+def block_oracle(data, nthreads=None):
+    from paper_2408_13933_amd import block as blk
+    from paper_2408_13933_amd import workloads as wl
+
+    d = wl.BLOCK_DIMS
+    T, H, G, D = data.T, d["heads"], d["kv_heads"], d["head_dim"]
+    f = blk.formats(data.ranges, oracle.act_params)
+    out = {"h0": oracle.quantize_act(data.h0, *f["h0"], 16)}
+    packed = {n: oracle.pack_weights(w, 8) for n, w in data.w.items()}
+
+    def linear(stage):
+        name, src = blk.LINEARS[stage]
+        wq, ws, _ = packed[name]
+        out[stage] = oracle.qlinear(out[src], wq, 8, ws, *f[src], *f[stage],
+                                    blk.STAGE_BITS[stage], nthreads=nthreads)
+
+    out["x1"] = oracle.rmsnorm(out["h0"], *f["h0"], data.gamma1, d["eps"], *f["x1"], 8)
+    for s in ("q", "k", "v"):
+        linear(s)
+    out["qr"] = oracle.rope(out["q"], H, *f["q"], *f["qr"], 16, base=d["rope_base"])
+    out["kr"] = oracle.rope(out["k"], G, *f["k"], *f["kr"], 8, base=d["rope_base"])
+    qh = np.ascontiguousarray(out["qr"].reshape(T, H, D).transpose(1, 0, 2))
+    kh = np.ascontiguousarray(out["kr"].reshape(T, G, D).transpose(1, 0, 2))
+    out["scores"] = oracle.attn_matmul(qh, kh, *f["qr"], *f["kr"], *f["scores"], 16,
+                                       nthreads=nthreads)
+    sa, sz = f["scores"]
+    out["probs"] = oracle.softmax(out["scores"].reshape(H * T, T), sa / D ** 0.5, sz,
+                                  *f["probs"], 16, causal_period=T).reshape(H, T, T)
+    vt = np.ascontiguousarray(out["v"].T).reshape(G, D, T)
+    ctx = oracle.attn_matmul(out["probs"], vt, *f["probs"], *f["v"], *f["ctx"], 8,
+                             nthreads=nthreads)
+    out["ctx"] = np.ascontiguousarray(ctx.transpose(1, 0, 2).reshape(T, H * D))
+    linear("o")
+    out["h1"] = oracle.add_requant(out["h0"], *f["h0"], out["o"], *f["o"], *f["h1"], 16)
+    out["x2"] = oracle.rmsnorm(out["h1"], *f["h1"], data.gamma2, d["eps"], *f["x2"], 8)
+    linear("gate")
+    linear("up")
+    lut = oracle.lut_build(oracle.LUT_SILU, *f["gate"], *f["silu"], 16)
+    out["silu"] = lut[out["gate"].astype(np.int64) + 32768]
+    out["mul"] = oracle.mul_requant(out["silu"], *f["silu"], out["up"], *f["up"], *f["mul"], 8)
+    linear("down")
+    out["h2"] = oracle.add_requant(out["h1"], *f["h1"], out["down"], *f["down"], *f["h2"], 16)
+    return out, f
