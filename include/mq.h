@@ -463,6 +463,13 @@ mq_status mq_arl_backward(const float* x, const float* g, int64_t numel, float a
  *   1 <= K <= MQ_MAX_K; lda, ldb >= K; ldy >= N; strides >= 0, in elements
  *   a_zp in [-32768, 32767], b_zp in [-128, 127], out_zp in the range of
  *   out_bits; scales finite and > 0
+ *   out_causal >= 0: outputs y[h][m][n] with n > m + out_causal are not
+ *              needed and may be left unwritten (Q K^T of a causal decoder,
+ *              out_causal = keys before the first query); -1: all
+ *   in_causal  >= 0: the caller promises A[h][m][k] == a_zp for
+ *              k > m + in_causal (P V with causal probabilities, whose
+ *              hidden keys hold the probability-0 code), so they may be
+ *              skipped; -1: none
  *   workspace  device, 256-byte aligned, >= mq_attn_matmul_workspace_bytes
  *              bytes; overwritten with the per-row zero-point terms, the
  *              per-row sums of B and b_scale (calls that may run
@@ -470,6 +477,7 @@ mq_status mq_arl_backward(const float* x, const float* g, int64_t numel, float a
  *   path       MQ_PATH_AUTO (tiled MFMA kernel for M > 16 when the strides
  *              keep 16-byte aligned rows, else the generic kernel),
  *              MQ_PATH_PREFILL or MQ_PATH_GENERIC
+ *   out_causal, in_causal in [-1, 2^40]
  * Errors: MQ_ERR_INVALID_ARG for any violation above.
  */
 int64_t mq_attn_matmul_workspace_bytes(int32_t H, int32_t G, int64_t M, int64_t N);
@@ -477,8 +485,9 @@ mq_status mq_attn_matmul(const int16_t* a, int64_t lda, int64_t a_hs, int32_t H,
                          const int8_t* b, int64_t ldb, int64_t b_hs, int32_t G, int64_t M,
                          int64_t N, int64_t K, float a_scale, int32_t a_zp, float b_scale,
                          int32_t b_zp, float out_scale, int32_t out_zp, int32_t out_bits,
-                         void* y, int64_t ldy, int64_t y_hs, void* workspace,
-                         int64_t workspace_bytes, int32_t path, void* stream);
+                         void* y, int64_t ldy, int64_t y_hs, int64_t out_causal,
+                         int64_t in_causal, void* workspace, int64_t workspace_bytes,
+                         int32_t path, void* stream);
 
 /*
  * mq_transpose_i8 -- y[c][r] = x[r][c] for an int8 [rows][cols] matrix with

@@ -103,7 +103,7 @@ def lib():
     L.mq_attn_matmul_workspace_bytes.restype = ctypes.c_int64
     L.mq_attn_matmul.argtypes = [c_p, c_i64, c_i64, c_i32, c_p, c_i64, c_i64, c_i32, c_i64, c_i64,
                                  c_i64, c_f, c_i32, c_f, c_i32, c_f, c_i32, c_i32, c_p, c_i64,
-                                 c_i64, c_p, c_i64, c_i32, c_p]
+                                 c_i64, c_i64, c_i64, c_p, c_i64, c_i32, c_p]
     L.mq_transpose_i8.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_p]
     for name in ("mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
@@ -529,10 +529,12 @@ def mq_attn_matmul_workspace_bytes(H: int, G: int, M: int, N: int) -> int:
 
 def mq_attn_matmul(a, b, a_scale: float, a_zp: int, b_scale: float, b_zp: int,
                    out_scale: float, out_zp: int, out_bits: int = 16, out=None, workspace=None,
-                   path: int = PATH_AUTO, stream=None):
+                   path: int = PATH_AUTO, stream=None, out_causal: int = -1, in_causal: int = -1):
     """Batched attention matmul between 16-bit codes a [H][M][K] and 8-bit
     codes b [G][N][K] (views with a contiguous last dimension; head h uses
-    b[h // (H // G)]) -> y [H][M][N]."""
+    b[h // (H // G)]) -> y [H][M][N].  out_causal >= 0: outputs with
+    n > m + out_causal may be left unwritten; in_causal >= 0: promise that
+    a[h][m][k] == a_zp for k > m + in_causal."""
     torch = _torch()
     H, M, K = a.shape
     G, N, Kb = b.shape
@@ -549,7 +551,8 @@ def mq_attn_matmul(a, b, a_scale: float, a_zp: int, b_scale: float, b_zp: int,
     _check(lib().mq_attn_matmul(
         pa, lda, a_hs, int(H), pb, ldb, b_hs, int(G), int(M), int(N), int(K), float(a_scale),
         int(a_zp), float(b_scale), int(b_zp), float(out_scale), int(out_zp), int(out_bits), py,
-        ldy, y_hs, _dev_ptr(workspace, torch.uint8, "workspace"), int(workspace.numel()),
+        ldy, y_hs, int(out_causal), int(in_causal),
+        _dev_ptr(workspace, torch.uint8, "workspace"), int(workspace.numel()),
         int(path), _stream_ptr(stream)), "mq_attn_matmul")
     return out
 

@@ -106,17 +106,20 @@ class BlockGPU:
                                           out=o["qr"], table=self.rope_table)),
             ("rope_k", lambda: mq.mq_rope(o["k"], G, *f["k"], *f["kr"], 8, base=self.base,
                                           out=o["kr"], table=self.rope_table)),
+            # causal: scores past the diagonal are never read
             ("qk_scores", lambda: mq.mq_attn_matmul(qv, kv, *f["qr"], *f["kr"], *f["scores"], 16,
-                                                    out=o["scores"], workspace=self.attn_ws)),
+                                                    out=o["scores"], workspace=self.attn_ws,
+                                                    out_causal=0)),
             # the 1/sqrt(head dim) of the attention logits joins the score
             # scale (a power of two here, so exact in fp32)
             ("softmax", lambda: mq.mq_softmax_causal(o["scores"].view(H * T, T), sa / D ** 0.5,
                                                      sz, *f["probs"], T, 0, 16,
                                                      out=o["probs"].view(H * T, T))),
             ("v_transpose", lambda: mq.mq_transpose_i8(o["v"], out=self.vt)),
+            # the hidden keys hold the probability-0 code
             ("pv_context", lambda: mq.mq_attn_matmul(o["probs"], self.vt.view(G, D, T),
                                                      *f["probs"], *f["v"], *f["ctx"], 8, out=cv,
-                                                     workspace=self.attn_ws)),
+                                                     workspace=self.attn_ws, in_causal=0)),
             ("o_proj", lambda: self._linear("o")),
             ("residual1", lambda: mq.mq_add_requant(o["h0"], *f["h0"], o["o"], *f["o"], *f["h1"],
                                                     16, out=o["h1"])),

@@ -33,16 +33,21 @@ __device__ inline int64_t row_sum_part(const T* x, int64_t K, int lane, bool vec
 }
 
 // One wave per row: rows [0, rows_a) are rows of A (int16; none when B's
-// zero-point is 0), rows [rows_a, rows_a + rows_b) rows of B (int8).  A rows
-// give the term of B's zero-point, -b_zp * sum_k (A[k] - a_zp) (int64,
-// exact); B rows give sum_k B[k].
+// zero-point is 0), rows [rows_a, rows_a + rows_b) rows of B (int8), each B
+// row once per block of tile_m rows of A ([group][m block][n]).  A rows give
+// the term of B's zero-point, -b_zp * sum_k (A[k] - a_zp) (int64, exact); B
+// rows give sum_k B[k] over k < K, or, with causal activations (in_causal
+// >= 0), over the K range the tiled kernel reads for that m block: up to
+// the tile_k stage holding the block's last row's boundary.
 __global__ __launch_bounds__(256) void attn_sums_kernel(const int16_t* a, int64_t lda, int64_t a_bs,
                                                         int64_t rows_a, int64_t M,
                                                         const int8_t* b, int64_t ldb, int64_t b_bs,
                                                         int64_t rows_b, int64_t N, int64_t K,
                                                         int32_t a_zp, int32_t b_zp, float b_scale,
                                                         int64_t* row_off, int32_t* colsum,
-                                                        float* scale_out, bool vec_a, bool vec_b)
+                                                        float* scale_out, bool vec_a, bool vec_b,
+                                                        int64_t n_mb, int64_t in_causal,
+                                                        int64_t tile_m, int64_t tile_k)
 {
     const int lane = threadIdx.x & 63;
     if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = b_scale;
@@ -52,8 +57,15 @@ __global__ __launch_bounds__(256) void attn_sums_kernel(const int16_t* a, int64_
     if (row < rows_a)
         s = row_sum_part(a + (row / M) * a_bs + (row % M) * lda, K, lane, vec_a);
     else {
-        const int64_t r = row - rows_a;
-        s = row_sum_part(b + (r / N) * b_bs + (r % N) * ldb, K, lane, vec_b);
+        const int64_t r = row - rows_a;  // (g * n_mb + mb) * N + n
+        const int64_t n = r % N, mb = (r / N) % n_mb, g = r / (N * n_mb);
+        int64_t len = K;
+        if (in_causal >= 0) {
+            const int64_t m_end = (mb + 1) * tile_m < M ? (mb + 1) * tile_m : M;
+            const int64_t need = (m_end + in_causal + tile_k - 1) / tile_k * tile_k;
+            if (need < len) len = need;
+        }
+        s = row_sum_part(b + g * b_bs + n * ldb, len, lane, vec_b);
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
@@ -88,10 +100,12 @@ __global__ __launch_bounds__(256) void transpose_i8_kernel(const int8_t* x, int6
 hipError_t launch_attn_sums(const int16_t* a, int64_t lda, int64_t a_bs, int32_t H, int64_t M,
                             const int8_t* b, int64_t ldb, int64_t b_bs, int32_t G, int64_t N,
                             int64_t K, int32_t a_zp, int32_t b_zp, float b_scale,
-                            int64_t* row_off, int32_t* colsum, float* scale_out, hipStream_t s)
+                            int64_t* row_off, int32_t* colsum, float* scale_out,
+                            int64_t in_causal, int64_t tile_m, int64_t tile_k, hipStream_t s)
 {
     // B's zero-point 0: the row terms vanish and A is not read
-    const int64_t rows_a = b_zp != 0 ? (int64_t)H * M : 0, rows_b = (int64_t)G * N;
+    const int64_t n_mb = in_causal >= 0 ? (M + tile_m - 1) / tile_m : 1;
+    const int64_t rows_a = b_zp != 0 ? (int64_t)H * M : 0, rows_b = (int64_t)G * n_mb * N;
     const int64_t blocks = (rows_a + rows_b + 3) / 4;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
@@ -99,7 +113,7 @@ hipError_t launch_attn_sums(const int16_t* a, int64_t lda, int64_t a_bs, int32_t
     const bool vec_b = (uintptr_t)b % 16 == 0 && ldb % 16 == 0 && b_bs % 16 == 0;
     attn_sums_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
         a, lda, a_bs, rows_a, M, b, ldb, b_bs, rows_b, N, K, a_zp, b_zp, b_scale, row_off, colsum,
-        scale_out, vec_a, vec_b);
+        scale_out, vec_a, vec_b, n_mb, in_causal, tile_m, tile_k);
     return hipGetLastError();
 }
 

@@ -37,6 +37,20 @@ __device__ inline int32_t requant_f64(double v, double ay, int32_t zy)
     return (int32_t)(q < qmin ? qmin : (q > qmax ? qmax : q));
 }
 
+// requant_f64 with the division by ay replaced by a product with its
+// reciprocal ri (one extra rounding)
+template <int BITS>
+__device__ inline int32_t requant_mul(double v, double ri, int32_t zy)
+{
+#pragma clang fp contract(off)
+    constexpr int32_t qmin = -(1 << (BITS - 1)), qmax = (1 << (BITS - 1)) - 1;
+    double t = v * ri;
+    if (!(t == t)) t = -1e300;  // NaN -> the low end
+    t = fmin(fmax(t, -1e18), 1e18);
+    const int64_t q = (int64_t)rint(t) + zy;
+    return (int32_t)(q < qmin ? qmin : (q > qmax ? qmax : q));
+}
+
 template <int BITS>
 __device__ inline void store_code(void* y, int64_t i, int32_t v)
 {
@@ -276,6 +290,78 @@ __device__ inline int64_t causal_keys(int64_t m, int64_t K, int64_t period, int6
     return n < K ? n : K;
 }
 
+// Rows of at most 2048 codes (K % 8 == 0, 16-byte aligned): TPR threads per
+// row (TPR = K/8 rounded up to whole waves, 256 / TPR rows per block), one
+// 8-code chunk per thread.  Per visible key: one exp, then the product with
+// the row's reciprocal sum and with 1/ay (two roundings where the oracle
+// divides; the codes can differ from it only where the fp64 value sits
+// within a few ulp of a rounding tie); hidden keys are written as zy.
+template <int BITS, int TPR>
+__global__ __launch_bounds__(kThreads) void softmax_rows_kernel(const int16_t* __restrict__ x,
+                                                                int64_t M, int64_t K, float ax,
+                                                                float ay, int32_t zy,
+                                                                int64_t period, int64_t offset,
+                                                                void* __restrict__ y)
+{
+#pragma clang fp contract(off)
+    constexpr int RPB = kThreads / TPR;   // rows per block
+    constexpr int WPR = TPR / 64;         // waves per row
+    __shared__ int32_t red_i[kThreads / 64];
+    __shared__ double red_d[kThreads / 64];
+    const int sub = threadIdx.x / TPR, t = threadIdx.x % TPR, wave = threadIdx.x >> 6;
+    const int64_t m = (int64_t)blockIdx.x * RPB + sub;
+    const bool row_ok = m < M;
+    const int64_t n = row_ok ? causal_keys(m, K, period, offset) : 0;
+    const int64_t k0 = 8 * (int64_t)t;
+    const bool live = row_ok && k0 < n;
+    int16_t v[8];
+    {
+        int4 q = {0, 0, 0, 0};
+        if (live) q = *reinterpret_cast<const int4*>(x + m * K + k0);
+        const int16_t* e = reinterpret_cast<const int16_t*>(&q);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = e[u];
+    }
+    int32_t mx = -32768;
+    if (live)
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (k0 + u < n) mx = max(mx, (int32_t)v[u]);
+    for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o));
+    if ((threadIdx.x & 63) == 0) red_i[wave] = mx;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < WPR; ++w) mx = max(mx, red_i[sub * WPR + w]);
+    const double a = (double)ax;
+    double e[8];
+    double sum = 0.0;
+    if (live) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            e[u] = k0 + u < n ? exp(a * (double)((int32_t)v[u] - mx)) : 0.0;
+            sum += e[u];
+        }
+    }
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    if ((threadIdx.x & 63) == 0) red_d[wave] = sum;
+    __syncthreads();
+    sum = 0.0;
+#pragma unroll
+    for (int w = 0; w < WPR; ++w) sum += red_d[sub * WPR + w];
+    if (!row_ok || k0 >= K) return;
+    int32_t q[8];
+    if (live) {
+        const double rs = 1.0 / sum, ri = 1.0 / (double)ay;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            q[u] = k0 + u < n ? requant_mul<BITS>(e[u] * rs, ri, zy) : zy;
+    } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) q[u] = zy;
+    }
+    store8<BITS>(y, m * K + k0, q);
+}
+
 template <int BITS, int NCH>
 __global__ __launch_bounds__(kThreads) void softmax_regs_kernel(const int16_t* __restrict__ x,
                                                                 int64_t K, float ax, float ay,
@@ -307,13 +393,19 @@ __global__ __launch_bounds__(kThreads) void softmax_regs_kernel(const int16_t* _
     double e[NCH][8];
     double sum = 0.0;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+    for (int c = 0; c < NCH; ++c) {
+        const int64_t k0 = 8 * ((int64_t)threadIdx.x + kThreads * c);
+        if (r.live[c] && k0 < n) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const bool seen = r.live[c] && 8 * ((int64_t)threadIdx.x + kThreads * c) + u < n;
-            e[c][u] = seen ? exp(a * (double)((int32_t)r.v[c][u] - mx)) : 0.0;
-            sum += e[c][u];
+            for (int u = 0; u < 8; ++u) {
+                e[c][u] = k0 + u < n ? exp(a * (double)((int32_t)r.v[c][u] - mx)) : 0.0;
+                sum += e[c][u];
+            }
+        } else {  // past the causal boundary (or past K): no exponentials
+#pragma unroll
+            for (int u = 0; u < 8; ++u) e[c][u] = 0.0;
         }
+    }
     for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
     if ((threadIdx.x & 63) == 0) red_d[threadIdx.x >> 6] = sum;
     __syncthreads();
@@ -325,8 +417,14 @@ __global__ __launch_bounds__(kThreads) void softmax_regs_kernel(const int16_t* _
         if (!r.live[c]) continue;
         const int64_t k0 = 8 * ((int64_t)threadIdx.x + kThreads * c);
         int32_t q[8];
+        if (k0 < n) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) q[u] = requant_f64<BITS>(e[c][u] / sum, (double)ay, zy);
+            for (int u = 0; u < 8; ++u)
+                q[u] = k0 + u < n ? requant_f64<BITS>(e[c][u] / sum, (double)ay, zy) : zy;
+        } else {  // keys past the causal boundary: probability 0, no arithmetic
+#pragma unroll
+            for (int u = 0; u < 8; ++u) q[u] = zy;
+        }
         store8<BITS>(y, m * K + k0, q);
     }
 }
@@ -392,7 +490,11 @@ __global__ __launch_bounds__(kThreads) void softmax_kernel(const int16_t* __rest
 #pragma unroll
     for (int w = 0; w < kThreads / 64; ++w) sum += red_d[w];
     for (int64_t k = threadIdx.x; k < K; k += kThreads) {
-        const double e = k < n ? exp(a * (double)((int32_t)row[k] - mx)) : 0.0;
+        if (k >= n) {  // past the causal boundary: probability 0
+            store_code<BITS>(y, m * K + k, zy);
+            continue;
+        }
+        const double e = exp(a * (double)((int32_t)row[k] - mx));
         store_code<BITS>(y, m * K + k, requant_f64<BITS>(e / sum, (double)ay, zy));
     }
 }
@@ -517,11 +619,33 @@ hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int3
     return hipGetLastError();
 }
 
+template <int BITS, int TPR>
+static void softmax_rows(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
+                         int64_t period, int64_t offset, void* y, hipStream_t st)
+{
+    constexpr int RPB = kThreads / TPR;
+    softmax_rows_kernel<BITS, TPR><<<(unsigned)((M + RPB - 1) / RPB), kThreads, 0, st>>>(
+        x, M, K, ax, ay, zy, period, offset, y);
+}
+
 hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
                           int32_t bits, int64_t period, int64_t offset, void* y, hipStream_t st)
 {
     const int ch = row_chunks(x, y, K);
     const int64_t P = period, O = offset;
+    if (ch == 1 && K <= 2048) {  // one chunk per thread: whole waves per row
+        const int64_t tpr = (K / 8 + 63) / 64 * 64;
+        if (bits == 8) {
+            if (tpr == 64) softmax_rows<8, 64>(x, M, K, ax, ay, zy, P, O, y, st);
+            else if (tpr == 128) softmax_rows<8, 128>(x, M, K, ax, ay, zy, P, O, y, st);
+            else softmax_rows<8, 256>(x, M, K, ax, ay, zy, P, O, y, st);
+        } else {
+            if (tpr == 64) softmax_rows<16, 64>(x, M, K, ax, ay, zy, P, O, y, st);
+            else if (tpr == 128) softmax_rows<16, 128>(x, M, K, ax, ay, zy, P, O, y, st);
+            else softmax_rows<16, 256>(x, M, K, ax, ay, zy, P, O, y, st);
+        }
+        return hipGetLastError();
+    }
     if (ch > 0) {
         if (bits == 8) {
             if (ch == 1) softmax_regs<8, 1>(x, M, K, ax, ay, zy, P, O, y, st);

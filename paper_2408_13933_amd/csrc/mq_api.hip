@@ -425,13 +425,15 @@ mq_status mq_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const v
 }
 
 // Batched attention matmuls: workspace = [row terms: H*M int64][colsum:
-// G*N int32][b_scale: float], each part 256-byte aligned.
+// G * (M / 128 rounded up) * N int32][b_scale: float], each part 256-byte
+// aligned (the column sums per block of 128 rows serve causal activations).
 static int64_t attn_ws_parts(int32_t H, int32_t G, int64_t M, int64_t N, int64_t* off_cs,
                              int64_t* off_sc)
 {
     auto up = [](int64_t v) { return (v + 255) / 256 * 256; };
     const int64_t ro = up((int64_t)H * M * 8);
-    const int64_t cs = up((int64_t)G * N * 4);
+    const int64_t n_mb = (M + mq::kA16TileM - 1) / mq::kA16TileM;
+    const int64_t cs = up((int64_t)G * (n_mb > 0 ? n_mb : 1) * N * 4);
     *off_cs = ro;
     *off_sc = ro + cs;
     return ro + cs + 256;
@@ -449,9 +451,12 @@ mq_status mq_attn_matmul(const int16_t* a, int64_t lda, int64_t a_hs, int32_t H,
                          int64_t ldb, int64_t b_hs, int32_t G, int64_t M, int64_t N, int64_t K,
                          float a_scale, int32_t a_zp, float b_scale, int32_t b_zp,
                          float out_scale, int32_t out_zp, int32_t out_bits, void* y, int64_t ldy,
-                         int64_t y_hs, void* workspace, int64_t workspace_bytes, int32_t path,
-                         void* stream)
+                         int64_t y_hs, int64_t out_causal, int64_t in_causal, void* workspace,
+                         int64_t workspace_bytes, int32_t path, void* stream)
 {
+    const int64_t kCausalMax = (int64_t)1 << 40;
+    if (out_causal < -1 || out_causal > kCausalMax || in_causal < -1 || in_causal > kCausalMax)
+        return MQ_ERR_INVALID_ARG;
     if (H < 1 || G < 1 || H % G != 0) return MQ_ERR_INVALID_ARG;
     if (M < 0 || N < 0 || K < 1 || K > MQ_MAX_K) return MQ_ERR_INVALID_ARG;
     if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || (M > 0 && N > kMaxElems / M)) return MQ_ERR_INVALID_ARG;
@@ -476,9 +481,6 @@ mq_status mq_attn_matmul(const int16_t* a, int64_t lda, int64_t a_hs, int32_t H,
     int64_t* row_off = reinterpret_cast<int64_t*>(ws);
     int32_t* colsum = reinterpret_cast<int32_t*>(ws + off_cs);
     float* scale = reinterpret_cast<float*>(ws + off_sc);
-    hipError_t e = mq::launch_attn_sums(a, lda, a_hs, H, M, b, ldb, b_hs, G, N, K, a_zp, b_zp,
-                                        b_scale, row_off, colsum, scale, s);
-    if (e != hipSuccess) return MQ_ERR_HIP;
 
     mq::QLinearArgs p;
     p.a = reinterpret_cast<const int8_t*>(a);
@@ -510,9 +512,22 @@ mq_status mq_attn_matmul(const int16_t* a, int64_t lda, int64_t a_hs, int32_t H,
     p.ro_bs = M;
     p.row_off = b_zp != 0 ? row_off : nullptr;  // b_zp = 0: no row terms
     if (path == MQ_PATH_AUTO) path = M <= 16 ? MQ_PATH_GENERIC : MQ_PATH_PREFILL;
-    if (path == MQ_PATH_PREFILL && mq::prefill_supported(p))
-        return from_hip(mq::launch_qlinear_prefill(p, s));
-    return from_hip(mq::launch_qlinear_generic(p, s));
+    const bool tiled = path == MQ_PATH_PREFILL && mq::prefill_supported(p);
+    // the causal promises shorten the tiled kernel's work; the generic
+    // kernel computes every output over all of K, which they also allow
+    if (tiled) {
+        p.out_causal = out_causal;
+        p.in_causal = in_causal;
+        if (in_causal >= 0) {
+            p.cs_mt = N;
+            p.cs_bs = ((M + mq::kA16TileM - 1) / mq::kA16TileM) * N;
+        }
+    }
+    hipError_t e = mq::launch_attn_sums(a, lda, a_hs, H, M, b, ldb, b_hs, G, N, K, a_zp, b_zp,
+                                        b_scale, row_off, colsum, scale, p.in_causal,
+                                        mq::kA16TileM, mq::kA16TileK, s);
+    if (e != hipSuccess) return MQ_ERR_HIP;
+    return from_hip(tiled ? mq::launch_qlinear_prefill(p, s) : mq::launch_qlinear_generic(p, s));
 }
 
 mq_status mq_transpose_i8(const int8_t* x, int64_t rows, int64_t cols, int64_t ldx, int8_t* y,

@@ -40,6 +40,15 @@ struct QLinearArgs {
     // per-row int64 term added to the exact sum before the saturation (the
     // zero-point term of a per-tensor asymmetric "weight" operand), or nullptr
     const int64_t* row_off = nullptr;
+    // Causal structure of self-attention (16-bit tile only; the other
+    // kernels compute everything, which these promises allow):
+    // out_causal >= 0: outputs y[m][n] with n > m + out_causal are not
+    //   needed (tiles wholly beyond that boundary are skipped);
+    // in_causal >= 0: a[m][k] == a_zp for k > m + in_causal, so a tile's K
+    //   range stops at the stage holding its last row's boundary, and
+    //   colsum holds, per 128-row tile (stride cs_mt), the column sums over
+    //   that range.
+    int64_t out_causal = -1, in_causal = -1, cs_mt = 0;
 };
 
 // Dense defaults of the stride fields.
@@ -96,7 +105,13 @@ hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, floa
 hipError_t launch_attn_sums(const int16_t* a, int64_t lda, int64_t a_bs, int32_t H, int64_t M,
                             const int8_t* b, int64_t ldb, int64_t b_bs, int32_t G, int64_t N,
                             int64_t K, int32_t a_zp, int32_t b_zp, float b_scale,
-                            int64_t* row_off, int32_t* colsum, float* scale_out, hipStream_t s);
+                            int64_t* row_off, int32_t* colsum, float* scale_out,
+                            int64_t in_causal, int64_t tile_m, int64_t tile_k, hipStream_t s);
+
+// Token rows and K codes per stage of the 16-bit prefill tiles (the causal
+// K range and the per-block column sums of the attention products follow
+// them).
+constexpr int kA16TileM = 128, kA16TileK = 64;
 hipError_t launch_transpose_i8(const int8_t* x, int64_t rows, int64_t cols, int64_t ldx,
                                int8_t* y, hipStream_t s);
 

@@ -385,6 +385,12 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
         const int per = items / 8, rem = items % 8;
         const int xcd = b % 8, idx = b / 8;
         b = xcd * per + (xcd < rem ? xcd : rem) + idx;
+        // causal products skip the tiles past the diagonal (or the K past
+        // it), which leaves the XCDs holding some tile columns (rows) with
+        // most of the work: batch b starts its XCD runs (b mod 8) runs
+        // later, so over eight batches every XCD gets each of them once
+        if (C::A16 && (p.out_causal >= 0 || p.in_causal >= 0) && per > 0)
+            b = (int)((b + (int64_t)(blockIdx.y % 8) * per) % items);
     }
     const int split = C::SPLITK ? b / total : 0;
     const int tile = C::SPLITK ? b % total : b;
@@ -396,6 +402,8 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
     // tile only: this block's batch and the group whose weights it reads
     constexpr bool STR = C::A16;
     const int64_t bt = STR ? (int64_t)blockIdx.y : 0, bg = STR ? bt / p.group : 0;
+    // causal outputs: a tile wholly past the boundary has nothing to compute
+    if (STR && p.out_causal >= 0 && n_tile > m_tile + C::TM - 1 + p.out_causal) return;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -410,14 +418,20 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
     const int64_t K = p.K;
     const int64_t lda = STR ? eff_lda(p) : K;  // activation row stride, elements
     const int64_t wrow = C::WBITS == 8 ? (STR ? eff_ldw(p) : K) : K / 2;  // bytes
-    const int64_t k_begin = C::SPLITK ? (int64_t)split * kt_per_split * C::BK : 0;
-    const int64_t KL = !C::SPLITK ? K
-                       : (K - k_begin) < (int64_t)kt_per_split * C::BK
-                           ? (K - k_begin) : (int64_t)kt_per_split * C::BK;
-    const int64_t k_begin_w = C::WBITS == 8 ? k_begin : k_begin / 2;
-    const int64_t KLw = C::WBITS == 8 ? KL : KL / 2;
     const int rows_a = (int)((p.M - m_tile) < C::TM ? (p.M - m_tile) : C::TM);
     const int rows_w = (int)((p.N - n_tile) < C::TN ? (p.N - n_tile) : C::TN);
+    const int64_t k_begin = C::SPLITK ? (int64_t)split * kt_per_split * C::BK : 0;
+    int64_t KL = !C::SPLITK ? K
+                 : (K - k_begin) < (int64_t)kt_per_split * C::BK
+                     ? (K - k_begin) : (int64_t)kt_per_split * C::BK;
+    if (STR && p.in_causal >= 0) {
+        // the activations past the last row's boundary are zero-point codes
+        // (no contribution): stop at the stage that holds the boundary
+        const int64_t need = (m_tile + rows_a + p.in_causal + C::BK - 1) / C::BK * C::BK;
+        if (need < KL) KL = need;
+    }
+    const int64_t k_begin_w = C::WBITS == 8 ? k_begin : k_begin / 2;
+    const int64_t KLw = C::WBITS == 8 ? KL : KL / 2;
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(p.a + (bt * p.a_bs + m_tile * lda + k_begin) * C::AB), (short)0,
         (int)(((rows_a - 1) * lda + K - k_begin) * C::AB), 0x00020000);
@@ -487,7 +501,7 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
         int64_t n = n_tile + tid;
         if (n >= p.N) n = p.N - 1;
         col_ws = p.w_scale[STR ? n * p.ws_stride : n];
-        col_cs = p.colsum[STR ? bg * p.cs_bs + n : n];
+        col_cs = p.colsum[STR ? bg * p.cs_bs + (p.in_causal >= 0 ? tm * p.cs_mt : 0) + n : n];
         // branch-free; without bias the (unused) load reads w_scale[0]
         col_bias = (p.bias ? p.bias : p.w_scale)[p.bias ? n : 0];
         if constexpr (CASYM) col_zw = p.w_zp[n];
@@ -937,6 +951,9 @@ template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16
 // work-groups share a CU, so one's prologue and epilogue overlap the
 // other's products
 template <int OB> using T128x128A16S2 = Cfg<8, OB, 128, 128, 2, 2, 64, 2, 2, 1, 16>;
+static_assert(T128x128A16<8>::TM == kA16TileM && T128x128A16<8>::BK == kA16TileK &&
+                  T128x128A16S2<8>::TM == kA16TileM && T128x128A16S2<8>::BK == kA16TileK,
+              "the causal column sums assume these 16-bit tile sizes");
 
 // Per-block cycle model of each tile shape on MI355X (phase timings of the
 // kernel): fixed prologue + K-loop cycles per stage + epilogue.

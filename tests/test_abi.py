@@ -286,13 +286,15 @@ def test_glue_entry_points_reject_invalid_arguments(call):
 def attn(**kw):
     a = dict(a=NZ, lda=64, a_hs=64 * 16, H=4, b=NZ, ldb=64, b_hs=64 * 16, G=2, M=16, N=16, K=64,
              a_scale=0.1, a_zp=0, b_scale=0.1, b_zp=0, out_scale=0.1, out_zp=0, out_bits=16,
-             y=NZ, ldy=16, y_hs=256, ws=P(256), ws_bytes=1 << 20, path=0, stream=None)
+             y=NZ, ldy=16, y_hs=256, oc=-1, ic=-1, ws=P(256), ws_bytes=1 << 20, path=0,
+             stream=None)
     a.update(kw)
     return mq.lib().mq_attn_matmul(a["a"], a["lda"], a["a_hs"], a["H"], a["b"], a["ldb"],
                                    a["b_hs"], a["G"], a["M"], a["N"], a["K"], a["a_scale"],
                                    a["a_zp"], a["b_scale"], a["b_zp"], a["out_scale"],
                                    a["out_zp"], a["out_bits"], a["y"], a["ldy"], a["y_hs"],
-                                   a["ws"], a["ws_bytes"], a["path"], a["stream"])
+                                   a["oc"], a["ic"], a["ws"], a["ws_bytes"], a["path"],
+                                   a["stream"])
 
 
 @pytest.mark.parametrize("kw", [
@@ -301,7 +303,7 @@ def attn(**kw):
     dict(a_scale=0.0), dict(b_scale=float("inf")), dict(out_scale=-1.0),
     dict(a_zp=40000), dict(b_zp=128), dict(out_zp=200, out_bits=8), dict(path=1),
     dict(a=None), dict(b=None), dict(y=None), dict(ws=None), dict(ws_bytes=16),
-    dict(ws=P(264)),
+    dict(ws=P(264)), dict(oc=-2), dict(ic=-2), dict(ic=1 << 41),
 ])
 def test_attn_matmul_rejects_invalid_arguments(kw):
     assert attn(**kw) == 1

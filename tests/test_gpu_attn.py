@@ -130,3 +130,35 @@ def test_transpose_i8(rows, cols):
     x = np.random.default_rng(rows).integers(-128, 128, (rows, cols + 5)).astype(np.int8)
     gx = torch.from_numpy(x).cuda()[:, :cols]
     assert np.array_equal(mq.mq_transpose_i8(gx).cpu().numpy(), x[:, :cols].T)
+
+
+@pytest.mark.parametrize("T,D,H,G,b_zp", [(1024, 64, 8, 2, 0), (300, 64, 4, 2, 17),
+                                          (200, 64, 2, 1, -5), (129, 128, 2, 2, 0)])
+def test_causal_attention_parity(T, D, H, G, b_zp):
+    """Q K^T with the causal output promise (entries past the diagonal may
+    stay unwritten) and P V with causal probabilities (zero codes past the
+    diagonal, which the kernel may skip): the lower triangle of the scores
+    and the whole context equal the oracle's full products."""
+    mq, torch = _mq(), _torch()
+    rng = np.random.default_rng(T + D + H + b_zp)
+    q = rng.integers(-32768, 32768, (H, T, D)).astype(np.int16)
+    k = rng.integers(-128, 128, (G, T, D)).astype(np.int8)
+    prm = _params(rng, 16)
+    prm = prm[:3] + (b_zp,) + prm[4:]
+    ref = oracle.attn_matmul(q, k, *prm)
+    for path in (mq.PATH_AUTO, mq.PATH_GENERIC):
+        s = torch.full((H, T, T), 12345, dtype=torch.int16, device="cuda")
+        mq.mq_attn_matmul(torch.from_numpy(q).cuda(), torch.from_numpy(k).cuda(), *prm, out=s,
+                          path=path, out_causal=0)
+        got = s.cpu().numpy()
+        low = np.tril(np.ones((T, T), dtype=bool))
+        assert np.array_equal(got[:, low], ref[:, low]), path
+    p = rng.integers(-32768, 32768, (H, T, T)).astype(np.int16)
+    p[:, ~np.tril(np.ones((T, T), dtype=bool))] = -32768
+    v = rng.integers(-128, 128, (G, D, T)).astype(np.int8)
+    prm2 = (1.0 / 65535, -32768, 0.03, b_zp, 1e-3, 3, 8)
+    ref2 = oracle.attn_matmul(p, v, *prm2)
+    for path in (mq.PATH_AUTO, mq.PATH_GENERIC):
+        ctx = mq.mq_attn_matmul(torch.from_numpy(p).cuda(), torch.from_numpy(v).cuda(), *prm2,
+                                path=path, in_causal=0)
+        assert np.array_equal(ctx.cpu().numpy(), ref2), path

@@ -28,6 +28,9 @@ def test_block_stages_match_the_oracle(T):
     for stage in blk.STAGE_BITS:
         got = g.out[stage].cpu().numpy()
         exp = ref[stage]
+        if stage == "scores":  # only the causal lower triangle is computed
+            low = np.tril(np.ones((T, T), dtype=bool))
+            got, exp = got[:, low], exp[:, low]
         assert got.shape == exp.shape and got.dtype == exp.dtype, stage
         diff = got.astype(np.int64) - exp.astype(np.int64)
         n_bad = int(np.count_nonzero(diff))
