@@ -938,10 +938,13 @@ template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2
 // 96 tokens x 64 channels: while one wave of a SIMD waits (stage barrier,
 // LDS reads, DMA issue) the other keeps the matrix core busy, and the two
 // interleave their epilogues (measured on MI355X: ~9% faster than four
-// waves of 96 x 128).  int4 weights keep four waves: their smaller stages
-// leave no room for eight waves' staged stores.
+// waves of 96 x 128).  Two stages of 128 k (one in flight while the other
+// is read, its DMA spread over two steps) beat four of 64: half the stage
+// barriers, 27.2-28.0 against 29.1-29.2 us on the 2048x2048x5632 layer.
+// int4 weights keep four waves: their smaller stages leave no room for
+// eight waves' staged stores.
 template <int WB, int OB>
-using T192x256 = std::conditional_t<WB == 8, Cfg<WB, OB, 192, 256, 2, 4, 64, 4, 2, 1>,
+using T192x256 = std::conditional_t<WB == 8, Cfg<WB, OB, 192, 256, 2, 4, 128, 2, 2, 2>,
                                     Cfg<WB, OB, 192, 256, 2, 2, 64, 4, 2, 1>>;
 // 16-bit activation codes: 128x128 tokens x channels, 64 k per stage (128
 // bytes of each activation row), DMA spread over both steps of a stage
@@ -965,7 +968,7 @@ constexpr TileModel kTiles[] = {
     {256, 256, 64, 6500, 1450, 9800},
     {256, 128, 128, 6000, 1500, 6000},
     {128, 128, 128, 5300, 980, 3300},
-    {192, 256, 64, 5600, 990, 4600},  // eight waves (int8 weights)
+    {192, 256, 128, 5600, 1770, 4600},  // eight waves, two 128-deep stages (int8 weights)
 };
 // the 192x256 tile with int4 weights runs four waves
 constexpr TileModel kTile192x256W4 = {192, 256, 64, 7000, 1175, 8300};
