@@ -290,76 +290,138 @@ __device__ inline int64_t causal_keys(int64_t m, int64_t K, int64_t period, int6
     return n < K ? n : K;
 }
 
-// Rows of at most 2048 codes (K % 8 == 0, 16-byte aligned): TPR threads per
-// row (TPR = K/8 rounded up to whole waves, 256 / TPR rows per block), one
-// 8-code chunk per thread.  Per visible key: one exp, then the product with
-// the row's reciprocal sum and with 1/ay (two roundings where the oracle
-// divides; the codes can differ from it only where the fp64 value sits
-// within a few ulp of a rounding tie); hidden keys are written as zy.
-template <int BITS, int TPR>
-__global__ __launch_bounds__(kThreads) void softmax_rows_kernel(const int16_t* __restrict__ x,
-                                                                int64_t M, int64_t K, float ax,
-                                                                float ay, int32_t zy,
-                                                                int64_t period, int64_t offset,
-                                                                void* __restrict__ y)
+// Rows of at most 2048 codes (K % 8 == 0, 16-byte aligned), one wave per
+// row, NC chunks of eight codes per lane (chunk c of lane t holds keys
+// 8 (t + 64 c) .. +7).  The exponent alpha (x_k - max) is -alpha d with
+// d = max - x_k an integer in [0, 65535] and alpha an fp32 scale, so
+// alpha d is exact in fp64 and, for d = 256 h + l,
+//   exp(-alpha d) = exp(-256 alpha h) exp(-alpha l).
+// Each block evaluates the two 256-entry factor tables once (one exp per
+// entry, in LDS); a key then costs two table reads and one fp64 product,
+// within three ulp of the direct exp.  The probability is e times the
+// reciprocal row sum times 1/ay (two roundings where the oracle divides);
+// the codes can differ from the oracle's only where the fp64 value sits
+// within a few ulp of a rounding tie.  Hidden keys are written as zy.
+// Each wave takes two rows, m and 2G - 1 - m (G waves in the grid): under
+// a causal mask with period dividing 2G their key counts sum to the
+// period plus one.
+constexpr int kSmWaves = 8;
+
+__device__ inline int32_t wave_max_i32(int32_t v)
+{
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ inline double wave_sum_f64(double v)
 {
 #pragma clang fp contract(off)
-    constexpr int RPB = kThreads / TPR;   // rows per block
-    constexpr int WPR = TPR / 64;         // waves per row
-    __shared__ int32_t red_i[kThreads / 64];
-    __shared__ double red_d[kThreads / 64];
-    const int sub = threadIdx.x / TPR, t = threadIdx.x % TPR, wave = threadIdx.x >> 6;
-    const int64_t m = (int64_t)blockIdx.x * RPB + sub;
-    const bool row_ok = m < M;
-    const int64_t n = row_ok ? causal_keys(m, K, period, offset) : 0;
-    const int64_t k0 = 8 * (int64_t)t;
-    const bool live = row_ok && k0 < n;
-    int16_t v[8];
-    {
-        int4 q = {0, 0, 0, 0};
-        if (live) q = *reinterpret_cast<const int4*>(x + m * K + k0);
-        const int16_t* e = reinterpret_cast<const int16_t*>(&q);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = e[u];
-    }
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+template <int BITS, int NC>
+__device__ inline void softmax_table_row(const int16_t* __restrict__ x, int64_t m, int64_t K,
+                                         int64_t n, const int4* q, const double* tab, double ri,
+                                         int32_t zy, void* __restrict__ y)
+{
+#pragma clang fp contract(off)
+    constexpr int32_t qmax = (1 << (BITS - 1)) - 1, qmin = -(1 << (BITS - 1));
+    const int lane = threadIdx.x & 63;
     int32_t mx = -32768;
-    if (live)
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (k0 + u < n) mx = max(mx, (int32_t)v[u]);
-    for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o));
-    if ((threadIdx.x & 63) == 0) red_i[wave] = mx;
-    __syncthreads();
+    for (int c = 0; c < NC; ++c) {
+        const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
+        const int16_t* v = reinterpret_cast<const int16_t*>(&q[c]);
+        if (k0 + 8 <= n) {
 #pragma unroll
-    for (int w = 0; w < WPR; ++w) mx = max(mx, red_i[sub * WPR + w]);
-    const double a = (double)ax;
-    double e[8];
-    double sum = 0.0;
-    if (live) {
+            for (int u = 0; u < 8; ++u) mx = max(mx, (int32_t)v[u]);
+        } else if (k0 < n) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            e[u] = k0 + u < n ? exp(a * (double)((int32_t)v[u] - mx)) : 0.0;
-            sum += e[u];
+            for (int u = 0; u < 8; ++u)
+                if (k0 + u < n) mx = max(mx, (int32_t)v[u]);
         }
     }
-    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
-    if ((threadIdx.x & 63) == 0) red_d[wave] = sum;
-    __syncthreads();
-    sum = 0.0;
+    mx = wave_max_i32(mx);
+    double e[NC][8];
+    double sum = 0.0;
 #pragma unroll
-    for (int w = 0; w < WPR; ++w) sum += red_d[sub * WPR + w];
-    if (!row_ok || k0 >= K) return;
-    int32_t q[8];
-    if (live) {
-        const double rs = 1.0 / sum, ri = 1.0 / (double)ay;
+    for (int c = 0; c < NC; ++c) {
+        const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
+        const int16_t* v = reinterpret_cast<const int16_t*>(&q[c]);
+        // d = mx - x_k is in [0, 65535] for a visible key; hidden keys read
+        // entry 0 and are zeroed
+        if (k0 + 8 <= n) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-            q[u] = k0 + u < n ? requant_mul<BITS>(e[u] * rs, ri, zy) : zy;
-    } else {
+            for (int u = 0; u < 8; ++u) {
+                const int32_t d = mx - (int32_t)v[u];
+                e[c][u] = tab[d >> 8] * tab[256 + (d & 255)];
+            }
+        } else if (k0 < n) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) q[u] = zy;
+            for (int u = 0; u < 8; ++u) {
+                const bool vis = k0 + u < n;
+                const int32_t d = vis ? mx - (int32_t)v[u] : 0;
+                const double p = tab[d >> 8] * tab[256 + (d & 255)];
+                e[c][u] = vis ? p : 0.0;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) e[c][u] = 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sum += e[c][u];
     }
-    store8<BITS>(y, m * K + k0, q);
+    sum = wave_sum_f64(sum);
+    const double rs = 1.0 / sum;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
+        if (k0 >= K) continue;
+        int32_t o[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            // t >= 0 and finite (e <= 1, sum >= 1, ay > 0 finite)
+            const double t = fmin((e[c][u] * rs) * ri, 1e9);
+            const int32_t r = (int32_t)rint(t) + zy;
+            o[u] = k0 + u < n ? min(max(r, qmin), qmax) : zy;
+        }
+        store8<BITS>(y, m * K + k0, o);
+    }
+}
+
+template <int BITS, int NC>
+__global__ __launch_bounds__(kSmWaves * 64) void softmax_table_kernel(
+    const int16_t* __restrict__ x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
+    int64_t period, int64_t offset, void* __restrict__ y)
+{
+#pragma clang fp contract(off)
+    __shared__ double tab[512];  // [0, 256): exp(-256 alpha h); [256, 512): exp(-alpha l)
+    const int t = threadIdx.x, lane = t & 63;
+    const double a = (double)ax;
+    for (int i = t; i < 512; i += kSmWaves * 64)
+        tab[i] = i < 256 ? exp(-(a * (double)(256 * i))) : exp(-(a * (double)(i - 256)));
+    const int64_t G = (int64_t)gridDim.x * kSmWaves;
+    const int64_t g = (int64_t)blockIdx.x * kSmWaves + (t >> 6);
+    const int64_t rows[2] = {g, 2 * G - 1 - g};
+    int4 q[2][NC];
+    int64_t n[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int64_t m = rows[r];
+        n[r] = m < M ? causal_keys(m, K, period, offset) : 0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
+            q[r][c] = k0 < n[r] ? *reinterpret_cast<const int4*>(x + m * K + k0)
+                                : make_int4(0, 0, 0, 0);
+        }
+    }
+    __syncthreads();
+    const double ri = 1.0 / (double)ay;
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+        if (rows[r] < M) softmax_table_row<BITS, NC>(x, rows[r], K, n[r], q[r], tab, ri, zy, y);
 }
 
 template <int BITS, int NCH>
@@ -619,12 +681,12 @@ hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int3
     return hipGetLastError();
 }
 
-template <int BITS, int TPR>
-static void softmax_rows(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
-                         int64_t period, int64_t offset, void* y, hipStream_t st)
+template <int BITS, int NC>
+static void softmax_table(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
+                          int64_t period, int64_t offset, void* y, hipStream_t st)
 {
-    constexpr int RPB = kThreads / TPR;
-    softmax_rows_kernel<BITS, TPR><<<(unsigned)((M + RPB - 1) / RPB), kThreads, 0, st>>>(
+    constexpr int RPB = 2 * kSmWaves;  // two rows per wave
+    softmax_table_kernel<BITS, NC><<<(unsigned)((M + RPB - 1) / RPB), kSmWaves * 64, 0, st>>>(
         x, M, K, ax, ay, zy, period, offset, y);
 }
 
@@ -633,16 +695,16 @@ hipError_t launch_softmax(const int16_t* x, int64_t M, int64_t K, float ax, floa
 {
     const int ch = row_chunks(x, y, K);
     const int64_t P = period, O = offset;
-    if (ch == 1 && K <= 2048) {  // one chunk per thread: whole waves per row
-        const int64_t tpr = (K / 8 + 63) / 64 * 64;
+    if (ch == 1 && K <= 2048) {  // one wave per row, 8 NC codes per lane
+        const int nc = K <= 512 ? 1 : K <= 1024 ? 2 : 4;
         if (bits == 8) {
-            if (tpr == 64) softmax_rows<8, 64>(x, M, K, ax, ay, zy, P, O, y, st);
-            else if (tpr == 128) softmax_rows<8, 128>(x, M, K, ax, ay, zy, P, O, y, st);
-            else softmax_rows<8, 256>(x, M, K, ax, ay, zy, P, O, y, st);
+            if (nc == 1) softmax_table<8, 1>(x, M, K, ax, ay, zy, P, O, y, st);
+            else if (nc == 2) softmax_table<8, 2>(x, M, K, ax, ay, zy, P, O, y, st);
+            else softmax_table<8, 4>(x, M, K, ax, ay, zy, P, O, y, st);
         } else {
-            if (tpr == 64) softmax_rows<16, 64>(x, M, K, ax, ay, zy, P, O, y, st);
-            else if (tpr == 128) softmax_rows<16, 128>(x, M, K, ax, ay, zy, P, O, y, st);
-            else softmax_rows<16, 256>(x, M, K, ax, ay, zy, P, O, y, st);
+            if (nc == 1) softmax_table<16, 1>(x, M, K, ax, ay, zy, P, O, y, st);
+            else if (nc == 2) softmax_table<16, 2>(x, M, K, ax, ay, zy, P, O, y, st);
+            else softmax_table<16, 4>(x, M, K, ax, ay, zy, P, O, y, st);
         }
         return hipGetLastError();
     }

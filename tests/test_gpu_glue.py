@@ -118,6 +118,51 @@ def test_softmax_causal_parity(M, K, period, offset):
     assert np.all(y[~mask] == zy)
 
 
+# Rows of at most 2048 codes with K % 8 == 0 take the one-wave-per-row
+# kernel whose exponentials come from two 256-entry factor tables; these
+# cases cover one, two and four chunks per lane, a last lane past K, grids
+# whose second row of a wave lies past M, the full code range (the largest
+# difference, 65535, reads the last entry of both tables), scales whose
+# tables underflow to zero and subnormals, and causal boundaries inside a
+# chunk.
+@pytest.mark.parametrize("M,K,out_bits,ax,causal", [
+    (1, 8, 8, 1e-3, None),
+    (17, 512, 8, 2e-3, (17, 0)),
+    (40, 2048, 8, 5e-4, None),
+    (1024, 1024, 8, 3e-4, (1024, 0)),
+    (64, 1016, 16, 0.05, None),
+    (33, 2048, 8, 1e-3, (33, 2000)),
+    (300, 200, 16, 0.0113, (300, 0)),
+])
+def test_softmax_table_rows(M, K, out_bits, ax, causal):
+    import torch
+    mq = _mq()
+    rng = np.random.default_rng(M * K + out_bits)
+    x = rng.integers(-32768, 32768, (M, K)).astype(np.int16)
+    x[:, 0] = -32768
+    x[:, -1] = 32767
+    x[M // 2] = rng.integers(100, 104, K)          # a narrow row
+    zx = -5
+    ay, zy = (1.0 / 255, -128) if out_bits == 8 else (1.0 / 65535, -32768)
+    if causal is None:
+        y = mq.mq_softmax(_dev(x), ax, zx, ay, zy, out_bits).cpu().numpy()
+        ref = oracle.softmax(x, ax, zx, ay, zy, out_bits)
+        n = np.full(M, K)
+    else:
+        period, offset = causal
+        y = mq.mq_softmax_causal(_dev(x), ax, zx, ay, zy, period, offset, out_bits)
+        y = y.cpu().numpy()
+        ref = oracle.softmax(x, ax, zx, ay, zy, out_bits, causal_period=period,
+                             causal_offset=offset)
+        n = np.minimum(np.arange(M) % period + offset + 1, K)
+    mask = np.arange(K)[None, :] < n[:, None]
+    xr = np.float64(np.float32(ax)) * (x.astype(np.float64) - zx)
+    xr = np.where(mask, xr, -np.inf)
+    pre = torch.softmax(torch.tensor(xr), dim=1).numpy() / np.float64(np.float32(ay))
+    _equal_but_ties(y, ref, pre)
+    assert np.all(y[~mask] == zy)
+
+
 @pytest.mark.parametrize("n", [1, 777, 1024 * 5632])
 @pytest.mark.parametrize("out_bits", [8, 16])
 def test_mul_requant_parity(n, out_bits):
