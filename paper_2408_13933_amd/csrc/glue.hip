@@ -298,72 +298,154 @@ __device__ inline int64_t causal_keys(int64_t m, int64_t K, int64_t period, int6
 //   exp(-alpha d) = exp(-256 alpha h) exp(-alpha l).
 // Each block evaluates the two 256-entry factor tables once (one exp per
 // entry, in LDS); a key then costs two table reads and one fp64 product,
-// within three ulp of the direct exp.  The probability is e times the
-// reciprocal row sum times 1/ay (two roundings where the oracle divides);
+// within three ulp of the direct exp.  The code is rint(e * s) + zy with
+// s = (1 / sum) (1 / ay) (two roundings where the oracle divides twice);
 // the codes can differ from the oracle's only where the fp64 value sits
 // within a few ulp of a rounding tie.  Hidden keys are written as zy.
-// Each wave takes two rows, m and 2G - 1 - m (G waves in the grid): under
-// a causal mask with period dividing 2G their key counts sum to the
-// period plus one.
-constexpr int kSmWaves = 8;
+// Each wave takes kSmRows rows in snake order (m, 2G - 1 - m, 2G + m, ...
+// for G waves in the grid): under a causal mask whose period divides 2G
+// the key counts of each pair sum to the period plus one.
+constexpr int kSmWaves = 8, kSmRows = 4;
 
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline s16x2 as_s16x2(int v) { return __builtin_bit_cast(s16x2, v); }
+
+// DPP lane moves within rows of 16 lanes (all 64 lanes active)
+template <int CTRL>
+__device__ inline int dpp_mov(int v)
+{
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+template <int CTRL>
+__device__ inline double dpp_f64(double v)
+{
+    const long long b = __double_as_longlong(v);
+    const int lo = dpp_mov<CTRL>((int)b), hi = dpp_mov<CTRL>((int)(b >> 32));
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+__device__ inline double readlane_f64(double v, int l)
+{
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)b, l);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+// wave-wide max and fp64 sum: butterfly within each 16-lane row, then the
+// four row results; every lane gets the same value
 __device__ inline int32_t wave_max_i32(int32_t v)
 {
-    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
-    return v;
+    v = max(v, dpp_mov<kDppXor1>(v));
+    v = max(v, dpp_mov<kDppXor2>(v));
+    v = max(v, dpp_mov<kDppHalfMirror>(v));
+    v = max(v, dpp_mov<kDppMirror>(v));
+    const int a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+    const int c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+    return max(max(a, b), max(c, d));
 }
 
 __device__ inline double wave_sum_f64(double v)
 {
 #pragma clang fp contract(off)
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    v = v + dpp_f64<kDppXor1>(v);
+    v = v + dpp_f64<kDppXor2>(v);
+    v = v + dpp_f64<kDppHalfMirror>(v);
+    v = v + dpp_f64<kDppMirror>(v);
+    return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
-template <int BITS, int NC>
-__device__ inline void softmax_table_row(const int16_t* __restrict__ x, int64_t m, int64_t K,
-                                         int64_t n, const int4* q, const double* tab, double ri,
-                                         int32_t zy, void* __restrict__ y)
+// the factor products of the two keys of one packed word
+__device__ inline void exp_pair(int w, s16x2 mx2, const double* tab, double& e0, double& e1)
+{
+#pragma clang fp contract(off)
+    const uint32_t D = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, mx2 - as_s16x2(w)));
+    const char* tb = reinterpret_cast<const char*>(tab);
+    e0 = *reinterpret_cast<const double*>(tb + (((D >> 8) & 255u) << 3)) *
+         *reinterpret_cast<const double*>(tb + 2048 + ((D & 255u) << 3));
+    e1 = *reinterpret_cast<const double*>(tb + ((D >> 24) << 3)) *
+         *reinterpret_cast<const double*>(tb + 2048 + (((D >> 16) & 255u) << 3));
+}
+
+// rint(e s) + zy, clamped.  Adding 1.5 * 2^52 rounds t in [0, 2^31) to an
+// integer (to nearest, ties to even) held in the low word; CLAMP caps t
+// when s (an upper bound of t, e <= 1) exceeds 1e9.
+template <int BITS, bool CLAMP>
+__device__ inline int32_t requant_prob(double e, double s, int32_t zy)
 {
 #pragma clang fp contract(off)
     constexpr int32_t qmax = (1 << (BITS - 1)) - 1, qmin = -(1 << (BITS - 1));
+    double t = e * s;
+    if (CLAMP) t = fmin(t, 1e9);
+    t = t + 6755399441055744.0;
+    const int32_t r = (int32_t)(uint32_t)__double_as_longlong(t) + zy;
+    return min(max(r, qmin), qmax);
+}
+
+template <int BITS, bool CLAMP>
+__device__ inline void requant_chunk(const double* e, int k0, int n, double s, int32_t zy,
+                                     void* y, int64_t base)
+{
+    int32_t o[8];
+    if (k0 + 8 <= n) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) o[u] = requant_prob<BITS, CLAMP>(e[u], s, zy);
+    } else if (k0 < n) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) o[u] = k0 + u < n ? requant_prob<BITS, CLAMP>(e[u], s, zy) : zy;
+    } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) o[u] = zy;
+    }
+    store8<BITS>(y, base + k0, o);
+}
+
+// one row: m and n (keys visible, 1 <= n <= K <= 512 NC) are wave-uniform
+template <int BITS, int NC>
+__device__ inline void softmax_table_row(int64_t m, int K, int n, const int4* q,
+                                         const double* tab, double ri, int32_t zy,
+                                         void* __restrict__ y)
+{
+#pragma clang fp contract(off)
     const int lane = threadIdx.x & 63;
     int32_t mx = -32768;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-        const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
-        const int16_t* v = reinterpret_cast<const int16_t*>(&q[c]);
+        const int k0 = 8 * (lane + 64 * c);
+        const int4 w = q[c];
         if (k0 + 8 <= n) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) mx = max(mx, (int32_t)v[u]);
+            const s16x2 a = __builtin_elementwise_max(as_s16x2(w.x), as_s16x2(w.y));
+            const s16x2 b = __builtin_elementwise_max(as_s16x2(w.z), as_s16x2(w.w));
+            const s16x2 h = __builtin_elementwise_max(a, b);
+            mx = max(mx, max((int32_t)h.x, (int32_t)h.y));
         } else if (k0 < n) {
+            const int16_t* v = reinterpret_cast<const int16_t*>(&q[c]);
 #pragma unroll
             for (int u = 0; u < 8; ++u)
                 if (k0 + u < n) mx = max(mx, (int32_t)v[u]);
         }
     }
     mx = wave_max_i32(mx);
+    const s16x2 mx2 = {(short)mx, (short)mx};
     double e[NC][8];
     double sum = 0.0;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-        const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
-        const int16_t* v = reinterpret_cast<const int16_t*>(&q[c]);
-        // d = mx - x_k is in [0, 65535] for a visible key; hidden keys read
-        // entry 0 and are zeroed
-        if (k0 + 8 <= n) {
+        const int k0 = 8 * (lane + 64 * c);
+        if (k0 < n) {
+            // hidden keys of a partial chunk read valid entries (their
+            // codes are zero or real scores) and are zeroed below
+            exp_pair(q[c].x, mx2, tab, e[c][0], e[c][1]);
+            exp_pair(q[c].y, mx2, tab, e[c][2], e[c][3]);
+            exp_pair(q[c].z, mx2, tab, e[c][4], e[c][5]);
+            exp_pair(q[c].w, mx2, tab, e[c][6], e[c][7]);
+            if (k0 + 8 > n) {
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int32_t d = mx - (int32_t)v[u];
-                e[c][u] = tab[d >> 8] * tab[256 + (d & 255)];
-            }
-        } else if (k0 < n) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const bool vis = k0 + u < n;
-                const int32_t d = vis ? mx - (int32_t)v[u] : 0;
-                const double p = tab[d >> 8] * tab[256 + (d & 255)];
-                e[c][u] = vis ? p : 0.0;
+                for (int u = 0; u < 8; ++u) e[c][u] = k0 + u < n ? e[c][u] : 0.0;
             }
         } else {
 #pragma unroll
@@ -372,21 +454,21 @@ __device__ inline void softmax_table_row(const int16_t* __restrict__ x, int64_t 
 #pragma unroll
         for (int u = 0; u < 8; ++u) sum += e[c][u];
     }
-    sum = wave_sum_f64(sum);
-    const double rs = 1.0 / sum;
+    sum = wave_sum_f64(sum);  // >= 1: the maximum key contributes exp(0)
+    const double s = (1.0 / sum) * ri;
+    const int64_t base = m * K;
+    if (s <= 1e9) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-        const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
-        if (k0 >= K) continue;
-        int32_t o[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            // t >= 0 and finite (e <= 1, sum >= 1, ay > 0 finite)
-            const double t = fmin((e[c][u] * rs) * ri, 1e9);
-            const int32_t r = (int32_t)rint(t) + zy;
-            o[u] = k0 + u < n ? min(max(r, qmin), qmax) : zy;
+        for (int c = 0; c < NC; ++c) {
+            const int k0 = 8 * (lane + 64 * c);
+            if (k0 < K) requant_chunk<BITS, false>(e[c], k0, n, s, zy, y, base);
         }
-        store8<BITS>(y, m * K + k0, o);
+    } else {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int k0 = 8 * (lane + 64 * c);
+            if (k0 < K) requant_chunk<BITS, true>(e[c], k0, n, s, zy, y, base);
+        }
     }
 }
 
@@ -402,26 +484,44 @@ __global__ __launch_bounds__(kSmWaves * 64) void softmax_table_kernel(
     for (int i = t; i < 512; i += kSmWaves * 64)
         tab[i] = i < 256 ? exp(-(a * (double)(256 * i))) : exp(-(a * (double)(i - 256)));
     const int64_t G = (int64_t)gridDim.x * kSmWaves;
-    const int64_t g = (int64_t)blockIdx.x * kSmWaves + (t >> 6);
-    const int64_t rows[2] = {g, 2 * G - 1 - g};
+    const int64_t g = (int64_t)blockIdx.x * kSmWaves + __builtin_amdgcn_readfirstlane(t >> 6);
+    auto row_of = [&](int r) -> int64_t {
+        return (r & 1) ? (int64_t)(r + 1) * G - 1 - g : (int64_t)r * G + g;
+    };
+    // keys row m sees (0 past M); M < 2^31, so m % period fits 32 bits
+    auto keys_of = [&](int64_t m) -> int {
+        if (m >= M) return 0;
+        if (period <= 0) return (int)K;
+        const int64_t r = period > m ? m : (int64_t)((uint32_t)m % (uint32_t)period);
+        const int64_t n = r + offset + 1;
+        return (int)(n < K ? n : K);
+    };
+    // chunks from ceil(n / 8) on lie outside the row's descriptor and read
+    // as zeros without a memory access
     int4 q[2][NC];
-    int64_t n[2];
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-        const int64_t m = rows[r];
-        n[r] = m < M ? causal_keys(m, K, period, offset) : 0;
+    int n[2];
+    auto load = [&](int slot, int r) {
+        const int64_t m = row_of(r);
+        n[slot] = keys_of(m);
+        const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(x + (m < M ? m : 0) * K), (short)0, (n[slot] + 7) / 8 * 16, 0x00020000);
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const int64_t k0 = 8 * (int64_t)(lane + 64 * c);
-            q[r][c] = k0 < n[r] ? *reinterpret_cast<const int4*>(x + m * K + k0)
-                                : make_int4(0, 0, 0, 0);
+            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rx, 16 * (lane + 64 * c), 0, 0);
+            q[slot][c] = make_int4((int)v[0], (int)v[1], (int)v[2], (int)v[3]);
         }
-    }
+    };
+    load(0, 0);
+    load(1, 1);
     __syncthreads();
     const double ri = 1.0 / (double)ay;
 #pragma unroll
-    for (int r = 0; r < 2; ++r)
-        if (rows[r] < M) softmax_table_row<BITS, NC>(x, rows[r], K, n[r], q[r], tab, ri, zy, y);
+    for (int r = 0; r < kSmRows; ++r) {
+        const int slot = r & 1;
+        const int64_t m = row_of(r);
+        if (m < M) softmax_table_row<BITS, NC>(m, (int)K, n[slot], q[slot], tab, ri, zy, y);
+        if (r + 2 < kSmRows) load(slot, r + 2);
+    }
 }
 
 template <int BITS, int NCH>
@@ -685,7 +785,7 @@ template <int BITS, int NC>
 static void softmax_table(const int16_t* x, int64_t M, int64_t K, float ax, float ay, int32_t zy,
                           int64_t period, int64_t offset, void* y, hipStream_t st)
 {
-    constexpr int RPB = 2 * kSmWaves;  // two rows per wave
+    constexpr int RPB = kSmRows * kSmWaves;
     softmax_table_kernel<BITS, NC><<<(unsigned)((M + RPB - 1) / RPB), kSmWaves * 64, 0, st>>>(
         x, M, K, ax, ay, zy, period, offset, y);
 }
