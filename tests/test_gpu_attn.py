@@ -29,7 +29,7 @@ def _params(rng, out_bits):
 
 
 @pytest.mark.parametrize("T,D,H,G", [(200, 64, 8, 2), (128, 64, 4, 4), (17, 64, 2, 1),
-                                     (300, 128, 6, 3)])
+                                     (300, 128, 6, 3), (40, 4, 2, 2), (33, 24, 3, 1)])
 @pytest.mark.parametrize("out_bits", [16, 8])
 def test_scores_qkt_parity(T, D, H, G, out_bits):
     """Q K^T on head views of the projections' [token][heads * D] outputs."""
