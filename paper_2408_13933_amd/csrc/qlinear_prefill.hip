@@ -86,6 +86,12 @@ struct Cfg {
     // work-groups per CU the register budget is sized for: the short-K
     // 16-bit tile (two stages) shares a CU between two
     static constexpr int OCC = (ABITS_ == 16 && STAGES_ == 2) ? 2 : 1;
+    // the short-K 16-bit tile (two stages) serves K <= 128 without bias
+    // only: then |c| = |sum_k (a - a_zp)(b - b_zp)| <= 128 * 65535 * 255 <
+    // 2^31, the saturation is the identity and its terms sum in int32
+    // (wrapping to the exact value)
+    static constexpr bool A16_I32 = ABITS_ == 16 && STAGES_ == 2;
+    static constexpr int A16_I32_MAX_K = 128;
     static constexpr int THREADS = 64 * NWAVES;
     static constexpr int FM = TM / (WM * 32);   // 32-token fragments per wave
     static constexpr int FN = TN / (WN * 32);   // 32-channel fragments per wave
@@ -225,13 +231,15 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
     constexpr bool ROFF = ASYM && C::A16;    // int64 row terms
     int32_t rs[C::FM];  // this lane's token rows
     int64_t roff[C::FM];
+    uint32_t roff32[C::FM];  // the int32 form: low words
 #pragma unroll
     for (int j = 0; j < C::FM; ++j) {
         const int row = x.wave_row0 + j * 32 + x.r32;
         rs[j] = CASYM && !FAST ? x.e_rs[row] : 0;
-        roff[j] = ROFF ? (int64_t)(((uint64_t)(uint32_t)x.e_rhi[row] << 32) |
-                                   (uint64_t)(uint32_t)x.e_rs[row])
-                       : 0;
+        roff[j] = ROFF && !C::A16_I32 ? (int64_t)(((uint64_t)(uint32_t)x.e_rhi[row] << 32) |
+                                                  (uint64_t)(uint32_t)x.e_rs[row])
+                                      : 0;
+        roff32[j] = ROFF && C::A16_I32 ? (uint32_t)x.e_rs[row] : 0u;
     }
 #pragma unroll
     for (int pass = 0; pass < PASSES; ++pass) {
@@ -264,7 +272,13 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                     int32_t a32 = acc[i][j][4 * g + r];
                     if constexpr (C::WBITS == 4) a32 >>= 4;  // exact: a multiple of 16
                     int32_t c = a32;  // fast form: off is already in the accumulator
-                    if constexpr (C::A16) {
+                    if constexpr (C::A16_I32) {
+                        // the same sum modulo 2^32, whose exact value fits
+                        uint32_t u = ((uint32_t)a32 << 8) + (uint32_t)acc2[i][j][4 * g + r];
+                        if constexpr (!FAST) u += ((uint32_t)off[r] << 8) + (uint32_t)nzw[r];
+                        if constexpr (ROFF) u += roff32[j];
+                        c = (int32_t)u;
+                    } else if constexpr (C::A16) {
                         // high plane * 256 + low plane (+ the offset, split
                         // the same way, when it is not in the start values)
                         int64_t c64 = ((int64_t)a32 << 8) + acc2[i][j][4 * g + r];
@@ -954,6 +968,8 @@ template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16
 // work-groups share a CU, so one's prologue and epilogue overlap the
 // other's products
 template <int OB> using T128x128A16S2 = Cfg<8, OB, 128, 128, 2, 2, 64, 2, 2, 1, 16>;
+static_assert(T128x128A16S2<8>::A16_I32 && !T128x128A16<8>::A16_I32,
+              "the int32 epilogue belongs to the short-K tile");
 static_assert(T128x128A16<8>::TM == kA16TileM && T128x128A16<8>::BK == kA16TileK &&
                   T128x128A16S2<8>::TM == kA16TileM && T128x128A16S2<8>::BK == kA16TileK,
               "the causal column sums assume these 16-bit tile sizes");
@@ -1086,7 +1102,7 @@ template <int>
 hipError_t launch_a16(const QLinearArgs& p, hipStream_t s)
 {
     const bool ro = p.row_off != nullptr, o8 = p.out_bits == 8;
-    if (p.K <= 128) {
+    if (p.K <= T128x128A16S2<8>::A16_I32_MAX_K && p.bias == nullptr) {
         if (ro) return o8 ? launch_cfg<T128x128A16S2<8>, true>(p, 1, s)
                           : launch_cfg<T128x128A16S2<16>, true>(p, 1, s);
         return o8 ? launch_cfg<T128x128A16S2<8>, false>(p, 1, s)

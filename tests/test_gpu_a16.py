@@ -55,11 +55,12 @@ def test_a16_paths_agree(w_bits, out_bits, M):
     assert np.array_equal(outs[0], oracle_layer(ld).y_q)
 
 
-@pytest.mark.parametrize("K", [65536, 4096, 64])
-def test_a16_extreme_codes(K):
+@pytest.mark.parametrize("K,has_bias", [(65536, True), (4096, True), (64, True), (128, False)])
+def test_a16_extreme_codes(K, has_bias):
     """Activation codes and zero-points at the int16 ends, weights at the
     int8 ends: sums far beyond int32 (the accumulator saturates), an offset
-    beyond int32, and sums that stay inside it, on every kernel path."""
+    beyond int32, and sums that stay inside it, on every kernel path (K =
+    128 without bias: the int32 epilogue at its largest sums)."""
     mq, torch = _mq(), _torch()
     dev = torch.device("cuda", 0)
     rng = np.random.default_rng(K)
@@ -71,6 +72,8 @@ def test_a16_extreme_codes(K):
     ws = rng.uniform(1e-4, 1e-3, N).astype(np.float32)
     bias = (rng.standard_normal(N) * 50.0).astype(np.float32)
     g_w, g_ws, g_cs, g_b = (torch.from_numpy(v).to(dev) for v in (codes, ws, cs, bias))
+    if not has_bias:
+        bias, g_b = None, None
     for M, path in ((16, mq.PATH_DECODE), (300, mq.PATH_PREFILL), (16, mq.PATH_GENERIC)):
         a = np.where(rng.random((M, K)) < 0.5, -32768, 32767).astype(np.int16)
         a[0] = 32767

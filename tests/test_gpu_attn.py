@@ -92,6 +92,27 @@ def test_attn_small_m_and_extremes(M):
         assert np.array_equal(y, ref)
 
 
+@pytest.mark.parametrize("K", [128, 64, 16])
+def test_attn_short_k_extremes(K):
+    """K <= 128 without bias takes the int32 epilogue: its largest sums,
+    |sum_k (a - a_zp)(b - b_zp)| up to 128 * 65535 * 255, must come out
+    exact, with and without B's zero-point."""
+    mq, torch = _mq(), _torch()
+    rng = np.random.default_rng(K)
+    H, G, M, N = 2, 1, 96, 160
+    a = np.full((H, M, K), -32768, np.int16)
+    b = np.full((G, N, K), 127, np.int8)
+    a[:, 1::3] = np.where(rng.random((H, len(range(1, M, 3)), K)) < 0.5, -32768, 32767)
+    b[:, 1::4] = np.where(rng.random((G, len(range(1, N, 4)), K)) < 0.5, -128, 127)
+    for prm in ((3e-5, 32767, 0.03, -128, 200.0, 0, 16), (3e-5, 32767, 0.03, 0, 1e4, -3, 8),
+                (3e-5, -5, 0.03, 77, 1e-2, 1, 16)):
+        ref = oracle.attn_matmul(a, b, *prm)
+        for path in (mq.PATH_AUTO, mq.PATH_PREFILL):
+            y = mq.mq_attn_matmul(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda(), *prm,
+                                  path=path).cpu().numpy()
+            assert np.array_equal(y, ref), (prm, path, int((y != ref).sum()))
+
+
 def test_attn_tinyllama_full_size_sampled_heads():
     """The 1024-token TinyLlama attention (32 query heads, 4 key/value
     heads, head dimension 64) through the tiled kernel; heads 0, 7, 8 and
