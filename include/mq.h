@@ -348,6 +348,29 @@ mq_status mq_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, i
                   double base, int64_t pos0, float ay, int32_t zy, int32_t out_bits,
                   double* table, void* y, void* stream);
 
+/*
+ * mq_rope_table -- the angle table of mq_rope alone: table[2 (t D/2 + i)]
+ * and table[2 (t D/2 + i) + 1] get cos and sin of (t + pos0) *
+ * base^(-2i/D) for t < T, i < D/2 (the same fp64 evaluation as mq_rope).
+ * The table depends only on T, D, base and pos0, so one table serves the
+ * queries and keys of every layer.
+ *   table  device fp64 [T * D], written
+ *   T >= 0, D >= 2 even, base finite and > 1, 0 <= pos0 <= 2^40.
+ */
+mq_status mq_rope_table(int64_t T, int64_t D, double base, int64_t pos0, double* table,
+                        void* stream);
+
+/*
+ * mq_rope_apply -- mq_rope's rotation and requantization with an angle
+ * table made by mq_rope_table (same T and D); mq_rope equals
+ * mq_rope_table followed by mq_rope_apply.
+ *   x      device int16 [T][H * D]; y device int8 or int16 [T][H * D]
+ *   table  device fp64 [T * D], read only
+ */
+mq_status mq_rope_apply(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                        const double* table, float ay, int32_t zy, int32_t out_bits, void* y,
+                        void* stream);
+
 /* Table operators of mq_lut_build. */
 #define MQ_LUT_SILU 1
 

@@ -89,6 +89,9 @@ def lib():
                                  c_p]
     L.mq_rope.argtypes = [c_p, c_i64, c_i64, c_i64, c_f, c_i32, ctypes.c_double, c_i64, c_f, c_i32,
                           c_i32, c_p, c_p, c_p]
+    L.mq_rope_table.argtypes = [c_i64, c_i64, ctypes.c_double, c_i64, c_p, c_p]
+    L.mq_rope_apply.argtypes = [c_p, c_i64, c_i64, c_i64, c_f, c_i32, c_p, c_f, c_i32, c_i32, c_p,
+                                c_p]
     L.mq_softmax_causal.argtypes = [c_p, c_i64, c_i64, c_f, c_i32, c_f, c_i32, c_i32, c_i64,
                                     c_i64, c_p, c_p]
     L.mq_smooth_scales.argtypes = [c_p, c_i64, c_i64, c_p, c_i64, c_f, c_p, c_p, c_p, c_p]
@@ -111,7 +114,7 @@ def lib():
                  "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
                  "mq_arl_backward", "mq_add_requant", "mq_lut_build", "mq_lut_apply",
                  "mq_rmsnorm", "mq_softmax", "mq_softmax_causal", "mq_mul_requant",
-                 "mq_rope"):
+                 "mq_rope", "mq_rope_table", "mq_rope_apply"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -396,6 +399,39 @@ def mq_mul_requant(x1, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy
                                 float(ay), int(zy), int(out_bits),
                                 _dev_ptr(out, _act_dtype(out_bits), "out", tuple(x1.shape)),
                                 _stream_ptr(stream)), "mq_mul_requant")
+    return out
+
+
+def mq_rope_table(T: int, D: int, base: float = 10000.0, pos0: int = 0, out=None, device=None,
+                  stream=None):
+    """cos/sin table of the rotary angles, fp64 [T * D] (mq_rope's first step)."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty(max(T * D, 1), dtype=torch.float64, device=device or "cuda")
+    if out.numel() < T * D:
+        raise ValueError("table needs T * D fp64 values")
+    _check(lib().mq_rope_table(int(T), int(D), float(base), int(pos0),
+                               _dev_ptr(out, torch.float64, "table"), _stream_ptr(stream)),
+           "mq_rope_table")
+    return out
+
+
+def mq_rope_apply(x, heads: int, ax: float, zx: int, ay: float, zy: int, table,
+                  out_bits: int = 16, out=None, stream=None):
+    """Rotary position embedding with a table from mq_rope_table."""
+    torch = _torch()
+    T, HD = x.shape
+    D = HD // int(heads)
+    if D * int(heads) != HD:
+        raise ValueError("x's row length must be heads * D")
+    if table.numel() < T * D:
+        raise ValueError("table needs T * D fp64 values")
+    out = torch.empty((T, HD), dtype=_act_dtype(out_bits), device=x.device) if out is None else out
+    _check(lib().mq_rope_apply(_dev_ptr(x, torch.int16, "x"), T, int(heads), D, float(ax),
+                               int(zx), _dev_ptr(table, torch.float64, "table"), float(ay),
+                               int(zy), int(out_bits),
+                               _dev_ptr(out, _act_dtype(out_bits), "out", (T, HD)),
+                               _stream_ptr(stream)), "mq_rope_apply")
     return out
 
 

@@ -68,7 +68,9 @@ class BlockGPU:
                     for s, shp in shapes.items()}
         self.out["h0"] = self.h0
         self.vt = torch.empty((G * D, T), dtype=i8, device=dev)
-        self.rope_table = torch.empty(T * D, dtype=torch.float64, device=dev)
+        # the rotary angles depend only on T, D and the base: one table for
+        # the queries and the keys, built once
+        self.rope_table = mq.mq_rope_table(T, D, base=self.base, device=dev)
         # the SiLU table depends only on the static formats: built once
         self.lut = mq.mq_lut_build(mq.LUT_SILU, *self.fmt["gate"], *self.fmt["silu"], 16)
         ws = max(mq.mq_qlinear_workspace_bytes(T, K, N, 8, STAGE_BITS[s])
@@ -102,10 +104,10 @@ class BlockGPU:
             ("q_proj", lambda: self._linear("q")),
             ("k_proj", lambda: self._linear("k")),
             ("v_proj", lambda: self._linear("v")),
-            ("rope_q", lambda: mq.mq_rope(o["q"], H, *f["q"], *f["qr"], 16, base=self.base,
-                                          out=o["qr"], table=self.rope_table)),
-            ("rope_k", lambda: mq.mq_rope(o["k"], G, *f["k"], *f["kr"], 8, base=self.base,
-                                          out=o["kr"], table=self.rope_table)),
+            ("rope_q", lambda: mq.mq_rope_apply(o["q"], H, *f["q"], *f["qr"], self.rope_table,
+                                                16, out=o["qr"])),
+            ("rope_k", lambda: mq.mq_rope_apply(o["k"], G, *f["k"], *f["kr"], self.rope_table, 8,
+                                                out=o["kr"])),
             # causal: scores past the diagonal are never read
             ("qk_scores", lambda: mq.mq_attn_matmul(qv, kv, *f["qr"], *f["kr"], *f["scores"], 16,
                                                     out=o["scores"], workspace=self.attn_ws,

@@ -848,20 +848,21 @@ __global__ __launch_bounds__(256) void rope_table_kernel(int64_t T, int64_t half
     cs[2 * idx + 1] = sin(ang);
 }
 
+// grid (ceil(H * D/2 / 256), min(T, 65535)): block row t holds the pairs
+// (h, i) of tokens t, t + gridDim.y, ..., one per thread
 template <int BITS>
 __global__ __launch_bounds__(256) void rope_kernel(const int16_t* __restrict__ x, int64_t T,
-                                                   int64_t H, int64_t D, float ax, int32_t zx,
+                                                   int32_t H,
+                                                   int32_t half, float ax, int32_t zx,
                                                    const double* __restrict__ cs, float ay,
                                                    int32_t zy, void* __restrict__ y)
 {
 #pragma clang fp contract(off)
-    const int64_t half = D / 2;
-    const int64_t pairs = T * H * half;
-    const int64_t stride = (int64_t)gridDim.x * 256;
-    for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < pairs; p += stride) {
-        const int64_t i = p % half, th = p / half;  // th = t * H + h
-        const int64_t t = th / H;
-        const int64_t j0 = th * D + i, j1 = j0 + half;
+    const int32_t q = (int32_t)blockIdx.x * 256 + (int32_t)threadIdx.x;
+    if (q >= H * half) return;
+    const int32_t h = q / half, i = q - h * half;
+    for (int64_t t = blockIdx.y; t < T; t += gridDim.y) {
+        const int64_t j0 = (t * H + h) * (int64_t)(2 * half) + i, j1 = j0 + half;
         const double c = cs[2 * (t * half + i)], sn = cs[2 * (t * half + i) + 1];
         const double u = (double)ax * (double)((int32_t)x[j0] - zx);
         const double w = (double)ax * (double)((int32_t)x[j1] - zx);
@@ -872,23 +873,41 @@ __global__ __launch_bounds__(256) void rope_kernel(const int16_t* __restrict__ x
 
 }  // namespace
 
-hipError_t launch_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
-                       double base, int64_t pos0, float ay, int32_t zy, int32_t bits,
-                       double* table, void* y, hipStream_t st)
+hipError_t launch_rope_table(int64_t T, int64_t D, double base, int64_t pos0, double* table,
+                             hipStream_t st)
 {
     const int64_t half = D / 2;
     const int64_t entries = T * half;
     if (entries == 0) return hipSuccess;
     rope_table_kernel<<<(unsigned)((entries + 255) / 256), 256, 0, st>>>(T, half, D, base, pos0,
                                                                          table);
-    const int64_t pairs = T * H * half;
-    int64_t g = (pairs + 255) / 256;
-    if (g > 256 * 64) g = 256 * 64;
-    if (bits == 8)
-        rope_kernel<8><<<(unsigned)g, 256, 0, st>>>(x, T, H, D, ax, zx, table, ay, zy, y);
-    else
-        rope_kernel<16><<<(unsigned)g, 256, 0, st>>>(x, T, H, D, ax, zx, table, ay, zy, y);
     return hipGetLastError();
+}
+
+hipError_t launch_rope_apply(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax,
+                             int32_t zx, const double* table, float ay, int32_t zy, int32_t bits,
+                             void* y, hipStream_t st)
+{
+    const int64_t half = D / 2;
+    if (T == 0) return hipSuccess;
+    if (H * half > 0x7FFFFFFF - 256) return hipErrorInvalidValue;
+    const dim3 g((unsigned)((H * half + 255) / 256), (unsigned)(T < 65535 ? T : 65535));
+    if (bits == 8)
+        rope_kernel<8><<<g, 256, 0, st>>>(x, T, (int32_t)H, (int32_t)half, ax, zx, table, ay, zy,
+                                          y);
+    else
+        rope_kernel<16><<<g, 256, 0, st>>>(x, T, (int32_t)H, (int32_t)half, ax, zx, table, ay,
+                                           zy, y);
+    return hipGetLastError();
+}
+
+hipError_t launch_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                       double base, int64_t pos0, float ay, int32_t zy, int32_t bits,
+                       double* table, void* y, hipStream_t st)
+{
+    const hipError_t e = launch_rope_table(T, D, base, pos0, table, st);
+    if (e != hipSuccess) return e;
+    return launch_rope_apply(x, T, H, D, ax, zx, table, ay, zy, bits, y, st);
 }
 
 }  // namespace mq

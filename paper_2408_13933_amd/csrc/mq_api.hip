@@ -178,6 +178,32 @@ mq_status mq_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, i
                                     as_stream(stream)));
 }
 
+mq_status mq_rope_table(int64_t T, int64_t D, double base, int64_t pos0, double* table,
+                        void* stream)
+{
+    if (T < 0 || D < 2 || D % 2 != 0 || D > kMaxElems) return MQ_ERR_INVALID_ARG;
+    if (T > 0 && T > kMaxElems / D) return MQ_ERR_INVALID_ARG;
+    if (!std::isfinite(base) || !(base > 1.0)) return MQ_ERR_INVALID_ARG;
+    if (pos0 < 0 || pos0 > ((int64_t)1 << 40)) return MQ_ERR_INVALID_ARG;
+    if (T == 0) return MQ_OK;
+    if (!table) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_rope_table(T, D, base, pos0, table, as_stream(stream)));
+}
+
+mq_status mq_rope_apply(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
+                        const double* table, float ay, int32_t zy, int32_t out_bits, void* y,
+                        void* stream)
+{
+    if (T < 0 || H < 1 || D < 2 || D % 2 != 0 || !act_bits_ok(out_bits)) return MQ_ERR_INVALID_ARG;
+    if (H > kMaxElems / D || (T > 0 && T > kMaxElems / (H * D))) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(ax) || !finite_pos(ay)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(zx, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (T == 0) return MQ_OK;
+    if (!x || !y || !table) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_rope_apply(x, T, H, D, ax, zx, table, ay, zy, out_bits, y,
+                                          as_stream(stream)));
+}
+
 mq_status mq_lut_build(int32_t op, float ax, int32_t zx, float ay, int32_t zy, int32_t out_bits,
                        void* lut, void* stream)
 {

@@ -89,6 +89,11 @@ hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int
 hipError_t launch_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
                               float a2, int32_t z2, int64_t n, float ay, int32_t zy,
                               int32_t bits, void* y, hipStream_t st);
+hipError_t launch_rope_table(int64_t T, int64_t D, double base, int64_t pos0, double* table,
+                             hipStream_t st);
+hipError_t launch_rope_apply(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax,
+                             int32_t zx, const double* table, float ay, int32_t zy, int32_t bits,
+                             void* y, hipStream_t st);
 hipError_t launch_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
                        double base, int64_t pos0, float ay, int32_t zy, int32_t bits,
                        double* table, void* y, hipStream_t st);

@@ -344,6 +344,17 @@ def test_softmax_causal_rejects_invalid_arguments(call):
     lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, 10000.0, -1, 1.0, 0, 16, NZ, NZ, None),
     lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, 10000.0, 0, 1.0, 0, 16, None, NZ, None),
     lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, float("nan"), 0, 1.0, 0, 16, NZ, NZ, None),
+    lambda L: L.mq_rope_table(4, 3, 10000.0, 0, NZ, None),
+    lambda L: L.mq_rope_table(4, 8, 0.5, 0, NZ, None),
+    lambda L: L.mq_rope_table(4, 8, 10000.0, -1, NZ, None),
+    lambda L: L.mq_rope_table(4, 8, 10000.0, 0, None, None),
+    lambda L: L.mq_rope_table(-1, 8, 10000.0, 0, NZ, None),
+    lambda L: L.mq_rope_apply(NZ, 4, 2, 3, 1.0, 0, NZ, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_rope_apply(NZ, 4, 0, 8, 1.0, 0, NZ, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_rope_apply(NZ, 4, 2, 8, 0.0, 0, NZ, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_rope_apply(NZ, 4, 2, 8, 1.0, 0, None, 1.0, 0, 16, NZ, None),
+    lambda L: L.mq_rope_apply(NZ, 4, 2, 8, 1.0, 0, NZ, 1.0, 300, 8, NZ, None),
+    lambda L: L.mq_rope_apply(NZ, 4, 2, 8, 1.0, 0, NZ, 1.0, 0, 12, NZ, None),
 ])
 def test_mul_and_rope_reject_invalid_arguments(call):
     assert call(mq.lib()) == 1

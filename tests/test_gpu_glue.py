@@ -177,6 +177,34 @@ def test_mul_requant_parity(n, out_bits):
     assert np.array_equal(y.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("T,H,D,pos0,out_bits", [(1024, 32, 64, 0, 16), (300, 4, 64, 9, 8),
+                                                 (70000, 1, 2, 3, 16), (5, 3, 6, 0, 8)])
+def test_rope_table_then_apply(T, H, D, pos0, out_bits):
+    """mq_rope_table + mq_rope_apply give mq_rope's bits; one table serves
+    several tensors (queries and keys of any head count); past 65535 tokens
+    the apply kernel's grid wraps over the token rows."""
+    mq = _mq()
+    rng = np.random.default_rng(T + D)
+    x = rng.integers(-30000, 30000, (T, H * D)).astype(np.int16)
+    xk = rng.integers(-30000, 30000, (T, 2 * D)).astype(np.int16)
+    ax, zx = 2e-4, -7
+    ay, zy = (3e-4, 4) if out_bits == 16 else (0.05, -2)
+    table = mq.mq_rope_table(T, D, pos0=pos0)
+    for xx, hh in ((x, H), (xk, 2)):
+        y = mq.mq_rope_apply(_dev(xx), hh, ax, zx, ay, zy, table, out_bits).cpu().numpy()
+        y1 = mq.mq_rope(_dev(xx), hh, ax, zx, ay, zy, out_bits, pos0=pos0).cpu().numpy()
+        assert np.array_equal(y, y1)
+        if T <= 1024:
+            ref = oracle.rope(xx, hh, ax, zx, ay, zy, out_bits, pos0=pos0)
+            assert np.mean(y != ref) < 1e-3 and np.max(np.abs(y.astype(np.int64) - ref)) <= 1
+    if T > 65535:  # the last rows, against the oracle on those rows alone
+        tail = x[-5:]
+        ref = oracle.rope(np.ascontiguousarray(tail), H, ax, zx, ay, zy, out_bits,
+                          pos0=pos0 + T - 5)
+        got = mq.mq_rope_apply(_dev(x), H, ax, zx, ay, zy, table, out_bits).cpu().numpy()[-5:]
+        assert np.max(np.abs(got.astype(np.int64) - ref)) <= 1
+
+
 @pytest.mark.parametrize("T,H,D,pos0,out_bits", [(1024, 32, 64, 0, 16), (1024, 4, 64, 0, 8),
                                                  (7, 3, 128, 1000, 16), (1, 2, 2, 5, 8)])
 def test_rope_parity(T, H, D, pos0, out_bits):
