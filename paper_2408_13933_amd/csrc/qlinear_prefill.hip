@@ -968,10 +968,15 @@ template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16
 // work-groups share a CU, so one's prologue and epilogue overlap the
 // other's products
 template <int OB> using T128x128A16S2 = Cfg<8, OB, 128, 128, 2, 2, 64, 2, 2, 1, 16>;
-static_assert(T128x128A16S2<8>::A16_I32 && !T128x128A16<8>::A16_I32,
+// at most 64 channels (P V over a 64-dimensional head): a 128x128 tile
+// would leave half of its products and weight loads idle
+template <int OB> using T128x64A16 = Cfg<8, OB, 128, 64, 2, 2, 64, 4, 2, 2, 16>;
+static_assert(T128x128A16S2<8>::A16_I32 && !T128x128A16<8>::A16_I32 &&
+                  !T128x64A16<8>::A16_I32,
               "the int32 epilogue belongs to the short-K tile");
 static_assert(T128x128A16<8>::TM == kA16TileM && T128x128A16<8>::BK == kA16TileK &&
-                  T128x128A16S2<8>::TM == kA16TileM && T128x128A16S2<8>::BK == kA16TileK,
+                  T128x128A16S2<8>::TM == kA16TileM && T128x128A16S2<8>::BK == kA16TileK &&
+                  T128x64A16<8>::TM == kA16TileM && T128x64A16<8>::BK == kA16TileK,
               "the causal column sums assume these 16-bit tile sizes");
 
 // Per-block cycle model of each tile shape on MI355X (phase timings of the
@@ -1107,6 +1112,12 @@ hipError_t launch_a16(const QLinearArgs& p, hipStream_t s)
                           : launch_cfg<T128x128A16S2<16>, true>(p, 1, s);
         return o8 ? launch_cfg<T128x128A16S2<8>, false>(p, 1, s)
                   : launch_cfg<T128x128A16S2<16>, false>(p, 1, s);
+    }
+    if (p.N <= 64) {
+        if (ro) return o8 ? launch_cfg<T128x64A16<8>, true>(p, 1, s)
+                          : launch_cfg<T128x64A16<16>, true>(p, 1, s);
+        return o8 ? launch_cfg<T128x64A16<8>, false>(p, 1, s)
+                  : launch_cfg<T128x64A16<16>, false>(p, 1, s);
     }
     if (ro) return o8 ? launch_cfg<T128x128A16<8>, true>(p, 1, s)
                       : launch_cfg<T128x128A16<16>, true>(p, 1, s);
