@@ -57,12 +57,15 @@ __global__ __launch_bounds__(256) void attn_sums_kernel(const int16_t* a, int64_
     // rows past the end still take part in the reduction (all lanes of a
     // group reach the shuffles) with a zero sum
     const bool live = row < rows_a + rows_b;
+    // row indices below 2^32 (the host's check) divide in 32 bits
     int64_t s = 0;
-    if (live && row < rows_a)
-        s = row_sum_part(a + (row / M) * a_bs + (row % M) * lda, K, li, lpr, vec_a);
-    else if (live) {
-        const int64_t r = row - rows_a;  // (g * n_mb + mb) * N + n
-        const int64_t n = r % N, mb = (r / N) % n_mb, g = r / (N * n_mb);
+    if (live && row < rows_a) {
+        const uint32_t h = (uint32_t)row / (uint32_t)M, m = (uint32_t)row - h * (uint32_t)M;
+        s = row_sum_part(a + (int64_t)h * a_bs + (int64_t)m * lda, K, li, lpr, vec_a);
+    } else if (live) {
+        const uint32_t r = (uint32_t)(row - rows_a);  // (g * n_mb + mb) * N + n
+        const uint32_t q = r / (uint32_t)N, n = r - q * (uint32_t)N;
+        const uint32_t g = q / (uint32_t)n_mb, mb = q - g * (uint32_t)n_mb;
         int64_t len = K;
         if (in_causal >= 0) {
             const int64_t m_end = (mb + 1) * tile_m < M ? (mb + 1) * tile_m : M;
@@ -115,6 +118,9 @@ hipError_t launch_attn_sums(const int16_t* a, int64_t lda, int64_t a_bs, int32_t
     const int64_t rpb = 256 / lpr;
     const int64_t blocks = (rows_a + rows_b + rpb - 1) / rpb;
     if (blocks == 0) return hipSuccess;
+    if (rows_a + rows_b >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 32) ||
+        N >= ((int64_t)1 << 32))
+        return hipErrorInvalidValue;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     const bool vec_a = (uintptr_t)a % 16 == 0 && (lda * 2) % 16 == 0 && (a_bs * 2) % 16 == 0;
     const bool vec_b = (uintptr_t)b % 16 == 0 && ldb % 16 == 0 && b_bs % 16 == 0;
