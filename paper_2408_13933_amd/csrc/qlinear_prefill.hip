@@ -291,7 +291,9 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                         else
                             c = __builtin_elementwise_add_sat(a32, off[r]);
                     }
-                    if constexpr (!FAST || PRE || C::A16) {
+                    // (no column of the tile with a pre-shift: bnd = 2^31 - 1 and
+                    // pre = 0, both the identity)
+                    if constexpr (!FAST || PRE) {
                         c = max(min(c, bnd[r]), -bnd[r]);
                         c = (int32_t)((uint32_t)c << pre[r]);
                     }
