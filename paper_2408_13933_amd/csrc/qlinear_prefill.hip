@@ -440,10 +440,15 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
     int64_t KL = !C::SPLITK ? K
                  : (K - k_begin) < (int64_t)kt_per_split * C::BK
                      ? (K - k_begin) : (int64_t)kt_per_split * C::BK;
+    // causal activations: the column sums come per block of kA16TileM rows
+    // (a tile of fewer rows uses its enclosing block's), each over the K
+    // range up to the stage that holds that block's last row's boundary
+    const int64_t m_blk = m_tile / kA16TileM;
     if (STR && p.in_causal >= 0) {
-        // the activations past the last row's boundary are zero-point codes
-        // (no contribution): stop at the stage that holds the boundary
-        const int64_t need = (m_tile + rows_a + p.in_causal + C::BK - 1) / C::BK * C::BK;
+        // the activations past the boundary are zero-point codes (no
+        // contribution), so the tile stops at the same stage
+        const int64_t m_end = (m_blk + 1) * kA16TileM < p.M ? (m_blk + 1) * kA16TileM : p.M;
+        const int64_t need = (m_end + p.in_causal + C::BK - 1) / C::BK * C::BK;
         if (need < KL) KL = need;
     }
     const int64_t k_begin_w = C::WBITS == 8 ? k_begin : k_begin / 2;
@@ -517,7 +522,7 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
         int64_t n = n_tile + tid;
         if (n >= p.N) n = p.N - 1;
         col_ws = p.w_scale[STR ? n * p.ws_stride : n];
-        col_cs = p.colsum[STR ? bg * p.cs_bs + (p.in_causal >= 0 ? tm * p.cs_mt : 0) + n : n];
+        col_cs = p.colsum[STR ? bg * p.cs_bs + (p.in_causal >= 0 ? m_blk * p.cs_mt : 0) + n : n];
         // branch-free; without bias the (unused) load reads w_scale[0]
         col_bias = (p.bias ? p.bias : p.w_scale)[p.bias ? n : 0];
         if constexpr (CASYM) col_zw = p.w_zp[n];
@@ -971,14 +976,16 @@ template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16
 // other's products
 template <int OB> using T128x128A16S2 = Cfg<8, OB, 128, 128, 2, 2, 64, 2, 2, 1, 16>;
 // at most 64 channels (P V over a 64-dimensional head): a 128x128 tile
-// would leave half of its products and weight loads idle
-template <int OB> using T128x64A16 = Cfg<8, OB, 128, 64, 2, 2, 64, 4, 2, 2, 16>;
+// would leave half of its products and weight loads idle, and 64-row tiles
+// double the work-groups (P V at 1024 tokens: 512 instead of 256; the
+// causal form's longest tile has half the rows)
+template <int OB> using T64x64A16 = Cfg<8, OB, 64, 64, 2, 2, 64, 4, 2, 2, 16>;
 static_assert(T128x128A16S2<8>::A16_I32 && !T128x128A16<8>::A16_I32 &&
-                  !T128x64A16<8>::A16_I32,
+                  !T64x64A16<8>::A16_I32,
               "the int32 epilogue belongs to the short-K tile");
 static_assert(T128x128A16<8>::TM == kA16TileM && T128x128A16<8>::BK == kA16TileK &&
                   T128x128A16S2<8>::TM == kA16TileM && T128x128A16S2<8>::BK == kA16TileK &&
-                  T128x64A16<8>::TM == kA16TileM && T128x64A16<8>::BK == kA16TileK,
+                  kA16TileM % T64x64A16<8>::TM == 0 && T64x64A16<8>::BK == kA16TileK,
               "the causal column sums assume these 16-bit tile sizes");
 
 // Per-block cycle model of each tile shape on MI355X (phase timings of the
@@ -1116,10 +1123,10 @@ hipError_t launch_a16(const QLinearArgs& p, hipStream_t s)
                   : launch_cfg<T128x128A16S2<16>, false>(p, 1, s);
     }
     if (p.N <= 64) {
-        if (ro) return o8 ? launch_cfg<T128x64A16<8>, true>(p, 1, s)
-                          : launch_cfg<T128x64A16<16>, true>(p, 1, s);
-        return o8 ? launch_cfg<T128x64A16<8>, false>(p, 1, s)
-                  : launch_cfg<T128x64A16<16>, false>(p, 1, s);
+        if (ro) return o8 ? launch_cfg<T64x64A16<8>, true>(p, 1, s)
+                          : launch_cfg<T64x64A16<16>, true>(p, 1, s);
+        return o8 ? launch_cfg<T64x64A16<8>, false>(p, 1, s)
+                  : launch_cfg<T64x64A16<16>, false>(p, 1, s);
     }
     if (ro) return o8 ? launch_cfg<T128x128A16<8>, true>(p, 1, s)
                       : launch_cfg<T128x128A16<16>, true>(p, 1, s);

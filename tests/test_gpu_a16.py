@@ -33,7 +33,7 @@ A16_CASES = [
     (200, 1024, 300, 4, 16, False),    # int4 weights above 16 tokens: generic kernel
     (300, 64, 257, 8, 16, True),       # short K: the two-stage tile
     (129, 128, 200, 8, 8, False),
-    (300, 1024, 48, 8, 16, True),      # at most 64 channels: the 128x64 tile, ragged N
+    (300, 1024, 48, 8, 16, True),      # at most 64 channels: the 64x64 tile, ragged N
     (129, 2048, 64, 8, 8, False),
 ]
 
