@@ -601,7 +601,7 @@ def block_sweep(T=1024):
     """One TinyLlama decoder block on integer codes, every step on the GPU
     (paper_2408_13933_amd.block): RMSNorm, q/k/v projections, RoPE, Q K^T,
     causal softmax, P V, o projection, residual add, RMSNorm, gate/up, SiLU
-    table, gated product, down projection, residual add.  Inputs: seeded
+    table fused with the gated product, down projection, residual add.  Inputs: seeded
     synthetic residual stream and weights (workloads.make_block), static
     formats from the float pass.  Prints the graph-replayed time of each
     step and of the whole block."""

@@ -333,6 +333,22 @@ mq_status mq_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t*
                          int32_t out_bits, void* y, void* stream);
 
 /*
+ * mq_lut_mul -- a table lookup and the product of mq_mul_requant in one
+ * pass (the gated unit SiLU(gate) * up with the SiLU codes kept out of
+ * memory): u = lut[x1[i] + 32768], a code of the table's format (a1, z1),
+ *   y[i] = code(a1 (u - z1) * a2 (x2[i] - z2))
+ * with the arithmetic of mq_mul_requant, so y equals mq_lut_apply followed
+ * by mq_mul_requant bit for bit.
+ *   x1, x2 device int16 [numel]; lut device table of mq_lut_build,
+ *   lut_bits 8 or 16 (its entries); y device int8 or int16 [numel]
+ *   a1, a2, ay finite and > 0; z1 in the lut_bits range, z2 in int16,
+ *   zy in the out_bits range.
+ */
+mq_status mq_lut_mul(const int16_t* x1, const void* lut, int32_t lut_bits, float a1, int32_t z1,
+                     const int16_t* x2, float a2, int32_t z2, int64_t numel, float ay,
+                     int32_t zy, int32_t out_bits, void* y, void* stream);
+
+/*
  * mq_rope -- rotary position embedding on the query or key codes of a
  * Llama-family block (the paper's models; a non-linear operator kept at 16
  * bits): for token t, head h and pair i < D/2 (dimensions i and i + D/2 of

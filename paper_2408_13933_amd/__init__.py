@@ -89,6 +89,8 @@ def lib():
                                  c_p]
     L.mq_rope.argtypes = [c_p, c_i64, c_i64, c_i64, c_f, c_i32, ctypes.c_double, c_i64, c_f, c_i32,
                           c_i32, c_p, c_p, c_p]
+    L.mq_lut_mul.argtypes = [c_p, c_p, c_i32, c_f, c_i32, c_p, c_f, c_i32, c_i64, c_f, c_i32,
+                             c_i32, c_p, c_p]
     L.mq_rope_table.argtypes = [c_i64, c_i64, ctypes.c_double, c_i64, c_p, c_p]
     L.mq_rope_apply.argtypes = [c_p, c_i64, c_i64, c_i64, c_f, c_i32, c_p, c_f, c_i32, c_i32, c_p,
                                 c_p]
@@ -114,7 +116,7 @@ def lib():
                  "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
                  "mq_arl_backward", "mq_add_requant", "mq_lut_build", "mq_lut_apply",
                  "mq_rmsnorm", "mq_softmax", "mq_softmax_causal", "mq_mul_requant",
-                 "mq_rope", "mq_rope_table", "mq_rope_apply"):
+                 "mq_rope", "mq_rope_table", "mq_rope_apply", "mq_lut_mul"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -399,6 +401,24 @@ def mq_mul_requant(x1, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy
                                 float(ay), int(zy), int(out_bits),
                                 _dev_ptr(out, _act_dtype(out_bits), "out", tuple(x1.shape)),
                                 _stream_ptr(stream)), "mq_mul_requant")
+    return out
+
+
+def mq_lut_mul(x1, lut, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy: int,
+               out_bits: int = 8, out=None, stream=None):
+    """lut[x1 + 32768] (format a1, z1) times the codes x2, requantized: the
+    gated unit in one pass (mq_lut_apply then mq_mul_requant)."""
+    torch = _torch()
+    if tuple(x1.shape) != tuple(x2.shape):
+        raise ValueError("x1 and x2 must have the same shape")
+    bits = _bits_of(lut)
+    out = torch.empty(x1.shape, dtype=_act_dtype(out_bits), device=x1.device) if out is None else out
+    _check(lib().mq_lut_mul(_dev_ptr(x1, torch.int16, "x1"),
+                            _dev_ptr(lut, lut.dtype, "lut", (65536,)), int(bits), float(a1),
+                            int(z1), _dev_ptr(x2, torch.int16, "x2"), float(a2), int(z2),
+                            x1.numel(), float(ay), int(zy), int(out_bits),
+                            _dev_ptr(out, _act_dtype(out_bits), "out", tuple(x1.shape)),
+                            _stream_ptr(stream)), "mq_lut_mul")
     return out
 
 

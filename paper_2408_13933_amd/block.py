@@ -28,6 +28,8 @@ from . import workloads as wl
 # stage -> output bit width
 STAGE_BITS = dict(h0=16, x1=8, q=16, k=16, v=8, qr=16, kr=8, scores=16, probs=16, ctx=8, o=16,
                   h1=16, x2=8, gate=16, up=16, silu=16, mul=8, down=16, h2=16)
+# stages whose codes the GPU block keeps out of memory (fused into the next step)
+NOT_STORED = ("silu",)
 # stage -> (weight, input stage) of the linears
 LINEARS = dict(q=("q_proj", "x1"), k=("k_proj", "x1"), v=("v_proj", "x1"), o=("o_proj", "ctx"),
                gate=("gate_proj", "x2"), up=("up_proj", "x2"), down=("down_proj", "mul"))
@@ -65,7 +67,7 @@ class BlockGPU:
                       o=(T, hid), h1=(T, hid), x2=(T, hid), gate=(T, ffn), up=(T, ffn),
                       silu=(T, ffn), mul=(T, ffn), down=(T, hid), h2=(T, hid))
         self.out = {s: torch.empty(shp, dtype=i8 if STAGE_BITS[s] == 8 else i16, device=dev)
-                    for s, shp in shapes.items()}
+                    for s, shp in shapes.items() if s not in NOT_STORED}
         self.out["h0"] = self.h0
         self.vt = torch.empty((G * D, T), dtype=i8, device=dev)
         # the rotary angles depend only on T, D and the base: one table for
@@ -129,9 +131,10 @@ class BlockGPU:
                                                8, out=o["x2"])),
             ("gate_proj", lambda: self._linear("gate")),
             ("up_proj", lambda: self._linear("up")),
-            ("silu", lambda: mq.mq_lut_apply(o["gate"], self.lut, out=o["silu"])),
-            ("gated_product", lambda: mq.mq_mul_requant(o["silu"], *f["silu"], o["up"], *f["up"],
-                                                        *f["mul"], 8, out=o["mul"])),
+            # SiLU table and gated product in one pass: the SiLU codes stay
+            # in registers (the "silu" buffer is not written)
+            ("silu_gated", lambda: mq.mq_lut_mul(o["gate"], self.lut, *f["silu"], o["up"],
+                                                 *f["up"], *f["mul"], 8, out=o["mul"])),
             ("down_proj", lambda: self._linear("down")),
             ("residual2", lambda: mq.mq_add_requant(o["h1"], *f["h1"], o["down"], *f["down"],
                                                     *f["h2"], 16, out=o["h2"])),

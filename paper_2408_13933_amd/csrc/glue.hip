@@ -221,6 +221,45 @@ __device__ inline void store8(void* y, int64_t i, const int32_t* q)
     }
 }
 
+// Table lookup fused with the product of two dequantized codes: the gated
+// unit SiLU(gate) * up without the SiLU codes going through memory.
+// u = lut[x1 + 32768] (LB-bit entries in format (a1, z1)), then the product
+// of mul_one with x2: the same two steps as mq_lut_apply and
+// mq_mul_requant, so the same bits.
+template <int LB, int OB>
+__global__ __launch_bounds__(kLutThreads) void lut_mul_kernel(
+    const int16_t* __restrict__ x1, const void* __restrict__ lut, float a1, int32_t z1,
+    const int16_t* __restrict__ x2, float a2, int32_t z2, int64_t n8, int64_t begin, int64_t n,
+    float ay, int32_t zy, void* __restrict__ y)
+{
+    using T = typename std::conditional<LB == 8, int8_t, int16_t>::type;
+    extern __shared__ __align__(16) int8_t lds_table[];
+    const T* tab = reinterpret_cast<const T*>(lds_table);
+    {
+        const int4* src = static_cast<const int4*>(lut);
+        int4* dst = reinterpret_cast<int4*>(lds_table);
+        constexpr int chunks = 65536 * sizeof(T) / 16;
+        for (int i = threadIdx.x; i < chunks; i += kLutThreads) dst[i] = src[i];
+    }
+    __syncthreads();
+    const int64_t stride = (int64_t)gridDim.x * kLutThreads;
+    const int64_t t0 = (int64_t)blockIdx.x * kLutThreads + threadIdx.x;
+    for (int64_t i = t0; i < n8; i += stride) {
+        const int4 g = reinterpret_cast<const int4*>(x1)[i];
+        const int4 v = reinterpret_cast<const int4*>(x2)[i];
+        const int16_t* gc = reinterpret_cast<const int16_t*>(&g);
+        const int16_t* vc = reinterpret_cast<const int16_t*>(&v);
+        int32_t q[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            q[u] = mul_one<OB>(tab[(int32_t)gc[u] + 32768], vc[u], a1, z1, a2, z2, ay, zy);
+        store8<OB>(y, 8 * i, q);
+    }
+    for (int64_t i = begin + t0; i < n; i += stride)
+        store_code<OB>(y, i, mul_one<OB>(tab[(int32_t)x1[i] + 32768], x2[i], a1, z1, a2, z2, ay,
+                                         zy));
+}
+
 template <int NCH>
 struct RowRegs {
     int16_t v[NCH][8];
@@ -708,13 +747,14 @@ hipError_t launch_lut_apply(const int16_t* x, int64_t n, const void* lut, int32_
                             hipStream_t st)
 {
     // one or two blocks per CU (the table fills 64 or 128 KiB of LDS), each
-    // streaming at least 32 codes per thread
+    // streaming at least 16 codes per thread (the 1024 x 5632 SiLU input
+    // then fills all 256 CUs)
     const uintptr_t ya = bits == 8 ? 8 : 16;
     const bool vec = ((uintptr_t)x % 16) == 0 && ((uintptr_t)y % ya) == 0 &&
                      ((uintptr_t)lut % 16) == 0;
     const int64_t n8 = vec ? n / 8 : 0;
     const int cap = bits == 8 ? 512 : 256;
-    const int g = grid_for(n, kLutThreads * 32, cap);
+    const int g = grid_for(n, kLutThreads * 16, cap);
     const size_t lds = 65536 * (bits / 8);
     if (bits == 8) {
         static const hipError_t a8 = hipFuncSetAttribute(
@@ -730,6 +770,38 @@ hipError_t launch_lut_apply(const int16_t* x, int64_t n, const void* lut, int32_
         lut_apply_kernel<16><<<g, kLutThreads, lds, st>>>(x, n8, n8 * 8, n, lut, y);
     }
     return hipGetLastError();
+}
+
+template <int LB, int OB>
+static hipError_t lut_mul_launch(const int16_t* x1, const void* lut, float a1, int32_t z1,
+                                 const int16_t* x2, float a2, int32_t z2, int64_t n, float ay,
+                                 int32_t zy, void* y, hipStream_t st)
+{
+    const uintptr_t ya = OB == 8 ? 8 : 16;
+    const bool vec = ((uintptr_t)x1 % 16) == 0 && ((uintptr_t)x2 % 16) == 0 &&
+                     ((uintptr_t)y % ya) == 0 && ((uintptr_t)lut % 16) == 0;
+    const int64_t n8 = vec ? n / 8 : 0;
+    const int g = grid_for(n, kLutThreads * 16, LB == 8 ? 512 : 256);
+    const size_t lds = 65536 * (LB / 8);
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&lut_mul_kernel<LB, OB>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (attr != hipSuccess) return attr;
+    lut_mul_kernel<LB, OB><<<g, kLutThreads, lds, st>>>(x1, lut, a1, z1, x2, a2, z2, n8, n8 * 8,
+                                                       n, ay, zy, y);
+    return hipGetLastError();
+}
+
+hipError_t launch_lut_mul(const int16_t* x1, const void* lut, int32_t lut_bits, float a1,
+                          int32_t z1, const int16_t* x2, float a2, int32_t z2, int64_t n,
+                          float ay, int32_t zy, int32_t bits, void* y, hipStream_t st)
+{
+    if (n == 0) return hipSuccess;
+    if (lut_bits == 8)
+        return bits == 8 ? lut_mul_launch<8, 8>(x1, lut, a1, z1, x2, a2, z2, n, ay, zy, y, st)
+                         : lut_mul_launch<8, 16>(x1, lut, a1, z1, x2, a2, z2, n, ay, zy, y, st);
+    return bits == 8 ? lut_mul_launch<16, 8>(x1, lut, a1, z1, x2, a2, z2, n, ay, zy, y, st)
+                     : lut_mul_launch<16, 16>(x1, lut, a1, z1, x2, a2, z2, n, ay, zy, y, st);
 }
 
 template <int BITS, int NCH>

@@ -162,6 +162,20 @@ mq_status mq_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t*
                                            as_stream(stream)));
 }
 
+mq_status mq_lut_mul(const int16_t* x1, const void* lut, int32_t lut_bits, float a1, int32_t z1,
+                     const int16_t* x2, float a2, int32_t z2, int64_t numel, float ay,
+                     int32_t zy, int32_t out_bits, void* y, void* stream)
+{
+    if (numel < 0 || numel > kMaxElems || !act_bits_ok(out_bits) || !act_bits_ok(lut_bits))
+        return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(a1) || !finite_pos(a2) || !finite_pos(ay)) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(z1, lut_bits) || !zp_ok(z2, 16) || !zp_ok(zy, out_bits)) return MQ_ERR_INVALID_ARG;
+    if (numel == 0) return MQ_OK;
+    if (!x1 || !lut || !x2 || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_lut_mul(x1, lut, lut_bits, a1, z1, x2, a2, z2, numel, ay, zy,
+                                       out_bits, y, as_stream(stream)));
+}
+
 mq_status mq_rope(const int16_t* x, int64_t T, int64_t H, int64_t D, float ax, int32_t zx,
                   double base, int64_t pos0, float ay, int32_t zy, int32_t out_bits,
                   double* table, void* y, void* stream)

@@ -10,7 +10,7 @@ import pytest
 
 pytestmark = pytest.mark.gpu
 
-TIE_STAGES = ("qr", "kr", "probs", "silu")
+TIE_STAGES = ("qr", "kr", "probs", "mul")  # "mul": through the SiLU table
 
 
 @pytest.mark.parametrize("T", [128, 200])
@@ -26,6 +26,8 @@ def test_block_stages_match_the_oracle(T):
     assert fmt == g.fmt
     diverged = None
     for stage in blk.STAGE_BITS:
+        if stage in blk.NOT_STORED:  # fused into the next step
+            continue
         got = g.out[stage].cpu().numpy()
         exp = ref[stage]
         if stage == "scores":  # only the causal lower triangle is computed

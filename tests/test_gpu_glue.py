@@ -177,6 +177,31 @@ def test_mul_requant_parity(n, out_bits):
     assert np.array_equal(y.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("n,lut_bits,out_bits", [(1024 * 5632, 16, 8), (777, 8, 16), (1, 16, 16),
+                                                (4099, 8, 8)])
+def test_lut_mul_equals_lookup_then_product(n, lut_bits, out_bits):
+    """The fused lookup and product give the bits of the oracle's table
+    lookup followed by its product (and of the two GPU steps)."""
+    mq = _mq()
+    rng = np.random.default_rng(n + lut_bits)
+    ax, zx = 1e-3, -100
+    a1, z1 = (0.05, -7) if lut_bits == 8 else (4e-4, 11)
+    lut = oracle.lut_build(oracle.LUT_SILU, ax, zx, a1, z1, lut_bits)
+    x1 = rng.integers(-32768, 32768, n).astype(np.int16)
+    x2 = rng.integers(-32768, 32768, n).astype(np.int16)
+    a2, z2 = 7.7e-4, 300
+    ay, zy = (0.05, 5) if out_bits == 8 else (1e-3, -5)
+    ref = oracle.mul_requant(lut[x1.astype(np.int64) + 32768].astype(np.int16), a1, z1, x2, a2,
+                             z2, ay, zy, out_bits)
+    glut = _dev(lut)
+    y = mq.mq_lut_mul(_dev(x1), glut, a1, z1, _dev(x2), a2, z2, ay, zy, out_bits)
+    assert np.array_equal(y.cpu().numpy(), ref)
+    import torch
+    two = mq.mq_mul_requant(mq.mq_lut_apply(_dev(x1), glut).to(torch.int16), a1, z1, _dev(x2),
+                            a2, z2, ay, zy, out_bits)
+    assert np.array_equal(two.cpu().numpy(), ref)
+
+
 @pytest.mark.parametrize("T,H,D,pos0,out_bits", [(1024, 32, 64, 0, 16), (300, 4, 64, 9, 8),
                                                  (70000, 1, 2, 3, 16), (5, 3, 6, 0, 8)])
 def test_rope_table_then_apply(T, H, D, pos0, out_bits):
