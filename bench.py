@@ -600,7 +600,7 @@ def attn_sweep():
 def block_sweep(T=1024):
     """One TinyLlama decoder block on integer codes, every step on the GPU
     (paper_2408_13933_amd.block): RMSNorm, q/k/v projections, RoPE, Q K^T,
-    causal softmax, P V, o projection, residual add, RMSNorm, gate/up, SiLU
+    causal softmax, P V, o projection, residual add fused with the RMSNorm, gate/up, SiLU
     table fused with the gated product, down projection, residual add.  Inputs: seeded
     synthetic residual stream and weights (workloads.make_block), static
     formats from the float pass.  Prints the graph-replayed time of each

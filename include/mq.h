@@ -333,6 +333,21 @@ mq_status mq_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t*
                          int32_t out_bits, void* y, void* stream);
 
 /*
+ * mq_add_rmsnorm -- the residual add and the RMSNorm of its result in one
+ * pass: h = mq_add_requant(x1, x2) as int16 codes in format (ah, zh),
+ * written to h, and y = mq_rmsnorm(h) (gamma, eps, ay, zy, out_bits), with
+ * the arithmetic of those two calls, so the same bits (rows that do not
+ * fit the one-pass kernel run the two steps).
+ *   x1, x2 device int16 [M][K]; h device int16 [M][K], written;
+ *   y device int8 or int16 [M][K]; gamma device fp32 [K] or NULL
+ *   1 <= K <= 2^20; scales finite and > 0; eps finite and >= 0.
+ */
+mq_status mq_add_rmsnorm(const int16_t* x1, float a1, int32_t z1, const int16_t* x2, float a2,
+                         int32_t z2, int64_t M, int64_t K, float ah, int32_t zh, int16_t* h,
+                         const float* gamma, float eps, float ay, int32_t zy, int32_t out_bits,
+                         void* y, void* stream);
+
+/*
  * mq_lut_mul -- a table lookup and the product of mq_mul_requant in one
  * pass (the gated unit SiLU(gate) * up with the SiLU codes kept out of
  * memory): u = lut[x1[i] + 32768], a code of the table's format (a1, z1),

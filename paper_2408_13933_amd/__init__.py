@@ -89,6 +89,8 @@ def lib():
                                  c_p]
     L.mq_rope.argtypes = [c_p, c_i64, c_i64, c_i64, c_f, c_i32, ctypes.c_double, c_i64, c_f, c_i32,
                           c_i32, c_p, c_p, c_p]
+    L.mq_add_rmsnorm.argtypes = [c_p, c_f, c_i32, c_p, c_f, c_i32, c_i64, c_i64, c_f, c_i32, c_p,
+                                 c_p, c_f, c_f, c_i32, c_i32, c_p, c_p]
     L.mq_lut_mul.argtypes = [c_p, c_p, c_i32, c_f, c_i32, c_p, c_f, c_i32, c_i64, c_f, c_i32,
                              c_i32, c_p, c_p]
     L.mq_rope_table.argtypes = [c_i64, c_i64, ctypes.c_double, c_i64, c_p, c_p]
@@ -116,7 +118,8 @@ def lib():
                  "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
                  "mq_arl_backward", "mq_add_requant", "mq_lut_build", "mq_lut_apply",
                  "mq_rmsnorm", "mq_softmax", "mq_softmax_causal", "mq_mul_requant",
-                 "mq_rope", "mq_rope_table", "mq_rope_apply", "mq_lut_mul"):
+                 "mq_rope", "mq_rope_table", "mq_rope_apply", "mq_lut_mul",
+                 "mq_add_rmsnorm"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -402,6 +405,27 @@ def mq_mul_requant(x1, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy
                                 _dev_ptr(out, _act_dtype(out_bits), "out", tuple(x1.shape)),
                                 _stream_ptr(stream)), "mq_mul_requant")
     return out
+
+
+def mq_add_rmsnorm(x1, a1: float, z1: int, x2, a2: float, z2: int, ah: float, zh: int, gamma,
+                   eps: float, ay: float, zy: int, out_bits: int = 8, h=None, out=None,
+                   stream=None):
+    """Residual add (int16 codes h, format ah, zh) and RMSNorm of h in one
+    pass; returns (h, y)."""
+    torch = _torch()
+    M, K = x1.shape
+    if tuple(x2.shape) != (M, K):
+        raise ValueError("x1 and x2 must have the same shape")
+    h = torch.empty((M, K), dtype=torch.int16, device=x1.device) if h is None else h
+    out = torch.empty((M, K), dtype=_act_dtype(out_bits), device=x1.device) if out is None else out
+    g = None if gamma is None else _dev_ptr(gamma, torch.float32, "gamma", (K,))
+    _check(lib().mq_add_rmsnorm(_dev_ptr(x1, torch.int16, "x1"), float(a1), int(z1),
+                                _dev_ptr(x2, torch.int16, "x2"), float(a2), int(z2), M, K,
+                                float(ah), int(zh), _dev_ptr(h, torch.int16, "h", (M, K)), g,
+                                float(eps), float(ay), int(zy), int(out_bits),
+                                _dev_ptr(out, _act_dtype(out_bits), "out", (M, K)),
+                                _stream_ptr(stream)), "mq_add_rmsnorm")
+    return h, out
 
 
 def mq_lut_mul(x1, lut, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy: int,

@@ -125,10 +125,12 @@ class BlockGPU:
                                                      *f["probs"], *f["v"], *f["ctx"], 8, out=cv,
                                                      workspace=self.attn_ws, in_causal=0)),
             ("o_proj", lambda: self._linear("o")),
-            ("residual1", lambda: mq.mq_add_requant(o["h0"], *f["h0"], o["o"], *f["o"], *f["h1"],
-                                                    16, out=o["h1"])),
-            ("rmsnorm2", lambda: mq.mq_rmsnorm(o["h1"], *f["h1"], self.gamma2, self.eps, *f["x2"],
-                                               8, out=o["x2"])),
+            # the residual add and the RMSNorm of its sum in one pass (both
+            # outputs written)
+            ("residual1_rmsnorm2", lambda: mq.mq_add_rmsnorm(o["h0"], *f["h0"], o["o"], *f["o"],
+                                                             *f["h1"], self.gamma2, self.eps,
+                                                             *f["x2"], 8, h=o["h1"],
+                                                             out=o["x2"])),
             ("gate_proj", lambda: self._linear("gate")),
             ("up_proj", lambda: self._linear("up")),
             # SiLU table and gated product in one pass: the SiLU codes stay

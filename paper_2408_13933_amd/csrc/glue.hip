@@ -320,6 +320,57 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_regs_kernel(const int16_t* _
     }
 }
 
+// Residual add fused with the RMSNorm that reads its result: per row, the
+// sum codes h = code_h(a1 (x1 - z1) + a2 (x2 - z2)) (add_one) are written
+// and, still in registers, normalized as rmsnorm_regs_kernel normalizes its
+// input.  The same operations as mq_add_requant then mq_rmsnorm, so the
+// same bits, with one read of h less and one launch less.
+template <int BITS, int NCH>
+__global__ __launch_bounds__(kThreads) void add_rmsnorm_kernel(
+    const int16_t* __restrict__ x1, float a1, int32_t z1, const int16_t* __restrict__ x2,
+    float a2, int32_t z2, int64_t K, float ah, int32_t zh, int16_t* __restrict__ h,
+    const float* __restrict__ gamma, float eps, float ay, int32_t zy, void* __restrict__ y)
+{
+#pragma clang fp contract(off)
+    __shared__ int64_t red[kThreads / 64];
+    const int64_t m = blockIdx.x;
+    RowRegs<NCH> r1, r2;
+    r1.load(x1 + m * K, K);
+    r2.load(x2 + m * K, K);
+    int32_t hc[NCH][8];
+    int64_t ss = 0;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (!r1.live[c]) continue;
+        const int64_t k0 = 8 * ((int64_t)threadIdx.x + kThreads * c);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            hc[c][u] = add_one<16>(r1.v[c][u], r2.v[c][u], a1, z1, a2, z2, ah, zh);
+            const int64_t d = (int64_t)hc[c][u] - zh;
+            ss += d * d;
+        }
+        store8<16>(h, m * K + k0, hc[c]);
+    }
+    ss = block_sum_i64(ss, red);
+    const double a = (double)ah;
+    const double ms = a * a * (double)ss / (double)K + (double)eps;
+    const double rt = sqrt(ms);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (!r1.live[c]) continue;
+        const int64_t k0 = 8 * ((int64_t)threadIdx.x + kThreads * c);
+        int32_t q[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            double v = a * (double)((int64_t)hc[c][u] - zh);
+            if (gamma) v = v * (double)gamma[k0 + u];
+            v = v / rt;
+            q[u] = requant_f64<BITS>(v, (double)ay, zy);
+        }
+        store8<BITS>(y, m * K + k0, q);
+    }
+}
+
 // Keys row m of a causal softmax sees: (m mod period) + offset + 1, at most
 // K (period 0: all K).
 __device__ inline int64_t causal_keys(int64_t m, int64_t K, int64_t period, int64_t offset)
@@ -851,6 +902,32 @@ hipError_t launch_rmsnorm(const int16_t* x, int64_t M, int64_t K, float ax, int3
     else
         rmsnorm_kernel<16><<<(unsigned)M, kThreads, 0, st>>>(x, K, ax, zx, gamma, eps, ay, zy, y);
     return hipGetLastError();
+}
+
+hipError_t launch_add_rmsnorm(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                             float a2, int32_t z2, int64_t M, int64_t K, float ah, int32_t zh,
+                             int16_t* h, const float* gamma, float eps, float ay, int32_t zy,
+                             int32_t bits, void* y, hipStream_t st)
+{
+    if (M == 0) return hipSuccess;
+    const int ch = row_chunks(x1, y, K);
+    if (ch > 0 && row_chunks(x2, h, K) > 0) {
+        const dim3 g((unsigned)M), b(kThreads);
+        if (bits == 8) {
+            if (ch == 1) add_rmsnorm_kernel<8, 1><<<g, b, 0, st>>>(x1, a1, z1, x2, a2, z2, K, ah, zh, h, gamma, eps, ay, zy, y);
+            else if (ch == 2) add_rmsnorm_kernel<8, 2><<<g, b, 0, st>>>(x1, a1, z1, x2, a2, z2, K, ah, zh, h, gamma, eps, ay, zy, y);
+            else add_rmsnorm_kernel<8, 4><<<g, b, 0, st>>>(x1, a1, z1, x2, a2, z2, K, ah, zh, h, gamma, eps, ay, zy, y);
+        } else {
+            if (ch == 1) add_rmsnorm_kernel<16, 1><<<g, b, 0, st>>>(x1, a1, z1, x2, a2, z2, K, ah, zh, h, gamma, eps, ay, zy, y);
+            else if (ch == 2) add_rmsnorm_kernel<16, 2><<<g, b, 0, st>>>(x1, a1, z1, x2, a2, z2, K, ah, zh, h, gamma, eps, ay, zy, y);
+            else add_rmsnorm_kernel<16, 4><<<g, b, 0, st>>>(x1, a1, z1, x2, a2, z2, K, ah, zh, h, gamma, eps, ay, zy, y);
+        }
+        return hipGetLastError();
+    }
+    // rows that do not fit the register kernel: the two steps
+    const hipError_t e = launch_add_requant(x1, a1, z1, x2, a2, z2, M * K, ah, zh, 16, h, st);
+    if (e != hipSuccess) return e;
+    return launch_rmsnorm(h, M, K, ah, zh, gamma, eps, ay, zy, bits, y, st);
 }
 
 template <int BITS, int NC>

@@ -162,6 +162,25 @@ mq_status mq_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t*
                                            as_stream(stream)));
 }
 
+mq_status mq_add_rmsnorm(const int16_t* x1, float a1, int32_t z1, const int16_t* x2, float a2,
+                         int32_t z2, int64_t M, int64_t K, float ah, int32_t zh, int16_t* h,
+                         const float* gamma, float eps, float ay, int32_t zy, int32_t out_bits,
+                         void* y, void* stream)
+{
+    if (M < 0 || M > 0x7FFFFFFF || K < 1 || K > (1 << 20) || !act_bits_ok(out_bits))
+        return MQ_ERR_INVALID_ARG;
+    if (M > 0 && M > kMaxElems / K) return MQ_ERR_INVALID_ARG;
+    if (!finite_pos(a1) || !finite_pos(a2) || !finite_pos(ah) || !finite_pos(ay))
+        return MQ_ERR_INVALID_ARG;
+    if (!std::isfinite(eps) || eps < 0.0f) return MQ_ERR_INVALID_ARG;
+    if (!zp_ok(z1, 16) || !zp_ok(z2, 16) || !zp_ok(zh, 16) || !zp_ok(zy, out_bits))
+        return MQ_ERR_INVALID_ARG;
+    if (M == 0) return MQ_OK;
+    if (!x1 || !x2 || !h || !y) return MQ_ERR_INVALID_ARG;
+    return from_hip(mq::launch_add_rmsnorm(x1, a1, z1, x2, a2, z2, M, K, ah, zh, h, gamma, eps, ay,
+                                           zy, out_bits, y, as_stream(stream)));
+}
+
 mq_status mq_lut_mul(const int16_t* x1, const void* lut, int32_t lut_bits, float a1, int32_t z1,
                      const int16_t* x2, float a2, int32_t z2, int64_t numel, float ay,
                      int32_t zy, int32_t out_bits, void* y, void* stream)

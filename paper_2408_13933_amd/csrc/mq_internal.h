@@ -89,6 +89,10 @@ hipError_t launch_add_requant(const int16_t* x1, float a1, int32_t z1, const int
 hipError_t launch_lut_mul(const int16_t* x1, const void* lut, int32_t lut_bits, float a1,
                           int32_t z1, const int16_t* x2, float a2, int32_t z2, int64_t n,
                           float ay, int32_t zy, int32_t bits, void* y, hipStream_t st);
+hipError_t launch_add_rmsnorm(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
+                             float a2, int32_t z2, int64_t M, int64_t K, float ah, int32_t zh,
+                             int16_t* h, const float* gamma, float eps, float ay, int32_t zy,
+                             int32_t bits, void* y, hipStream_t st);
 hipError_t launch_mul_requant(const int16_t* x1, float a1, int32_t z1, const int16_t* x2,
                               float a2, int32_t z2, int64_t n, float ay, int32_t zy,
                               int32_t bits, void* y, hipStream_t st);

@@ -344,6 +344,11 @@ def test_softmax_causal_rejects_invalid_arguments(call):
     lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, 10000.0, -1, 1.0, 0, 16, NZ, NZ, None),
     lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, 10000.0, 0, 1.0, 0, 16, None, NZ, None),
     lambda L: L.mq_rope(NZ, 4, 2, 8, 1.0, 0, float("nan"), 0, 1.0, 0, 16, NZ, NZ, None),
+    lambda L: L.mq_add_rmsnorm(NZ, 1.0, 0, NZ, 1.0, 0, 4, 0, 1.0, 0, NZ, None, 1e-5, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_add_rmsnorm(NZ, 1.0, 0, NZ, 1.0, 0, 4, 8, 0.0, 0, NZ, None, 1e-5, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_add_rmsnorm(NZ, 1.0, 0, NZ, 1.0, 0, 4, 8, 1.0, 0, NZ, None, -1.0, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_add_rmsnorm(NZ, 1.0, 0, NZ, 1.0, 0, 4, 8, 1.0, 0, None, None, 1e-5, 1.0, 0, 8, NZ, None),
+    lambda L: L.mq_add_rmsnorm(NZ, 1.0, 0, NZ, 1.0, 0, 4, 8, 1.0, 0, NZ, None, 1e-5, 1.0, 300, 8, NZ, None),
     lambda L: L.mq_lut_mul(NZ, NZ, 12, 1.0, 0, NZ, 1.0, 0, 10, 1.0, 0, 8, NZ, None),
     lambda L: L.mq_lut_mul(NZ, NZ, 8, 1.0, 200, NZ, 1.0, 0, 10, 1.0, 0, 8, NZ, None),
     lambda L: L.mq_lut_mul(NZ, NZ, 16, 0.0, 0, NZ, 1.0, 0, 10, 1.0, 0, 8, NZ, None),

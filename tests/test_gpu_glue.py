@@ -177,6 +177,27 @@ def test_mul_requant_parity(n, out_bits):
     assert np.array_equal(y.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("M,K,gamma,out_bits", [(1024, 2048, True, 8), (3, 777, False, 16),
+                                               (64, 5632, True, 8), (5, 8, False, 8)])
+def test_add_rmsnorm_equals_add_then_rmsnorm(M, K, gamma, out_bits):
+    """The fused residual add and RMSNorm give the oracle's bits for both
+    outputs (K = 777: the two-step fallback)."""
+    mq = _mq()
+    rng = np.random.default_rng(M * K)
+    x1 = rng.integers(-32768, 32768, (M, K)).astype(np.int16)
+    x2 = rng.integers(-32768, 32768, (M, K)).astype(np.int16)
+    x2[0] = x1[0]                                  # a row of one repeated sum
+    a1, z1, a2, z2, ah, zh = 3.1e-4, -12, 7.7e-4, 300, 1.3e-3, 5
+    g = rng.uniform(0.5, 1.5, K).astype(np.float32) if gamma else None
+    eps, ay, zy = 1e-5, (0.02 if out_bits == 8 else 1e-4), -3
+    h_ref = oracle.add_requant(x1, a1, z1, x2, a2, z2, ah, zh, 16)
+    y_ref = oracle.rmsnorm(h_ref, ah, zh, g, eps, ay, zy, out_bits)
+    h, y = mq.mq_add_rmsnorm(_dev(x1), a1, z1, _dev(x2), a2, z2, ah, zh,
+                             None if g is None else _dev(g), eps, ay, zy, out_bits)
+    assert np.array_equal(h.cpu().numpy(), h_ref)
+    assert np.array_equal(y.cpu().numpy(), y_ref)
+
+
 @pytest.mark.parametrize("n,lut_bits,out_bits", [(1024 * 5632, 16, 8), (777, 8, 16), (1, 16, 16),
                                                 (4099, 8, 8)])
 def test_lut_mul_equals_lookup_then_product(n, lut_bits, out_bits):
