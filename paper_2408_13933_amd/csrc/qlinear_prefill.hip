@@ -953,6 +953,11 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
 template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2, 1>;
 template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2, 4>;
 template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
+// 64x64: layers with few output tiles (1024 tokens x 256 channels: 64
+// tiles instead of 16), four waves of 32x32; int8 weights, no K split
+// (the chooser offers it for nothing else)
+template <int OB> using T64x64 = Cfg<8, OB, 64, 64, 2, 2, 128, 4, 2, 4>;
+constexpr int kTile64x64 = 4;
 // 192 tokens x 256 channels: 3/4 of the 256x256 tile's work per block, so a
 // layer whose 256x256 tiles leave CUs idle (2048 x 5632: 176 tiles on 256
 // CUs) fills more of the chip (242 tiles).  Eight waves, two per SIMD, each
@@ -989,16 +994,22 @@ static_assert(T128x128A16<8>::TM == kA16TileM && T128x128A16<8>::BK == kA16TileK
               "the causal column sums assume these 16-bit tile sizes");
 
 // Per-block cycle model of each tile shape on MI355X (phase timings of the
-// kernel): fixed prologue + K-loop cycles per stage + epilogue.
+// kernel): fixed prologue + K-loop cycles per stage + epilogue; occ blocks
+// share a CU within one round.
 struct TileModel {
     int tm, tn, bk;
     double prologue, per_stage, epilogue;
+    int occ = 1;
 };
 constexpr TileModel kTiles[] = {
     {256, 256, 64, 6500, 1450, 9800},
     {256, 128, 128, 6000, 1500, 6000},
     {128, 128, 128, 5300, 980, 3300},
     {192, 256, 128, 5600, 1770, 4600},  // eight waves, two 128-deep stages (int8 weights)
+    // 64 KiB of stage ring: two blocks per CU.  Measured: 1024x2048x256 in
+    // 8.2-8.5 us (128x128: 11.9-12.8), 1024x2048x2048 in 11.2 (14.1),
+    // 1024x5632x2048 in 24.1 (26.6)
+    {64, 64, 128, 5000, 660, 1500, 2},
 };
 // the 192x256 tile with int4 weights runs four waves
 constexpr TileModel kTile192x256W4 = {192, 256, 64, 7000, 1175, 8300};
@@ -1028,15 +1039,16 @@ Choice choose(const QLinearArgs& p, bool can_split)
         if (v >= 0 && v < kNumTiles) only = v;
     }
     for (int c = 0; c < kNumTiles; ++c) {
-        if (only >= 0 && c != only) continue;
+        if (c == kTile64x64 && p.w_bits != 8) continue;
+        if (only >= 0 && c != only && !(only == kTile64x64 && p.w_bits != 8)) continue;
         const TileModel& t = c == 3 && p.w_bits == 4 ? kTile192x256W4 : kTiles[c];
         const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn);
         const int64_t kt = (p.K + t.bk - 1) / t.bk;
-        const bool tile_splits = t.tm * t.tn < 256 * 256;  // Cfg::SPLITK
+        const bool tile_splits = t.tm * t.tn < 256 * 256 && c != kTile64x64;
         for (int sp = 1; sp <= (can_split && tile_splits ? kMaxSplits : 1); sp *= 2) {
             const int64_t per = (kt + sp - 1) / sp;
             if (sp > 1 && per < 4) break;  // slices too thin to pipeline
-            const int64_t rounds = (tiles * sp + kCUs - 1) / kCUs;
+            const int64_t rounds = (tiles * sp + kCUs * t.occ - 1) / (kCUs * t.occ);
             const double stage = t.per_stage * (p.w_bits == 4 ? kInt4StageFactor : 1.0);
             const double t_blk = t.prologue + stage * (double)per + t.epilogue;
             const double exchange =
@@ -1070,6 +1082,9 @@ hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
     case 0: return launch_cfg<T256x256<WB, OB>, ASYM>(p, ch.splits, s);
     case 1: return launch_cfg<T256x128<WB, OB>, ASYM>(p, ch.splits, s);
     case 3: return launch_cfg<T192x256<WB, OB>, ASYM>(p, ch.splits, s);
+    case kTile64x64:
+        if constexpr (WB == 8) return launch_cfg<T64x64<OB>, ASYM>(p, 1, s);
+        return hipErrorInvalidValue;  // not chosen for int4 weights
     default: return launch_cfg<T128x128<WB, OB>, ASYM>(p, ch.splits, s);
     }
 }

@@ -112,9 +112,11 @@ SPLIT_CASES = [
 
 
 @pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: "x".join(map(str, c[:5])))
-def test_split_k_parity(case):
-    """K split across work-groups (workspace path): bit-identical to the
-    oracle, twice in a row on one workspace, which ends zero-filled."""
+def test_split_k_parity(case, monkeypatch):
+    """K split across work-groups (workspace path, on the 128x128 tile, which
+    the chooser splits for these shapes): bit-identical to the oracle, twice
+    in a row on one workspace, which ends zero-filled."""
+    monkeypatch.setenv("MQ_PREFILL_TILE", "2")
     mq, torch = _mq(), _torch()
     M, K, N, wb, ob, has_bias = case
     nbytes = mq.mq_qlinear_workspace_bytes(M, K, N, wb, ob)
@@ -268,7 +270,7 @@ def test_extreme_accumulators_at_max_k(w_bits):
             assert np.array_equal(y.cpu().numpy(), ref), (M, path, a_zp)
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "2", "3"])
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4"])
 @pytest.mark.parametrize("asym", [False, True])
 def test_prefill_epilogue_forms(tile, asym, monkeypatch):
     """Every epilogue form of every prefill tile: per-column rescale factors
