@@ -56,8 +56,18 @@ typedef enum {
     MQ_PATH_AUTO = 0,     /* M <= 16 -> decode, otherwise prefill          */
     MQ_PATH_DECODE = 1,   /* wavefront GEMV kernel, any M <= 16            */
     MQ_PATH_PREFILL = 2,  /* LDS-tiled MFMA GEMM kernel, any M             */
-    MQ_PATH_GENERIC = 3   /* one thread per output, any shape or alignment */
+    MQ_PATH_GENERIC = 3,  /* one thread per output, any shape or alignment */
+    /* MQ_PATH_PREFILL_TILE0 + t, t = 0..MQ_PREFILL_TILES-1: the prefill
+     * kernel with output tile t (0: 256x256, 1: 256x128, 2: 128x128,
+     * 3: 192x256, 4: 64x64 tokens x channels) instead of the one its cost
+     * model picks -- a hook for tests and measurements; the results are the
+     * same bits.  With a workspace the K split is the cost model's best for
+     * that tile and may need more bytes than mq_qlinear_workspace_bytes
+     * reports (at most 256*ceil(T/64) + 8*T*tm*tn*4 bytes for T tiles of
+     * tm x tn); with fewer bytes it does not split. */
+    MQ_PATH_PREFILL_TILE0 = 16
 } mq_path;
+#define MQ_PREFILL_TILES 5
 
 /* Largest K accepted: keeps |sum_k A_q W_q| below 2^30 so the int32
  * accumulator cannot overflow. */

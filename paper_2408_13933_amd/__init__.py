@@ -20,6 +20,7 @@ __all__ = [
     "mq_add_requant", "mq_lut_build", "mq_lut_apply", "mq_rmsnorm", "mq_softmax", "LUT_SILU",
     "mq_qlinear_workspace_bytes",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
+    "PATH_PREFILL_TILE0", "PREFILL_TILES", "prefill_tile_path",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -27,6 +28,16 @@ lib_path = os.path.join(_HERE, "libmq.so")
 
 MQ_OK, MQ_ERR_INVALID_ARG, MQ_ERR_UNSUPPORTED, MQ_ERR_HIP = 0, 1, 2, 3
 PATH_AUTO, PATH_DECODE, PATH_PREFILL, PATH_GENERIC = 0, 1, 2, 3
+# the prefill kernel with one explicit output tile (tests and measurements)
+PATH_PREFILL_TILE0, PREFILL_TILES = 16, 5
+PREFILL_TILE_SHAPES = ((256, 256), (256, 128), (128, 128), (192, 256), (64, 64))
+
+
+def prefill_tile_path(tile: int) -> int:
+    """Path value that runs the prefill kernel on output tile ``tile``."""
+    if not 0 <= tile < PREFILL_TILES:
+        raise ValueError(f"tile {tile} outside 0..{PREFILL_TILES - 1}")
+    return PATH_PREFILL_TILE0 + tile
 MAX_K = 65536
 ARL_PARTIALS = 1024
 LUT_SILU = 1

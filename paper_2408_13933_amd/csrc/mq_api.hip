@@ -378,16 +378,18 @@ mq_status mq_qlinear_ex(const int8_t* a_q, int64_t M, int64_t K, int64_t N, cons
 
 }  // extern "C"
 
-namespace {
+namespace mq {
 
-// Validation and dispatch shared by the symmetric and asymmetric entry
-// points; w_zp and a_rowsum are both null (symmetric) or both set.
-mq_status qlinear_impl(const void* a_q, int32_t a_bits, const int32_t* a_rowsum, int64_t M,
-                       int64_t K, int64_t N, const void* w_q, int32_t w_bits,
-                       const float* w_scale, const int32_t* w_zp, const int32_t* w_colsum,
-                       float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
-                       int32_t out_bits, const float* bias, void* y_q, void* workspace,
-                       int64_t workspace_bytes, int32_t path, void* stream)
+// Validation shared by the qlinear entry points (w_zp and a_rowsum are both
+// null, symmetric, or both set); fills the kernel arguments and resolves
+// the path.  MQ_OK with M == 0 or N == 0: nothing to launch.
+mq_status qlinear_validate(const void* a_q, int32_t a_bits, const int32_t* a_rowsum, int64_t M,
+                           int64_t K, int64_t N, const void* w_q, int32_t w_bits,
+                           const float* w_scale, const int32_t* w_zp, const int32_t* w_colsum,
+                           float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                           int32_t out_bits, const float* bias, void* y_q, void* workspace,
+                           int64_t workspace_bytes, int32_t path, QLinearArgs* out,
+                           int32_t* path_out)
 {
     if (workspace_bytes < 0) return MQ_ERR_INVALID_ARG;
     if (workspace && ((uintptr_t)workspace % 256) != 0) return MQ_ERR_INVALID_ARG;
@@ -398,13 +400,21 @@ mq_status qlinear_impl(const void* a_q, int32_t a_bits, const int32_t* a_rowsum,
     if (w_bits == 4 && (K % 2) != 0) return MQ_ERR_INVALID_ARG;
     if (!finite_pos(a_scale) || !finite_pos(out_scale)) return MQ_ERR_INVALID_ARG;
     if (!zp_ok(a_zp, a_bits) || !zp_ok(out_zp, out_bits)) return MQ_ERR_INVALID_ARG;
+    int32_t force_tile = -1;
+    if (path >= MQ_PATH_PREFILL_TILE0 && path < MQ_PATH_PREFILL_TILE0 + MQ_PREFILL_TILES) {
+        force_tile = path - MQ_PATH_PREFILL_TILE0;
+        path = MQ_PATH_PREFILL;
+    }
     if (path < MQ_PATH_AUTO || path > MQ_PATH_GENERIC) return MQ_ERR_INVALID_ARG;
     if (path == MQ_PATH_DECODE && M > 16) return MQ_ERR_INVALID_ARG;
+    QLinearArgs& p = *out;
+    p.M = M;
+    p.K = K;
+    p.N = N;
     if (M == 0 || N == 0) return MQ_OK;
     if (!a_q || !w_q || !w_scale || !w_colsum || !y_q) return MQ_ERR_INVALID_ARG;
     if ((w_zp == nullptr) != (a_rowsum == nullptr)) return MQ_ERR_INVALID_ARG;
 
-    mq::QLinearArgs p;
     p.a = static_cast<const int8_t*>(a_q);
     p.a_bits = a_bits;
     p.w = w_q;
@@ -412,9 +422,6 @@ mq_status qlinear_impl(const void* a_q, int32_t a_bits, const int32_t* a_rowsum,
     p.colsum = w_colsum;
     p.bias = bias;
     p.y = y_q;
-    p.M = M;
-    p.K = K;
-    p.N = N;
     p.a_scale = a_scale;
     p.out_scale = out_scale;
     p.a_zp = a_zp;
@@ -425,14 +432,40 @@ mq_status qlinear_impl(const void* a_q, int32_t a_bits, const int32_t* a_rowsum,
     p.ws_bytes = workspace ? workspace_bytes : 0;
     p.w_zp = w_zp;
     p.a_rowsum = a_rowsum;
+    p.force_tile = force_tile;
+    *path_out = path == MQ_PATH_AUTO ? (M <= 16 ? MQ_PATH_DECODE : MQ_PATH_PREFILL) : path;
+    return MQ_OK;
+}
 
-    hipStream_t s = as_stream(stream);
-    if (path == MQ_PATH_AUTO) path = M <= 16 ? MQ_PATH_DECODE : MQ_PATH_PREFILL;
-    if (path == MQ_PATH_DECODE && mq::decode_supported(p))
-        return from_hip(mq::launch_qlinear_decode(p, s));
-    if (path == MQ_PATH_PREFILL && mq::prefill_supported(p))
-        return from_hip(mq::launch_qlinear_prefill(p, s));
-    return from_hip(mq::launch_qlinear_generic(p, s));
+// Launch of a validated call on the resolved path; the tuned kernels fall
+// back to the generic one when the shape or alignment rules are not met.
+mq_status qlinear_dispatch(const QLinearArgs& p, int32_t path, hipStream_t s)
+{
+    if (p.M == 0 || p.N == 0) return MQ_OK;
+    if (path == MQ_PATH_DECODE && decode_supported(p)) return from_hip(launch_qlinear_decode(p, s));
+    if (path == MQ_PATH_PREFILL && prefill_supported(p))
+        return from_hip(launch_qlinear_prefill(p, s));
+    return from_hip(launch_qlinear_generic(p, s));
+}
+
+}  // namespace mq
+
+namespace {
+
+mq_status qlinear_impl(const void* a_q, int32_t a_bits, const int32_t* a_rowsum, int64_t M,
+                       int64_t K, int64_t N, const void* w_q, int32_t w_bits,
+                       const float* w_scale, const int32_t* w_zp, const int32_t* w_colsum,
+                       float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                       int32_t out_bits, const float* bias, void* y_q, void* workspace,
+                       int64_t workspace_bytes, int32_t path, void* stream)
+{
+    mq::QLinearArgs p;
+    int32_t resolved = MQ_PATH_AUTO;
+    const mq_status st = mq::qlinear_validate(
+        a_q, a_bits, a_rowsum, M, K, N, w_q, w_bits, w_scale, w_zp, w_colsum, a_scale, a_zp,
+        out_scale, out_zp, out_bits, bias, y_q, workspace, workspace_bytes, path, &p, &resolved);
+    if (st != MQ_OK) return st;
+    return mq::qlinear_dispatch(p, resolved, as_stream(stream));
 }
 
 }  // namespace

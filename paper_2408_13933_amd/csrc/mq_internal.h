@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "mq.h"
+
 namespace mq {
 
 // Scalars every qlinear kernel needs besides its buffers.
@@ -49,6 +51,8 @@ struct QLinearArgs {
     //   colsum holds, per 128-row tile (stride cs_mt), the column sums over
     //   that range.
     int64_t out_causal = -1, in_causal = -1, cs_mt = 0;
+    // prefill tile requested explicitly (0..4), or -1: chosen by the cost model
+    int32_t force_tile = -1;
 };
 
 // Dense defaults of the stride fields.
@@ -135,8 +139,23 @@ hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s);
 // (0 when it would not split).
 int64_t prefill_workspace_bytes(const QLinearArgs& p);
 
+// Bytes at the start of the split-K workspace that hold the per-tile
+// arrival counters for this shape (0 when it would not split).
+int64_t prefill_counter_bytes(const QLinearArgs& p);
+
 // Shape/alignment rules of the tuned kernels.
 bool decode_supported(const QLinearArgs& p);
 bool prefill_supported(const QLinearArgs& p);
+
+// Host side of the qlinear entry points: validation (fills the kernel
+// arguments and resolves MQ_PATH_AUTO and the tile paths) and the launch.
+mq_status qlinear_validate(const void* a_q, int32_t a_bits, const int32_t* a_rowsum, int64_t M,
+                           int64_t K, int64_t N, const void* w_q, int32_t w_bits,
+                           const float* w_scale, const int32_t* w_zp, const int32_t* w_colsum,
+                           float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
+                           int32_t out_bits, const float* bias, void* y_q, void* workspace,
+                           int64_t workspace_bytes, int32_t path, QLinearArgs* out,
+                           int32_t* path_out);
+mq_status qlinear_dispatch(const QLinearArgs& p, int32_t path, hipStream_t s);
 
 }  // namespace mq

@@ -26,7 +26,6 @@
 //   an exact shift.
 // - Block ids are remapped so blocks that share weight tiles run on the same
 //   XCD (each XCD has its own L2).
-#include <cstdlib>
 #include <type_traits>
 
 #include "mq_internal.h"
@@ -121,6 +120,11 @@ struct Cfg {
     // K slices (split-K) for the smaller tiles; the 256x256 tile has no
     // registers to spare for the slice bookkeeping
     static constexpr bool SPLITK = TM * TN < 256 * 256 && !A16;
+    // split-K merge: fragment rows of the other slices' partial sums loaded
+    // per batch (16 chunks, 64 registers in flight), never more than the
+    // wave has, and a whole number of batches per wave
+    static constexpr int MERGE_IB = 16 / (FM * 4) < 1 ? 1 : (16 / (FM * 4) > FN ? FN : 16 / (FM * 4));
+    static_assert(FN % MERGE_IB == 0, "whole merge batches per wave");
     static constexpr int A_BYTES = A_PER_WAVE * NWAVES * 1024;
     static constexpr int W_BYTES = W_PER_WAVE * NWAVES * 1024;
     static constexpr int STAGE = A_BYTES + W_BYTES;
@@ -854,7 +858,7 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
         if (arrived != splits - 1) return;
         // the other slices, 16 chunks (64 registers) in flight per batch: each
         // batch costs one memory round trip, not one per chunk
-        constexpr int IB = 16 / (C::FM * 4) > 0 ? 16 / (C::FM * 4) : 1;  // fragment rows per batch
+        constexpr int IB = C::MERGE_IB;  // fragment rows per batch
         for (int s = 0; s < splits; ++s) {
             if (s == split) continue;
 #pragma unroll
@@ -954,10 +958,13 @@ template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2,
 template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2, 4>;
 template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
 // 64x64: layers with few output tiles (1024 tokens x 256 channels: 64
-// tiles instead of 16), four waves of 32x32; int8 weights, no K split
-// (the chooser offers it for nothing else)
-template <int OB> using T64x64 = Cfg<8, OB, 64, 64, 2, 2, 128, 4, 2, 4>;
+// tiles instead of 16), four waves of 32x32
+template <int WB, int OB> using T64x64 = Cfg<WB, OB, 64, 64, 2, 2, 128, 4, 2, 4>;
 constexpr int kTile64x64 = 4;
+// whether the automatic choice also offers the 64x64 tile to int4 weights
+// and with a K split (otherwise it offers it to int8 weights unsplit; the
+// rest only when the tile is requested explicitly)
+constexpr bool kTile64x64Auto = false;
 // 192 tokens x 256 channels: 3/4 of the 256x256 tile's work per block, so a
 // layer whose 256x256 tiles leave CUs idle (2048 x 5632: 176 tiles on 256
 // CUs) fills more of the chip (242 tiles).  Eight waves, two per SIMD, each
@@ -1033,18 +1040,18 @@ Choice choose(const QLinearArgs& p, bool can_split)
 {
     Choice best{0, 1};
     double best_t = 1e300;
-    int only = -1;
-    if (const char* e = std::getenv("MQ_PREFILL_TILE")) {
-        const int v = std::atoi(e);
-        if (v >= 0 && v < kNumTiles) only = v;
-    }
+    // an explicitly requested tile (measurement and test hook of the ABI)
+    const int only = p.force_tile >= 0 && p.force_tile < kNumTiles ? p.force_tile : -1;
     for (int c = 0; c < kNumTiles; ++c) {
-        if (c == kTile64x64 && p.w_bits != 8) continue;
-        if (only >= 0 && c != only && !(only == kTile64x64 && p.w_bits != 8)) continue;
+        // without the request, the 64x64 tile serves int8 weights unsplit
+        // unless kTile64x64Auto
+        const bool narrow64 = only < 0 && c == kTile64x64 && !kTile64x64Auto;
+        if (narrow64 && p.w_bits != 8) continue;
+        if (only >= 0 && c != only) continue;
         const TileModel& t = c == 3 && p.w_bits == 4 ? kTile192x256W4 : kTiles[c];
         const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn);
         const int64_t kt = (p.K + t.bk - 1) / t.bk;
-        const bool tile_splits = t.tm * t.tn < 256 * 256 && c != kTile64x64;
+        const bool tile_splits = t.tm * t.tn < 256 * 256 && !narrow64;
         for (int sp = 1; sp <= (can_split && tile_splits ? kMaxSplits : 1); sp *= 2) {
             const int64_t per = (kt + sp - 1) / sp;
             if (sp > 1 && per < 4) break;  // slices too thin to pipeline
@@ -1082,9 +1089,7 @@ hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
     case 0: return launch_cfg<T256x256<WB, OB>, ASYM>(p, ch.splits, s);
     case 1: return launch_cfg<T256x128<WB, OB>, ASYM>(p, ch.splits, s);
     case 3: return launch_cfg<T192x256<WB, OB>, ASYM>(p, ch.splits, s);
-    case kTile64x64:
-        if constexpr (WB == 8) return launch_cfg<T64x64<OB>, ASYM>(p, 1, s);
-        return hipErrorInvalidValue;  // not chosen for int4 weights
+    case kTile64x64: return launch_cfg<T64x64<WB, OB>, ASYM>(p, ch.splits, s);
     default: return launch_cfg<T128x128<WB, OB>, ASYM>(p, ch.splits, s);
     }
 }
@@ -1103,12 +1108,15 @@ bool prefill_supported(const QLinearArgs& p)
     const int64_t lda = eff_lda(p) * ab, ldy = eff_ldy(p) * ob;
     const int64_t ldw = p.w_bits == 8 ? eff_ldw(p) : (p.ldw ? p.ldw : p.K / 2);
     // whole 16-byte chunks per row (packed int4 rows too), 16-byte aligned
-    // rows and batches, 8-byte aligned output rows and batches
+    // rows and batches; output rows and batches aligned to one store of four
+    // channels (4 bytes of int8, 8 of int16), so every channel group of the
+    // epilogue is one aligned store
+    const int64_t og = 4 * ob;
     const bool kok = p.w_bits == 8 ? (p.K % 16 == 0) : (p.K % 32 == 0);
     const bool align = ((uintptr_t)p.a % 16) == 0 && ((uintptr_t)p.w % 16) == 0 &&
-                       ((uintptr_t)p.y % 8) == 0 && lda % 16 == 0 && ldw % 16 == 0 &&
-                       ldy % 8 == 0 && (p.a_bs * ab) % 16 == 0 && p.w_bs % 16 == 0 &&
-                       (p.y_bs * ob) % 8 == 0;
+                       ((uintptr_t)p.y % og) == 0 && lda % 16 == 0 && ldw % 16 == 0 &&
+                       ldy % og == 0 && (p.a_bs * ab) % 16 == 0 && p.w_bs % 16 == 0 &&
+                       (p.y_bs * ob) % og == 0;
     // byte offsets inside one 256-row tile must fit the 32-bit buffer offset
     const int64_t lim = (int64_t)1 << 31;
     const bool nok = 256 * ldy < lim && 256 * lda < lim && 256 * ldw < lim;
@@ -1124,6 +1132,14 @@ bool prefill_supported(const QLinearArgs& p)
 int64_t prefill_workspace_bytes(const QLinearArgs& p)
 {
     return workspace_for(p, choose(p, true));
+}
+
+int64_t prefill_counter_bytes(const QLinearArgs& p)
+{
+    const Choice ch = choose(p, true);
+    if (ch.splits <= 1) return 0;
+    const TileModel& t = kTiles[ch.tile];
+    return split_counter_bytes(((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn));
 }
 
 // 16-bit activation codes: no K split; ASYM: int64 row terms

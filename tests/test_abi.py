@@ -66,7 +66,8 @@ def qlin(**kw):
     dict(a_scale=0.0), dict(a_scale=-1.0), dict(a_scale=float("nan")), dict(a_scale=float("inf")),
     dict(out_scale=0.0), dict(out_scale=float("nan")),
     dict(a_zp=128), dict(a_zp=-129), dict(out_zp=128), dict(out_bits=16, out_zp=40000),
-    dict(path=7), dict(path=-1), dict(path=1, M=17),
+    dict(path=7), dict(path=-1), dict(path=1, M=17), dict(path=15), dict(path=21),
+    dict(path=16, a_q=None),
 ])
 def test_qlinear_rejects_invalid_arguments(kw):
     assert qlin(**kw) == 1
