@@ -221,6 +221,31 @@ mq_status mq_qlinear_ws(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
                         int64_t workspace_bytes, int32_t path, void* stream);
 
 /*
+ * mq_qlinear_noalloc -- mq_qlinear for callers that cannot allocate device
+ * memory: code under HIP graph capture, serving loops and harnesses that
+ * forbid hipMalloc.  It allocates nothing (no hipMalloc, hipFree or
+ * allocating library call).  Arguments and results are those of mq_qlinear;
+ * the results are the bits mq_qlinear_ws gives with a workspace of
+ * mq_qlinear_workspace_bytes(M, K, N, w_bits, out_bits) bytes, because that
+ * K split runs here too, with its workspace in a static device array of
+ * MQ_NOALLOC_SCRATCH_BYTES on each GPU (held from the library's load until
+ * the process ends; the first call on a device looks up that device's copy).
+ *   Returns MQ_ERR_UNSUPPORTED, launching nothing, when the shape's K split
+ *   needs more than MQ_NOALLOC_SCRATCH_BYTES; other errors as mq_qlinear.
+ *   Each call clears the arrival counters it uses with a fill kernel on
+ *   `stream` (no memset node, so the call can be captured).  All calls on
+ *   one GPU share that GPU's array and it keeps the last call's contents:
+ *   calls that may overlap on one GPU (unordered streams, concurrent graph
+ *   branches) race and give wrong results.
+ */
+#define MQ_NOALLOC_SCRATCH_BYTES (32 << 20)
+mq_status mq_qlinear_noalloc(const int8_t* a_q, int64_t M, int64_t K, int64_t N,
+                             const void* w_q, int32_t w_bits, const float* w_scale,
+                             const int32_t* w_colsum, float a_scale, int32_t a_zp,
+                             float out_scale, int32_t out_zp, int32_t out_bits,
+                             const float* bias, void* y_q, void* stream);
+
+/*
  * mq_pack_weights_asym -- asymmetric weight quantizer and packer (Section
  * 5.1: the W8A8 and W4A8 settings quantize weights asymmetrically over the
  * full integer range; W8A8 with one range per tensor except the MLP down

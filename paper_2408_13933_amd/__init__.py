@@ -18,7 +18,7 @@ __all__ = [
     "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum", "mq_qlinear_asym",
     "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward", "mq_arl_backward", "ARL_PARTIALS",
     "mq_add_requant", "mq_lut_build", "mq_lut_apply", "mq_rmsnorm", "mq_softmax", "LUT_SILU",
-    "mq_qlinear_workspace_bytes",
+    "mq_qlinear_workspace_bytes", "mq_qlinear_noalloc", "NOALLOC_SCRATCH_BYTES",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
     "PATH_PREFILL_TILE0", "PREFILL_TILES", "prefill_tile_path",
 ]
@@ -39,6 +39,7 @@ def prefill_tile_path(tile: int) -> int:
         raise ValueError(f"tile {tile} outside 0..{PREFILL_TILES - 1}")
     return PATH_PREFILL_TILE0 + tile
 MAX_K = 65536
+NOALLOC_SCRATCH_BYTES = 32 << 20
 ARL_PARTIALS = 1024
 LUT_SILU = 1
 
@@ -83,6 +84,8 @@ def lib():
                                 c_f, c_i32, c_i32, c_p, c_p, c_i32, c_p]
     L.mq_qlinear_ws.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32,
                                 c_f, c_i32, c_i32, c_p, c_p, c_p, c_i64, c_i32, c_p]
+    L.mq_qlinear_noalloc.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_f, c_i32,
+                                     c_f, c_i32, c_i32, c_p, c_p, c_p]
     L.mq_qlinear_workspace_bytes.argtypes = [c_i64, c_i64, c_i64, c_i32, c_i32]
     L.mq_qlinear_workspace_bytes.restype = c_i64
     L.mq_dequant.argtypes = [c_p, c_i32, c_i64, c_f, c_i32, c_p, c_p]
@@ -125,6 +128,7 @@ def lib():
     L.mq_transpose_i8.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_p]
     for name in ("mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
+                 "mq_qlinear_noalloc",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
                  "mq_qlinear_asym", "mq_qlinear_a16", "mq_smooth_scales", "mq_arl_forward",
                  "mq_arl_backward", "mq_add_requant", "mq_lut_build", "mq_lut_apply",
@@ -701,6 +705,28 @@ def mq_qlinear(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: i
     else:
         st = lib().mq_qlinear_ex(*args, int(path), _stream_ptr(stream))
     _check(st, "mq_qlinear")
+    return out
+
+
+def mq_qlinear_noalloc(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: int,
+                       out_scale: float, out_zp: int, out_bits: int = 8, bias=None, out=None,
+                       stream=None):
+    """mq_qlinear whose K split uses the library's static per-GPU array
+    instead of any allocation (pass `out` to allocate nothing here either)."""
+    torch = _torch()
+    M, K = a_q.shape
+    N = w_q.shape[0]
+    wq_dtype, wq_shape = (torch.int8, (N, K)) if w_bits == 8 else (torch.uint8, (N, K // 2))
+    out = (torch.empty((M, N), dtype=_act_dtype(out_bits), device=a_q.device)
+           if out is None else out)
+    bptr = None if bias is None else _dev_ptr(bias, torch.float32, "bias", (N,))
+    _check(lib().mq_qlinear_noalloc(
+        _dev_ptr(a_q, torch.int8, "a_q"), M, K, N, _dev_ptr(w_q, wq_dtype, "w_q", wq_shape),
+        int(w_bits), _dev_ptr(w_scale, torch.float32, "w_scale", (N,)),
+        _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)), float(a_scale), int(a_zp),
+        float(out_scale), int(out_zp), int(out_bits), bptr,
+        _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), _stream_ptr(stream)),
+        "mq_qlinear_noalloc")
     return out
 
 

@@ -73,6 +73,41 @@ def test_qlinear_rejects_invalid_arguments(kw):
     assert qlin(**kw) == 1
 
 
+def qlin_noalloc(**kw):
+    a = dict(a_q=NZ, M=4, K=64, N=8, w_q=NZ, w_bits=8, w_scale=NZ, w_colsum=NZ, a_scale=0.1,
+             a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None, y_q=NZ, stream=None)
+    a.update(kw)
+    return mq.lib().mq_qlinear_noalloc(a["a_q"], a["M"], a["K"], a["N"], a["w_q"], a["w_bits"],
+                                       a["w_scale"], a["w_colsum"], a["a_scale"], a["a_zp"],
+                                       a["out_scale"], a["out_zp"], a["out_bits"], a["bias"],
+                                       a["y_q"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(a_q=None), dict(w_q=None), dict(y_q=None), dict(M=-1), dict(K=0), dict(K=65537),
+    dict(w_bits=2), dict(w_bits=4, K=63), dict(out_bits=32), dict(a_scale=0.0),
+    dict(out_scale=float("nan")), dict(a_zp=128), dict(out_bits=16, out_zp=40000),
+])
+def test_qlinear_noalloc_rejects_invalid_arguments(kw):
+    assert qlin_noalloc(**kw) == 1
+
+
+def test_qlinear_noalloc_rejects_split_beyond_its_array():
+    # the K split of this shape needs more than MQ_NOALLOC_SCRATCH_BYTES:
+    # refused on the host before any device work
+    need = mq.mq_qlinear_workspace_bytes(1024, 65536, 2048, 8, 16)
+    assert need > mq.NOALLOC_SCRATCH_BYTES
+    assert qlin_noalloc(M=1024, K=65536, N=2048, out_bits=16) == 2
+    # nothing to do: no device work either
+    assert qlin_noalloc(M=0) == 0 and qlin_noalloc(N=0) == 0
+
+
+def test_noalloc_scratch_size_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define MQ_NOALLOC_SCRATCH_BYTES \((\d+) << (\d+)\)", text)
+    assert m and (int(m.group(1)) << int(m.group(2))) == mq.NOALLOC_SCRATCH_BYTES
+
+
 def qlin_ws(workspace, workspace_bytes, **kw):
     a = dict(a_q=NZ, M=64, K=4096, N=64, w_q=NZ, w_bits=8, w_scale=NZ, w_colsum=NZ, a_scale=0.1,
              a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None, y_q=NZ, path=0,
