@@ -58,16 +58,16 @@ typedef enum {
     MQ_PATH_PREFILL = 2,  /* LDS-tiled MFMA GEMM kernel, any M             */
     MQ_PATH_GENERIC = 3,  /* one thread per output, any shape or alignment */
     /* MQ_PATH_PREFILL_TILE0 + t, t = 0..MQ_PREFILL_TILES-1: the prefill
-     * kernel with output tile t (0: 256x256, 1: 256x128, 2: 128x128,
-     * 3: 192x256, 4: 64x64 tokens x channels) instead of the one its cost
-     * model picks -- a hook for tests and measurements; the results are the
-     * same bits.  With a workspace the K split is the cost model's best for
+     * kernel with output tile t (0: 256x256 on four waves, 1: 256x128,
+     * 2: 128x128, 3: 192x256, 4: 64x64, 5: 256x256 on eight waves; tokens x
+     * channels) instead of the one its cost model picks -- a hook for tests
+     * and measurements; the results are the same bits.  With a workspace the K split is the cost model's best for
      * that tile and may need more bytes than mq_qlinear_workspace_bytes
      * reports (at most 256*ceil(T/64) + 8*T*tm*tn*4 bytes for T tiles of
      * tm x tn); with fewer bytes it does not split. */
     MQ_PATH_PREFILL_TILE0 = 16
 } mq_path;
-#define MQ_PREFILL_TILES 5
+#define MQ_PREFILL_TILES 6
 
 /* Largest K accepted: keeps |sum_k A_q W_q| below 2^30 so the int32
  * accumulator cannot overflow. */
@@ -596,6 +596,24 @@ mq_status mq_transpose_i8(const int8_t* x, int64_t rows, int64_t cols, int64_t l
  */
 mq_status mq_dequant(const void* q, int32_t bits, int64_t numel, float alpha,
                      int32_t zp, float* y, void* stream);
+
+/*
+ * mq_probe_read -- a measurement helper, not a step of the method: reads
+ * `bytes` bytes of device memory at `src` with `blocks` work-groups of
+ * `waves` wavefronts (the grid of the kernel whose memory floor is being
+ * measured).  Block b reads bytes [b*per, (b+1)*per), per = bytes/blocks
+ * rounded up to 1 KiB, as 1 KiB wave loads (16 bytes per lane) with
+ * `unroll` loads per lane in flight per round.  Each wave writes the XOR of
+ * what it read to sink[b*waves + w], so no load can be dropped.
+ *   src    device, any alignment of 16 bytes or more (null when bytes == 0)
+ *   bytes  >= 0, bytes/blocks < 2^31    blocks > 0    waves in [1, 16]
+ *   unroll 1, 2, 4, 8 or 16
+ *   sink   device int32 [blocks * waves], written
+ * Errors: MQ_ERR_INVALID_ARG for a violation above, MQ_ERR_UNSUPPORTED for
+ * a per-block range of 2 GiB or more, MQ_ERR_HIP for a failed launch.
+ */
+mq_status mq_probe_read(const void* src, int64_t bytes, int32_t blocks, int32_t waves,
+                        int32_t unroll, int32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

@@ -20,7 +20,7 @@ __all__ = [
     "mq_add_requant", "mq_lut_build", "mq_lut_apply", "mq_rmsnorm", "mq_softmax", "LUT_SILU",
     "mq_qlinear_workspace_bytes", "mq_qlinear_noalloc", "NOALLOC_SCRATCH_BYTES",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
-    "PATH_PREFILL_TILE0", "PREFILL_TILES", "prefill_tile_path",
+    "PATH_PREFILL_TILE0", "PREFILL_TILES", "prefill_tile_path", "mq_probe_read",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -29,8 +29,8 @@ lib_path = os.path.join(_HERE, "libmq.so")
 MQ_OK, MQ_ERR_INVALID_ARG, MQ_ERR_UNSUPPORTED, MQ_ERR_HIP = 0, 1, 2, 3
 PATH_AUTO, PATH_DECODE, PATH_PREFILL, PATH_GENERIC = 0, 1, 2, 3
 # the prefill kernel with one explicit output tile (tests and measurements)
-PATH_PREFILL_TILE0, PREFILL_TILES = 16, 5
-PREFILL_TILE_SHAPES = ((256, 256), (256, 128), (128, 128), (192, 256), (64, 64))
+PATH_PREFILL_TILE0, PREFILL_TILES = 16, 6
+PREFILL_TILE_SHAPES = ((256, 256), (256, 128), (128, 128), (192, 256), (64, 64), (256, 256))
 
 
 def prefill_tile_path(tile: int) -> int:
@@ -126,7 +126,8 @@ def lib():
                                  c_i64, c_f, c_i32, c_f, c_i32, c_f, c_i32, c_i32, c_p, c_i64,
                                  c_i64, c_i64, c_i64, c_p, c_i64, c_i32, c_p]
     L.mq_transpose_i8.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_p]
-    for name in ("mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
+    L.mq_probe_read.argtypes = [c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_p]
+    for name in ("mq_probe_read", "mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
                  "mq_qlinear_noalloc",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
@@ -728,6 +729,23 @@ def mq_qlinear_noalloc(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float,
         _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), _stream_ptr(stream)),
         "mq_qlinear_noalloc")
     return out
+
+
+def mq_probe_read(buf, blocks: int, waves: int, unroll: int = 8, sink=None, stream=None):
+    """Measurement helper: stream every byte of the device tensor `buf`
+    through a grid of `blocks` x `waves` wavefronts (the read floor of a
+    kernel with that grid); returns the int32 sink [blocks * waves]."""
+    torch = _torch()
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous GPU tensor")
+    sink = (torch.empty(blocks * waves, dtype=torch.int32, device=buf.device)
+            if sink is None else sink)
+    _check(lib().mq_probe_read(ctypes.c_void_p(buf.data_ptr()),
+                               buf.numel() * buf.element_size(), int(blocks), int(waves),
+                               int(unroll), _dev_ptr(sink, torch.int32, "sink",
+                                                     (blocks * waves,)),
+                               _stream_ptr(stream)), "mq_probe_read")
+    return sink
 
 
 def mq_dequant(q, alpha: float, zp: int, out=None, stream=None):

@@ -51,7 +51,8 @@ struct QLinearArgs {
     //   colsum holds, per 128-row tile (stride cs_mt), the column sums over
     //   that range.
     int64_t out_causal = -1, in_causal = -1, cs_mt = 0;
-    // prefill tile requested explicitly (0..4), or -1: chosen by the cost model
+    // prefill tile requested explicitly (0..MQ_PREFILL_TILES-1), or -1: chosen by
+    // the cost model
     int32_t force_tile = -1;
 };
 

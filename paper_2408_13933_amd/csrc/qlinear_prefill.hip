@@ -117,9 +117,12 @@ struct Cfg {
         return n;
     }
     static constexpr int NSW = nsw();
-    // K slices (split-K) for the smaller tiles; the 256x256 tile has no
-    // registers to spare for the slice bookkeeping
-    static constexpr bool SPLITK = TM * TN < 256 * 256 && !A16;
+    // more than 12 accumulator fragments per wave (the four-wave 256x256
+    // tile: 256 registers) leave no registers for the slice bookkeeping of a
+    // K split or for the pre-shift epilogue forms
+    static constexpr bool BIG_ACC = FM * FN > 12;
+    // K slices (split-K) for the tiles with registers to spare
+    static constexpr bool SPLITK = !BIG_ACC && !A16;
     // split-K merge: fragment rows of the other slices' partial sums loaded
     // per batch (16 chunks, 64 registers in flight), never more than the
     // wave has, and a whole number of batches per wave
@@ -191,7 +194,16 @@ struct Staging {
     static constexpr int OB = C::OBITS / 8;
     static constexpr int WR = C::TM / C::WM;  // sub-tile rows
     static constexpr int WC = C::TN / C::WN;  // sub-tile channels
-    static constexpr int PASS_COLS = WC * OB > 128 ? 128 / OB : WC;
+    // channels staged per pass: at most 128 bytes of a row, and few enough
+    // that every wave's staging area fits the stage ring (the eight-wave
+    // 256x256 tile with int16 outputs stages 32 channels at a time)
+    static constexpr int pass_cols()
+    {
+        int c = WC * OB > 128 ? 128 / OB : WC;
+        while (c > 32 && C::NWAVES * WR * (c * OB + 16) > C::STAGES * C::STAGE) c /= 2;
+        return c;
+    }
+    static constexpr int PASS_COLS = pass_cols();
     static constexpr int PASSES = WC / PASS_COLS;
     static constexpr int FNP = C::FN / PASSES;  // 32-channel fragments per pass
     static constexpr int PB = PASS_COLS * OB;   // staged bytes per row
@@ -607,9 +619,9 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
     const bool zp_fold = (flags & 2) != 0;
     // the fast epilogue form: one mul_hi per output, zero-point in the
     // rounding constant, off in the accumulator's start value; pre0: no
-    // column of the tile needs the pre-shift.  The 256x256 tile has no
-    // registers left for the pre-shift forms.
-    constexpr bool kPreForms = C::TM * C::TN < 256 * 256;
+    // column of the tile needs the pre-shift.  The four-wave 256x256 tile
+    // has no registers left for the pre-shift forms.
+    constexpr bool kPreForms = !C::BIG_ACC;
     const bool pre0 = (flags & 1) != 0;
     const bool fast = (kPreForms ? (flags & 6) == 6 : flags == 7) && (p.N % 4) == 0;
     if (zp_fold && tid < C::TN) e_rnd[tid] += p.out_zp * (1 << (e_sp[tid] & 0xFF));
@@ -961,10 +973,6 @@ template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2
 // tiles instead of 16), four waves of 32x32
 template <int WB, int OB> using T64x64 = Cfg<WB, OB, 64, 64, 2, 2, 128, 4, 2, 4>;
 constexpr int kTile64x64 = 4;
-// whether the automatic choice also offers the 64x64 tile to int4 weights
-// and with a K split (otherwise it offers it to int8 weights unsplit; the
-// rest only when the tile is requested explicitly)
-constexpr bool kTile64x64Auto = false;
 // 192 tokens x 256 channels: 3/4 of the 256x256 tile's work per block, so a
 // layer whose 256x256 tiles leave CUs idle (2048 x 5632: 176 tiles on 256
 // CUs) fills more of the chip (242 tiles).  Eight waves, two per SIMD, each
@@ -979,6 +987,15 @@ constexpr bool kTile64x64Auto = false;
 template <int WB, int OB>
 using T192x256 = std::conditional_t<WB == 8, Cfg<WB, OB, 192, 256, 2, 4, 128, 2, 2, 2>,
                                     Cfg<WB, OB, 192, 256, 2, 2, 64, 4, 2, 1>>;
+// 256x256 with eight waves, two per SIMD, each 128 tokens x 64 channels (4x2
+// fragments: 8 MFMAs per 6 fragment reads from LDS, against 6 per 5 for the
+// 192x256 tile's 3x2), two 128-deep stages.  128 accumulator registers per
+// wave leave room for the K split and the pre-shift epilogue forms.
+template <int WB, int OB> using T256x256W8 = Cfg<WB, OB, 256, 256, 2, 4, 128, 2, 2, 2>;
+constexpr int kTile256x256W8 = 5;
+static_assert(!T256x256<8, 8>::SPLITK && T256x256W8<8, 16>::SPLITK &&
+                  T256x256W8<4, 16>::SPLITK && T192x256<4, 8>::SPLITK,
+              "split-capable tiles");
 // 16-bit activation codes: 128x128 tokens x channels, 64 k per stage (128
 // bytes of each activation row), DMA spread over both steps of a stage
 template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16>;
@@ -1000,35 +1017,43 @@ static_assert(T128x128A16<8>::TM == kA16TileM && T128x128A16<8>::BK == kA16TileK
                   kA16TileM % T64x64A16<8>::TM == 0 && T64x64A16<8>::BK == kA16TileK,
               "the causal column sums assume these 16-bit tile sizes");
 
-// Per-block cycle model of each tile shape on MI355X (phase timings of the
-// kernel): fixed prologue + K-loop cycles per stage + epilogue; occ blocks
-// share a CU within one round.
+// Time model of each tile shape on MI355X, fitted to forced-tile
+// measurements of the workload layers (graph replay, one box; every tile on
+// M = 512..2048, K = 2048..16384, N = 256..256000, int8 and int4 weights).
+// A block costs a fixed part (the first memory round trip, the epilogue and
+// its stores) plus a time per K stage; with more CUs busy a stage takes
+// longer (the chip clocks down under the MFMA load and the blocks share the
+// memory system): stage * (1 + kBusySlowdown * busy fraction).  occ blocks
+// share a CU within one round.  Units: microseconds.  Over the 60 measured
+// (shape, tile) points the model is within about 20%, and it picks the
+// measured fastest tile on every one of the ten unsplit shapes.
 struct TileModel {
     int tm, tn, bk;
-    double prologue, per_stage, epilogue;
+    double fixed_us, stage_us;
     int occ = 1;
+    bool splits = true;  // whether the tile takes a K split
 };
 constexpr TileModel kTiles[] = {
-    {256, 256, 64, 6500, 1450, 9800},
-    {256, 128, 128, 6000, 1500, 6000},
-    {128, 128, 128, 5300, 980, 3300},
-    {192, 256, 128, 5600, 1770, 4600},  // eight waves, two 128-deep stages (int8 weights)
-    // 64 KiB of stage ring: two blocks per CU.  Measured: 1024x2048x256 in
-    // 8.2-8.5 us (128x128: 11.9-12.8), 1024x2048x2048 in 11.2 (14.1),
-    // 1024x5632x2048 in 24.1 (26.6)
-    {64, 64, 128, 5000, 660, 1500, 2},
+    {256, 256, 64, 13.4, 0.531, 1, false},
+    {256, 128, 128, 8.05, 0.593},
+    {128, 128, 128, 5.58, 0.348},
+    {192, 256, 128, 6.98, 0.845},  // eight waves, two 128-deep stages (int8 weights)
+    {64, 64, 128, 3.63, 0.232, 2},  // 64 KiB of stage ring: two blocks per CU
+    {256, 256, 128, 10.5, 0.912},   // eight waves of 128x64, two 128-deep stages
 };
-// the 192x256 tile with int4 weights runs four waves
-constexpr TileModel kTile192x256W4 = {192, 256, 64, 7000, 1175, 8300};
+// the 192x256 tile with int4 weights runs four waves on 64-deep stages
+constexpr TileModel kTile192x256W4 = {192, 256, 64, 8.0, 0.45};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
-// A split adds round trips to memory (partial stores, the counter, the
-// partial loads) and moves every slice's int32 tile through memory and back
-// (write-through, read around the caches): ~4 TB/s, about 2 KB per cycle
-// for the whole chip.  Measured on MI355X: a split pays from K ~ 4096 on.
-constexpr double kSplitFixed = 9000;
+static_assert(kNumTiles == MQ_PREFILL_TILES, "one explicit path per tile");
+constexpr double kBusySlowdown = 0.60;
 // int4 weights: the in-register unpack makes a K-loop stage ~1.35x longer
 constexpr double kInt4StageFactor = 1.35;
-constexpr double kExchangeBytesPerCycle = 2048;
+// A K split adds round trips to memory (partial stores, the counter, the
+// partial loads) and moves every slice's int32 tile through memory and back
+// (written through, read around the caches): fitted, 5.2 us plus 0.24 us
+// per MB of partial sums stored and loaded.
+constexpr double kSplitFixedUs = 5.2;
+constexpr double kSplitUsPerMB = 0.24;
 constexpr int kCUs = 256;
 constexpr int kMaxSplits = 8;
 
@@ -1043,24 +1068,23 @@ Choice choose(const QLinearArgs& p, bool can_split)
     // an explicitly requested tile (measurement and test hook of the ABI)
     const int only = p.force_tile >= 0 && p.force_tile < kNumTiles ? p.force_tile : -1;
     for (int c = 0; c < kNumTiles; ++c) {
-        // without the request, the 64x64 tile serves int8 weights unsplit
-        // unless kTile64x64Auto
-        const bool narrow64 = only < 0 && c == kTile64x64 && !kTile64x64Auto;
-        if (narrow64 && p.w_bits != 8) continue;
         if (only >= 0 && c != only) continue;
         const TileModel& t = c == 3 && p.w_bits == 4 ? kTile192x256W4 : kTiles[c];
         const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn);
         const int64_t kt = (p.K + t.bk - 1) / t.bk;
-        const bool tile_splits = t.tm * t.tn < 256 * 256 && !narrow64;
-        for (int sp = 1; sp <= (can_split && tile_splits ? kMaxSplits : 1); sp *= 2) {
+        const int64_t slots = (int64_t)kCUs * t.occ;
+        for (int sp = 1; sp <= (can_split && t.splits ? kMaxSplits : 1); sp *= 2) {
             const int64_t per = (kt + sp - 1) / sp;
             if (sp > 1 && per < 4) break;  // slices too thin to pipeline
-            const int64_t rounds = (tiles * sp + kCUs * t.occ - 1) / (kCUs * t.occ);
-            const double stage = t.per_stage * (p.w_bits == 4 ? kInt4StageFactor : 1.0);
-            const double t_blk = t.prologue + stage * (double)per + t.epilogue;
+            const int64_t items = tiles * sp;
+            const int64_t rounds = (items + slots - 1) / slots;
+            const double busy = (double)(items < slots ? items : slots) / (double)slots;
+            const double stage = t.stage_us * (p.w_bits == 4 ? kInt4StageFactor : 1.0) *
+                                 (1.0 + kBusySlowdown * busy);
+            const double t_blk = t.fixed_us + stage * (double)per;
             const double exchange =
-                sp > 1 ? kSplitFixed + (double)tiles * (2 * sp - 1) * t.tm * t.tn * 4 /
-                                           kExchangeBytesPerCycle
+                sp > 1 ? kSplitFixedUs + kSplitUsPerMB * (double)tiles * (2 * sp - 1) * t.tm *
+                                             t.tn * 4 * 1e-6
                        : 0.0;
             const double tt = (double)rounds * t_blk + exchange;
             if (tt < best_t * 0.97) {  // a split has to win clearly
@@ -1090,6 +1114,7 @@ hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
     case 1: return launch_cfg<T256x128<WB, OB>, ASYM>(p, ch.splits, s);
     case 3: return launch_cfg<T192x256<WB, OB>, ASYM>(p, ch.splits, s);
     case kTile64x64: return launch_cfg<T64x64<WB, OB>, ASYM>(p, ch.splits, s);
+    case kTile256x256W8: return launch_cfg<T256x256W8<WB, OB>, ASYM>(p, ch.splits, s);
     default: return launch_cfg<T128x128<WB, OB>, ASYM>(p, ch.splits, s);
     }
 }

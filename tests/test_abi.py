@@ -66,7 +66,7 @@ def qlin(**kw):
     dict(a_scale=0.0), dict(a_scale=-1.0), dict(a_scale=float("nan")), dict(a_scale=float("inf")),
     dict(out_scale=0.0), dict(out_scale=float("nan")),
     dict(a_zp=128), dict(a_zp=-129), dict(out_zp=128), dict(out_bits=16, out_zp=40000),
-    dict(path=7), dict(path=-1), dict(path=1, M=17), dict(path=15), dict(path=21),
+    dict(path=7), dict(path=-1), dict(path=1, M=17), dict(path=15), dict(path=16 + mq.PREFILL_TILES),
     dict(path=16, a_q=None),
 ])
 def test_qlinear_rejects_invalid_arguments(kw):
@@ -404,3 +404,19 @@ def test_softmax_causal_rejects_invalid_arguments(call):
 ])
 def test_mul_and_rope_reject_invalid_arguments(call):
     assert call(mq.lib()) == 1
+
+
+def test_probe_read_validation():
+    L = mq.lib()
+    ok = dict(src=NZ, bytes=4096, blocks=4, waves=4, unroll=8, sink=NZ)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return L.mq_probe_read(a["src"], a["bytes"], a["blocks"], a["waves"], a["unroll"],
+                               a["sink"], None)
+
+    for bad in (dict(bytes=-1), dict(blocks=0), dict(waves=0), dict(waves=17), dict(unroll=3),
+                dict(unroll=32), dict(sink=None), dict(src=None)):
+        assert call(**bad) == mq.MQ_ERR_INVALID_ARG, bad
+    assert call(bytes=1 << 40, blocks=1) == mq.MQ_ERR_UNSUPPORTED

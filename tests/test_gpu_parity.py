@@ -114,12 +114,13 @@ def split_workspace_bound(M, N, tile):
     return counters + 8 * tiles * tm * tn * 4, counters
 
 
-@pytest.mark.parametrize("tile", [2, 4])
+@pytest.mark.parametrize("tile", [2, 4, 5])
 @pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: "x".join(map(str, c[:5])))
 def test_split_k_parity(case, tile):
-    """K split across work-groups (workspace path) on the 128x128 and the
-    64x64 tile, whose cost model splits these shapes: bit-identical to the
-    oracle, twice in a row on one workspace, whose counters end at zero."""
+    """K split across work-groups (workspace path) on the 128x128, the 64x64
+    and the eight-wave 256x256 tile, whose cost model splits these shapes:
+    bit-identical to the oracle, twice in a row on one workspace, whose
+    counters end at zero."""
     mq, torch = _mq(), _torch()
     M, K, N, wb, ob, has_bias = case
     nbytes, counters = split_workspace_bound(M, N, tile)
@@ -282,7 +283,7 @@ def _pack_int4(codes):
     return (lo | (hi << 4)).astype(np.uint8)
 
 
-@pytest.mark.parametrize("tile", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("tile", list(range(6)))
 @pytest.mark.parametrize("asym", [False, True])
 @pytest.mark.parametrize("w_bits", [8, 4])
 def test_prefill_epilogue_forms(tile, asym, w_bits):
