@@ -134,6 +134,9 @@ hipError_t launch_transpose_i8(const int8_t* x, int64_t rows, int64_t cols, int6
 
 hipError_t launch_qlinear_generic(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);
+// one token (M = 1, 8-bit codes): the vector-ALU GEMV the decode path takes
+hipError_t launch_qlinear_gemv(const QLinearArgs& p, hipStream_t s);
+bool gemv_supported(const QLinearArgs& p);
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s);
 
 // Workspace bytes the prefill kernel would use to split K for this shape

@@ -1,4 +1,5 @@
-// Decode-shaped qlinear (M <= 16 tokens): a weight-streaming GEMV.
+// Decode-shaped qlinear (2 <= M <= 16 tokens; a single token takes the
+// vector-ALU GEMV of qlinear_gemv.hip): a weight-streaming GEMV.
 //
 // Generation is bound by weight traffic (the paper finds autoregressive
 // decoding partly memory-bound, Section 5.6, and 4-bit weights help it most,
@@ -287,6 +288,8 @@ bool decode_supported(const QLinearArgs& p)
 
 hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s)
 {
+    // a single token: the GEMV whose every load lane carries weight bytes
+    if (gemv_supported(p)) return launch_qlinear_gemv(p, s);
     if (p.w_bits == 8 && p.out_bits == 8) return launch_t<8, 8>(p, s);
     if (p.w_bits == 8) return launch_t<8, 16>(p, s);
     if (p.out_bits == 8) return launch_t<4, 8>(p, s);

@@ -94,6 +94,25 @@ def test_decode_multi_round_k(w_bits, out_bits, M, K, N):
     assert np.array_equal(d, g)
 
 
+@pytest.mark.parametrize("w_bits,out_bits", [(8, 8), (8, 16), (4, 8), (4, 16)])
+@pytest.mark.parametrize("K,N", [(2048, 2048), (5632, 7), (272, 9), (16384, 33), (64, 1),
+                                 (1056, 4099)])
+@pytest.mark.parametrize("asym", [False, True])
+def test_one_token_gemv(w_bits, out_bits, K, N, asym):
+    """The one-token path (M = 1, the vector-ALU GEMV): ragged N (blocks of
+    8 channels), K that is not a multiple of one wave load's 128 row bytes,
+    several load rounds per wave (K = 16384), asymmetric weights and a bias,
+    against the oracle and the generic kernel.  int4 rows need K % 32 == 0
+    (K = 272 takes the MFMA decode kernel)."""
+    mq = _mq()
+    layer = wl.Layer("x", 1, K, N, w_bits=w_bits, out_bits=out_bits, bias=True, asym=asym)
+    ld = wl.make_layer("gemv", layer)
+    o = oracle_layer(ld)
+    g = gpu_layer(ld, path=mq.PATH_DECODE)
+    assert_same(g, o)
+    assert np.array_equal(gpu_layer(ld, path=mq.PATH_GENERIC).y_q, o.y_q)
+
+
 SPLIT_CASES = [
     # M, K, N, w_bits, out_bits, bias: few output tiles, long K (N a whole
     # number of 4-channel output groups: the tuned kernel's store rule)
@@ -265,9 +284,10 @@ def test_extreme_accumulators_at_max_k(w_bits):
     wq, ws, cs = mq.mq_pack_weights(w, w_bits)
     o_wq, o_ws, o_cs = oracle.pack_weights(wf, w_bits)
     assert np.array_equal(wq.cpu().numpy(), o_wq) and np.array_equal(cs.cpu().numpy(), o_cs)
-    for M, path in ((3, mq.PATH_DECODE), (20, mq.PATH_PREFILL), (3, mq.PATH_GENERIC)):
+    for M, path in ((3, mq.PATH_DECODE), (1, mq.PATH_DECODE), (20, mq.PATH_PREFILL),
+                    (3, mq.PATH_GENERIC)):
         a = np.full((M, K), -128, np.int8)
-        a[1] = 127
+        a[M // 2] = 127 if M > 1 else -128
         a_q = torch.from_numpy(a).to(dev)
         for a_zp, out_scale in ((0, 10.0), (-128, 1e-4), (127, 1.0)):
             y = mq.mq_qlinear(a_q, wq, w_bits, ws, cs, 0.5, a_zp, out_scale, 0, 16, path=path)
