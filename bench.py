@@ -57,6 +57,7 @@ TRAFFIC_FILES = {
 }
 KERNEL_SOURCES = ("paper_2408_13933_amd/csrc/qlinear_prefill.hip",
                   "paper_2408_13933_amd/csrc/qlinear_decode.hip",
+                  "paper_2408_13933_amd/csrc/qlinear_gemv.hip",
                   "paper_2408_13933_amd/csrc/requant.h",
                   "paper_2408_13933_amd/csrc/mq_internal.h")
 # decode-shaped layers of the other workloads timed cold beside the
@@ -72,7 +73,8 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
-                    help="also time the step replayed from a captured HIP graph")
+                    help="also time the step replayed from a captured HIP graph, and the "
+                         "dominant layer's launches replayed back to back")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -96,6 +98,10 @@ def parse():
                          "different copy of the weights, >= 512 MB per sweep; prints one JSON "
                          "line per layer (run under rocprofv3 --kernel-trace for kernel-only "
                          "durations) and exits")
+    ap.add_argument("--trace-summary", metavar="KERNEL_TRACE_CSV",
+                    help="summarise a rocprofv3 --kernel-trace -f csv kernel_trace.csv: per "
+                         "(kernel, grid, work-group) the dispatch count and the mean, median and "
+                         "minimum duration, and exit")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE "
                          "and WRITE_SIZE passes over a run with --calib-copy-mib) and exit")
@@ -150,7 +156,8 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
         factor = copy_mib * 1024.0 / (sum(c) / len(c))  # the copy reads and writes copy_mib
         groups = {}
         for n, g, v in rows:
-            if "qlinear_prefill_kernel" in n or "qlinear_decode_kernel" in n:
+            if ("qlinear_prefill_kernel" in n or "qlinear_decode_kernel" in n or
+                    "qlinear_gemv_kernel" in n):
                 groups.setdefault((n, g), []).append(v)
         per[key] = (groups, factor, sum(c) / len(c))
 
@@ -170,19 +177,22 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
         out["hbm_over_alg"] = total / alg
         return out
 
-    # the dominant prefill launches: the prefill (kernel, grid) with the most
-    # dispatches (one per step plus the graph-replay cross-check)
+    # the dominant prefill launches: the prefill (kernel, grid) that fetches
+    # the most bytes per dispatch (the layer with the most operations)
     pre = {k: v for k, v in per["fetch"][0].items() if "qlinear_prefill_kernel" in k[0]}
-    (kname, grid), _ = max(pre.items(), key=lambda kv: len(kv[1]))
+    (kname, grid), _ = max(pre.items(), key=lambda kv: sum(kv[1]) / len(kv[1]))
     res = {"workload": workload, "source_hash": kernel_source_hash(), "copy_mib": copy_mib,
            "prefill": dict(layer=f"{L.name} M={L.M} K={L.K} N={L.N} w{L.w_bits}/o{L.out_bits}",
                            **entry(kname, grid, L.alg_bytes())),
            "decode": []}
     # decode layers: the decode (kernel, grid) with their weight and output
     # widths (template arguments), the most dispatched group of each
-    dec = {k: v for k, v in per["fetch"][0].items() if "qlinear_decode_kernel" in k[0]}
+    dec = {k: v for k, v in per["fetch"][0].items()
+           if "qlinear_decode_kernel" in k[0] or "qlinear_gemv_kernel" in k[0]}
     for wname, D in _decode_layers(workload):
-        pat = re.compile(rf"qlinear_decode_kernel<{D.w_bits}, {D.out_bits},")
+        # one token of 8-bit codes runs the GEMV, more tokens the MFMA kernel
+        kern = "qlinear_gemv_kernel" if D.M == 1 and D.a_bits == 8 else "qlinear_decode_kernel"
+        pat = re.compile(rf"{kern}<{D.w_bits}, {D.out_bits},")
         cand = [(k, v) for k, v in dec.items() if pat.search(k[0])]
         if not cand:
             continue
@@ -191,6 +201,42 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
                                         f"w{D.w_bits}/o{D.out_bits}",
                                   **entry(kname, grid, D.alg_bytes())))
     return res
+
+
+def trace_summary(path):
+    """Per (kernel, grid, work-group size) of a rocprofv3 kernel trace:
+    dispatches and durations (us), largest total time first."""
+    import re
+
+    groups = {}
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            name = r["Kernel_Name"]
+            # namespaces and the argument list off; template arguments kept
+            short = re.sub(r"\(anonymous namespace\)::|mq::|at::native::", "", name)
+            short = re.sub(r"^void ", "", short)
+            depth, cut = 0, len(short)
+            for i, ch in enumerate(short):
+                if ch == "<":
+                    depth += 1
+                elif ch == ">":
+                    depth -= 1
+                elif ch == "(" and depth == 0:
+                    cut = i
+                    break
+            short = short[:cut]
+            grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+            wg = int(r["Workgroup_Size_X"]) * int(r["Workgroup_Size_Y"]) * int(r["Workgroup_Size_Z"])
+            us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            groups.setdefault((short, grid, wg), []).append(us)
+    rows = sorted(groups.items(), key=lambda kv: -sum(kv[1]))
+    out = [f"{'kernel':<78} {'grid':>9} {'wg':>5} {'n':>6} {'avg_us':>9} {'med_us':>9} "
+           f"{'min_us':>9}"]
+    for (k, grid, wg), v in rows:
+        v = sorted(v)
+        out.append(f"{k[:78]:<78} {grid:>9} {wg:>5} {len(v):>6} {sum(v) / len(v):>9.2f} "
+                   f"{v[len(v) // 2]:>9.2f} {v[0]:>9.2f}")
+    return "\n".join(out)
 
 
 def read_traffic(workload):
@@ -428,6 +474,29 @@ DECODE_LAYERS = (("decode_w8a8_m16", "linear"), ("w4a8_down_tinyllama", "down_pr
                  ("gemma2b_w8a8", "lm_head_m1"))
 
 
+def decode_grid(L):
+    """(work-groups, waves per work-group) of the decode kernel the library
+    launches for layer L: the launch rules of qlinear_gemv.hip (one token)
+    and qlinear_decode.hip (2..16 tokens), restated for the floor probe."""
+    if L.M == 1 and L.a_bits == 8 and L.K % (16 if L.w_bits == 8 else 32) == 0:
+        wrow = L.K * L.w_bits // 8
+        steps = -(-wrow // 128)
+        nw = 1
+        while nw < 8 and nw * 4 < steps:
+            nw *= 2
+        return -(-L.N // 8), nw
+    R = 8 if -(-L.N // 16) < 256 else 16
+    blocks = -(-L.N // R)
+    steps = -(-L.K // 64)
+    nw, nwmax = 1, 8 if L.a_bits == 16 else 16
+    while nw < nwmax and nw * 8 < steps:
+        nw *= 2
+    if blocks < 2048:
+        while nw < 4 and nw < steps:
+            nw *= 2
+    return blocks, nw
+
+
 def decode_sweep(launches_per_layer=400):
     """Cold decode launches.  Weight codes are random (the kernel's time does
     not depend on their values); shapes, formats and bias follow the
@@ -490,15 +559,40 @@ def decode_sweep(launches_per_layer=400):
         s1.record()
         torch.cuda.synchronize()
         graph_us = s0.elapsed_time(s1) * 1e3 / (reps * copies)
+        # the floor: a plain streaming read of the same weight copies with the
+        # kernel's grid (mq_probe_read), replayed the same way
+        blocks, waves = decode_grid(L)
+        per_wave_kib = -(-wbytes // (blocks * waves * 1024))
+        unroll = 1
+        while unroll < 8 and unroll < per_wave_kib:
+            unroll *= 2
+        sink = torch.empty(blocks * waves, dtype=torch.int32, device=dev)
+        fgraph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(fgraph, stream=cap):
+                for w in ws:
+                    mq.mq_probe_read(w, blocks, waves, unroll, sink=sink)
+        torch.cuda.current_stream().wait_stream(cap)
+        fgraph.replay()
+        torch.cuda.synchronize()
+        s0.record()
+        for _ in range(reps):
+            fgraph.replay()
+        s1.record()
+        torch.cuda.synchronize()
+        floor_us = s0.elapsed_time(s1) * 1e3 / (reps * copies)
         alg = L.alg_bytes()
         print(json.dumps({"layer": f"{wname}/{lname}", "M": L.M, "K": L.K, "N": L.N,
                           "w_bits": L.w_bits, "out_bits": L.out_bits, "weight_copies": copies,
                           "launches": 2 * reps * copies + copies, "alg_bytes": alg,
                           "event_us_per_launch": event_us, "graph_us_per_launch": graph_us,
                           "graph_GBps": alg / (graph_us * 1e-6) / 1e9,
-                          "graph_frac_hbm": alg / (graph_us * 1e-6) / 1e9 / PEAK_HBM_GBS}),
+                          "graph_frac_hbm": alg / (graph_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                          "floor": {"grid": [blocks, waves], "unroll": unroll,
+                                    "bytes": wbytes, "graph_us_per_launch": floor_us,
+                                    "kernel_over_floor": graph_us / floor_us}}),
               flush=True)
-        del ws, graph
+        del ws, graph, fgraph
         torch.cuda.empty_cache()
 
 
@@ -724,6 +818,9 @@ def main():
     if args.decode_sweep:
         decode_sweep()
         return
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary))
+        return
     if args.pmc_summary:
         if args.calib_copy_mib <= 0:
             raise SystemExit("--pmc-summary needs the --calib-copy-mib size of the profiled run")
@@ -788,30 +885,32 @@ def main():
     if dom is not None:
         L = layers[dom]
         k_us = layer_us[dom]
-        # Cross-check of the dominant kernel's duration, outside the timed
-        # region: its launches replayed back to back from a HIP graph (no
-        # host launch gaps), the steady state a kernel trace of this replay
-        # sees.
-        reps = 10
-        gk = torch.cuda.CUDAGraph()
-        s_k = torch.cuda.Stream()
-        s_k.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s_k):
-            with torch.cuda.graph(gk, stream=s_k):
-                for _ in range(reps):
-                    prep.launch_layer(dom)
-        torch.cuda.current_stream().wait_stream(s_k)
-        gk.replay()
-        torch.cuda.synchronize()
-        k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        n_replay = 5
-        k0.record()
-        for _ in range(n_replay):
+        k_graph_us = None
+        if args.graph:
+            # Cross-check of the dominant kernel's duration, outside the
+            # timed region: its launches replayed back to back from a HIP
+            # graph (no host launch gaps; sustained, so the chip runs hotter
+            # and clocks lower than within the step)
+            reps = 10
+            gk = torch.cuda.CUDAGraph()
+            s_k = torch.cuda.Stream()
+            s_k.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s_k):
+                with torch.cuda.graph(gk, stream=s_k):
+                    for _ in range(reps):
+                        prep.launch_layer(dom)
+            torch.cuda.current_stream().wait_stream(s_k)
             gk.replay()
-        k1.record()
-        torch.cuda.synchronize()
-        k_graph_us = k0.elapsed_time(k1) * 1e3 / (n_replay * reps)
-        del gk
+            torch.cuda.synchronize()
+            k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            n_replay = 5
+            k0.record()
+            for _ in range(n_replay):
+                gk.replay()
+            k1.record()
+            torch.cuda.synchronize()
+            k_graph_us = k0.elapsed_time(k1) * 1e3 / (n_replay * reps)
+            del gk
         achieved = L.ops / (k_us * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                 "frac": achieved / PEAK_INT8_TOPS, "traffic": None}
@@ -824,8 +923,9 @@ def main():
                                       "algorithmic": t["alg_bytes_per_launch"]}
         roof.update({"kernel": f"qlinear_prefill {L.name} M={L.M} K={L.K} N={L.N} "
                                f"w{L.w_bits}/o{L.out_bits}",
-                     "ops_per_launch": L.ops, "kernel_us": k_us,
-                     "kernel_us_graph_replay": k_graph_us})
+                     "ops_per_launch": L.ops, "kernel_us": k_us})
+        if k_graph_us is not None:
+            roof["kernel_us_graph_replay"] = k_graph_us
         line["roofline"] = roof
 
     # decode half of the metric: cold weights (each launch reads another copy
