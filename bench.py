@@ -526,6 +526,7 @@ def cpu_baseline(prep: Prepared, target_s: float):
         reps += 1
     dec = [e["layer"].name for e in prep.layers if e["layer"].M <= 16]
     model = cpu_model()
+    single = cpu_single_thread()
     return {"value": total_ops / total_dt / 1e12, "unit": "TOPS", "cores": nthreads,
             "kind": "oracle",
             "sample": f"first {rows} token rows of each prefill-shaped layer"
@@ -533,7 +534,32 @@ def cpu_baseline(prep: Prepared, target_s: float):
                          f"one thread)" if dec else "")
                       + f" (quantize + integer GEMM + requant), {reps} pass(es), "
                         f"{total_dt:.1f} s on {nthreads} host threads of {model}",
-            "cpu_model": model}
+            "cpu_model": model, "single_thread": single}
+
+
+def cpu_single_thread(min_s: float = 1.0):
+    """The oracle on one host thread over the whole single W8A8 layer
+    (16 x 2048 x 2048 with bias): quantize + integer GEMM + requant."""
+    import oracle
+    from paper_2408_13933_amd import workloads as wl
+
+    L = next(l for l in wl.WORKLOADS["decode_w8a8_m16"].layers if l.name == "linear")
+    ld = wl.make_layer("decode_w8a8_m16", L)
+    wq, ws, _ = oracle.pack_weights(ld.w, L.w_bits)
+    a_scale, a_zp = oracle.act_params(*ld.act_range, L.a_bits)
+    o_scale, o_zp = oracle.act_params(*ld.out_range, L.out_bits)
+    reps, dt = 0, 0.0
+    t0 = time.perf_counter()
+    while dt < min_s:
+        a = oracle.quantize_act(ld.x, a_scale, a_zp, L.a_bits)
+        oracle.qlinear(a, wq, L.w_bits, ws, a_scale, a_zp, o_scale, o_zp, L.out_bits,
+                       bias=ld.bias, nthreads=1)
+        reps += 1
+        dt = time.perf_counter() - t0
+    return {"value": reps * L.ops / dt / 1e12, "unit": "TOPS", "cores": 1, "kind": "oracle",
+            "sample": f"decode_w8a8_m16/linear 16x2048x2048 whole, {reps} pass(es), "
+                      f"{dt:.2f} s on one host thread",
+            "ms_per_layer": dt / reps * 1e3}
 
 
 DECODE_LAYERS = (("decode_w8a8_m16", "linear"), ("w4a8_down_tinyllama", "down_proj_m1"),
