@@ -61,6 +61,24 @@ __device__ inline v4i unpack_int4_x16(uint32_t x0, uint32_t x1)
     return r;
 }
 
+// v_med3_i32: x clamped to [lo, hi] (lo <= hi) in one instruction; the
+// compiler emits two (v_min, v_max) when the bounds are not constants
+__device__ __forceinline__ int32_t med3_i32(int32_t x, int32_t lo, int32_t hi)
+{
+    int32_t r;
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(lo), "v"(hi));
+    return r;
+}
+
+// v_cvt_pk_i16_i32: two int32 saturated to the int16 range and packed, the
+// first in the low half (one instruction for what two clamps and a byte
+// permute do; saturation checked on MI355X at the int16 and int32 ends)
+__device__ __forceinline__ uint32_t pack_sat_i16(int32_t lo, int32_t hi)
+{
+    typedef short v2s __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16(lo, hi));
+}
+
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding:
 // vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
 template <int N>
@@ -273,15 +291,18 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
             const v4i sp = *reinterpret_cast<const v4i*>(x.e_sp + nl);
             const int32_t col_off = (x.n_tile + nl) * OB;
             const bool col_ok = nl < x.n_left;
-            int32_t shr[4], pre[4], bnd[4];  // per column, hoisted out of the token loop
+            int32_t shr[4], pre[4], bnd[4], nbnd[4];  // per column, hoisted out of the token loop
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 shr[r] = sp[r] & 0xFF;
                 pre[r] = sp[r] >> 8;
                 bnd[r] = pre[r] ? (1 << (30 - pre[r])) : 0x7FFFFFFF;
+                nbnd[r] = -bnd[r];
             }
 #pragma unroll
             for (int j = 0; j < C::FM; ++j) {
+                // int8 outputs: clamped codes; int16 outputs: the unclamped
+                // values, saturated by the pack (pack_sat_i16) or per element
                 int32_t y[4];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -310,12 +331,12 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                     // (no column of the tile with a pre-shift: bnd = 2^31 - 1 and
                     // pre = 0, both the identity)
                     if constexpr (!FAST || PRE) {
-                        c = max(min(c, bnd[r]), -bnd[r]);
+                        c = med3_i32(c, nbnd[r], bnd[r]);
                         c = (int32_t)((uint32_t)c << pre[r]);
                     }
                     int32_t v = (__mulhi(c, m0[r]) + rnd[r]) >> shr[r];
                     if constexpr (!FAST) v += x.out_zp;
-                    y[r] = max(min(v, qmax), qmin);
+                    y[r] = C::OBITS == 16 ? v : max(min(v, qmax), qmin);
                 }
                 if constexpr (STAGED) {
                     // tile-local row j*32 + r32, pass-local channel nl - first
@@ -331,8 +352,8 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                     } else {
                         typedef unsigned v2u __attribute__((ext_vector_type(2)));
                         v2u v;
-                        v[0] = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x05040100u);
-                        v[1] = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x05040100u);
+                        v[0] = pack_sat_i16(y[0], y[1]);
+                        v[1] = pack_sat_i16(y[2], y[3]);
                         *reinterpret_cast<MQ_LDS v2u*>(dst) = v;
                     }
                     continue;
@@ -349,8 +370,8 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                     } else {
                         typedef unsigned v2u __attribute__((ext_vector_type(2)));
                         v2u v;
-                        v[0] = __builtin_amdgcn_perm((uint32_t)y[1], (uint32_t)y[0], 0x05040100u);
-                        v[1] = __builtin_amdgcn_perm((uint32_t)y[3], (uint32_t)y[2], 0x05040100u);
+                        v[0] = pack_sat_i16(y[0], y[1]);
+                        v[1] = pack_sat_i16(y[2], y[3]);
                         __builtin_amdgcn_raw_buffer_store_b64(v, x.ry, voff, 0, 0);
                     }
                 } else {
@@ -362,8 +383,8 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                         if constexpr (C::OBITS == 8)
                             __builtin_amdgcn_raw_buffer_store_b8((unsigned char)y[r], x.ry, voff, 0, 0);
                         else
-                            __builtin_amdgcn_raw_buffer_store_b16((unsigned short)y[r], x.ry, voff,
-                                                                  0, 0);
+                            __builtin_amdgcn_raw_buffer_store_b16(
+                                (unsigned short)max(min(y[r], qmax), qmin), x.ry, voff, 0, 0);
                     }
                 }
             }
