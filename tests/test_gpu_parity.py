@@ -156,6 +156,34 @@ def test_split_k_parity(case, tile):
     assert np.array_equal(gpu_layer(ld, path=path).y_q, o.y_q)
 
 
+MANY_TILE_CASES = [
+    # M, K, N, w_bits, out_bits, bias, asym: more 256x256 output tiles than
+    # the chip has CUs (two to three rounds of work-groups), ragged M and N
+    # (the last tile column takes the unstaged epilogue), K of one to five
+    # stages
+    (300, 128, 40004, 8, 16, True, False),
+    (520, 256, 33024, 8, 8, False, False),
+    (768, 384, 22016, 4, 16, True, False),
+    (300, 256, 40004, 8, 8, True, True),
+    (257, 640, 65536, 4, 8, False, True),
+    (1024, 128, 49152, 8, 16, True, False),
+]
+
+
+@pytest.mark.parametrize("case", MANY_TILE_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_eight_wave_tile_many_rounds(case):
+    """The eight-wave 256x256 tile (the LM head's) without a K split on
+    layers of several rounds of tiles: bit-identical to the oracle, twice in
+    a row."""
+    mq = _mq()
+    M, K, N, wb, ob, has_bias, asym = case
+    layer = wl.Layer("x", M, K, N, w_bits=wb, out_bits=ob, bias=has_bias, asym=asym)
+    ld = wl.make_layer("rounds", layer)
+    o = oracle_layer(ld)
+    for _ in range(2):
+        assert_same(gpu_layer(ld, path=mq.prefill_tile_path(5)), o)
+
+
 @pytest.mark.parametrize("w_bits", [8, 4])
 def test_prefill_equals_generic_ragged(w_bits):
     mq = _mq()
