@@ -3,7 +3,9 @@
 One step = one pass of the hot path over one batch of a workload's
 synthetic, seeded inputs: quantize each distinct layer input (Section 4.2,
 Eq.(4)), run every qlinear of the workload with its fused fixed-point
-requant epilogue, and dequantize the last layer's output.  Weights are
+requant epilogue, and dequantize the last layer's output.  The layers that
+read one input and write one code width (gate and up) go out as one
+mq_qlinear_group launch (--no-group: one launch per layer).  Weights are
 folded/packed once before timing (offline steps).
 
 The default workload is the Gemma-2B-shaped one (the largest of the layer
@@ -14,14 +16,14 @@ int16 outputs; the dequantized step output is the 512 x 256000 logits.
 
 `value` is whole-step int8 TOPS = sum(2*M*N*K) / step time, inputs already
 in HBM.  The JSON line also carries
-* `roofline`: the dominant prefill kernel (the layer with the most
+* `roofline`: the dominant prefill kernel (the launch with the most
   operations), int8 TOP/s against the MFMA peak, timed with HIP events on
   the launch stream inside the timed steps;
 * `decode`: the decode-shaped layers (M <= 16) with cold weights, GB/s of
   algorithmic bytes against the HBM peak -- the workload's own and those of
   the single-layer W8A8 (16 x 2048 x 2048) and W4A8 (1 x 5632 x 2048)
   workloads;
-* `layers`: every layer's average kernel time in the timed steps;
+* `layers`: every launch's average kernel time in the timed steps;
 * `cpu_baseline`: the CPU oracle's rate on a bounded sample of the step.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--workload NAME]
@@ -30,6 +32,7 @@ from __future__ import annotations
 
 import argparse
 import csv
+import gc
 import hashlib
 import json
 import os
@@ -72,6 +75,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-group", action="store_true",
+                    help="launch every layer on its own (by default the layers that read one "
+                         "quantized input and write one code width go out as one "
+                         "mq_qlinear_group launch)")
     ap.add_argument("--graph", action="store_true",
                     help="also time the step replayed from a captured HIP graph, and the "
                          "dominant layer's launches replayed back to back")
@@ -137,7 +144,43 @@ def _decode_layers(workload):
     return own + extra
 
 
-def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
+def launch_groups(workload, layers, group=True, max_group=4):
+    """The layers (indices) of each launch of a step: consecutive
+    prefill-shaped layers with 8-bit inputs that read one input (same
+    activation and token count) and write one code width, up to max_group,
+    form one mq_qlinear_group launch; every other layer is a launch of its
+    own."""
+    from paper_2408_13933_amd import workloads as wl
+
+    out = []
+    for i, L in enumerate(layers):
+        if out and group:
+            F = layers[out[-1][0]]
+            if ((wl._x_key(workload, L), L.M) == (wl._x_key(workload, F), F.M) and L.M > 16 and
+                    L.a_bits == 8 and (L.w_bits, L.out_bits, L.asym) ==
+                    (F.w_bits, F.out_bits, F.asym) and len(out[-1]) < max_group):
+                out[-1].append(i)
+                continue
+        out.append([i])
+    return out
+
+
+def launch_alg_bytes(layers, idx):
+    """Minimum bytes one launch moves: its shared input (and row sums) once,
+    each layer's weights, outputs and per-channel parameters."""
+    Ls = [layers[i] for i in idx]
+    F = Ls[0]
+    shared = F.M * F.K * F.a_bits // 8 + (F.M * 4 if F.asym else 0)
+    return sum(L.alg_bytes() for L in Ls) - (len(Ls) - 1) * shared
+
+
+def launch_label(layers, idx):
+    Ls = [layers[i] for i in idx]
+    return (f"{'+'.join(L.name for L in Ls)} M={Ls[0].M} K={Ls[0].K} "
+            f"N={'+'.join(str(L.N) for L in Ls)}")
+
+
+def pmc_summary(fetch_csv, write_csv, copy_mib, workload, group=True):
     """HBM bytes per launch of the dominant prefill kernel and of each
     decode-shaped layer, each counter scaled by what it reads for the plain
     copy of known size in the same run."""
@@ -146,7 +189,9 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
     from paper_2408_13933_amd import workloads as wl
 
     layers = wl.WORKLOADS[workload].layers
-    L = max(layers, key=lambda l: l.ops)
+    launches = launch_groups(workload, layers, group)
+    dom = max(launches, key=lambda idx: sum(layers[i].ops for i in idx))
+    L = layers[dom[0]]
     per = {}
     for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         rows = _pmc_rows(path, counter)
@@ -156,7 +201,7 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
         factor = copy_mib * 1024.0 / (sum(c) / len(c))  # the copy reads and writes copy_mib
         groups = {}
         for n, g, v in rows:
-            if ("qlinear_prefill_kernel" in n or "qlinear_decode_kernel" in n or
+            if ("qlinear_prefill" in n or "qlinear_decode_kernel" in n or
                     "qlinear_gemv_kernel" in n):
                 groups.setdefault((n, g), []).append(v)
         per[key] = (groups, factor, sum(c) / len(c))
@@ -178,12 +223,12 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
         return out
 
     # the dominant prefill launches: the prefill (kernel, grid) that fetches
-    # the most bytes per dispatch (the layer with the most operations)
-    pre = {k: v for k, v in per["fetch"][0].items() if "qlinear_prefill_kernel" in k[0]}
+    # the most bytes per dispatch (the launch with the most operations)
+    pre = {k: v for k, v in per["fetch"][0].items() if "qlinear_prefill" in k[0]}
     (kname, grid), _ = max(pre.items(), key=lambda kv: sum(kv[1]) / len(kv[1]))
     res = {"workload": workload, "source_hash": kernel_source_hash(), "copy_mib": copy_mib,
-           "prefill": dict(layer=f"{L.name} M={L.M} K={L.K} N={L.N} w{L.w_bits}/o{L.out_bits}",
-                           **entry(kname, grid, L.alg_bytes())),
+           "prefill": dict(layer=f"{launch_label(layers, dom)} w{L.w_bits}/o{L.out_bits}",
+                           **entry(kname, grid, launch_alg_bytes(layers, dom))),
            "decode": []}
     # decode layers: the decode (kernel, grid) with their weight and output
     # widths (template arguments), the most dispatched group of each
@@ -335,7 +380,7 @@ class TimingEvent:
 class Prepared:
     """Device-resident inputs and packed weights of one workload."""
 
-    def __init__(self, workload_name):
+    def __init__(self, workload_name, group=True):
         import torch
 
         import paper_2408_13933_amd as mq
@@ -398,6 +443,9 @@ class Prepared:
                           else None)
         last = self.layers[-1]
         self.deq = torch.empty(last["y"].shape, dtype=torch.float32, device=dev)
+        # launches: gate/up (q/k/v) as one mq_qlinear_group call each
+        self.launches = launch_groups(workload_name, [e["layer"] for e in self.layers], group,
+                                      mq.MAX_GROUP)
         torch.cuda.synchronize()
 
     def qlinear(self, e, w_q=None, workspace=None):
@@ -420,14 +468,29 @@ class Prepared:
                                e["a_scale"], e["a_zp"], e["out_scale"], e["out_zp"], L.out_bits,
                                bias=e["bias"], out=e["y"], workspace=workspace)
 
-    def launch_layer(self, i):
-        """One qlinear launch of layer i on its already quantized input."""
-        self.qlinear(self.layers[i], workspace=self.workspace)
+    def launch(self, j):
+        """Launch j (one layer, or a group of layers on one input) on its
+        already quantized input."""
+        idx = self.launches[j]
+        if len(idx) == 1:
+            self.qlinear(self.layers[idx[0]], workspace=self.workspace)
+            return
+        es = [self.layers[i] for i in idx]
+        L = es[0]["layer"]
+        inp = self.inputs[es[0]["key"]]
+        lin = [dict(w_q=e["w_q"], w_scale=e["w_scale"], w_zp=e["w_zp"], w_colsum=e["w_colsum"],
+                    bias=e["bias"], out_scale=e["out_scale"], out_zp=e["out_zp"], out=e["y"])
+               for e in es]
+        self.mq.mq_qlinear_group(inp["q"], lin, L.w_bits, es[0]["a_scale"], es[0]["a_zp"],
+                                 L.out_bits, a_rowsum=inp["rs"] if L.asym else None)
+
+    def launch_name(self, j):
+        return launch_label([e["layer"] for e in self.layers], self.launches[j])
 
     def step(self, events=None):
-        """One pass of the hot path.  `events`: len(layers) + 1 events, the
-        first recorded before the first qlinear launch and event i + 1 after
-        launch i (all on the launch stream)."""
+        """One pass of the hot path.  `events`: len(launches) + 1 events, the
+        first recorded before the first qlinear launch and event j + 1 after
+        launch j (all on the launch stream)."""
         mq = self.mq
         for inp in self.inputs.values():
             if inp["rs"] is not None:  # codes and their row sums in one pass
@@ -437,10 +500,10 @@ class Prepared:
                 mq.mq_quantize_act(inp["x"], inp["scale"], inp["zp"], inp["bits"], out=inp["q"])
         if events is not None:
             events[0].record()
-        for i, e in enumerate(self.layers):
-            self.qlinear(e, workspace=self.workspace)
+        for j in range(len(self.launches)):
+            self.launch(j)
             if events is not None:
-                events[i + 1].record()
+                events[j + 1].record()
         last = self.layers[-1]
         mq.mq_dequant(last["y"], last["out_scale"], last["out_zp"], out=self.deq)
 
@@ -917,7 +980,8 @@ def main():
         if args.calib_copy_mib <= 0:
             raise SystemExit("--pmc-summary needs the --calib-copy-mib size of the profiled run")
         print(json.dumps(pmc_summary(args.pmc_summary[0], args.pmc_summary[1],
-                                     args.calib_copy_mib, args.workload)))
+                                     args.calib_copy_mib, args.workload,
+                                     group=not args.no_group)))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "the qlinear path is measured on one GPU only (its multi-GPU "
@@ -925,22 +989,30 @@ def main():
         sys.exit(2)
     import torch
 
-    prep = Prepared(args.workload)
+    prep = Prepared(args.workload, group=not args.no_group)
     layers = [e["layer"] for e in prep.layers]
     ops_step = sum(L.ops for L in layers)
-    # dominant kernel: the prefill-shaped layer with the most operations
-    dom = max((i for i, L in enumerate(layers) if L.M > 16), key=lambda i: layers[i].ops,
-              default=None)
+    # operations of each launch (a layer, or a group of layers on one input)
+    launch_ops = [sum(layers[i].ops for i in idx) for idx in prep.launches]
+    launch_m = [layers[idx[0]].M for idx in prep.launches]
+    # dominant kernel: the prefill-shaped launch with the most operations
+    dom = max((j for j in range(len(prep.launches)) if launch_m[j] > 16),
+              key=lambda j: launch_ops[j], default=None)
 
     for _ in range(args.warmup):
         prep.step()
     torch.cuda.synchronize()
 
     # per-layer events inside the timed steps: timing-only (no system fence)
-    evs = [[TimingEvent() for _ in range(len(layers) + 1)] for _ in range(args.steps)]
+    evs = [[TimingEvent() for _ in range(len(prep.launches) + 1)] for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    # no garbage-collection pause of the launching thread inside the timed
+    # steps (the events time the stream, so a stalled host shows up as GPU
+    # idle time)
+    gc.collect()
+    gc.disable()
     t_wall = time.perf_counter()
     start.record()
     for s in range(args.steps):
@@ -948,10 +1020,11 @@ def main():
     end.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
+    gc.enable()
     ms = start.elapsed_time(end) / args.steps
-    # average duration of each layer's launch inside the timed steps
-    layer_us = [float(np.mean([ev[i].elapsed_time(ev[i + 1]) for ev in evs])) * 1e3
-                for i in range(len(layers))]
+    # average duration of each launch inside the timed steps
+    launch_us = [float(np.mean([ev[j].elapsed_time(ev[j + 1]) for ev in evs])) * 1e3
+                 for j in range(len(prep.launches))]
 
     line = {
         "metric": METRIC,
@@ -969,14 +1042,17 @@ def main():
         "config": {"workload": args.workload,
                    "layers": [f"{l.name} M={l.M} K={l.K} N={l.N} w{l.w_bits} o{l.out_bits}"
                               for l in layers],
-                   "step": "quantize inputs + qlinear x%d + dequant of last output" % len(layers),
+                   "step": "quantize inputs + %d qlinear launches (%s) + dequant of last output"
+                           % (len(prep.launches),
+                              ", ".join(prep.launch_name(j).split(" ")[0]
+                                        for j in range(len(prep.launches)))),
                    "ops_per_step": ops_step},
     }
     tr = read_traffic(args.workload)
 
     if dom is not None:
-        L = layers[dom]
-        k_us = layer_us[dom]
+        L = layers[prep.launches[dom][0]]
+        k_us = launch_us[dom]
         k_graph_us = None
         if args.graph:
             # Cross-check of the dominant kernel's duration, outside the
@@ -990,7 +1066,7 @@ def main():
             with torch.cuda.stream(s_k):
                 with torch.cuda.graph(gk, stream=s_k):
                     for _ in range(reps):
-                        prep.launch_layer(dom)
+                        prep.launch(dom)
             torch.cuda.current_stream().wait_stream(s_k)
             gk.replay()
             torch.cuda.synchronize()
@@ -1003,19 +1079,19 @@ def main():
             torch.cuda.synchronize()
             k_graph_us = k0.elapsed_time(k1) * 1e3 / (n_replay * reps)
             del gk
-        achieved = L.ops / (k_us * 1e-6) / 1e12
+        achieved = launch_ops[dom] / (k_us * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                 "frac": achieved / PEAK_INT8_TOPS, "traffic": None}
-        if tr is not None:
+        if tr is not None and tr["prefill"]["layer"].startswith(prep.launch_name(dom) + " "):
             t = tr["prefill"]
             roof["traffic"] = t["hbm_bytes_per_launch"]
             roof["traffic_detail"] = {"unit": "bytes per launch",
                                       "fetch": t["fetch"]["bytes_per_launch"],
                                       "write": t["write"]["bytes_per_launch"],
                                       "algorithmic": t["alg_bytes_per_launch"]}
-        roof.update({"kernel": f"qlinear_prefill {L.name} M={L.M} K={L.K} N={L.N} "
+        roof.update({"kernel": f"qlinear_prefill {prep.launch_name(dom)} "
                                f"w{L.w_bits}/o{L.out_bits}",
-                     "ops_per_launch": L.ops, "kernel_us": k_us})
+                     "ops_per_launch": launch_ops[dom], "kernel_us": k_us})
         if k_graph_us is not None:
             roof["kernel_us_graph_replay"] = k_graph_us
         line["roofline"] = roof
@@ -1044,11 +1120,11 @@ def main():
     if dec:
         line["decode"] = dec[0]
         line["decode_layers"] = dec
-    line["layers"] = [{"layer": f"{L.name} M={L.M} K={L.K} N={L.N}", "kernel_us": u,
-                       ("TOP/s" if L.M > 16 else "GB/s"):
-                           (L.ops / (u * 1e-6) / 1e12 if L.M > 16
-                            else L.alg_bytes() / (u * 1e-6) / 1e9)}
-                      for L, u in zip(layers, layer_us)]
+    line["layers"] = [{"layer": prep.launch_name(j), "kernel_us": u,
+                       ("TOP/s" if launch_m[j] > 16 else "GB/s"):
+                           (launch_ops[j] / (u * 1e-6) / 1e12 if launch_m[j] > 16
+                            else launch_alg_bytes(layers, prep.launches[j]) / (u * 1e-6) / 1e9)}
+                      for j, u in enumerate(launch_us)]
     line["wall_s_timed"] = t_wall
 
     if args.graph:

@@ -58,16 +58,17 @@ typedef enum {
     MQ_PATH_PREFILL = 2,  /* LDS-tiled MFMA GEMM kernel, any M             */
     MQ_PATH_GENERIC = 3,  /* one thread per output, any shape or alignment */
     /* MQ_PATH_PREFILL_TILE0 + t, t = 0..MQ_PREFILL_TILES-1: the prefill
-     * kernel with output tile t (0: 256x256 on four waves, 1: 256x128,
-     * 2: 128x128, 3: 192x256, 4: 64x64, 5: 256x256 on eight waves; tokens x
-     * channels) instead of the one its cost model picks -- a hook for tests
-     * and measurements; the results are the same bits.  With a workspace the K split is the cost model's best for
-     * that tile and may need more bytes than mq_qlinear_workspace_bytes
-     * reports (at most 256*ceil(T/64) + 8*T*tm*tn*4 bytes for T tiles of
-     * tm x tn); with fewer bytes it does not split. */
+     * kernel with output tile t (0: 256x128, 1: 128x128, 2: 192x256,
+     * 3: 64x64, 4: 256x256 on eight waves; tokens x channels) instead of
+     * the one its cost model picks -- a hook for tests and measurements;
+     * the results are the same bits.  With a workspace the K split is the
+     * cost model's best for that tile and may need more bytes than
+     * mq_qlinear_workspace_bytes reports (at most 256*ceil(T/64) +
+     * 8*T*tm*tn*4 bytes for T tiles of tm x tn); with fewer bytes it does
+     * not split. */
     MQ_PATH_PREFILL_TILE0 = 16
 } mq_path;
-#define MQ_PREFILL_TILES 6
+#define MQ_PREFILL_TILES 5
 
 /* Largest K accepted: keeps |sum_k A_q W_q| below 2^30 so the int32
  * accumulator cannot overflow. */
@@ -319,6 +320,52 @@ mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M,
                           float out_scale, int32_t out_zp, int32_t out_bits,
                           const float* bias, void* y_q, void* workspace,
                           int64_t workspace_bytes, int32_t path, void* stream);
+
+/* Most linears one mq_qlinear_group call takes. */
+#define MQ_MAX_GROUP 4
+
+/*
+ * mq_qlinear_out -- one linear of an mq_qlinear_group call: what differs
+ * between linears that read the same activations.
+ */
+typedef struct mq_qlinear_out {
+    const void* w_q;          /* device, layout of mq_pack_weights for the call's w_bits */
+    const float* w_scale;     /* device fp32 [N] */
+    const int32_t* w_zp;      /* device int32 [N] (asymmetric weights), or NULL */
+    const int32_t* w_colsum;  /* device int32 [N] */
+    const float* bias;        /* device fp32 [N], or NULL */
+    int64_t N;                /* output channels, >= 0 */
+    float out_scale;          /* finite, > 0 */
+    int32_t out_zp;           /* within the range of the call's out_bits */
+    void* y_q;                /* device [M][N] int8 or int16 (out_bits); must not overlap
+                                 the inputs or another linear's output */
+} mq_qlinear_out;
+
+/*
+ * mq_qlinear_group -- the linears that read one activation input (the
+ * query, key and value projections of an attention layer; the gate and
+ * up projections of a gated MLP; Section 4.1's block), each the operation
+ * of mq_qlinear (symmetric weights: every w_zp NULL) or mq_qlinear_asym
+ * (every w_zp set, a_rowsum set) on a_q, bit for bit, in one call.  On the
+ * prefill path (M > 16 with MQ_PATH_AUTO) with K % 16 == 0 (int8) or
+ * K % 32 == 0 (int4) and 16-byte-aligned buffers, one launch takes the
+ * output tiles of all the linears, so a set of small layers fills the chip
+ * as one large one would; otherwise each linear runs on the path
+ * mq_qlinear_ex would take with the same path argument.  No K split.
+ *   a_q       device int8 [M][K]   a_rowsum  device int32 [M] or NULL (as
+ *             for mq_qlinear_asym)
+ *   w_bits, a_scale, a_zp, out_bits  as for mq_qlinear, shared
+ *   outs      host array of n_outs linears, 1 <= n_outs <= MQ_MAX_GROUP;
+ *             each N may differ (N = 0: that linear has nothing to do)
+ *   path      as for mq_qlinear_ex; MQ_PATH_PREFILL_TILE0 + t forces tile
+ *             t for the whole launch
+ *   M >= 0, 1 <= K <= MQ_MAX_K.  Errors: MQ_ERR_INVALID_ARG when any
+ *   linear's arguments are invalid (nothing is launched).
+ */
+mq_status mq_qlinear_group(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
+                           int32_t w_bits, float a_scale, int32_t a_zp, int32_t out_bits,
+                           const mq_qlinear_out* outs, int32_t n_outs, int32_t path,
+                           void* stream);
 
 /*
  * mq_qlinear_a16 -- mq_qlinear_ex with 16-bit activation codes (the W8A16

@@ -21,6 +21,7 @@ __all__ = [
     "mq_qlinear_workspace_bytes", "mq_qlinear_noalloc", "NOALLOC_SCRATCH_BYTES",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
     "PATH_PREFILL_TILE0", "PREFILL_TILES", "prefill_tile_path", "mq_probe_read",
+    "mq_qlinear_group", "MAX_GROUP", "QLinearOut",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -29,8 +30,8 @@ lib_path = os.path.join(_HERE, "libmq.so")
 MQ_OK, MQ_ERR_INVALID_ARG, MQ_ERR_UNSUPPORTED, MQ_ERR_HIP = 0, 1, 2, 3
 PATH_AUTO, PATH_DECODE, PATH_PREFILL, PATH_GENERIC = 0, 1, 2, 3
 # the prefill kernel with one explicit output tile (tests and measurements)
-PATH_PREFILL_TILE0, PREFILL_TILES = 16, 6
-PREFILL_TILE_SHAPES = ((256, 256), (256, 128), (128, 128), (192, 256), (64, 64), (256, 256))
+PATH_PREFILL_TILE0, PREFILL_TILES = 16, 5
+PREFILL_TILE_SHAPES = ((256, 128), (128, 128), (192, 256), (64, 64), (256, 256))
 
 
 def prefill_tile_path(tile: int) -> int:
@@ -57,6 +58,17 @@ def _status_string(status: int) -> str:
         return lib().mq_status_string(status).decode()
     except Exception:
         return f"status {status}"
+
+
+MAX_GROUP = 4  # MQ_MAX_GROUP
+
+
+class QLinearOut(ctypes.Structure):
+    """mq_qlinear_out of mq.h: one linear of an mq_qlinear_group call."""
+    _fields_ = [("w_q", ctypes.c_void_p), ("w_scale", ctypes.c_void_p),
+                ("w_zp", ctypes.c_void_p), ("w_colsum", ctypes.c_void_p),
+                ("bias", ctypes.c_void_p), ("N", ctypes.c_int64), ("out_scale", ctypes.c_float),
+                ("out_zp", ctypes.c_int32), ("y_q", ctypes.c_void_p)]
 
 
 def lib():
@@ -127,7 +139,9 @@ def lib():
                                  c_i64, c_i64, c_i64, c_p, c_i64, c_i32, c_p]
     L.mq_transpose_i8.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_p]
     L.mq_probe_read.argtypes = [c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_p]
-    for name in ("mq_probe_read", "mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
+    L.mq_qlinear_group.argtypes = [c_p, c_p, c_i64, c_i64, c_i32, c_f, c_i32, c_i32,
+                                   ctypes.POINTER(QLinearOut), c_i32, c_i32, c_p]
+    for name in ("mq_qlinear_group", "mq_probe_read", "mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
                  "mq_qlinear_noalloc",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
@@ -343,6 +357,42 @@ def mq_qlinear_asym(a_q, a_rowsum, w_q, w_bits: int, w_scale, w_zp, w_colsum, a_
         _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), ws, ws_bytes, int(path),
         _stream_ptr(stream)), "mq_qlinear_asym")
     return out
+
+
+def mq_qlinear_group(a_q, linears, w_bits: int, a_scale: float, a_zp: int, out_bits: int = 8,
+                     a_rowsum=None, path: int = PATH_AUTO, stream=None):
+    """Linears that read one activation input, in one call (one launch on the
+    prefill path).  ``linears``: up to MAX_GROUP dicts with w_q, w_scale,
+    w_colsum, out_scale, out_zp and optionally w_zp (all or none), bias and
+    out.  Returns the outputs, each as mq_qlinear / mq_qlinear_asym would."""
+    torch = _torch()
+    M, K = a_q.shape
+    n = len(linears)
+    if n < 1 or n > MAX_GROUP:
+        raise MQError(f"mq_qlinear_group: {n} linears (1..{MAX_GROUP})")
+    arr = (QLinearOut * n)()
+    outs = []
+    for i, d in enumerate(linears):
+        N = d["w_q"].shape[0]
+        wq_dtype, wq_shape = (torch.int8, (N, K)) if w_bits == 8 else (torch.uint8, (N, K // 2))
+        out = d.get("out")
+        if out is None:
+            out = torch.empty((M, N), dtype=_act_dtype(out_bits), device=a_q.device)
+        outs.append(out)
+        zp, bias = d.get("w_zp"), d.get("bias")
+        arr[i] = QLinearOut(
+            _dev_ptr(d["w_q"], wq_dtype, "w_q", wq_shape),
+            _dev_ptr(d["w_scale"], torch.float32, "w_scale", (N,)),
+            None if zp is None else _dev_ptr(zp, torch.int32, "w_zp", (N,)),
+            _dev_ptr(d["w_colsum"], torch.int32, "w_colsum", (N,)),
+            None if bias is None else _dev_ptr(bias, torch.float32, "bias", (N,)),
+            N, float(d["out_scale"]), int(d["out_zp"]),
+            _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)))
+    rs = None if a_rowsum is None else _dev_ptr(a_rowsum, torch.int32, "a_rowsum", (M,))
+    _check(lib().mq_qlinear_group(_dev_ptr(a_q, torch.int8, "a_q"), rs, M, K, int(w_bits),
+                                  float(a_scale), int(a_zp), int(out_bits), arr, n, int(path),
+                                  _stream_ptr(stream)), "mq_qlinear_group")
+    return outs
 
 
 def mq_add_requant(x1, a1: float, z1: int, x2, a2: float, z2: int, ay: float, zy: int,

@@ -4,14 +4,14 @@ linears, 16-bit activations around the non-linear operators; Section 5.6:
 attention products between 16-bit and 8-bit activations).
 
     x1 = RMSNorm(h0)                  int16 -> int8
-    q, k, v = x1 Wq^T, x1 Wk^T, x1 Wv^T    -> int16, int16, int8
+    q, k, v = x1 Wq^T, x1 Wk^T, x1 Wv^T    -> int16, int16, int8 (q, k: one launch)
     q, k = RoPE(q), RoPE(k)                -> int16, int8
     s = q k^T per head (grouped keys)      -> int16 scores
     p = causal softmax(s / sqrt(64))       -> int16 probabilities
     c = p v per head                       -> int8 context
     h1 = h0 + c Wo^T                       -> int16
     x2 = RMSNorm(h1)                       -> int8
-    g, u = x2 Wg^T, x2 Wu^T                -> int16
+    g, u = x2 Wg^T, x2 Wu^T                -> int16 (one launch)
     m = SiLU(g) * u                        -> int16 table lookup, int8 product
     h2 = h1 + m Wd^T                       -> int16
 
@@ -91,6 +91,19 @@ class BlockGPU:
         self.mq.mq_qlinear(self.out[src], wq, 8, ws, cs, a, z, oa, oz, STAGE_BITS[stage],
                            out=self.out[stage], workspace=self.ws)
 
+    def _group(self, stages):
+        """Linears that read one input (and write one code width) in one
+        call: one launch on the prefill path, each output as _linear's."""
+        src = LINEARS[stages[0]][1]
+        a, z = self.fmt[src]
+        lin = []
+        for st in stages:
+            wq, ws, cs = self.w[LINEARS[st][0]]
+            oa, oz = self.fmt[st]
+            lin.append(dict(w_q=wq, w_scale=ws, w_colsum=cs, out_scale=oa, out_zp=oz,
+                            out=self.out[st]))
+        self.mq.mq_qlinear_group(self.out[src], lin, 8, a, z, STAGE_BITS[stages[0]])
+
     def stages(self):
         """(name, callable) per step of the block, in order; each callable
         only enqueues kernels on the current stream."""
@@ -103,8 +116,8 @@ class BlockGPU:
         return [
             ("rmsnorm1", lambda: mq.mq_rmsnorm(o["h0"], *f["h0"], self.gamma1, self.eps, *f["x1"],
                                                8, out=o["x1"])),
-            ("q_proj", lambda: self._linear("q")),
-            ("k_proj", lambda: self._linear("k")),
+            # q and k (16-bit outputs) in one launch; v writes 8-bit codes
+            ("qk_proj", lambda: self._group(("q", "k"))),
             ("v_proj", lambda: self._linear("v")),
             ("rope_q", lambda: mq.mq_rope_apply(o["q"], H, *f["q"], *f["qr"], self.rope_table,
                                                 16, out=o["qr"])),
@@ -131,8 +144,7 @@ class BlockGPU:
                                                              *f["h1"], self.gamma2, self.eps,
                                                              *f["x2"], 8, h=o["h1"],
                                                              out=o["x2"])),
-            ("gate_proj", lambda: self._linear("gate")),
-            ("up_proj", lambda: self._linear("up")),
+            ("gate_up_proj", lambda: self._group(("gate", "up"))),
             # SiLU table and gated product in one pass: the SiLU codes stay
             # in registers (the "silu" buffer is not written)
             ("silu_gated", lambda: mq.mq_lut_mul(o["gate"], self.lut, *f["silu"], o["up"],

@@ -507,6 +507,56 @@ mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M,
                         workspace_bytes, path, stream);
 }
 
+mq_status mq_qlinear_group(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
+                           int32_t w_bits, float a_scale, int32_t a_zp, int32_t out_bits,
+                           const mq_qlinear_out* outs, int32_t n_outs, int32_t path,
+                           void* stream)
+{
+    if (!outs || n_outs < 1 || n_outs > MQ_MAX_GROUP) return MQ_ERR_INVALID_ARG;
+    const bool asym = outs[0].w_zp != nullptr;
+    mq::QLinearArgs ps[MQ_MAX_GROUP];
+    int32_t resolved[MQ_MAX_GROUP];
+    // every linear is checked before anything is launched
+    for (int i = 0; i < n_outs; ++i) {
+        const mq_qlinear_out& o = outs[i];
+        if ((o.w_zp != nullptr) != asym) return MQ_ERR_INVALID_ARG;
+        const mq_status st = mq::qlinear_validate(
+            a_q, 8, a_rowsum, M, K, o.N, o.w_q, w_bits, o.w_scale, o.w_zp, o.w_colsum, a_scale,
+            a_zp, o.out_scale, o.out_zp, out_bits, o.bias, o.y_q, nullptr, 0, path, &ps[i],
+            &resolved[i]);
+        if (st != MQ_OK) return st;
+    }
+    const hipStream_t s = as_stream(stream);
+    // the linears with work; one launch when each of them would take the
+    // prefill kernel on its own
+    mq::GroupArgs g{};
+    int first = -1;
+    bool one_launch = true;
+    for (int i = 0; i < n_outs; ++i) {
+        const mq::QLinearArgs& p = ps[i];
+        if (p.M == 0 || p.N == 0) continue;
+        if (first < 0) first = i;
+        one_launch = one_launch && resolved[i] == MQ_PATH_PREFILL && mq::prefill_supported(p);
+        mq::GroupPart& gp = g.part[g.n++];
+        gp.w = p.w;
+        gp.w_scale = p.w_scale;
+        gp.colsum = p.colsum;
+        gp.bias = p.bias;
+        gp.w_zp = p.w_zp;
+        gp.y = p.y;
+        gp.N = p.N;
+        gp.out_scale = p.out_scale;
+        gp.out_zp = p.out_zp;
+    }
+    if (g.n == 0) return MQ_OK;
+    if (one_launch && g.n > 1) return from_hip(mq::launch_qlinear_prefill_group(ps[first], g, s));
+    for (int i = 0; i < n_outs; ++i) {
+        const mq_status st = mq::qlinear_dispatch(ps[i], resolved[i], s);
+        if (st != MQ_OK) return st;
+    }
+    return MQ_OK;
+}
+
 mq_status mq_qlinear(const int8_t* a_q, int64_t M, int64_t K, int64_t N, const void* w_q,
                      int32_t w_bits, const float* w_scale, const int32_t* w_colsum,
                      float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,

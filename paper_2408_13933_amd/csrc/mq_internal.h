@@ -56,6 +56,29 @@ struct QLinearArgs {
     int32_t force_tile = -1;
 };
 
+// Several linears on one activation input in one prefill launch: the
+// fields of each that differ (the shared ones stay in QLinearArgs).  tile0
+// and tiles_n are set by the launch: the linear's first tile index and its
+// tile columns.
+constexpr int kMaxGroup = MQ_MAX_GROUP;
+struct GroupPart {
+    const void* w;
+    const float* w_scale;
+    const int32_t* colsum;
+    const float* bias;
+    const int32_t* w_zp;
+    void* y;
+    int64_t N;
+    float out_scale;
+    int32_t out_zp;
+    int32_t tile0;
+    int32_t tiles_n;
+};
+struct GroupArgs {
+    GroupPart part[kMaxGroup];
+    int32_t n;
+};
+
 // Dense defaults of the stride fields.
 __host__ __device__ inline int64_t eff_lda(const QLinearArgs& p) { return p.lda ? p.lda : p.K; }
 __host__ __device__ inline int64_t eff_ldw(const QLinearArgs& p) { return p.ldw ? p.ldw : p.K; }
@@ -138,6 +161,9 @@ hipError_t launch_qlinear_decode(const QLinearArgs& p, hipStream_t s);
 hipError_t launch_qlinear_gemv(const QLinearArgs& p, hipStream_t s);
 bool gemv_supported(const QLinearArgs& p);
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s);
+// the linears of g on p's input (8-bit codes, dense, every part meeting
+// prefill_supported), one launch, no K split
+hipError_t launch_qlinear_prefill_group(const QLinearArgs& p, GroupArgs g, hipStream_t s);
 
 // Workspace bytes the prefill kernel would use to split K for this shape
 // (0 when it would not split).

@@ -135,12 +135,11 @@ struct Cfg {
         return n;
     }
     static constexpr int NSW = nsw();
-    // more than 12 accumulator fragments per wave (the four-wave 256x256
-    // tile: 256 registers) leave no registers for the slice bookkeeping of a
-    // K split or for the pre-shift epilogue forms
-    static constexpr bool BIG_ACC = FM * FN > 12;
-    // K slices (split-K) for the tiles with registers to spare
-    static constexpr bool SPLITK = !BIG_ACC && !A16;
+    // K slices (split-K) for the 8-bit activation tiles
+    static constexpr bool SPLITK = !A16;
+    // at most 12 accumulator fragments per wave leave registers for the
+    // slice bookkeeping of a K split and the pre-shift epilogue forms
+    static_assert(FM * FN <= 12, "accumulator registers");
     // split-K merge: fragment rows of the other slices' partial sums loaded
     // per batch (16 chunks, 64 registers in flight), never more than the
     // wave has, and a whole number of batches per wave
@@ -406,11 +405,14 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
     }
 }
 
-template <class C, bool ASYM>
-__global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLinearArgs p,
-                                                                       int tiles_n, int tiles_m,
-                                                                       int splits,
-                                                                       int kt_per_split)
+// One work-group's tile of the product.  GROUP: tiles of several linears
+// that share the activation input, one block per tile of any of them (g
+// holds each linear's weights, per-channel inputs, output and requant
+// constants, tiles_n the tile columns of all of them); p carries the shared
+// fields and takes those of the block's linear.
+template <class C, bool ASYM, bool GROUP>
+__device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g, int tiles_n,
+                                             int tiles_m, int splits, int kt_per_split)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
     constexpr int32_t qmax = (1 << (C::OBITS - 1)) - 1;
@@ -446,7 +448,25 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
             b = (int)((b + (int64_t)(blockIdx.y % 8) * per) % items);
     }
     const int split = C::SPLITK ? b / total : 0;
-    const int tile = C::SPLITK ? b % total : b;
+    int tile = C::SPLITK ? b % total : b;
+    if constexpr (GROUP) {
+        // the linear whose tile columns hold this tile (block-uniform)
+        int k = 0;
+#pragma unroll
+        for (int i = 1; i < kMaxGroup; ++i)
+            if (i < g->n && tile >= g->part[i].tile0) k = i;
+        const GroupPart& gp = g->part[k];
+        p.w = gp.w;
+        p.w_scale = gp.w_scale;
+        p.colsum = gp.colsum;
+        p.bias = gp.bias;
+        p.w_zp = gp.w_zp;
+        p.y = gp.y;
+        p.N = gp.N;
+        p.out_scale = gp.out_scale;
+        p.out_zp = gp.out_zp;
+        tile -= gp.tile0;
+    }
     const int tn = tile / tiles_m;
     const int tm = tile % tiles_m;
     const int64_t n_tile = (int64_t)tn * C::TN;
@@ -640,11 +660,9 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
     const bool zp_fold = (flags & 2) != 0;
     // the fast epilogue form: one mul_hi per output, zero-point in the
     // rounding constant, off in the accumulator's start value; pre0: no
-    // column of the tile needs the pre-shift.  The four-wave 256x256 tile
-    // has no registers left for the pre-shift forms.
-    constexpr bool kPreForms = !C::BIG_ACC;
+    // column of the tile needs the pre-shift
     const bool pre0 = (flags & 1) != 0;
-    const bool fast = (kPreForms ? (flags & 6) == 6 : flags == 7) && (p.N % 4) == 0;
+    const bool fast = (flags & 6) == 6 && (p.N % 4) == 0;
     if (zp_fold && tid < C::TN) e_rnd[tid] += p.out_zp * (1 << (e_sp[tid] & 0xFF));
     // stage STAGES-1: the part the stage switch step would issue; the rest
     // goes out during the first stage's steps, as for every later stage
@@ -949,16 +967,27 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
     // staged stores need the tile's channels inside N and 16-byte row chunks
     const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
                         ((uintptr_t)y_batch % 16) == 0;
-    if constexpr (kPreForms) {
-        if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true>(acc, acc2, ctx);
-        else if (staged) prefill_epilogue<C, ASYM, true, true, true>(acc, acc2, ctx);
-        else if (fast) prefill_epilogue<C, ASYM, true, true, false>(acc, acc2, ctx);
-        else prefill_epilogue<C, ASYM, false, false, false>(acc, acc2, ctx);
-    } else {
-        if (staged) prefill_epilogue<C, ASYM, true, false, true>(acc, acc2, ctx);
-        else if (fast) prefill_epilogue<C, ASYM, true, false, false>(acc, acc2, ctx);
-        else prefill_epilogue<C, ASYM, false, false, false>(acc, acc2, ctx);
-    }
+    if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true>(acc, acc2, ctx);
+    else if (staged) prefill_epilogue<C, ASYM, true, true, true>(acc, acc2, ctx);
+    else if (fast) prefill_epilogue<C, ASYM, true, true, false>(acc, acc2, ctx);
+    else prefill_epilogue<C, ASYM, false, false, false>(acc, acc2, ctx);
+}
+
+template <class C, bool ASYM>
+__global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLinearArgs p,
+                                                                       int tiles_n, int tiles_m,
+                                                                       int splits,
+                                                                       int kt_per_split)
+{
+    prefill_body<C, ASYM, false>(p, nullptr, tiles_n, tiles_m, splits, kt_per_split);
+}
+
+// several linears on one input, without a K split (kt: K stages)
+template <class C, bool ASYM>
+__global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_group_kernel(
+    QLinearArgs p, GroupArgs g, int tiles_n, int tiles_m, int kt)
+{
+    prefill_body<C, ASYM, true>(p, &g, tiles_n, tiles_m, 1, kt);
 }
 
 template <class C, bool ASYM>
@@ -983,17 +1012,42 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
     return hipGetLastError();
 }
 
-// Tile shapes, largest first.  (tokens x channels, wave grid, K bytes per
-// stage, stages, swizzle, steps the DMA of a stage is spread over; measured:
-// the 256x256 K loop is fastest with all DMA in the switch step, the
-// 128-deep tiles with it spread over the whole stage)
-template <int WB, int OB> using T256x256 = Cfg<WB, OB, 256, 256, 2, 2, 64, 4, 2, 1>;
+template <class C, bool ASYM>
+hipError_t launch_group_cfg(const QLinearArgs& p, GroupArgs g, hipStream_t s)
+{
+    const int64_t tiles_m = (p.M + C::TM - 1) / C::TM;
+    int64_t cols = 0;
+    for (int i = 0; i < g.n; ++i) {
+        g.part[i].tile0 = (int32_t)(cols * tiles_m);
+        g.part[i].tiles_n = (int32_t)((g.part[i].N + C::TN - 1) / C::TN);
+        cols += g.part[i].tiles_n;
+        if (cols * tiles_m > 0x7FFFFFFF) return hipErrorInvalidValue;
+    }
+    const int64_t kt = (p.K + C::BK - 1) / C::BK;
+    constexpr int lds = ASYM ? C::LDS_ASYM : C::LDS;
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&qlinear_prefill_group_kernel<C, ASYM>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (attr != hipSuccess) return attr;
+    qlinear_prefill_group_kernel<C, ASYM><<<dim3((unsigned)(cols * tiles_m)), dim3(C::THREADS),
+                                            lds, s>>>(p, g, (int)cols, (int)tiles_m, (int)kt);
+    return hipGetLastError();
+}
+
+// Tile shapes.  (tokens x channels, wave grid, K bytes per stage, stages,
+// swizzle, steps the DMA of a stage is spread over; measured: the
+// 128-deep four-wave tiles are fastest with the DMA spread over the whole
+// stage.)  A four-wave 256x256 tile (4x4 fragments per wave, 256
+// accumulator registers, no K split) was slower than the eight-wave one on
+// every measured shape and is gone.
 template <int WB, int OB> using T256x128 = Cfg<WB, OB, 256, 128, 2, 2, 128, 3, 2, 4>;
+constexpr int kTile256x128 = 0;
 template <int WB, int OB> using T128x128 = Cfg<WB, OB, 128, 128, 2, 2, 128, 4, 2, 4>;
+constexpr int kTile128x128 = 1;
 // 64x64: layers with few output tiles (1024 tokens x 256 channels: 64
 // tiles instead of 16), four waves of 32x32
 template <int WB, int OB> using T64x64 = Cfg<WB, OB, 64, 64, 2, 2, 128, 4, 2, 4>;
-constexpr int kTile64x64 = 4;
+constexpr int kTile64x64 = 3;
 // 192 tokens x 256 channels: 3/4 of the 256x256 tile's work per block, so a
 // layer whose 256x256 tiles leave CUs idle (2048 x 5632: 176 tiles on 256
 // CUs) fills more of the chip (242 tiles).  Eight waves, two per SIMD, each
@@ -1008,15 +1062,13 @@ constexpr int kTile64x64 = 4;
 template <int WB, int OB>
 using T192x256 = std::conditional_t<WB == 8, Cfg<WB, OB, 192, 256, 2, 4, 128, 2, 2, 2>,
                                     Cfg<WB, OB, 192, 256, 2, 2, 64, 4, 2, 1>>;
+constexpr int kTile192x256 = 2;
 // 256x256 with eight waves, two per SIMD, each 128 tokens x 64 channels (4x2
 // fragments: 8 MFMAs per 6 fragment reads from LDS, against 6 per 5 for the
 // 192x256 tile's 3x2), two 128-deep stages.  128 accumulator registers per
 // wave leave room for the K split and the pre-shift epilogue forms.
 template <int WB, int OB> using T256x256W8 = Cfg<WB, OB, 256, 256, 2, 4, 128, 2, 2, 2>;
-constexpr int kTile256x256W8 = 5;
-static_assert(!T256x256<8, 8>::SPLITK && T256x256W8<8, 16>::SPLITK &&
-                  T256x256W8<4, 16>::SPLITK && T192x256<4, 8>::SPLITK,
-              "split-capable tiles");
+constexpr int kTile256x256W8 = 4;
 // 16-bit activation codes: 128x128 tokens x channels, 64 k per stage (128
 // bytes of each activation row), DMA spread over both steps of a stage
 template <int OB> using T128x128A16 = Cfg<8, OB, 128, 128, 2, 2, 64, 4, 2, 2, 16>;
@@ -1055,7 +1107,6 @@ struct TileModel {
     bool splits = true;  // whether the tile takes a K split
 };
 constexpr TileModel kTiles[] = {
-    {256, 256, 64, 13.4, 0.531, 1, false},
     {256, 128, 128, 8.05, 0.593},
     {128, 128, 128, 5.58, 0.348},
     {192, 256, 128, 6.98, 0.845},  // eight waves, two 128-deep stages (int8 weights)
@@ -1066,6 +1117,13 @@ constexpr TileModel kTiles[] = {
 constexpr TileModel kTile192x256W4 = {192, 256, 64, 8.0, 0.45};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 static_assert(kNumTiles == MQ_PREFILL_TILES, "one explicit path per tile");
+static_assert(kTiles[kTile256x128].tn == T256x128<8, 8>::TN &&
+                  kTiles[kTile128x128].tm == T128x128<8, 8>::TM &&
+                  kTiles[kTile192x256].tm == T192x256<8, 8>::TM &&
+                  kTiles[kTile64x64].tm == T64x64<8, 8>::TM &&
+                  kTiles[kTile256x256W8].tn == T256x256W8<8, 8>::TN &&
+                  kTiles[kTile256x256W8].bk == T256x256W8<8, 8>::BK,
+              "the time model's rows follow the tile indices");
 constexpr double kBusySlowdown = 0.60;
 // int4 weights: the in-register unpack makes a K-loop stage ~1.35x longer
 constexpr double kInt4StageFactor = 1.35;
@@ -1082,7 +1140,9 @@ struct Choice {
     int tile, splits;
 };
 
-Choice choose(const QLinearArgs& p, bool can_split)
+// Ns: the output channels of each linear sharing the launch (one group of
+// tiles per linear), or nullptr for p.N alone
+Choice choose(const QLinearArgs& p, bool can_split, const int64_t* Ns = nullptr, int nN = 1)
 {
     Choice best{0, 1};
     double best_t = 1e300;
@@ -1090,8 +1150,10 @@ Choice choose(const QLinearArgs& p, bool can_split)
     const int only = p.force_tile >= 0 && p.force_tile < kNumTiles ? p.force_tile : -1;
     for (int c = 0; c < kNumTiles; ++c) {
         if (only >= 0 && c != only) continue;
-        const TileModel& t = c == 3 && p.w_bits == 4 ? kTile192x256W4 : kTiles[c];
-        const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * ((p.N + t.tn - 1) / t.tn);
+        const TileModel& t = c == kTile192x256 && p.w_bits == 4 ? kTile192x256W4 : kTiles[c];
+        int64_t cols = 0;
+        for (int i = 0; i < nN; ++i) cols += ((Ns ? Ns[i] : p.N) + t.tn - 1) / t.tn;
+        const int64_t tiles = ((p.M + t.tm - 1) / t.tm) * cols;
         const int64_t kt = (p.K + t.bk - 1) / t.bk;
         const int64_t slots = (int64_t)kCUs * t.occ;
         for (int sp = 1; sp <= (can_split && t.splits ? kMaxSplits : 1); sp *= 2) {
@@ -1131,9 +1193,8 @@ hipError_t launch_a(const QLinearArgs& p, hipStream_t s)
     Choice ch = choose(p, p.ws != nullptr);
     if (ch.splits > 1 && workspace_for(p, ch) > p.ws_bytes) ch = choose(p, false);
     switch (ch.tile) {
-    case 0: return launch_cfg<T256x256<WB, OB>, ASYM>(p, ch.splits, s);
-    case 1: return launch_cfg<T256x128<WB, OB>, ASYM>(p, ch.splits, s);
-    case 3: return launch_cfg<T192x256<WB, OB>, ASYM>(p, ch.splits, s);
+    case kTile256x128: return launch_cfg<T256x128<WB, OB>, ASYM>(p, ch.splits, s);
+    case kTile192x256: return launch_cfg<T192x256<WB, OB>, ASYM>(p, ch.splits, s);
     case kTile64x64: return launch_cfg<T64x64<WB, OB>, ASYM>(p, ch.splits, s);
     case kTile256x256W8: return launch_cfg<T256x256W8<WB, OB>, ASYM>(p, ch.splits, s);
     default: return launch_cfg<T128x128<WB, OB>, ASYM>(p, ch.splits, s);
@@ -1144,6 +1205,28 @@ template <int WB, int OB>
 hipError_t launch_t(const QLinearArgs& p, hipStream_t s)
 {
     return p.w_zp ? launch_a<WB, OB, true>(p, s) : launch_a<WB, OB, false>(p, s);
+}
+
+template <int WB, int OB, bool ASYM>
+hipError_t launch_group_a(const QLinearArgs& p, const GroupArgs& g, hipStream_t s)
+{
+    int64_t Ns[kMaxGroup];
+    for (int i = 0; i < g.n; ++i) Ns[i] = g.part[i].N;
+    const Choice ch = choose(p, false, Ns, g.n);
+    switch (ch.tile) {
+    case kTile256x128: return launch_group_cfg<T256x128<WB, OB>, ASYM>(p, g, s);
+    case kTile192x256: return launch_group_cfg<T192x256<WB, OB>, ASYM>(p, g, s);
+    case kTile64x64: return launch_group_cfg<T64x64<WB, OB>, ASYM>(p, g, s);
+    case kTile256x256W8: return launch_group_cfg<T256x256W8<WB, OB>, ASYM>(p, g, s);
+    default: return launch_group_cfg<T128x128<WB, OB>, ASYM>(p, g, s);
+    }
+}
+
+template <int WB, int OB>
+hipError_t launch_group_t(const QLinearArgs& p, const GroupArgs& g, hipStream_t s)
+{
+    return p.w_zp ? launch_group_a<WB, OB, true>(p, g, s)
+                  : launch_group_a<WB, OB, false>(p, g, s);
 }
 
 }  // namespace
@@ -1209,6 +1292,15 @@ hipError_t launch_a16(const QLinearArgs& p, hipStream_t s)
                       : launch_cfg<T128x128A16<16>, true>(p, 1, s);
     return o8 ? launch_cfg<T128x128A16<8>, false>(p, 1, s)
               : launch_cfg<T128x128A16<16>, false>(p, 1, s);
+}
+
+hipError_t launch_qlinear_prefill_group(const QLinearArgs& p, GroupArgs g, hipStream_t s)
+{
+    if (p.a_bits != 8 || g.n < 1 || g.n > kMaxGroup) return hipErrorInvalidValue;
+    if (p.w_bits == 8 && p.out_bits == 8) return launch_group_t<8, 8>(p, g, s);
+    if (p.w_bits == 8) return launch_group_t<8, 16>(p, g, s);
+    if (p.out_bits == 8) return launch_group_t<4, 8>(p, g, s);
+    return launch_group_t<4, 16>(p, g, s);
 }
 
 hipError_t launch_qlinear_prefill(const QLinearArgs& p, hipStream_t s)

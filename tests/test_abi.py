@@ -73,6 +73,54 @@ def test_qlinear_rejects_invalid_arguments(kw):
     assert qlin(**kw) == 1
 
 
+def qlin_group(parts=None, n=None, **kw):
+    """mq_qlinear_group with fake pointers; ``parts``: per-linear overrides."""
+    a = dict(a_q=NZ, a_rowsum=None, M=4, K=64, w_bits=8, a_scale=0.1, a_zp=0, out_bits=8,
+             path=0, stream=None)
+    a.update(kw)
+    parts = [{}, {}] if parts is None else parts
+    arr = (mq.QLinearOut * max(1, len(parts)))()
+    for i, over in enumerate(parts):
+        d = dict(w_q=NZ, w_scale=NZ, w_zp=None, w_colsum=NZ, bias=None, N=8, out_scale=0.1,
+                 out_zp=0, y_q=NZ)
+        d.update(over)
+        arr[i] = mq.QLinearOut(d["w_q"], d["w_scale"], d["w_zp"], d["w_colsum"], d["bias"],
+                               d["N"], d["out_scale"], d["out_zp"], d["y_q"])
+    return mq.lib().mq_qlinear_group(a["a_q"], a["a_rowsum"], a["M"], a["K"], a["w_bits"],
+                                     a["a_scale"], a["a_zp"], a["out_bits"],
+                                     arr if parts else None, len(parts) if n is None else n,
+                                     a["path"], a["stream"])
+
+
+def test_qlinear_out_layout():
+    # the C struct: five pointers, int64 N, float, int32, pointer (64 bytes)
+    assert ctypes.sizeof(mq.QLinearOut) == 64
+    assert mq.QLinearOut.N.offset == 40 and mq.QLinearOut.y_q.offset == 56
+    text = open(HEADER).read()
+    assert re.search(r"#define MQ_MAX_GROUP (\d+)", text).group(1) == str(mq.MAX_GROUP)
+
+
+@pytest.mark.parametrize("case", [
+    dict(parts=[]), dict(n=0), dict(n=-1), dict(parts=[{}] * 5),
+    dict(parts=[{}, {"w_zp": NZ}]),                              # asymmetric mixed with symmetric
+    dict(parts=[{"w_zp": NZ}, {"w_zp": NZ}]),                    # asymmetric without row sums
+    dict(parts=[{}, {}], a_rowsum=NZ),                            # row sums without zero-points
+    dict(parts=[{}, {"out_scale": 0.0}]), dict(parts=[{"y_q": None}, {}]),
+    dict(parts=[{}, {"N": -1}]), dict(parts=[{}, {"out_zp": 200}]),
+    dict(K=0), dict(M=-1), dict(w_bits=2), dict(out_bits=4), dict(a_scale=float("nan")),
+    dict(path=1, M=17), dict(path=16 + mq.PREFILL_TILES), dict(a_q=None),
+], ids=str)
+def test_qlinear_group_rejects_invalid_arguments(case):
+    assert qlin_group(**case) == 1
+
+
+def test_qlinear_group_nothing_to_do():
+    # no linear with work: nothing enqueued, no device touched
+    assert qlin_group(M=0) == 0
+    assert qlin_group(parts=[{"N": 0}, {"N": 0}]) == 0
+    assert qlin_group(parts=[{"N": 0}], M=0, a_q=None) == 0
+
+
 def qlin_noalloc(**kw):
     a = dict(a_q=NZ, M=4, K=64, N=8, w_q=NZ, w_bits=8, w_scale=NZ, w_colsum=NZ, a_scale=0.1,
              a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None, y_q=NZ, stream=None)
