@@ -3,9 +3,11 @@
 One step = one pass of the hot path over one batch of a workload's
 synthetic, seeded inputs: quantize each distinct layer input (Section 4.2,
 Eq.(4)), run every qlinear of the workload with its fused fixed-point
-requant epilogue, and dequantize the last layer's output.  The layers that
-read one input and write one code width (gate and up) go out as one
-mq_qlinear_group launch (--no-group: one launch per layer).  Weights are
+requant epilogue, and dequantize the last layer's output (written by that
+layer's own epilogue through mq_qlinear_dequant; --no-fuse-dequant: a pass
+of its own over the stored codes).  The layers that read one input and
+write one code width (gate and up) go out as one mq_qlinear_group launch
+(--no-group: one launch per layer).  Weights are
 folded/packed once before timing (offline steps).
 
 The default workload is the Gemma-2B-shaped one (the largest of the layer
@@ -75,6 +77,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fuse-dequant", action="store_true",
+                    help="dequantize the last layer's codes in a pass of their own (by default "
+                         "the last launch, mq_qlinear_dequant, writes the fp32 output itself)")
     ap.add_argument("--no-group", action="store_true",
                     help="launch every layer on its own (by default the layers that read one "
                          "quantized input and write one code width go out as one "
@@ -165,13 +170,17 @@ def launch_groups(workload, layers, group=True, max_group=4):
     return out
 
 
-def launch_alg_bytes(layers, idx):
+def launch_alg_bytes(layers, idx, f32_out=False):
     """Minimum bytes one launch moves: its shared input (and row sums) once,
-    each layer's weights, outputs and per-channel parameters."""
+    each layer's weights, outputs and per-channel parameters; f32_out: the
+    output written as fp32 values instead of codes (fused dequantization)."""
     Ls = [layers[i] for i in idx]
     F = Ls[0]
     shared = F.M * F.K * F.a_bits // 8 + (F.M * 4 if F.asym else 0)
-    return sum(L.alg_bytes() for L in Ls) - (len(Ls) - 1) * shared
+    b = sum(L.alg_bytes() for L in Ls) - (len(Ls) - 1) * shared
+    if f32_out:
+        b += sum(L.M * L.N * (4 - L.out_bits // 8) for L in Ls)
+    return b
 
 
 def launch_label(layers, idx):
@@ -180,7 +189,7 @@ def launch_label(layers, idx):
             f"N={'+'.join(str(L.N) for L in Ls)}")
 
 
-def pmc_summary(fetch_csv, write_csv, copy_mib, workload, group=True):
+def pmc_summary(fetch_csv, write_csv, copy_mib, workload, group=True, fuse_dequant=True):
     """HBM bytes per launch of the dominant prefill kernel and of each
     decode-shaped layer, each counter scaled by what it reads for the plain
     copy of known size in the same run."""
@@ -192,6 +201,8 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload, group=True):
     launches = launch_groups(workload, layers, group)
     dom = max(launches, key=lambda idx: sum(layers[i].ops for i in idx))
     L = layers[dom[0]]
+    # the step's last launch writes fp32 outputs when the dequantization is fused
+    f32 = fuse_dequant and dom is launches[-1] and len(dom) == 1 and L.a_bits == 8
     per = {}
     for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         rows = _pmc_rows(path, counter)
@@ -227,8 +238,9 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload, group=True):
     pre = {k: v for k, v in per["fetch"][0].items() if "qlinear_prefill" in k[0]}
     (kname, grid), _ = max(pre.items(), key=lambda kv: sum(kv[1]) / len(kv[1]))
     res = {"workload": workload, "source_hash": kernel_source_hash(), "copy_mib": copy_mib,
-           "prefill": dict(layer=f"{launch_label(layers, dom)} w{L.w_bits}/o{L.out_bits}",
-                           **entry(kname, grid, launch_alg_bytes(layers, dom))),
+           "prefill": dict(layer=f"{launch_label(layers, dom)} w{L.w_bits}/o{L.out_bits}"
+                                 + (" fp32 out" if f32 else ""),
+                           **entry(kname, grid, launch_alg_bytes(layers, dom, f32))),
            "decode": []}
     # decode layers: the decode (kernel, grid) with their weight and output
     # widths (template arguments), the most dispatched group of each
@@ -380,7 +392,7 @@ class TimingEvent:
 class Prepared:
     """Device-resident inputs and packed weights of one workload."""
 
-    def __init__(self, workload_name, group=True):
+    def __init__(self, workload_name, group=True, fuse_dequant=True):
         import torch
 
         import paper_2408_13933_amd as mq
@@ -446,6 +458,10 @@ class Prepared:
         # launches: gate/up (q/k/v) as one mq_qlinear_group call each
         self.launches = launch_groups(workload_name, [e["layer"] for e in self.layers], group,
                                       mq.MAX_GROUP)
+        # the last launch writes the step's dequantized output itself (its
+        # codes feed nothing else), unless fuse_dequant is off
+        L = last["layer"]
+        self.fuse_dequant = (fuse_dequant and len(self.launches[-1]) == 1 and L.a_bits == 8)
         torch.cuda.synchronize()
 
     def qlinear(self, e, w_q=None, workspace=None):
@@ -472,6 +488,16 @@ class Prepared:
         """Launch j (one layer, or a group of layers on one input) on its
         already quantized input."""
         idx = self.launches[j]
+        if j == len(self.launches) - 1 and self.fuse_dequant:
+            e = self.layers[idx[0]]
+            L = e["layer"]
+            inp = self.inputs[e["key"]]
+            self.mq.mq_qlinear_dequant(inp["q"], e["w_q"], L.w_bits, e["w_scale"], e["w_colsum"],
+                                       e["a_scale"], e["a_zp"], e["out_scale"], e["out_zp"],
+                                       L.out_bits, bias=e["bias"], out=self.deq, w_zp=e["w_zp"],
+                                       a_rowsum=inp["rs"] if L.asym else None,
+                                       workspace=self.workspace)
+            return
         if len(idx) == 1:
             self.qlinear(self.layers[idx[0]], workspace=self.workspace)
             return
@@ -504,8 +530,9 @@ class Prepared:
             self.launch(j)
             if events is not None:
                 events[j + 1].record()
-        last = self.layers[-1]
-        mq.mq_dequant(last["y"], last["out_scale"], last["out_zp"], out=self.deq)
+        if not self.fuse_dequant:
+            last = self.layers[-1]
+            mq.mq_dequant(last["y"], last["out_scale"], last["out_zp"], out=self.deq)
 
 
 def cold_graph_us(prep: Prepared, i: int, min_bytes: int = 512 * 10**6, replays: int = 5):
@@ -981,7 +1008,8 @@ def main():
             raise SystemExit("--pmc-summary needs the --calib-copy-mib size of the profiled run")
         print(json.dumps(pmc_summary(args.pmc_summary[0], args.pmc_summary[1],
                                      args.calib_copy_mib, args.workload,
-                                     group=not args.no_group)))
+                                     group=not args.no_group,
+                                     fuse_dequant=not args.no_fuse_dequant)))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "the qlinear path is measured on one GPU only (its multi-GPU "
@@ -989,7 +1017,8 @@ def main():
         sys.exit(2)
     import torch
 
-    prep = Prepared(args.workload, group=not args.no_group)
+    prep = Prepared(args.workload, group=not args.no_group,
+                    fuse_dequant=not args.no_fuse_dequant)
     layers = [e["layer"] for e in prep.layers]
     ops_step = sum(L.ops for L in layers)
     # operations of each launch (a layer, or a group of layers on one input)
@@ -1042,10 +1071,12 @@ def main():
         "config": {"workload": args.workload,
                    "layers": [f"{l.name} M={l.M} K={l.K} N={l.N} w{l.w_bits} o{l.out_bits}"
                               for l in layers],
-                   "step": "quantize inputs + %d qlinear launches (%s) + dequant of last output"
+                   "step": "quantize inputs + %d qlinear launches (%s) + dequant of last output%s"
                            % (len(prep.launches),
                               ", ".join(prep.launch_name(j).split(" ")[0]
-                                        for j in range(len(prep.launches)))),
+                                        for j in range(len(prep.launches))),
+                              " (written by the last launch's epilogue)" if prep.fuse_dequant
+                              else " (its own pass)"),
                    "ops_per_step": ops_step},
     }
     tr = read_traffic(args.workload)
@@ -1082,7 +1113,9 @@ def main():
         achieved = launch_ops[dom] / (k_us * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                 "frac": achieved / PEAK_INT8_TOPS, "traffic": None}
-        if tr is not None and tr["prefill"]["layer"].startswith(prep.launch_name(dom) + " "):
+        f32 = prep.fuse_dequant and dom == len(prep.launches) - 1
+        if (tr is not None and tr["prefill"]["layer"].startswith(prep.launch_name(dom) + " ") and
+                tr["prefill"]["layer"].endswith(" fp32 out") == f32):
             t = tr["prefill"]
             roof["traffic"] = t["hbm_bytes_per_launch"]
             roof["traffic_detail"] = {"unit": "bytes per launch",
@@ -1090,7 +1123,7 @@ def main():
                                       "write": t["write"]["bytes_per_launch"],
                                       "algorithmic": t["alg_bytes_per_launch"]}
         roof.update({"kernel": f"qlinear_prefill {prep.launch_name(dom)} "
-                               f"w{L.w_bits}/o{L.out_bits}",
+                               f"w{L.w_bits}/o{L.out_bits}" + (" fp32 out" if f32 else ""),
                      "ops_per_launch": launch_ops[dom], "kernel_us": k_us})
         if k_graph_us is not None:
             roof["kernel_us_graph_replay"] = k_graph_us

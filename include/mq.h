@@ -321,6 +321,28 @@ mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M,
                           const float* bias, void* y_q, void* workspace,
                           int64_t workspace_bytes, int32_t path, void* stream);
 
+/*
+ * mq_qlinear_dequant -- mq_qlinear_ws (mq_qlinear_asym when w_zp and
+ * a_rowsum are set) whose epilogue also writes the dequantized outputs,
+ *   y[m][n] = out_scale * (float)(Y_q[m][n] - out_zp)
+ * (the inverse of Eq.(4): mq_dequant of the codes, bit for bit), and the
+ * codes Y_q themselves only when y_q is not NULL: for a layer whose codes
+ * only feed the dequantization (the logits of the LM head), one pass
+ * instead of a qlinear, a store of the codes and a dequantization pass
+ * reading them back.
+ *   y         device fp32 [M][N] (16-byte aligned with N % 4 == 0 for the
+ *             tuned kernels); must not overlap the inputs or y_q
+ *   y_q       device [M][N] codes (out_bits), or NULL
+ *   a_rowsum, w_zp  both NULL (symmetric weights) or as for mq_qlinear_asym
+ *   everything else as in mq_qlinear_ws.
+ */
+mq_status mq_qlinear_dequant(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
+                             int64_t N, const void* w_q, int32_t w_bits, const float* w_scale,
+                             const int32_t* w_zp, const int32_t* w_colsum, float a_scale,
+                             int32_t a_zp, float out_scale, int32_t out_zp, int32_t out_bits,
+                             const float* bias, void* y_q, float* y, void* workspace,
+                             int64_t workspace_bytes, int32_t path, void* stream);
+
 /* Most linears one mq_qlinear_group call takes. */
 #define MQ_MAX_GROUP 4
 

@@ -21,7 +21,7 @@ __all__ = [
     "mq_qlinear_workspace_bytes", "mq_qlinear_noalloc", "NOALLOC_SCRATCH_BYTES",
     "PATH_AUTO", "PATH_DECODE", "PATH_PREFILL", "PATH_GENERIC", "MAX_K",
     "PATH_PREFILL_TILE0", "PREFILL_TILES", "prefill_tile_path", "mq_probe_read",
-    "mq_qlinear_group", "MAX_GROUP", "QLinearOut",
+    "mq_qlinear_group", "MAX_GROUP", "QLinearOut", "mq_qlinear_dequant",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -139,9 +139,12 @@ def lib():
                                  c_i64, c_i64, c_i64, c_p, c_i64, c_i32, c_p]
     L.mq_transpose_i8.argtypes = [c_p, c_i64, c_i64, c_i64, c_p, c_p]
     L.mq_probe_read.argtypes = [c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_p]
+    L.mq_qlinear_dequant.argtypes = [c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i32, c_p, c_p, c_p,
+                                     c_f, c_i32, c_f, c_i32, c_i32, c_p, c_p, c_p, c_p, c_i64,
+                                     c_i32, c_p]
     L.mq_qlinear_group.argtypes = [c_p, c_p, c_i64, c_i64, c_i32, c_f, c_i32, c_i32,
                                    ctypes.POINTER(QLinearOut), c_i32, c_i32, c_p]
-    for name in ("mq_qlinear_group", "mq_probe_read", "mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
+    for name in ("mq_qlinear_dequant", "mq_qlinear_group", "mq_probe_read", "mq_attn_matmul", "mq_transpose_i8", "mq_act_params", "mq_fold_weights", "mq_fold_acts", "mq_quantize_act",
                  "mq_pack_weights", "mq_qlinear", "mq_qlinear_ex", "mq_qlinear_ws", "mq_dequant",
                  "mq_qlinear_noalloc",
                  "mq_pack_weights_asym", "mq_act_rowsum", "mq_quantize_act_rowsum",
@@ -356,6 +359,33 @@ def mq_qlinear_asym(a_q, a_rowsum, w_q, w_bits: int, w_scale, w_zp, w_colsum, a_
         float(a_scale), int(a_zp), float(out_scale), int(out_zp), int(out_bits), bptr,
         _dev_ptr(out, _act_dtype(out_bits), "out", (M, N)), ws, ws_bytes, int(path),
         _stream_ptr(stream)), "mq_qlinear_asym")
+    return out
+
+
+def mq_qlinear_dequant(a_q, w_q, w_bits: int, w_scale, w_colsum, a_scale: float, a_zp: int,
+                       out_scale: float, out_zp: int, out_bits: int = 8, bias=None, out=None,
+                       codes=None, w_zp=None, a_rowsum=None, path: int = PATH_AUTO,
+                       stream=None, workspace=None):
+    """Integer-only linear layer whose epilogue writes the dequantized
+    outputs (fp32 ``out``, mq_dequant of the codes bit for bit) and the
+    codes only into ``codes`` when given."""
+    torch = _torch()
+    M, K = a_q.shape
+    N = w_q.shape[0]
+    wq_dtype, wq_shape = (torch.int8, (N, K)) if w_bits == 8 else (torch.uint8, (N, K // 2))
+    out = torch.empty((M, N), dtype=torch.float32, device=a_q.device) if out is None else out
+    bptr = None if bias is None else _dev_ptr(bias, torch.float32, "bias", (N,))
+    cptr = None if codes is None else _dev_ptr(codes, _act_dtype(out_bits), "codes", (M, N))
+    zptr = None if w_zp is None else _dev_ptr(w_zp, torch.int32, "w_zp", (N,))
+    rptr = None if a_rowsum is None else _dev_ptr(a_rowsum, torch.int32, "a_rowsum", (M,))
+    ws, ws_bytes = _workspace_args(workspace)
+    _check(lib().mq_qlinear_dequant(
+        _dev_ptr(a_q, torch.int8, "a_q"), rptr, M, K, N, _dev_ptr(w_q, wq_dtype, "w_q", wq_shape),
+        int(w_bits), _dev_ptr(w_scale, torch.float32, "w_scale", (N,)), zptr,
+        _dev_ptr(w_colsum, torch.int32, "w_colsum", (N,)), float(a_scale), int(a_zp),
+        float(out_scale), int(out_zp), int(out_bits), bptr, cptr,
+        _dev_ptr(out, torch.float32, "out", (M, N)), ws, ws_bytes, int(path),
+        _stream_ptr(stream)), "mq_qlinear_dequant")
     return out
 
 

@@ -389,7 +389,7 @@ mq_status qlinear_validate(const void* a_q, int32_t a_bits, const int32_t* a_row
                            float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
                            int32_t out_bits, const float* bias, void* y_q, void* workspace,
                            int64_t workspace_bytes, int32_t path, QLinearArgs* out,
-                           int32_t* path_out)
+                           int32_t* path_out, float* y_f)
 {
     if (workspace_bytes < 0) return MQ_ERR_INVALID_ARG;
     if (workspace && ((uintptr_t)workspace % 256) != 0) return MQ_ERR_INVALID_ARG;
@@ -412,8 +412,9 @@ mq_status qlinear_validate(const void* a_q, int32_t a_bits, const int32_t* a_row
     p.K = K;
     p.N = N;
     if (M == 0 || N == 0) return MQ_OK;
-    if (!a_q || !w_q || !w_scale || !w_colsum || !y_q) return MQ_ERR_INVALID_ARG;
+    if (!a_q || !w_q || !w_scale || !w_colsum || (!y_q && !y_f)) return MQ_ERR_INVALID_ARG;
     if ((w_zp == nullptr) != (a_rowsum == nullptr)) return MQ_ERR_INVALID_ARG;
+    if (y_f && a_bits != 8) return MQ_ERR_INVALID_ARG;
 
     p.a = static_cast<const int8_t*>(a_q);
     p.a_bits = a_bits;
@@ -422,6 +423,7 @@ mq_status qlinear_validate(const void* a_q, int32_t a_bits, const int32_t* a_row
     p.colsum = w_colsum;
     p.bias = bias;
     p.y = y_q;
+    p.y_f = y_f;
     p.a_scale = a_scale;
     p.out_scale = out_scale;
     p.a_zp = a_zp;
@@ -505,6 +507,24 @@ mq_status mq_qlinear_asym(const int8_t* a_q, const int32_t* a_rowsum, int64_t M,
     return qlinear_impl(a_q, 8, a_rowsum, M, K, N, w_q, w_bits, w_scale, w_zp, w_colsum,
                         a_scale, a_zp, out_scale, out_zp, out_bits, bias, y_q, workspace,
                         workspace_bytes, path, stream);
+}
+
+mq_status mq_qlinear_dequant(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,
+                             int64_t N, const void* w_q, int32_t w_bits, const float* w_scale,
+                             const int32_t* w_zp, const int32_t* w_colsum, float a_scale,
+                             int32_t a_zp, float out_scale, int32_t out_zp, int32_t out_bits,
+                             const float* bias, void* y_q, float* y, void* workspace,
+                             int64_t workspace_bytes, int32_t path, void* stream)
+{
+    if (M > 0 && N > 0 && !y) return MQ_ERR_INVALID_ARG;
+    mq::QLinearArgs p;
+    int32_t resolved = MQ_PATH_AUTO;
+    const mq_status st = mq::qlinear_validate(
+        a_q, 8, a_rowsum, M, K, N, w_q, w_bits, w_scale, w_zp, w_colsum, a_scale, a_zp,
+        out_scale, out_zp, out_bits, bias, y_q, workspace, workspace_bytes, path, &p, &resolved,
+        y);
+    if (st != MQ_OK) return st;
+    return mq::qlinear_dispatch(p, resolved, as_stream(stream));
 }
 
 mq_status mq_qlinear_group(const int8_t* a_q, const int32_t* a_rowsum, int64_t M, int64_t K,

@@ -16,7 +16,10 @@ struct QLinearArgs {
     const float* w_scale;   // [N]
     const int32_t* colsum;  // [N]
     const float* bias;      // [N] or nullptr
-    void* y;                // [M][N] int8 or int16
+    void* y;                // [M][N] int8 or int16, or nullptr when y_f is set
+    // [M][N] fp32, out_scale * (y - out_zp) written by the same pass (the
+    // dequantized outputs), or nullptr; dense 8-bit-activation products only
+    float* y_f = nullptr;
     int64_t M, K, N;
     float a_scale;
     float out_scale;
@@ -185,7 +188,7 @@ mq_status qlinear_validate(const void* a_q, int32_t a_bits, const int32_t* a_row
                            float a_scale, int32_t a_zp, float out_scale, int32_t out_zp,
                            int32_t out_bits, const float* bias, void* y_q, void* workspace,
                            int64_t workspace_bytes, int32_t path, QLinearArgs* out,
-                           int32_t* path_out);
+                           int32_t* path_out, float* y_f = nullptr);
 mq_status qlinear_dispatch(const QLinearArgs& p, int32_t path, hipStream_t s);
 
 }  // namespace mq

@@ -204,6 +204,20 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     }
     const int64_t nb = n0 + 4 * kg;
     const int64_t base = m * p.N + nb;
+    if (p.y_f) {
+        if (nb + 3 < p.N && (p.N % 4) == 0) {
+            *reinterpret_cast<float4*>(p.y_f + base) =
+                make_float4(dequant_code(out[0], p.out_scale, p.out_zp),
+                            dequant_code(out[1], p.out_scale, p.out_zp),
+                            dequant_code(out[2], p.out_scale, p.out_zp),
+                            dequant_code(out[3], p.out_scale, p.out_zp));
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                if (nb + r < p.N) p.y_f[base + r] = dequant_code(out[r], p.out_scale, p.out_zp);
+        }
+    }
+    if (!p.y) return;
     if (nb + 3 < p.N && (p.N % 4) == 0) {
         if constexpr (OBITS == 8) {
             const uint32_t v = ((uint32_t)out[0] & 0xFFu) | (((uint32_t)out[1] & 0xFFu) << 8) |
@@ -283,6 +297,7 @@ bool decode_supported(const QLinearArgs& p)
                        p.row_off == nullptr && p.ws_stride == 1;
     return dense && p.M <= 16 && p.K % 16 == 0 && ((uintptr_t)p.a % 16) == 0 &&
            ((uintptr_t)p.w % wa) == 0 && ((uintptr_t)p.y % 8) == 0 &&
+           ((uintptr_t)p.y_f % 16) == 0 &&
            (p.N + 15) / 16 <= 0x7FFFFFFF;
 }
 

@@ -161,10 +161,13 @@ __global__ __launch_bounds__(NW * 64) void qlinear_gemv_kernel(QLinearArgs p)
                       p.out_zp, qmin, qmax);
     else
         y = requant_out(sum, cp, p.out_zp, qmin, qmax);
-    if constexpr (OBITS == 8)
-        static_cast<int8_t*>(p.y)[n0 + lane] = (int8_t)y;
-    else
-        static_cast<int16_t*>(p.y)[n0 + lane] = (int16_t)y;
+    if (p.y) {
+        if constexpr (OBITS == 8)
+            static_cast<int8_t*>(p.y)[n0 + lane] = (int8_t)y;
+        else
+            static_cast<int16_t*>(p.y)[n0 + lane] = (int16_t)y;
+    }
+    if (p.y_f) p.y_f[n0 + lane] = dequant_code(y, p.out_scale, p.out_zp);
 }
 
 template <int WBITS, int OBITS, int NW, bool ASYM>

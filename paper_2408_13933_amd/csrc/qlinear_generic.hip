@@ -63,10 +63,13 @@ __global__ __launch_bounds__(256) void qlinear_generic_kernel(QLinearArgs p)
             y = requant_out((int32_t)acc, cp, p.out_zp, qmin, qmax);
         }
         const int64_t yi = bt * p.y_bs + m * ldy + n;
-        if constexpr (OBITS == 8)
-            static_cast<int8_t*>(p.y)[yi] = (int8_t)y;
-        else
-            static_cast<int16_t*>(p.y)[yi] = (int16_t)y;
+        if (p.y) {
+            if constexpr (OBITS == 8)
+                static_cast<int8_t*>(p.y)[yi] = (int8_t)y;
+            else
+                static_cast<int16_t*>(p.y)[yi] = (int16_t)y;
+        }
+        if (p.y_f) p.y_f[m * p.N + n] = dequant_code(y, p.out_scale, p.out_zp);
     }
 }
 

@@ -199,6 +199,14 @@ struct EpiCtx {
     int32_t wave_col0;     // first channel of this wave's sub-tile (tile-local)
     MQ_LDS int8_t* stage;  // this wave's LDS staging area (staged stores)
     __amdgpu_buffer_rsrc_t ry;  // output rows of this tile
+    // dequantized outputs (fp32): the layer's output format, this tile's
+    // fp32 rows, whether the codes are stored as well
+    float out_scale;
+    int32_t out_zp_code;   // the output zero-point (out_zp may be folded away)
+    int32_t row_bytes_f;
+    int32_t lane_row_off_f;
+    bool has_codes;
+    __amdgpu_buffer_rsrc_t ryf;
 };
 
 // Staged stores: a wave's outputs go through its own LDS area, PB bytes of
@@ -250,7 +258,11 @@ struct Staging {
 // int64 before the saturation.  With 16-bit codes ASYM instead adds an
 // int64 term per token row (a per-tensor zero-point of the other operand),
 // also before the saturation.
-template <class C, bool ASYM, bool FAST, bool PRE, bool STAGED, class Acc, class Acc2>
+// YF: also (or, without codes, only) the dequantized outputs in fp32.  The
+// staged form converts each 16-byte chunk of codes it reads back from LDS
+// (whole 128-byte row segments per four lanes); the other forms store four
+// channels of one token per lane from the accumulator layout.
+template <class C, bool ASYM, bool FAST, bool PRE, bool STAGED, bool YF, class Acc, class Acc2>
 __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const EpiCtx& x)
 {
     constexpr int32_t qmin = -(1 << (C::OBITS - 1));
@@ -358,6 +370,29 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
                     continue;
                 }
                 const int32_t row_off = x.lane_row_off + j * 32 * x.row_bytes;
+                if constexpr (YF) {
+                    float f[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        f[r] = dequant_code(max(min(y[r], qmax), qmin), x.out_scale,
+                                            x.out_zp_code);
+                    const int32_t row_f = x.lane_row_off_f + j * 32 * x.row_bytes_f;
+                    const int32_t col_f = (x.n_tile + nl) * 4;
+                    if (FAST || (x.n_left & 3) == 0 || nl + 3 < x.n_left) {
+                        const v4i v = {__builtin_bit_cast(int, f[0]), __builtin_bit_cast(int, f[1]),
+                                       __builtin_bit_cast(int, f[2]), __builtin_bit_cast(int, f[3])};
+                        __builtin_amdgcn_raw_buffer_store_b128(
+                            v, x.ryf, col_ok ? (uint32_t)(row_f + col_f) : kOOB, 0, 0);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            __builtin_amdgcn_raw_buffer_store_b32(
+                                __builtin_bit_cast(int, f[r]), x.ryf,
+                                nl + r < x.n_left ? (uint32_t)(row_f + col_f + 4 * r) : kOOB, 0,
+                                0);
+                    }
+                    if (!x.has_codes) continue;
+                }
                 if (FAST || (x.n_left & 3) == 0 || nl + 3 < x.n_left) {
                     const uint32_t voff = col_ok ? (uint32_t)(row_off + col_off) : kOOB;
                     if constexpr (C::OBITS == 8) {
@@ -398,8 +433,34 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
         for (int t = 0; t < S::WR / S::RPI; ++t) {
             const int lrow = t * S::RPI + lane / S::CPR;
             const v4i v = *reinterpret_cast<MQ_LDS const v4i*>(x.stage + lrow * S::PITCH + ch * 16);
-            const uint32_t voff = (uint32_t)((x.wave_row0 + lrow) * x.row_bytes + col_byte);
-            __builtin_amdgcn_raw_buffer_store_b128(v, x.ry, voff, 0, 0);
+            if (!YF || x.has_codes) {
+                const uint32_t voff = (uint32_t)((x.wave_row0 + lrow) * x.row_bytes + col_byte);
+                __builtin_amdgcn_raw_buffer_store_b128(v, x.ry, voff, 0, 0);
+            }
+            if constexpr (YF) {
+                // the chunk's 16 / OB codes (clamped already), four per store
+                const int32_t off_f = (x.wave_row0 + lrow) * x.row_bytes_f +
+                                      (x.n_tile + x.wave_col0 + pass * S::PASS_COLS) * 4 +
+                                      ch * (16 / OB) * 4;
+#pragma unroll
+                for (int q = 0; q < 4 / OB; ++q) {
+                    int32_t c[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int e = 4 * q + r;  // code index in the chunk
+                        const uint32_t d = (uint32_t)v[e * OB / 4];
+                        c[r] = OB == 2 ? (int32_t)(int16_t)(d >> (16 * (e & 1)))
+                                       : (int32_t)(int8_t)(d >> (8 * (e & 3)));
+                    }
+                    const v4i fv = {
+                        __builtin_bit_cast(int, dequant_code(c[0], x.out_scale, x.out_zp_code)),
+                        __builtin_bit_cast(int, dequant_code(c[1], x.out_scale, x.out_zp_code)),
+                        __builtin_bit_cast(int, dequant_code(c[2], x.out_scale, x.out_zp_code)),
+                        __builtin_bit_cast(int, dequant_code(c[3], x.out_scale, x.out_zp_code))};
+                    __builtin_amdgcn_raw_buffer_store_b128(fv, x.ryf, (uint32_t)(off_f + 16 * q),
+                                                           0, 0);
+                }
+            }
         }
     }
     }
@@ -410,7 +471,7 @@ __device__ __forceinline__ void prefill_epilogue(Acc& acc, Acc2& acc2, const Epi
 // holds each linear's weights, per-channel inputs, output and requant
 // constants, tiles_n the tile columns of all of them); p carries the shared
 // fields and takes those of the block's linear.
-template <class C, bool ASYM, bool GROUP>
+template <class C, bool ASYM, bool GROUP, bool YF = false>
 __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g, int tiles_n,
                                              int tiles_m, int splits, int kt_per_split)
 {
@@ -967,10 +1028,31 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
     // staged stores need the tile's channels inside N and 16-byte row chunks
     const bool staged = fast && n_tile + C::TN <= p.N && (ctx.row_bytes % 16) == 0 &&
                         ((uintptr_t)y_batch % 16) == 0;
-    if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true>(acc, acc2, ctx);
-    else if (staged) prefill_epilogue<C, ASYM, true, true, true>(acc, acc2, ctx);
-    else if (fast) prefill_epilogue<C, ASYM, true, true, false>(acc, acc2, ctx);
-    else prefill_epilogue<C, ASYM, false, false, false>(acc, acc2, ctx);
+    if constexpr (YF) {
+        ctx.out_scale = p.out_scale;
+        ctx.out_zp_code = p.out_zp;
+        ctx.row_bytes_f = (int32_t)(p.N * 4);
+        ctx.lane_row_off_f = (wm * (C::TM / C::WM) + r32) * ctx.row_bytes_f;
+        ctx.has_codes = p.y != nullptr;
+        ctx.ryf = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(p.y_f + m_tile * p.N), (short)0, (int)(rows_a * ctx.row_bytes_f),
+            0x00020000);
+        // staged: the tile's channels inside N, 16-byte fp32 row chunks, and
+        // the codes' own rules when they are stored too
+        const bool staged_f = fast && n_tile + C::TN <= p.N && (p.N % 4) == 0 &&
+                              (!ctx.has_codes || staged);
+        if (staged_f && pre0)
+            prefill_epilogue<C, ASYM, true, false, true, true>(acc, acc2, ctx);
+        else if (staged_f) prefill_epilogue<C, ASYM, true, true, true, true>(acc, acc2, ctx);
+        else if (fast && pre0) prefill_epilogue<C, ASYM, true, false, false, true>(acc, acc2, ctx);
+        else if (fast) prefill_epilogue<C, ASYM, true, true, false, true>(acc, acc2, ctx);
+        else prefill_epilogue<C, ASYM, false, false, false, true>(acc, acc2, ctx);
+        return;
+    }
+    if (staged && pre0) prefill_epilogue<C, ASYM, true, false, true, false>(acc, acc2, ctx);
+    else if (staged) prefill_epilogue<C, ASYM, true, true, true, false>(acc, acc2, ctx);
+    else if (fast) prefill_epilogue<C, ASYM, true, true, false, false>(acc, acc2, ctx);
+    else prefill_epilogue<C, ASYM, false, false, false, false>(acc, acc2, ctx);
 }
 
 template <class C, bool ASYM>
@@ -980,6 +1062,15 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_kernel(QLi
                                                                        int kt_per_split)
 {
     prefill_body<C, ASYM, false>(p, nullptr, tiles_n, tiles_m, splits, kt_per_split);
+}
+
+// the dequantized outputs (fp32) written by the epilogue, the codes too
+// when p.y is set
+template <class C, bool ASYM>
+__global__ __launch_bounds__(C::THREADS, C::OCC) void qlinear_prefill_dequant_kernel(
+    QLinearArgs p, int tiles_n, int tiles_m, int splits, int kt_per_split)
+{
+    prefill_body<C, ASYM, false, true>(p, nullptr, tiles_n, tiles_m, splits, kt_per_split);
 }
 
 // several linears on one input, without a K split (kt: K stages)
@@ -1002,12 +1093,23 @@ hipError_t launch_cfg(const QLinearArgs& p, int splits, hipStream_t s)
     if (total * splits > 0x7FFFFFFF || p.batch > 65535) return hipErrorInvalidValue;
     // more than 64 KiB of dynamic LDS must be opted into once per kernel
     constexpr int lds = ASYM || C::A16 ? C::LDS_ASYM : C::LDS;
+    const dim3 grid((unsigned)(total * splits), (unsigned)p.batch);
+    if constexpr (!C::A16) {
+        if (p.y_f) {
+            static const hipError_t attr_f = hipFuncSetAttribute(
+                reinterpret_cast<const void*>(&qlinear_prefill_dequant_kernel<C, ASYM>),
+                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+            if (attr_f != hipSuccess) return attr_f;
+            qlinear_prefill_dequant_kernel<C, ASYM><<<grid, dim3(C::THREADS), lds, s>>>(
+                p, (int)tiles_n, (int)tiles_m, splits, (int)kt_per_split);
+            return hipGetLastError();
+        }
+    }
     static const hipError_t attr = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&qlinear_prefill_kernel<C, ASYM>),
         hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (attr != hipSuccess) return attr;
-    qlinear_prefill_kernel<C, ASYM><<<dim3((unsigned)(total * splits), (unsigned)p.batch),
-                                      dim3(C::THREADS), lds, s>>>(
+    qlinear_prefill_kernel<C, ASYM><<<grid, dim3(C::THREADS), lds, s>>>(
         p, (int)tiles_n, (int)tiles_m, splits, (int)kt_per_split);
     return hipGetLastError();
 }
@@ -1248,14 +1350,17 @@ bool prefill_supported(const QLinearArgs& p)
                        (p.y_bs * ob) % og == 0;
     // byte offsets inside one 256-row tile must fit the 32-bit buffer offset
     const int64_t lim = (int64_t)1 << 31;
-    const bool nok = 256 * ldy < lim && 256 * lda < lim && 256 * ldw < lim;
+    const bool nok = 256 * ldy < lim && 256 * lda < lim && 256 * ldw < lim &&
+                     (!p.y_f || 256 * p.N * 4 < lim);
+    // fp32 outputs: 16-byte stores of four channels
+    const bool fok = !p.y_f || (((uintptr_t)p.y_f % 16) == 0 && p.N % 4 == 0);
     // 16-bit activation codes: int8 weights only (the W8A16 tile), which
     // also takes strides, batches and int64 row terms; the 8-bit tiles take
     // dense single products
     const bool dense = p.lda == 0 && p.ldw == 0 && p.ldy == 0 && p.batch == 1 &&
                        p.row_off == nullptr && p.ws_stride == 1;
     const bool aok = p.a_bits == 8 ? dense : (p.w_bits == 8 && p.w_zp == nullptr);
-    return kok && align && nok && aok && p.batch >= 1 && p.batch <= 65535;
+    return kok && align && nok && aok && fok && p.batch >= 1 && p.batch <= 65535;
 }
 
 int64_t prefill_workspace_bytes(const QLinearArgs& p)

@@ -98,6 +98,15 @@ __device__ inline int32_t requant_out(int32_t acc, const ColParams& p, int32_t o
     return requant_c(__builtin_elementwise_add_sat(acc, p.off), p, out_zp, qmin, qmax);
 }
 
+// The dequantized value of an output code (the inverse of Eq.(4), the
+// arithmetic of mq_dequant: one exact integer subtraction, one fp32
+// multiply), for the layers that write it in the same pass.
+__device__ inline float dequant_code(int32_t q, float alpha, int32_t zp)
+{
+#pragma clang fp contract(off)
+    return alpha * (float)(q - zp);
+}
+
 // 16-bit activations (W8A16): the kernels split each code a into an int8
 // high part h = a >> 8 and an offset low part l = (a & 255) - 128, so that
 // a = 256 h + l + 128 and

@@ -121,6 +121,32 @@ def test_qlinear_group_nothing_to_do():
     assert qlin_group(parts=[{"N": 0}], M=0, a_q=None) == 0
 
 
+def qlin_deq(**kw):
+    a = dict(a_q=NZ, a_rowsum=None, M=4, K=64, N=8, w_q=NZ, w_bits=8, w_scale=NZ, w_zp=None,
+             w_colsum=NZ, a_scale=0.1, a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None,
+             y_q=None, y=NZ, ws=None, ws_bytes=0, path=0, stream=None)
+    a.update(kw)
+    return mq.lib().mq_qlinear_dequant(a["a_q"], a["a_rowsum"], a["M"], a["K"], a["N"],
+                                       a["w_q"], a["w_bits"], a["w_scale"], a["w_zp"],
+                                       a["w_colsum"], a["a_scale"], a["a_zp"], a["out_scale"],
+                                       a["out_zp"], a["out_bits"], a["bias"], a["y_q"], a["y"],
+                                       a["ws"], a["ws_bytes"], a["path"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(y=None), dict(y=None, y_q=NZ), dict(a_q=None), dict(w_q=None), dict(K=0),
+    dict(w_bits=2), dict(out_bits=4), dict(out_scale=0.0), dict(a_zp=128),
+    dict(w_zp=NZ), dict(a_rowsum=NZ), dict(path=7), dict(path=16 + mq.PREFILL_TILES),
+    dict(ws=P(256 + 16), ws_bytes=4096),
+], ids=str)
+def test_qlinear_dequant_rejects_invalid_arguments(kw):
+    assert qlin_deq(**kw) == 1
+
+
+def test_qlinear_dequant_nothing_to_do():
+    assert qlin_deq(M=0, y=None) == 0 and qlin_deq(N=0, y=None) == 0
+
+
 def qlin_noalloc(**kw):
     a = dict(a_q=NZ, M=4, K=64, N=8, w_q=NZ, w_bits=8, w_scale=NZ, w_colsum=NZ, a_scale=0.1,
              a_zp=0, out_scale=0.1, out_zp=0, out_bits=8, bias=None, y_q=NZ, stream=None)
