@@ -104,3 +104,25 @@ def test_dequant_output_with_k_split():
 def test_dequant_output_decode_paths(M, K, N, w_bits, asym, with_codes):
     c = _case(M * 7 + N, M, K, N, w_bits, asym, True)
     _check(c, w_bits, 16, 0.004, 12, _mq().PATH_AUTO, with_codes)
+
+
+def test_dequant_output_full_size_lm_head():
+    """The Gemma-2B LM head at M = 512 (the bench step's last launch), full
+    size: every fused fp32 logit equals mq_dequant of mq_qlinear's codes
+    (which the full-size parity test compares with the oracle)."""
+    mq, torch = _mq(), _torch()
+    from paper_2408_13933_amd import workloads as wl
+    dev = torch.device("cuda", 0)
+    layer = next(l for l in wl.WORKLOADS["gemma2b_w8a8"].layers if l.name == "lm_head_m512")
+    ld = wl.make_layer("gemma2b_w8a8", layer)
+    a_scale, a_zp = mq.mq_act_params(*ld.act_range, 8)
+    o_scale, o_zp = mq.mq_act_params(*ld.out_range, layer.out_bits)
+    a_q = mq.mq_quantize_act(torch.from_numpy(ld.x).to(dev), a_scale, a_zp, 8)
+    wq, ws, cs = mq.mq_pack_weights(torch.from_numpy(ld.w).to(dev), layer.w_bits)
+    codes = mq.mq_qlinear(a_q, wq, layer.w_bits, ws, cs, a_scale, a_zp, o_scale, o_zp,
+                          layer.out_bits)
+    ref = mq.mq_dequant(codes, o_scale, o_zp)
+    del codes
+    y = mq.mq_qlinear_dequant(a_q, wq, layer.w_bits, ws, cs, a_scale, a_zp, o_scale, o_zp,
+                              layer.out_bits)
+    assert torch.equal(y, ref)
