@@ -155,12 +155,17 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     if constexpr (ASYM)
         asm volatile("" : "+v"(col_zw[0]), "+v"(col_zw[1]), "+v"(col_zw[2]), "+v"(col_zw[3]),
                      "+v"(row_sum));
+    // the fixed-point constants and their integer (mul_hi) form, off the
+    // critical path: the weight stream is still in flight
     ColParams cps[4] = {};
+    EpiInt eis[4] = {};
     if (wave == 0) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < 4; ++r) {
             cps[r] = derive_col_params_v(p.a_scale, col_ws[r], p.out_scale, p.bias != nullptr,
                                          col_b[r], col_cs[r], p.a_zp);
+            eis[r] = epi_int_params(cps[r]);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
     for (int64_t s = s_begin; s < s_end; s += U) {
@@ -191,16 +196,18 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
             int64_t sum = ((int64_t)acc[r] << 8) + acc2[r];
             if constexpr (WBITS == 4) sum >>= 4;  // exact: a multiple of 16
             const int64_t c = sum + a16_offset(cps[r], p.a_zp, col_cs[r]);
-            out[r] = requant_c(sat32(c), cps[r], p.out_zp, qmin, qmax);
+            out[r] = requant_int(sat32(c), 0, eis[r], p.out_zp, qmin, qmax);
             continue;
         }
         int32_t a32 = acc[r];
         if constexpr (WBITS == 4) a32 >>= 4;  // exact: the sum is a multiple of 16
+        // the integer form of the requant (requant_int, as the prefill
+        // epilogue): one mul_hi, no int64 arithmetic, no branches
         if constexpr (ASYM)
-            out[r] = requant_c(corrected_acc_asym(a32, cps[r].off, -col_zw[r], rs), cps[r],
-                               p.out_zp, qmin, qmax);
+            out[r] = requant_int(corrected_acc_asym(a32, cps[r].off, -col_zw[r], rs), 0, eis[r],
+                                 p.out_zp, qmin, qmax);
         else
-            out[r] = requant_out(a32, cps[r], p.out_zp, qmin, qmax);
+            out[r] = requant_int(a32, cps[r].off, eis[r], p.out_zp, qmin, qmax);
     }
     const int64_t nb = n0 + 4 * kg;
     const int64_t base = m * p.N + nb;

@@ -113,9 +113,12 @@ __global__ __launch_bounds__(NW * 64) void qlinear_gemv_kernel(QLinearArgs p)
     asm volatile("" : "+v"(col_ws), "+v"(col_cs), "+v"(col_b));
     if constexpr (ASYM) asm volatile("" : "+v"(col_zw), "+v"(row_sum));
     ColParams cp = {};
-    if (epi)
+    EpiInt ei = {};
+    if (epi) {
         cp = derive_col_params_v(p.a_scale, col_ws, p.out_scale, p.bias != nullptr, col_b,
                                  col_cs, p.a_zp);
+        ei = epi_int_params(cp);  // the integer (mul_hi) form of the requant
+    }
     __syncthreads();
 
     // |acc| <= K * 128 * 128 = K * 2^14 <= 2^30 (K <= 65536; int4 as 16*w
@@ -157,10 +160,10 @@ __global__ __launch_bounds__(NW * 64) void qlinear_gemv_kernel(QLinearArgs p)
     if constexpr (WBITS == 4) sum >>= 4;  // exact: the sum is a multiple of 16
     int32_t y;
     if constexpr (ASYM)
-        y = requant_c(corrected_acc_asym(sum, cp.off, -col_zw, row_sum - K32 * p.a_zp), cp,
-                      p.out_zp, qmin, qmax);
+        y = requant_int(corrected_acc_asym(sum, cp.off, -col_zw, row_sum - K32 * p.a_zp), 0, ei,
+                        p.out_zp, qmin, qmax);
     else
-        y = requant_out(sum, cp, p.out_zp, qmin, qmax);
+        y = requant_int(sum, cp.off, ei, p.out_zp, qmin, qmax);
     if (p.y) {
         if constexpr (OBITS == 8)
             static_cast<int8_t*>(p.y)[n0 + lane] = (int8_t)y;
