@@ -671,7 +671,8 @@ mq_status mq_dequant(const void* q, int32_t bits, int64_t numel, float alpha,
  * `bytes` bytes of device memory at `src` with `blocks` work-groups of
  * `waves` wavefronts (the grid of the kernel whose memory floor is being
  * measured).  Block b reads bytes [b*per, (b+1)*per), per = bytes/blocks
- * rounded up to 1 KiB, as 1 KiB wave loads (16 bytes per lane) with
+ * rounded up to 1 KiB, as 1 KiB wave loads (16 bytes per lane, the
+ * non-temporal cache policy of the decode kernels' weight loads) with
  * `unroll` loads per lane in flight per round.  Each wave writes the XOR of
  * what it read to sink[b*waves + w], so no load can be dropped.
  *   src    device, any alignment of 16 bytes or more (null when bytes == 0)

@@ -6,7 +6,8 @@
 // rounded up to 1 KiB.  Its waves take 1 KiB wave loads in turn (lane i
 // reads 16 bytes at 16*i), `unroll` loads per lane in flight per round, all
 // through a buffer descriptor over the whole buffer, so loads past its end
-// return zeros.  Each wave writes the XOR of what it read to one word of
+// return zeros.  The loads carry the non-temporal cache policy, as the
+// decode kernels' weight loads do.  Each wave writes the XOR of what it read to one word of
 // `sink`, so no load can be dropped.
 #include "mq_internal.h"
 
@@ -33,7 +34,7 @@ __global__ void probe_read_kernel(const int8_t* src, int64_t bytes, int64_t per,
 #pragma unroll
         for (int u = 0; u < U; ++u)
             v[u] = __builtin_amdgcn_raw_buffer_load_b128(
-                r, (uint32_t)(base + ((int64_t)u * waves + wave) * 1024 + lane * 16), 0, 0);
+                r, (uint32_t)(base + ((int64_t)u * waves + wave) * 1024 + lane * 16), 0, 2);
 #pragma unroll
         for (int u = 0; u < U; ++u) x ^= v[u];
     }

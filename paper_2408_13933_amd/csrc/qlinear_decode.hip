@@ -61,6 +61,7 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
     // beyond this wave's range) returns zeros without touching memory, so
     // every load is unconditional.
     constexpr uint32_t kOOB = 0x80000000u;
+    constexpr int kStreamLoad = 2;  // weights: non-temporal cache policy (read once per call)
     const int64_t wrow_bytes = WBITS == 8 ? p.K : p.K / 2;
     const int rows_w = (int)(p.N - n0 < R ? p.N - n0 : R);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
@@ -105,13 +106,13 @@ __global__ __launch_bounds__(NWAVES * 64) void qlinear_decode_kernel(QLinearArgs
             const uint32_t dead = (uint32_t)((su >= s_end32) | (k >= K32)) << 31;
             if constexpr (WBITS == 8) {
                 wv[u] = __builtin_amdgcn_raw_buffer_load_b128(rw, (uint32_t)(r16 * K32 + k) | dead,
-                                                              0, 0);
+                                                              0, kStreamLoad);
             } else {
                 // packed nibbles stay packed until the MFMA needs them, so
                 // the next load round is issued before this one lands
                 typedef unsigned v2u __attribute__((ext_vector_type(2)));
                 const v2u pk = __builtin_amdgcn_raw_buffer_load_b64(
-                    rw, (uint32_t)(r16 * (K32 / 2) + k / 2) | dead, 0, 0);
+                    rw, (uint32_t)(r16 * (K32 / 2) + k / 2) | dead, 0, kStreamLoad);
                 wv[u] = v4i{(int)pk[0], (int)pk[1], 0, 0};
             }
             if constexpr (A16) {

@@ -21,6 +21,11 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kOOB = 0x80000000u;  // any offset past num_records reads zero
+// cache policy of the weight loads: non-temporal (each weight byte is read
+// once per call).  Measured on MI355X for the 1 x 2048 x 256000 LM head:
+// 86.6 -> 78.1 us cold, and 112 -> 80 us after a layer that left 524 MB of
+// dirty outputs in the Infinity Cache (the stream no longer evicts them).
+constexpr int kStreamLoad = 2;
 constexpr int kCPB = 8;                 // output channels per block
 constexpr int kLPC = 64 / kCPB;         // lanes per channel in a wave load
 constexpr int kU = 4;                   // steps (wave loads) in flight per round
@@ -100,7 +105,7 @@ __global__ __launch_bounds__(NW * 64) void qlinear_gemv_kernel(QLinearArgs p)
             // steps past the wave's range and chunks past the row read zeros
             const uint32_t dead = (uint32_t)((su >= s_end) | (off >= wrow)) << 31;
             wv[u] = __builtin_amdgcn_raw_buffer_load_b128(rw, (uint32_t)(c * wrow + off) | dead, 0,
-                                                          0);
+                                                          kStreamLoad);
         }
     };
     load(s_begin);
