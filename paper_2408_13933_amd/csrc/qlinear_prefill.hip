@@ -810,12 +810,14 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
                 const int phys = (ks * 2 + hk) ^ swz<C::SWZ>(row, C::CW);
                 wf[i] = *reinterpret_cast<const v4i*>(sw + row * C::BKW + phys * 16);
             } else {
-                // the 32 weights of this k step are one packed 16-byte chunk
+                // the 32 weights of this k step are one packed 16-byte chunk;
+                // they stay packed until the step that multiplies them, so the
+                // read's latency is hidden behind a whole step as for int8
                 const int phys = ks ^ swz<C::SWZ>(row, C::CW);
                 typedef unsigned v2u __attribute__((ext_vector_type(2)));
                 const v2u pk =
                     *reinterpret_cast<const v2u*>(sw + row * C::BKW + phys * 16 + hk * 8);
-                wf[i] = unpack_int4_x16(pk[0], pk[1]);
+                wf[i] = v4i{(int)pk[0], (int)pk[1], 0, 0};
             }
         }
     };
@@ -823,6 +825,7 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
     // 16-bit codes (af = the split planes, high at 2j, low at 2j+1) the
     // plane is t % 2 and the pair index t / 2
     auto mfma_range = [&](const v4i* wf, const v4i* af, int t0, int t1) {
+        v4i wu = {0, 0, 0, 0};  // the unpacked int4 channel fragment
 #pragma unroll
         for (int t = t0; t < t1; ++t) {
             if constexpr (C::A16) {
@@ -835,8 +838,17 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
                                                                        acc2[i][j], 0, 0, 0);
             } else {
                 const int i = t / C::FM, j = t % C::FM;
-                acc[i][j] =
-                    __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
+                if constexpr (C::WBITS == 4) {
+                    // packed int4: unpacked to 16*w where the group first
+                    // multiplies this channel fragment (t is a compile-time
+                    // constant, so the test folds away)
+                    if (t == t0 || j == 0)
+                        wu = unpack_int4_x16((uint32_t)wf[i][0], (uint32_t)wf[i][1]);
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wu, af[j], acc[i][j], 0, 0, 0);
+                } else {
+                    acc[i][j] =
+                        __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[i], af[j], acc[i][j], 0, 0, 0);
+                }
             }
         }
     };
