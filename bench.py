@@ -118,6 +118,10 @@ def parse():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE "
                          "and WRITE_SIZE passes over a run with --calib-copy-mib) and exit")
+    ap.add_argument("--sq-summary", nargs=2, metavar=("PASS_A_CSV", "PASS_B_CSV"),
+                    help="summarise two rocprofv3 --pmc counter_collection.csv files of shader "
+                         "counters (pass A: " + " ".join(SQ_PASS_A) + "; pass B: "
+                         + " ".join(SQ_PASS_B) + ") per prefill kernel and exit")
     return ap.parse_args()
 
 
@@ -260,6 +264,58 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload, group=True, fuse_dequa
                                         f"w{D.w_bits}/o{D.out_bits}",
                                   **entry(kname, grid, D.alg_bytes())))
     return res
+
+
+# Shader counters of the prefill kernels, two rocprofv3 --pmc passes (at most
+# 8 SQ counters per pass) over the same bench command.
+SQ_PASS_A = ("SQ_WAVES", "SQ_BUSY_CU_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU",
+             "SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_INSTS_SALU", "SQ_WAVE_CYCLES", "GRBM_GUI_ACTIVE")
+SQ_PASS_B = ("SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_WAIT_INST_LDS", "SQ_WAIT_INST_ANY",
+             "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_ANY", "GRBM_GUI_ACTIVE")
+XCDS, SIMDS = 8, 1024
+
+
+def sq_summary(a_csv, b_csv):
+    """Per prefill (kernel, grid) of the two shader-counter passes, averaged
+    over dispatches: cycles (GRBM_GUI_ACTIVE is reported summed over the 8
+    XCDs), the MFMA-busy fraction of the SIMD-cycles, instructions per wave,
+    the LDS bank-conflict fraction of the LDS-active cycles, and the
+    fractions of wave time spent waiting to issue and issuing VALU / LDS."""
+    import re
+
+    groups = {}
+    for path in (a_csv, b_csv):
+        per = {}
+        with open(path, newline="") as f:
+            for r in csv.DictReader(f):
+                if "qlinear_prefill" not in r["Kernel_Name"]:
+                    continue
+                name = re.sub(r"\(anonymous namespace\)::|mq::", "", r["Kernel_Name"])
+                name = re.sub(r"^void ", "", name).split("(QLinearArgs")[0]
+                key = (name, int(r["Grid_Size"]))
+                d = per.setdefault(int(r["Dispatch_Id"]), (key, {}))[1]
+                d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        for key, d in per.values():
+            g = groups.setdefault(key, {})
+            for c, v in d.items():
+                g.setdefault(c, []).append(v)
+    rows = []
+    for (name, grid), g in groups.items():
+        m = {c: sum(v) / len(v) for c, v in g.items()}
+        waves, cyc = m["SQ_WAVES"], m["GRBM_GUI_ACTIVE"] / XCDS
+        rows.append({
+            "kernel": name, "grid": grid, "dispatches": len(g["SQ_WAVES"]),
+            "cycles": round(cyc),
+            "mfma_busy": round(m["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * SIMDS), 3),
+            "per_wave": {k: round(m["SQ_INSTS_" + k.upper()] / waves, 1)
+                         for k in ("valu", "mfma", "lds", "salu")},
+            "lds_bank_conflict": round(m["SQ_LDS_BANK_CONFLICT"] / max(1.0, m["SQ_LDS_IDX_ACTIVE"]), 3),
+            "wait_issue": round(m["SQ_WAIT_INST_ANY"] / max(1.0, m["SQ_WAVE_CYCLES"]), 3),
+            "active_valu": round(m["SQ_ACTIVE_INST_VALU"] / max(1.0, m["SQ_ACTIVE_INST_ANY"]), 3),
+            "active_lds": round(m["SQ_ACTIVE_INST_LDS"] / max(1.0, m["SQ_ACTIVE_INST_ANY"]), 3),
+        })
+    rows.sort(key=lambda r: -r["cycles"] * r["dispatches"])
+    return "\n".join(json.dumps(r) for r in rows)
 
 
 def trace_summary(path):
@@ -1010,6 +1066,9 @@ def main():
         return
     if args.trace_summary:
         print(trace_summary(args.trace_summary))
+        return
+    if args.sq_summary:
+        print(sq_summary(*args.sq_summary))
         return
     if args.pmc_summary:
         if args.calib_copy_mib <= 0:

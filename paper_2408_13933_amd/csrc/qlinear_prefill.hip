@@ -893,8 +893,12 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
     v4i wf0[C::FN], af0[C::FM * C::AB], wf1[C::FN], af1[C::FM * C::AB];
 #pragma unroll
     for (int g = 0; g < NRD; ++g) load_frag(0, 0, g, wf0, af0);
-    for (int kt = 0; kt < KT - 1; ++kt) {
-        const int buf = kt % C::STAGES;
+    // One stage kt (followed by a stage switch) held in LDS buffer bufv.  The
+    // main loop passes the buffer as a compile-time constant (its stages
+    // unrolled by STAGES), so a fragment read's LDS address is a lane offset
+    // held across the loop plus an immediate: no address arithmetic per read.
+    auto run_stage = [&](int kt, auto bufv) {
+        const int buf = (int)bufv;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             v4i* wc = (ks & 1) ? wf1 : wf0;
@@ -905,7 +909,7 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
                 // the rest of the DMA of stage kt+STAGES-1 (its buffer was
                 // freed by the previous stage switch)
                 step(wc, ac, true, buf, ks + 1, wx, ax, true, kt + C::STAGES - 1,
-                     (kt + C::STAGES - 1) % C::STAGES, ks + 1);
+                     (buf + C::STAGES - 1) % C::STAGES, ks + 1);
             } else {
                 // Stage switch at the start of the stage's last step: this
                 // step's fragments are already in registers, so buffer `buf`
@@ -918,10 +922,27 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
                 __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
                 __builtin_amdgcn_s_barrier();
                 __builtin_amdgcn_sched_barrier(0);
-                step(wc, ac, true, (kt + 1) % C::STAGES, 0, wx, ax, true, kt + C::STAGES, buf, 0);
+                step(wc, ac, true, (buf + 1) % C::STAGES, 0, wx, ax, true, kt + C::STAGES, buf, 0);
             }
         }
+    };
+    using B0 = std::integral_constant<int, 0>;
+    using B1 = std::integral_constant<int, 1>;
+    using B2 = std::integral_constant<int, 2>;
+    using B3 = std::integral_constant<int, 3>;
+    int kt0 = 0;  // a multiple of STAGES: stage kt0 + b sits in buffer b
+    for (; kt0 + C::STAGES <= KT - 1; kt0 += C::STAGES) {
+        run_stage(kt0, B0{});
+        run_stage(kt0 + 1, B1{});
+        if constexpr (C::STAGES > 2) run_stage(kt0 + 2, B2{});
+        if constexpr (C::STAGES > 3) run_stage(kt0 + 3, B3{});
     }
+    // the fewer than STAGES stages with a switch that remain
+    if (kt0 < KT - 1) run_stage(kt0, B0{});
+    if constexpr (C::STAGES > 2)
+        if (kt0 + 1 < KT - 1) run_stage(kt0 + 1, B1{});
+    if constexpr (C::STAGES > 3)
+        if (kt0 + 2 < KT - 1) run_stage(kt0 + 2, B2{});
     {  // last stage: no switch
         const int buf = (KT - 1) % C::STAGES;
 #pragma unroll
