@@ -614,14 +614,17 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
         if (idx < C::A_PER_WAVE) {
             const int i = idx, k0 = kt * C::BKA;  // bytes
             const int wl = wave + i * C::NWAVES;
-            const uint32_t voff =
-                (k0 + a_kb(i) < (int)KL * C::AB) ? a_off[i] + (uint32_t)k0 : kOOB;
+            // the stage's bytes left in the row (uniform): one compare per
+            // chunk against a lane constant, no per-lane sum
+            const int left = __builtin_amdgcn_readfirstlane((int)KL * C::AB - k0);
+            const uint32_t voff = a_kb(i) < left ? a_off[i] + (uint32_t)k0 : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (MQ_LDS void*)(base + wl * 1024), 16,
                                                      voff, 0, 0, 0);
         } else {
             const int i = idx - C::A_PER_WAVE, k0w = kt * C::BKW;
             const int wl = wave + i * C::NWAVES;
-            const uint32_t voff = (k0w + w_kb(i) < (int)KLw) ? w_off[i] + (uint32_t)k0w : kOOB;
+            const int left = __builtin_amdgcn_readfirstlane((int)KLw - k0w);
+            const uint32_t voff = w_kb(i) < left ? w_off[i] + (uint32_t)k0w : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rw, (MQ_LDS void*)(base + C::A_BYTES + wl * 1024), 16, voff, 0, 0, 0);
         }
