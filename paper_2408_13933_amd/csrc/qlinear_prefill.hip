@@ -617,16 +617,20 @@ __device__ __forceinline__ void prefill_body(QLinearArgs& p, const GroupArgs* g,
             // the stage's bytes left in the row (uniform): one compare per
             // chunk against a lane constant, no per-lane sum
             const int left = __builtin_amdgcn_readfirstlane((int)KL * C::AB - k0);
-            const uint32_t voff = a_kb(i) < left ? a_off[i] + (uint32_t)k0 : kOOB;
+            // the stage's K offset goes in the scalar offset: the lane's
+            // offset is its constant one, or out of range (which the
+            // hardware's range check turns into zeros whatever the scalar
+            // part adds)
+            const uint32_t voff = a_kb(i) < left ? a_off[i] : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (MQ_LDS void*)(base + wl * 1024), 16,
-                                                     voff, 0, 0, 0);
+                                                     voff, (uint32_t)k0, 0, 0);
         } else {
             const int i = idx - C::A_PER_WAVE, k0w = kt * C::BKW;
             const int wl = wave + i * C::NWAVES;
             const int left = __builtin_amdgcn_readfirstlane((int)KLw - k0w);
-            const uint32_t voff = w_kb(i) < left ? w_off[i] + (uint32_t)k0w : kOOB;
+            const uint32_t voff = w_kb(i) < left ? w_off[i] : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rw, (MQ_LDS void*)(base + C::A_BYTES + wl * 1024), 16, voff, 0, 0, 0);
+                rw, (MQ_LDS void*)(base + C::A_BYTES + wl * 1024), 16, voff, (uint32_t)k0w, 0, 0);
         }
     };
     auto issue = [&](int kt, int buf) {
