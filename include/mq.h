@@ -59,8 +59,9 @@ typedef enum {
     MQ_PATH_GENERIC = 3,  /* one thread per output, any shape or alignment */
     /* MQ_PATH_PREFILL_TILE0 + t, t = 0..MQ_PREFILL_TILES-1: the prefill
      * kernel with output tile t (0: 256x128, 1: 128x128, 2: 192x256,
-     * 3: 64x64, 4: 256x256 on eight waves; tokens x channels) instead of
-     * the one its cost model picks -- a hook for tests and measurements;
+     * 3: 64x64, 4: 256x256 on eight waves, 5: 128x64; tokens x channels)
+     * instead of the one its cost model picks -- a hook for tests and
+     * measurements;
      * the results are the same bits.  With a workspace the K split is the
      * cost model's best for that tile and may need more bytes than
      * mq_qlinear_workspace_bytes reports (at most 256*ceil(T/64) +
@@ -68,7 +69,7 @@ typedef enum {
      * not split. */
     MQ_PATH_PREFILL_TILE0 = 16
 } mq_path;
-#define MQ_PREFILL_TILES 5
+#define MQ_PREFILL_TILES 6
 
 /* Largest K accepted: keeps |sum_k A_q W_q| below 2^30 so the int32
  * accumulator cannot overflow. */

@@ -30,8 +30,8 @@ lib_path = os.path.join(_HERE, "libmq.so")
 MQ_OK, MQ_ERR_INVALID_ARG, MQ_ERR_UNSUPPORTED, MQ_ERR_HIP = 0, 1, 2, 3
 PATH_AUTO, PATH_DECODE, PATH_PREFILL, PATH_GENERIC = 0, 1, 2, 3
 # the prefill kernel with one explicit output tile (tests and measurements)
-PATH_PREFILL_TILE0, PREFILL_TILES = 16, 5
-PREFILL_TILE_SHAPES = ((256, 128), (128, 128), (192, 256), (64, 64), (256, 256))
+PATH_PREFILL_TILE0, PREFILL_TILES = 16, 6
+PREFILL_TILE_SHAPES = ((256, 128), (128, 128), (192, 256), (64, 64), (256, 256), (128, 64))
 
 
 def prefill_tile_path(tile: int) -> int:

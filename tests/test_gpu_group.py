@@ -103,7 +103,7 @@ def test_group_matches_oracle(case):
         assert np.array_equal(single[i], ref), i
 
 
-@pytest.mark.parametrize("tile", list(range(5)))
+@pytest.mark.parametrize("tile", list(range(6)))
 def test_group_every_tile(tile):
     """One launch on each prefill tile (forced): the same bits as the
     separate calls."""

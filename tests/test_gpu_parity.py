@@ -331,7 +331,7 @@ def _pack_int4(codes):
     return (lo | (hi << 4)).astype(np.uint8)
 
 
-@pytest.mark.parametrize("tile", list(range(5)))
+@pytest.mark.parametrize("tile", list(range(6)))
 @pytest.mark.parametrize("asym", [False, True])
 @pytest.mark.parametrize("w_bits", [8, 4])
 def test_prefill_epilogue_forms(tile, asym, w_bits):

@@ -79,7 +79,7 @@ def test_dequant_output_prefill_and_generic(case, with_codes):
     _check(c, w_bits, out_bits, out_scale, out_zp, _mq().PATH_AUTO, with_codes)
 
 
-@pytest.mark.parametrize("tile", list(range(5)))
+@pytest.mark.parametrize("tile", list(range(6)))
 def test_dequant_output_every_tile(tile):
     c = _case(tile, 264, 1024, 520, 8, False, True)
     _check(c, 8, 16, 0.002, 77, _mq().prefill_tile_path(tile), False)
